@@ -1,0 +1,575 @@
+/*
+ * oracle.c -- plain, slow CPU oracle for the canary-versus-reference drift
+ * detector of "Integrity of peer-to-peer distributed LLM inference under
+ * malicious nodes" (Cihangiroglu & Nocera).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark do.  It shares no code, header, constant or table with
+ * the HIP library: every constant below is written out here from its
+ * published definition.
+ *
+ * Precision rules.
+ *  - Drift (Eq. 4) and its sums are computed in fp64 directly from the
+ *    definition, element by element, in index order.
+ *  - AUROC (Eqs. 5-6 and the Mann-Whitney form stated right after Eq. 6) is
+ *    counted pair by pair (brute force) on the fp32 scores.
+ *  - The synthetic generator (the stand-in for the fp32 pipeline of Eq. 1 and
+ *    the live pass of Eqs. 2-3) must reproduce fp32 arithmetic bit for bit.
+ *    Every fp32 operation is computed as the fp64 operation on the fp32
+ *    operands and then rounded once to fp32 (r32).  For + - * / and sqrt this
+ *    equals the fp32 operation itself because 53 >= 2*24 + 2 (double rounding
+ *    is innocuous; S. Figueroa, "When is double rounding innocuous?", 1995).
+ *  - Build with -ffp-contract=off and without fast-math.
+ *
+ * The paper fixes none of the random number generator, the normal sampler or
+ * the fp16 rounding; the readings used (Philox4x32-10, an Irwin-Hall sum of
+ * four 16-bit uniforms, IEEE round-to-nearest-even) are listed with the
+ * other readings of the paper in the design notes that accompany the code.
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_VERSION 1
+
+int orc_version(void) { return ORC_VERSION; }
+
+/* Round an fp64 value to fp32 (IEEE round-to-nearest-even). */
+static float r32(double x) { return (float)x; }
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10: J. Salmon, M. Moraes, R. Dror, D. Shaw, "Parallel random   */
+/* numbers: as easy as 1, 2, 3", SC'11.  Ten rounds; each round multiplies   */
+/* counter words 0 and 2 by the two round multipliers (32x32 -> 64 bit),      */
+/* mixes the high halves with words 1 and 3 and the round key by XOR, and     */
+/* permutes the words.  The key is advanced by the two Weyl increments        */
+/* (golden ratio and sqrt(3) - 1, scaled to 32 bits) before rounds 2..10.     */
+/* ------------------------------------------------------------------------ */
+static const uint32_t PHILOX_MUL0 = 0xD2511F53u;
+static const uint32_t PHILOX_MUL1 = 0xCD9E8D57u;
+static const uint32_t PHILOX_WEYL0 = 0x9E3779B9u;
+static const uint32_t PHILOX_WEYL1 = 0xBB67AE85u;
+
+void orc_philox(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += PHILOX_WEYL0;
+            k1 += PHILOX_WEYL1;
+        }
+        uint64_t p0 = (uint64_t)PHILOX_MUL0 * (uint64_t)x0;
+        uint64_t p1 = (uint64_t)PHILOX_MUL1 * (uint64_t)x2;
+        uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+        uint32_t y1 = (uint32_t)p1;
+        uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+        uint32_t y3 = (uint32_t)p0;
+        x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+    }
+    out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* Random streams: the fourth counter word is (stream << 24) | id. */
+enum {
+    ST_REF = 0,      /* reference activations (stand-in for Eq. 1)      */
+    ST_BENIGN = 1,   /* benign hardware noise delta_i (Eq. 2)             */
+    ST_T12 = 2,      /* chi-square normals 1, 2 of the Student-t noise    */
+    ST_T3 = 3,       /* chi-square normal 3 of the Student-t noise        */
+    ST_TADD = 4,     /* Gaussian tamper direction (Eq. 3, Gaussian)       */
+    ST_TFLIP = 5,    /* sign-flip selection (Eq. 3, sign flip)            */
+    ST_SCRAMBLE = 6, /* scrambled-label stage j* (Section 4.5)            */
+    ST_RANDOM = 7,   /* random-baseline scores (Section 4.5)              */
+    ST_OUTLIER = 8,  /* outlier channel choice of the synthetic reference */
+    ST_ALT = 9       /* independent benign redraw (Section 4.5 ceiling)   */
+};
+
+static void philox_at(uint64_t seed, uint32_t w0, uint32_t w1, uint32_t w2,
+                      uint32_t stream, uint32_t id, uint32_t out[4])
+{
+    uint32_t ctr[4] = {w0, w1, w2, (stream << 24) | (id & 0xFFFFFFu)};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    orc_philox(ctr, key, out);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Standard normal stand-in: the Irwin-Hall sum of four independent 16-bit   */
+/* uniforms, centred and scaled to unit variance.  Each 16-bit uniform has    */
+/* mean (2^16-1)/2 and variance (2^32-1)/12, so the centred sum n has         */
+/* variance (2^32-1)/3 and z = n * sqrt(3/(2^32-1)).                          */
+/* ------------------------------------------------------------------------ */
+static float unit_scale_k16(void)
+{
+    return r32(sqrt(3.0 / 4294967295.0));
+}
+
+float orc_z16(uint32_t w0, uint32_t w1)
+{
+    int32_t n = (int32_t)(w0 & 0xFFFFu) + (int32_t)(w0 >> 16) + (int32_t)(w1 & 0xFFFFu) +
+                (int32_t)(w1 >> 16) - 131070;
+    return r32((double)(float)n * (double)unit_scale_k16());
+}
+
+float orc_k16(void) { return unit_scale_k16(); }
+
+/* One normal per element: element e uses Philox call q = e / 2, words 0-1 for
+ * even e and words 2-3 for odd e.  Counter = (q, c, s, stream|id). */
+static float normal1(uint64_t seed, uint32_t stream, uint32_t id, uint32_t s, uint32_t c,
+                     uint32_t e)
+{
+    uint32_t w[4];
+    philox_at(seed, e >> 1, c, s, stream, id, w);
+    return (e & 1u) ? orc_z16(w[2], w[3]) : orc_z16(w[0], w[1]);
+}
+
+/* Two normals per element from one Philox call with q = e. */
+static void normal2(uint64_t seed, uint32_t stream, uint32_t id, uint32_t s, uint32_t c,
+                    uint32_t e, float* z1, float* z2)
+{
+    uint32_t w[4];
+    philox_at(seed, e, c, s, stream, id, w);
+    *z1 = orc_z16(w[0], w[1]);
+    *z2 = orc_z16(w[2], w[3]);
+}
+
+/* One uniform 32-bit word per element: Philox call q = e / 4, word e mod 4. */
+static uint32_t word1(uint64_t seed, uint32_t stream, uint32_t id, uint32_t s, uint32_t c,
+                      uint32_t e)
+{
+    uint32_t w[4];
+    philox_at(seed, e >> 2, c, s, stream, id, w);
+    return w[e & 3u];
+}
+
+/* ------------------------------------------------------------------------ */
+/* IEEE 754 binary16 conversion, round to nearest, ties to even.  The live   */
+/* activations travel in fp16 (Section 3.3); subnormals are kept and values  */
+/* at or beyond the overflow midpoint become infinities.                     */
+/* ------------------------------------------------------------------------ */
+uint16_t orc_f16_rne(float xf)
+{
+    double x = (double)xf;
+    uint16_t sign = signbit(x) ? 0x8000u : 0u;
+    if (isnan(x))
+        return (uint16_t)(sign | 0x7E00u);
+    double ax = fabs(x);
+    /* Largest finite half is 65504 = 2047 * 2^5; the next step would be 2^16,
+     * so the midpoint 65520 and everything above rounds to infinity. */
+    if (ax >= 65520.0)
+        return (uint16_t)(sign | 0x7C00u);
+    /* Spacing of representable halves around ax. */
+    double quantum;
+    if (ax < 0x1p-14) {
+        quantum = 0x1p-24; /* subnormal spacing */
+    } else {
+        int e2;
+        frexp(ax, &e2); /* ax = f * 2^e2, f in [0.5, 1) */
+        quantum = ldexp(1.0, (e2 - 1) - 10);
+    }
+    double r = ax / quantum; /* exact: division by a power of two */
+    double f = floor(r);
+    double frac = r - f;     /* exact */
+    if (frac > 0.5 || (frac == 0.5 && fmod(f, 2.0) == 1.0))
+        f += 1.0;
+    double v = f * quantum; /* the rounded magnitude, exact */
+    if (v == 0.0)
+        return sign;
+    if (v < 0x1p-14)
+        return (uint16_t)(sign | (uint16_t)(v / 0x1p-24));
+    int e2;
+    frexp(v, &e2);
+    int ex = e2 - 1; /* v in [2^ex, 2^(ex+1)) */
+    uint16_t mant = (uint16_t)((v / ldexp(1.0, ex) - 1.0) * 1024.0);
+    return (uint16_t)(sign | (uint16_t)((ex + 15) << 10) | mant);
+}
+
+double orc_f16_value(uint16_t bits)
+{
+    double sign = (bits & 0x8000u) ? -1.0 : 1.0;
+    int ex = (bits >> 10) & 0x1F;
+    int mant = bits & 0x3FF;
+    if (ex == 0x1F)
+        return mant ? NAN : sign * INFINITY;
+    if (ex == 0)
+        return sign * ldexp((double)mant, -24);
+    return sign * ldexp(1.0 + (double)mant / 1024.0, ex - 15);
+}
+
+/* Convert count consecutive fp32 bit patterns starting at `start`. */
+void orc_f16_rne_range(uint64_t start, uint64_t count, uint16_t* out)
+{
+    for (uint64_t i = 0; i < count; ++i) {
+        uint32_t bits = (uint32_t)(start + i);
+        float x;
+        memcpy(&x, &bits, 4);
+        out[i] = orc_f16_rne(x);
+    }
+}
+
+void orc_f16_rne_array(uint64_t n, const float* x, uint16_t* out)
+{
+    for (uint64_t i = 0; i < n; ++i)
+        out[i] = orc_f16_rne(x[i]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Synthetic fp32 references (stand-in for the precomputed a*_i of Eq. 1 and */
+/* Section 3.3): a[s][c][t][j] = fp32(z_REF * gain[j]).  gain marks outlier  */
+/* channels: the n_out channels j with the smallest (word, j) pairs, word =  */
+/* Philox((j, 0, 0, OUTLIER|ref_set_id))[0], get gain `big`, the rest 1.      */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    uint32_t word;
+    uint32_t j;
+} orc_keyed;
+
+static int cmp_keyed(const void* pa, const void* pb)
+{
+    const orc_keyed* a = (const orc_keyed*)pa;
+    const orc_keyed* b = (const orc_keyed*)pb;
+    if (a->word != b->word)
+        return a->word < b->word ? -1 : 1;
+    if (a->j != b->j)
+        return a->j < b->j ? -1 : 1;
+    return 0;
+}
+
+int orc_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed, uint32_t ref_set_id,
+                     float* gain)
+{
+    if (n_out > H)
+        return 1;
+    orc_keyed* keys = (orc_keyed*)malloc(sizeof(orc_keyed) * (H ? H : 1));
+    if (!keys)
+        return 2;
+    for (uint32_t j = 0; j < H; ++j) {
+        uint32_t w[4];
+        philox_at(seed, j, 0, 0, ST_OUTLIER, ref_set_id, w);
+        keys[j].word = w[0];
+        keys[j].j = j;
+        gain[j] = 1.0f;
+    }
+    qsort(keys, H, sizeof(orc_keyed), cmp_keyed);
+    for (uint32_t r = 0; r < n_out; ++r)
+        gain[keys[r].j] = big;
+    free(keys);
+    return 0;
+}
+
+void orc_ref_block(uint32_t s, uint32_t c, uint32_t T, uint32_t H, uint64_t seed,
+                   uint32_t ref_set_id, const float* gain, float* out)
+{
+    for (uint32_t t = 0; t < T; ++t)
+        for (uint32_t j = 0; j < H; ++j) {
+            uint32_t e = t * H + j;
+            float z = normal1(seed, ST_REF, ref_set_id, s, c, e);
+            out[e] = r32((double)z * (double)gain[j]);
+        }
+}
+
+/* Whole reference array [S][C][T][H]. */
+void orc_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
+                   uint32_t ref_set_id, const float* gain, float* out)
+{
+    uint64_t n = (uint64_t)T * H;
+    for (uint32_t s = 0; s < S; ++s)
+        for (uint32_t c = 0; c < C; ++c)
+            orc_ref_block(s, c, T, H, seed, ref_set_id, gain, out + ((uint64_t)s * C + c) * n);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Block statistics of a reference block: sum of squares (gives the rms used */
+/* by the per-element Gaussian tamper) and sum of magnitudes (gives mu_i of   */
+/* Eq. 2, the mean absolute activation).                                      */
+/* ------------------------------------------------------------------------ */
+void orc_ref_stats_block(uint64_t n, const float* a, double* sumsq, double* sumabs)
+{
+    double q = 0.0, m = 0.0;
+    for (uint64_t e = 0; e < n; ++e) {
+        double x = (double)a[e];
+        q += x * x;
+        m += fabs(x);
+    }
+    *sumsq = q;
+    *sumabs = m;
+}
+
+void orc_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref, double* sumsq,
+                   double* sumabs)
+{
+    uint64_t n = (uint64_t)T * H;
+    for (uint64_t b = 0; b < (uint64_t)S * C; ++b)
+        orc_ref_stats_block(n, ref + b * n, sumsq + b, sumabs + b);
+}
+
+/* Per-block scale factors, each rounded once to fp32:
+ *   tscale = eps * sqrt(sumsq / (T H))     (Gaussian tamper, eps times rms)
+ *   bscale = sigma_b * (sumabs / (T H))    (Eq. 2 block noise sigma_hw mu_i) */
+void orc_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const double* sumsq,
+                      const double* sumabs, double eps, double sigma_b, float* tscale,
+                      float* bscale)
+{
+    double n = (double)T * (double)H;
+    for (uint64_t b = 0; b < nblocks; ++b) {
+        double rms = n > 0 ? sqrt(sumsq[b] / n) : 0.0;
+        double mu = n > 0 ? sumabs[b] / n : 0.0;
+        if (tscale)
+            tscale[b] = r32(eps * rms);
+        if (bscale)
+            bscale[b] = r32(sigma_b * mu);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Live activations of one (shard, canary) block.                            */
+/*  benign (Eq. 2):   v = a + sc * zb, sc = sigma_b |a| (elementwise) or the  */
+/*                    block scale sigma_hw mu_i; zb a unit normal or a unit-   */
+/*                    variance Student-t with 3 degrees of freedom.            */
+/*  tamper (Eq. 3), malicious shards only, applied to v (or to a when the     */
+/*  clean base is asked for), in this order:                                   */
+/*     Gaussian  v = v + tscale * zT                                          */
+/*     sign flip v = -v where the element is selected (all when p >= 1)       */
+/*     rescale   v = scale * v                                                */
+/*  output: h = fp16(v), round to nearest even.                               */
+/* ------------------------------------------------------------------------ */
+enum { ORC_NOISE_ELEMENTWISE = 0, ORC_NOISE_BLOCK = 1 };
+enum { ORC_DIST_GAUSS = 0, ORC_DIST_T3 = 1 };
+enum { ORC_T_ADD = 1, ORC_T_FLIP = 2, ORC_T_SCALE = 4 };
+enum { ORC_BASE_BENIGN = 0, ORC_BASE_CLEAN = 1 };
+
+/* Flip threshold: an element flips when its uniform 32-bit word u satisfies
+ * u < floor(p 2^32); p >= 1 flips every element. */
+static int flip_selected(double p, uint32_t u)
+{
+    if (p >= 1.0)
+        return 1;
+    if (!(p > 0.0))
+        return 0;
+    double thr = floor(p * 4294967296.0);
+    return (double)u < thr;
+}
+
+int orc_sim_block(uint32_t s, uint32_t c, uint32_t T, uint32_t H, uint64_t seed, uint32_t cfg_id,
+                  int benign_mode, int benign_dist, double sigma_b, float bscale, int malicious,
+                  uint32_t tamper, int tamper_base, float tscale, double flip_p, double scale,
+                  const float* ref, uint16_t* h)
+{
+    float sigma_f = r32(sigma_b);
+    float scale_f = r32(scale);
+    for (uint32_t t = 0; t < T; ++t)
+        for (uint32_t j = 0; j < H; ++j) {
+            uint32_t e = t * H + j;
+            float a = ref[e];
+
+            /* benign hardware noise, Eq. 2 */
+            float sc = (benign_mode == ORC_NOISE_BLOCK) ? bscale : r32((double)sigma_f * fabs((double)a));
+            float zb = normal1(seed, ST_BENIGN, cfg_id, s, c, e);
+            if (benign_dist == ORC_DIST_T3) {
+                float z1, z2;
+                normal2(seed, ST_T12, cfg_id, s, c, e, &z1, &z2);
+                float z3 = normal1(seed, ST_T3, cfg_id, s, c, e);
+                float q = r32((double)r32((double)r32((double)z1 * z1) + (double)r32((double)z2 * z2)) +
+                              (double)r32((double)z3 * z3));
+                zb = (q == 0.0f) ? 0.0f : r32((double)zb / (double)r32(sqrt((double)q)));
+            }
+            float benign = r32((double)a + (double)r32((double)sc * (double)zb));
+            float v = benign;
+
+            /* tampering, Eq. 3 */
+            if (malicious) {
+                if (tamper_base == ORC_BASE_CLEAN)
+                    v = a;
+                if (tamper & ORC_T_ADD) {
+                    float zt = normal1(seed, ST_TADD, cfg_id, s, c, e);
+                    v = r32((double)v + (double)r32((double)tscale * (double)zt));
+                }
+                if (tamper & ORC_T_FLIP) {
+                    uint32_t u = word1(seed, ST_TFLIP, cfg_id, s, c, e);
+                    if (flip_selected(flip_p, u))
+                        v = -v;
+                }
+                if (tamper & ORC_T_SCALE)
+                    v = r32((double)scale_f * (double)v);
+            }
+            h[e] = orc_f16_rne(v);
+        }
+    return 0;
+}
+
+/* Whole live array [S][C][T][H].  tscale and bscale are [S][C] (may be NULL
+ * when unused); bit s of mal_mask marks shard s malicious. */
+int orc_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed, uint32_t cfg_id,
+                   int benign_mode, int benign_dist, double sigma_b, const float* bscale,
+                   uint64_t mal_mask, uint32_t tamper, int tamper_base, const float* tscale,
+                   double flip_p, double scale, const float* ref, uint16_t* h)
+{
+    uint64_t n = (uint64_t)T * H;
+    for (uint32_t s = 0; s < S; ++s)
+        for (uint32_t c = 0; c < C; ++c) {
+            uint64_t b = (uint64_t)s * C + c;
+            int mal = s < 64 && ((mal_mask >> s) & 1u);
+            orc_sim_block(s, c, T, H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
+                          bscale ? bscale[b] : 0.0f, mal, tamper, tamper_base,
+                          tscale ? tscale[b] : 0.0f, flip_p, scale, ref + b * n, h + b * n);
+        }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Relative-L2 mismatch, Eq. 4:  m = ||h - a||_F / ||a||_F over the T x d    */
+/* block, with h the fp16 live activation (widened exactly) and a the fp32    */
+/* reference.  D = sum (h - a)^2 and R = sum a^2 in fp64, index order.        */
+/* Degenerate block: R = 0 gives m = 0 when D = 0 and +inf otherwise.         */
+/* ------------------------------------------------------------------------ */
+double orc_drift_block(uint64_t n, const uint16_t* h, const float* a, double* D_out, double* R_out)
+{
+    double D = 0.0, R = 0.0;
+    for (uint64_t e = 0; e < n; ++e) {
+        double hv = orc_f16_value(h[e]);
+        double av = (double)a[e];
+        double d = hv - av;
+        D += d * d;
+        R += av * av;
+    }
+    if (D_out)
+        *D_out = D;
+    if (R_out)
+        *R_out = R;
+    if (R == 0.0)
+        return D == 0.0 ? 0.0 : INFINITY;
+    return sqrt(D / R);
+}
+
+/* Scores of every block, written as [C][S] (one canary's k scores adjacent,
+ * as Eq. 5 ranks them), both as fp64 and as fp32. */
+void orc_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                     const float* ref, double* score64, float* score32, double* num_den)
+{
+    uint64_t n = (uint64_t)T * H;
+    for (uint32_t s = 0; s < S; ++s)
+        for (uint32_t c = 0; c < C; ++c) {
+            uint64_t b = (uint64_t)s * C + c;
+            double D, R;
+            double m = orc_drift_block(n, h + b * n, ref + b * n, &D, &R);
+            uint64_t o = (uint64_t)c * S + s;
+            if (score64)
+                score64[o] = m;
+            if (score32)
+                score32[o] = r32(m);
+            if (num_den) {
+                num_den[2 * o] = D;
+                num_den[2 * o + 1] = R;
+            }
+        }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Detection AUROC.                                                          */
+/* Score order: NaN below every number, NaN ties NaN, -0 ties +0, otherwise  */
+/* the numeric order.                                                         */
+/* ------------------------------------------------------------------------ */
+static int score_cmp(float x, float y)
+{
+    int nx = isnan(x), ny = isnan(y);
+    if (nx || ny)
+        return nx && ny ? 0 : (nx ? -1 : 1);
+    if (x > y)
+        return 1;
+    if (x < y)
+        return -1;
+    return 0;
+}
+
+int orc_score_cmp(float x, float y) { return score_cmp(x, y); }
+
+enum { ORC_AUROC_CONTROL = 1, ORC_AUROC_POOLED = 2, ORC_CTRL_INCLUDE_TRUE = 4 };
+
+/* Scrambled-label stage for canary t (Section 4.5): a uniformly chosen
+ * benign stage j* != i*.  With benign stages b_0 < b_1 < ... < b_{B-1},
+ * u = Philox((t, 0, 0, SCRAMBLE|cfg_id))[0] and j* = b_{u mod B}.
+ * Returns -1 when there is no benign stage. */
+int orc_scramble_jstar(uint32_t S, uint64_t pos_mask, uint64_t seed, uint32_t cfg_id, uint32_t t)
+{
+    uint32_t benign[64];
+    uint32_t B = 0;
+    for (uint32_t j = 0; j < S && j < 64; ++j)
+        if (!((pos_mask >> j) & 1u))
+            benign[B++] = j;
+    if (B == 0)
+        return -1;
+    uint32_t w[4];
+    philox_at(seed, t, 0, 0, ST_SCRAMBLE, cfg_id, w);
+    return (int)benign[w[0] % B];
+}
+
+/* One configuration: scores [C][S] (fp32), positives = shards in pos_mask.
+ * counts[0..5] = G, E, pairs (Eq. 5 summed over canaries: G counts
+ *   m_i > m_j, E counts m_i == m_j, over i in M, j not in M),
+ *   then the same three for the scrambled-label control;
+ * pooled[0..2] = G, E, pairs over all positive/negative score pairs of the
+ *   configuration (the Mann-Whitney U of all C*S scores pooled). */
+int orc_auroc_config(uint32_t S, uint32_t C, const float* scores, uint64_t pos_mask,
+                     uint64_t seed, uint32_t cfg_id, uint32_t flags, uint64_t* counts,
+                     uint64_t* pooled)
+{
+    if (S > 64)
+        return 1;
+    for (int k = 0; k < 6; ++k)
+        counts[k] = 0;
+    if (pooled)
+        for (int k = 0; k < 3; ++k)
+            pooled[k] = 0;
+
+    for (uint32_t t = 0; t < C; ++t) {
+        const float* m = scores + (uint64_t)t * S;
+        for (uint32_t i = 0; i < S; ++i) {
+            if (!((pos_mask >> i) & 1u))
+                continue;
+            for (uint32_t j = 0; j < S; ++j) {
+                if ((pos_mask >> j) & 1u)
+                    continue;
+                int r = score_cmp(m[i], m[j]);
+                counts[0] += (r > 0);
+                counts[1] += (r == 0);
+                counts[2] += 1;
+            }
+        }
+        if (flags & ORC_AUROC_CONTROL) {
+            int js = orc_scramble_jstar(S, pos_mask, seed, cfg_id, t);
+            if (js >= 0) {
+                for (uint32_t j = 0; j < S; ++j) {
+                    if (j == (uint32_t)js)
+                        continue;
+                    if (!(flags & ORC_CTRL_INCLUDE_TRUE) && ((pos_mask >> j) & 1u))
+                        continue;
+                    int r = score_cmp(m[js], m[j]);
+                    counts[3] += (r > 0);
+                    counts[4] += (r == 0);
+                    counts[5] += 1;
+                }
+            }
+        }
+    }
+
+    if (pooled && (flags & ORC_AUROC_POOLED)) {
+        for (uint32_t tp = 0; tp < C; ++tp)
+            for (uint32_t i = 0; i < S; ++i) {
+                if (!((pos_mask >> i) & 1u))
+                    continue;
+                float p = scores[(uint64_t)tp * S + i];
+                for (uint32_t tn = 0; tn < C; ++tn)
+                    for (uint32_t j = 0; j < S; ++j) {
+                        if ((pos_mask >> j) & 1u)
+                            continue;
+                        int r = score_cmp(p, scores[(uint64_t)tn * S + j]);
+                        pooled[0] += (r > 0);
+                        pooled[1] += (r == 0);
+                        pooled[2] += 1;
+                    }
+            }
+    }
+    return 0;
+}

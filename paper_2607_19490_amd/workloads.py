@@ -1,0 +1,188 @@
+"""Workload definitions: the shapes and parameter sets the detector is run on.
+
+Pure data (no step of the method lives here).  Shapes stand in for the
+paper's pipelines: k stages (shards) S, n canaries C, T tokens and hidden
+size d = H (Section 3.1), with one malicious stage at the middle of the
+pipeline as in the main factorial (Section 4.4).  All inputs are synthetic
+and seeded; no dataset item or model weight is used.
+
+Workloads
+  tiny        4 x 8 x 16 x 256, stage 2 malicious, no outlier channels
+  llama7b     8 x 64 x 128 x 4096 (32 layers as 8 shards), 41 outlier channels
+  llama70b    16 x 256 x 256 x 8192 (80 layers as 16 shards), 82 outliers
+  sweep       216-run factorial {8,16,32} shards x H {2048,4096,8192} x
+              benign sigma {1e-4,1e-3} x tamper sigma {0.005,0.02,0.1} x
+              {additive, sign flip, rescale, mixed}; 32 canaries x 64 tokens
+  snr         16 x 128 x 128 x 4096, benign sigma at 20 log-spaced values in
+              [1e-4, 1e-1], Gaussian and Student-t noise, tamper 0.02
+  paper       12 x 100 x 48 x 768 (the paper's GPT-2 / Pythia-160M shape),
+              block-scaled benign noise sigma_hw = 0.002, the six attacks
+"""
+from dataclasses import dataclass, field
+from typing import List, Tuple
+
+NOISE_ELEMENTWISE = 0
+NOISE_BLOCK = 1
+DIST_GAUSS = 0
+DIST_T3 = 1
+T_ADD = 1
+T_FLIP = 2
+T_SCALE = 4
+T_MIXED = T_ADD | T_FLIP | T_SCALE
+BASE_BENIGN = 0
+BASE_CLEAN = 1
+
+SEED = 0
+OUTLIER_GAIN = 20.0
+
+
+@dataclass(frozen=True)
+class Run:
+    """One simulated live pass over a reference set plus its scoring."""
+    cfg_id: int
+    benign_mode: int = NOISE_ELEMENTWISE
+    benign_dist: int = DIST_GAUSS
+    sigma_b: float = 1e-3
+    tamper: int = T_ADD
+    eps: float = 0.0        # Gaussian tamper magnitude (times the block rms)
+    flip_p: float = 0.0     # sign-flip fraction (1.0 = the paper's full flip)
+    scale: float = 1.0      # rescale factor 1 + alpha
+    tamper_base: int = BASE_BENIGN
+    label: str = ""
+
+
+@dataclass(frozen=True)
+class RefSet:
+    """One reference set [S][C][T][H] and the runs made against it."""
+    ref_set_id: int
+    S: int
+    C: int
+    T: int
+    H: int
+    n_out: int
+    mal_shards: Tuple[int, ...]
+    runs: Tuple[Run, ...] = field(default_factory=tuple)
+
+    @property
+    def mal_mask(self) -> int:
+        m = 0
+        for s in self.mal_shards:
+            m |= 1 << s
+        return m
+
+    @property
+    def elems(self) -> int:
+        return self.S * self.C * self.T * self.H
+
+    @property
+    def block_elems(self) -> int:
+        return self.T * self.H
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    ref_sets: Tuple[RefSet, ...]
+    seed: int = SEED
+
+    @property
+    def n_runs(self) -> int:
+        return sum(len(r.runs) for r in self.ref_sets)
+
+
+def n_outliers(H: int, frac: float = 0.01) -> int:
+    """Number of outlier channels: the nearest integer to frac * H."""
+    return int(frac * H + 0.5)
+
+
+def tiny() -> Workload:
+    rs = RefSet(0, 4, 8, 16, 256, 0, (2,),
+                (Run(0, sigma_b=1e-3, tamper=T_ADD, eps=0.05, label="add0.05"),))
+    return Workload("tiny", (rs,))
+
+
+def llama7b() -> Workload:
+    S, H = 8, 4096
+    runs = (Run(0, sigma_b=1e-3, tamper=T_ADD, eps=0.01, label="add0.01"),
+            Run(1, sigma_b=1e-3, tamper=T_ADD, eps=0.05, label="add0.05"))
+    return Workload("llama7b", (RefSet(0, S, 64, 128, H, n_outliers(H), (S // 2,), runs),))
+
+
+def llama70b() -> Workload:
+    S, H = 16, 8192
+    runs = (Run(0, sigma_b=1e-3, tamper=T_ADD, eps=0.05, label="add0.05"),
+            Run(1, sigma_b=1e-3, tamper=T_FLIP, flip_p=0.001, label="flip0.001"),
+            Run(2, sigma_b=1e-3, tamper=T_SCALE, scale=1.05, label="scale1.05"))
+    return Workload("llama70b", (RefSet(0, S, 256, 256, H, n_outliers(H), (S // 2,), runs),))
+
+
+SWEEP_SHARDS = (8, 16, 32)
+SWEEP_HIDDEN = (2048, 4096, 8192)
+SWEEP_SIGMA_B = (1e-4, 1e-3)
+SWEEP_SIGMA_T = (0.005, 0.02, 0.1)
+SWEEP_TYPES = (("add", T_ADD), ("flip", T_FLIP), ("scale", T_SCALE), ("mixed", T_MIXED))
+
+
+def _typed_run(cfg_id, sigma_b, sigma_t, tname, tflags):
+    return Run(cfg_id, sigma_b=sigma_b, tamper=tflags,
+               eps=sigma_t if tflags & T_ADD else 0.0,
+               flip_p=sigma_t if tflags & T_FLIP else 0.0,
+               scale=1.0 + sigma_t if tflags & T_SCALE else 1.0,
+               label=f"{tname}:sb{sigma_b:g}:st{sigma_t:g}")
+
+
+def sweep() -> Workload:
+    """The 216-run factorial; cfg_id follows the nested order
+    (shards, hidden, benign sigma, tamper sigma, tamper type)."""
+    sets = []
+    cfg_id = 0
+    for S in SWEEP_SHARDS:
+        for H in SWEEP_HIDDEN:
+            runs = []
+            for sb in SWEEP_SIGMA_B:
+                for st in SWEEP_SIGMA_T:
+                    for tname, tflags in SWEEP_TYPES:
+                        runs.append(_typed_run(cfg_id, sb, st, tname, tflags))
+                        cfg_id += 1
+            sets.append(RefSet(len(sets), S, 32, 64, H, n_outliers(H), (S // 2,), tuple(runs)))
+    return Workload("sweep", tuple(sets))
+
+
+def snr_sigmas() -> List[float]:
+    """20 benign noise levels, log-spaced from 1e-4 to 1e-1."""
+    return [10.0 ** (-4.0 + 3.0 * j / 19.0) for j in range(20)]
+
+
+def snr() -> Workload:
+    S, H = 16, 4096
+    runs = []
+    for j, sb in enumerate(snr_sigmas()):
+        for dist, dname in ((DIST_GAUSS, "gauss"), (DIST_T3, "t3")):
+            runs.append(Run(len(runs), benign_dist=dist, sigma_b=sb, tamper=T_ADD, eps=0.02,
+                            label=f"{dname}:sb{sb:.3g}"))
+    return Workload("snr", (RefSet(0, S, 128, 128, H, n_outliers(H), (S // 2,), tuple(runs)),))
+
+
+def paper() -> Workload:
+    """The paper's own pipeline shape: 12 stages, 100 canaries of 48 tokens,
+    d = 768, malicious stage floor(k/2) = 6 counted from 1 (index 5 here),
+    block-scaled benign noise at sigma_hw = 0.002 and the six attacks."""
+    S, H = 12, 768
+    runs = []
+    for eps in (0.02, 0.05, 0.10, 0.20):
+        runs.append(Run(len(runs), benign_mode=NOISE_BLOCK, sigma_b=0.002, tamper=T_ADD,
+                        eps=eps, label=f"gauss{eps:g}"))
+    runs.append(Run(len(runs), benign_mode=NOISE_BLOCK, sigma_b=0.002, tamper=T_FLIP,
+                    flip_p=1.0, label="signflip"))
+    runs.append(Run(len(runs), benign_mode=NOISE_BLOCK, sigma_b=0.002, tamper=T_SCALE,
+                    scale=1.10, label="rescale0.10"))
+    return Workload("paper", (RefSet(0, S, 100, 48, H, n_outliers(H), (S // 2 - 1,),
+                                     tuple(runs)),))
+
+
+WORKLOADS = {"tiny": tiny, "llama7b": llama7b, "llama70b": llama70b, "sweep": sweep,
+             "snr": snr, "paper": paper}
+
+
+def get(name: str) -> Workload:
+    return WORKLOADS[name]()

@@ -1,0 +1,175 @@
+"""Pins of the oracle's detection AUROC, Eqs. 5-6 (CPU only).
+
+Per canary t, A(t) counts benign stages j whose mismatch the malicious stage
+exceeds (Eq. 5); the aggregate is the mean over canaries (Eq. 6), which the
+paper equates with the normalised Mann-Whitney U.  Checked against
+scikit-learn's roc_auc_score and scipy's mannwhitneyu (library routines), a
+pure-Python brute force on tiny inputs exhaustive over label sets, closed
+forms (perfect separation, reversal, all ties) and the scrambled-label
+control's exchangeability (Section 4.5).
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy import stats
+from sklearn.metrics import roc_auc_score
+
+from paper_2607_19490_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _mask(shards):
+    m = 0
+    for s in shards:
+        m |= 1 << s
+    return m
+
+
+def _key(x):
+    # NaN lowest, NaN == NaN, otherwise numeric order (-0 == +0)
+    return (0, 0.0) if math.isnan(x) else (1, float(x))
+
+
+def _brute(scores, pos):
+    """Pure-Python counts of Eq. 5 summed over canaries."""
+    G = E = N = 0
+    C, S = scores.shape
+    for t in range(C):
+        for i in pos:
+            for j in range(S):
+                if j in pos:
+                    continue
+                ki, kj = _key(scores[t, i]), _key(scores[t, j])
+                G += ki > kj
+                E += ki == kj
+                N += 1
+    return G, E, N
+
+
+def test_perfect_separation_reversal_and_ties(orc):
+    C, S = 7, 6
+    sc = inputs.scores(C, S, seed=0, mal=(3,), gap=2.0)
+    counts, pooled = orc.auroc_config(sc, _mask([3]))
+    assert counts[0] == counts[2] == C * 5 and counts[1] == 0
+    assert orc.auroc_strict(counts) == 1.0 and pooled[0] == pooled[2]
+    sc = inputs.scores(C, S, seed=0, mal=(3,), gap=-2.0)
+    counts, pooled = orc.auroc_config(sc, _mask([3]))
+    assert counts[0] == 0 and counts[1] == 0 and pooled[0] == 0
+    sc = np.full((C, S), 0.25, np.float32)
+    counts, pooled = orc.auroc_config(sc, _mask([3]))
+    assert orc.auroc_strict(counts) == 0.0 and orc.auroc_mw(counts) == 0.5
+    assert pooled[1] == pooled[2]
+
+
+def test_matches_sklearn_per_canary(orc):
+    """Eq. 6 with ties counted one half is the mean of per-canary ROC AUCs."""
+    C, S = 40, 9
+    pos = (2, 6)
+    sc = inputs.scores(C, S, seed=1, mal=pos, gap=0.3, tie_levels=12)
+    counts, _ = orc.auroc_config(sc, _mask(pos))
+    labels = np.zeros(S, int)
+    labels[list(pos)] = 1
+    want = np.mean([roc_auc_score(labels, sc[t]) for t in range(C)])
+    assert abs(orc.auroc_mw(counts) - want) < 1e-12
+
+
+def test_pooled_matches_scipy_mannwhitneyu(orc):
+    C, S = 30, 8
+    pos = (4,)
+    sc = inputs.scores(C, S, seed=2, mal=pos, gap=0.1, tie_levels=20)
+    _, pooled = orc.auroc_config(sc, _mask(pos))
+    x = sc[:, list(pos)].ravel()
+    y = np.delete(sc, list(pos), axis=1).ravel()
+    U = stats.mannwhitneyu(x, y, alternative="two-sided", method="asymptotic").statistic
+    assert pooled[0] + pooled[1] / 2 == U
+    assert pooled[2] == x.size * y.size
+
+
+def test_exhaustive_label_sets_with_ties(orc):
+    """Every non-trivial malicious set for k <= 6, forced ties and NaNs."""
+    for S in (2, 3, 4, 6):
+        sc = inputs.scores(5, S, seed=S, tie_levels=3, nan_frac=0.1)
+        for r in range(1, S):
+            for pos in itertools.combinations(range(S), r):
+                counts, pooled = orc.auroc_config(sc, _mask(pos), flags=2)
+                assert tuple(int(x) for x in counts[:3]) == _brute(sc, set(pos))
+                # pooled: every positive against every negative, across canaries
+                flat_p = [sc[t, i] for t in range(sc.shape[0]) for i in pos]
+                flat_n = [sc[t, j] for t in range(sc.shape[0]) for j in range(S) if j not in pos]
+                G = sum(_key(p) > _key(n) for p in flat_p for n in flat_n)
+                E = sum(_key(p) == _key(n) for p in flat_p for n in flat_n)
+                assert (int(pooled[0]), int(pooled[1]), int(pooled[2])) == \
+                    (G, E, len(flat_p) * len(flat_n))
+
+
+def test_nan_and_signed_zero_order(orc):
+    assert orc.score_cmp(float("nan"), -math.inf) == -1
+    assert orc.score_cmp(float("nan"), float("nan")) == 0
+    assert orc.score_cmp(-0.0, 0.0) == 0
+    assert orc.score_cmp(math.inf, 1e30) == 1
+
+
+def test_scramble_draws_only_benign_stages_uniformly(orc):
+    S, pos = 8, (4,)
+    draws = [orc.scramble_jstar(S, _mask(pos), 0, 3, t) for t in range(7000)]
+    assert 4 not in draws
+    counts = np.bincount(draws, minlength=S)
+    benign = [j for j in range(S) if j not in pos]
+    chi2 = stats.chisquare(counts[benign]).pvalue
+    assert chi2 > 1e-4
+    # collusion: j* is never a colluder
+    draws = [orc.scramble_jstar(S, _mask((1, 5)), 0, 3, t) for t in range(500)]
+    assert not ({1, 5} & set(draws))
+    assert orc.scramble_jstar(3, _mask((0, 1, 2)), 0, 0, 0) == -1
+
+
+def test_control_counts_follow_definition(orc):
+    C, S, pos = 25, 6, (3,)
+    sc = inputs.scores(C, S, seed=4, tie_levels=5)
+    for include_true in (False, True):
+        flags = 1 | (4 if include_true else 0)
+        counts, _ = orc.auroc_config(sc, _mask(pos), seed=11, cfg_id=7, flags=flags)
+        G = E = N = 0
+        for t in range(C):
+            js = orc.scramble_jstar(S, _mask(pos), 11, 7, t)
+            for j in range(S):
+                if j == js or (j in pos and not include_true):
+                    continue
+                G += _key(sc[t, js]) > _key(sc[t, j])
+                E += _key(sc[t, js]) == _key(sc[t, j])
+                N += 1
+        assert tuple(int(x) for x in counts[3:]) == (G, E, N)
+
+
+def test_control_is_chance_on_the_true_scores(orc):
+    """Scrambling the label on scores where the malicious stage stands out
+    gives E[A] = 0.5 when the true stage is left out of the negatives, and
+    (k - 2) / (2 (k - 1)) when it is kept in."""
+    with open(os.path.join(GOLDEN, "paper_outcomes.json")) as f:
+        gold = json.load(f)
+    lo, hi = gold["control_window"]["value"]
+    C, S, pos = 4000, 8, (4,)
+    sc = inputs.scores(C, S, seed=5, mal=pos, gap=5.0)
+    counts, _ = orc.auroc_config(sc, _mask(pos), seed=0, cfg_id=1, flags=1)
+    a_ctrl = counts[3] / counts[5]
+    assert lo <= a_ctrl <= hi and abs(a_ctrl - 0.5) < 0.02
+    assert orc.auroc_strict(counts) >= gold["success_auroc"]["value"]
+    counts, _ = orc.auroc_config(sc, _mask(pos), seed=0, cfg_id=1, flags=1 | 4)
+    assert abs(counts[3] / counts[5] - (S - 2) / (2 * (S - 1))) < 0.02
+
+
+def test_degenerate_label_sets(orc):
+    sc = inputs.scores(3, 4, seed=6)
+    counts, pooled = orc.auroc_config(sc, 0)  # nobody malicious
+    assert counts[2] == 0 and pooled[2] == 0 and math.isnan(orc.auroc_strict(counts))
+    counts, pooled = orc.auroc_config(sc, 0b1111)  # everybody malicious
+    assert counts[2] == 0 and counts[5] == 0
+    counts, _ = orc.auroc_config(inputs.scores(3, 1, seed=7), 0b1)  # a single stage
+    assert counts[2] == 0
+    with pytest.raises(ValueError):
+        orc.auroc_config(inputs.scores(2, 65, seed=8), 1)

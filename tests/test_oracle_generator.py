@@ -1,0 +1,288 @@
+"""Pins of the oracle's synthetic generator (CPU only).
+
+The references stand in for the fp32 activations of Eq. 1 and the live pass
+follows Eqs. 2-3.  What the paper and the mathematics fix, checked here:
+  * special cases that reduce to numpy's fp16 conversion (sigma = 0, clean
+    base, full sign flip, power-of-two rescale);
+  * the noise scale of Eq. 2 (elementwise and block-scaled), the Student-t
+    tails, the Gaussian tamper magnitude m ~ eps, the flip fraction and
+    m ~ 2 sqrt(p), the rescale m ~ alpha;
+  * the outlier channel choice against an independent sort.
+"""
+import math
+import warnings
+
+import numpy as np
+import pytest
+from scipy import stats
+
+NOISE_ELEMENTWISE, NOISE_BLOCK = 0, 1
+DIST_GAUSS, DIST_T3 = 0, 1
+T_ADD, T_FLIP, T_SCALE = 1, 2, 4
+BASE_BENIGN, BASE_CLEAN = 0, 1
+
+
+def _f16(x):
+    with warnings.catch_warnings():
+        warnings.simplefilter("ignore")
+        return np.asarray(x, np.float32).astype(np.float16).view(np.uint16)
+
+
+def _h(bits):
+    return np.asarray(bits, np.uint16).view(np.float16).astype(np.float64)
+
+
+def _ref(orc, T=64, H=512, s=0, c=0, seed=3, gain=None):
+    if gain is None:
+        gain = np.ones(H, np.float32)
+    return orc.ref_block(s, c, T, H, seed, 0, gain)
+
+
+def _rel(h_bits, a):
+    d = _h(h_bits) - a.astype(np.float64)
+    return math.sqrt((d * d).sum() / (a.astype(np.float64) ** 2).sum())
+
+
+# ----------------------------------------------------------------------------
+# references and outlier channels
+# ----------------------------------------------------------------------------
+def test_outlier_channels_are_the_smallest_words(orc):
+    H, n_out = 4096, 41
+    g = orc.outlier_gain(H, n_out, 20.0, 5, 2)
+    words = np.array([orc.philox([j, 0, 0, (8 << 24) | 2], [5, 0])[0] for j in range(H)],
+                     np.uint64)
+    order = np.lexsort((np.arange(H), words))  # by word, then channel
+    want = np.ones(H, np.float32)
+    want[order[:n_out]] = 20.0
+    np.testing.assert_array_equal(g, want)
+    assert (g == 20.0).sum() == n_out
+
+
+def test_outlier_zero_and_all(orc):
+    assert np.all(orc.outlier_gain(256, 0, 20.0, 0, 0) == 1.0)
+    assert np.all(orc.outlier_gain(256, 256, 20.0, 0, 0) == 20.0)
+    with pytest.raises(ValueError):
+        orc.outlier_gain(8, 9, 20.0, 0, 0)
+
+
+def test_reference_gain_and_variance(orc):
+    H = 1024
+    gain = orc.outlier_gain(H, 10, 20.0, 0, 0)
+    a = _ref(orc, T=256, H=H, gain=gain)
+    out = gain == 20.0
+    # each channel holds z * gain: outlier channels have variance 400
+    v_in = a[:, ~out].astype(np.float64).var()
+    v_out = a[:, out].astype(np.float64).var()
+    assert abs(v_in - 1.0) < 0.02
+    assert abs(v_out / 400.0 - 1.0) < 0.1
+    # gain 20 multiplies exactly the unit-gain draw of the same element, rounded
+    z = _ref(orc, T=256, H=H)
+    np.testing.assert_array_equal(a[:, out], (z[:, out].astype(np.float64) * 20.0).astype(np.float32))
+    np.testing.assert_array_equal(a[:, ~out], z[:, ~out])
+
+
+def test_reference_blocks_are_distinct_and_deterministic(orc):
+    a00 = _ref(orc, T=8, H=64, s=0, c=0)
+    a01 = _ref(orc, T=8, H=64, s=0, c=1)
+    a10 = _ref(orc, T=8, H=64, s=1, c=0)
+    assert not np.array_equal(a00, a01) and not np.array_equal(a00, a10)
+    np.testing.assert_array_equal(a00, _ref(orc, T=8, H=64, s=0, c=0))
+    # whole-array generator lays blocks out as [S][C][T][H]
+    full = orc.ref_synth(2, 2, 8, 64, 3, 0, np.ones(64, np.float32))
+    np.testing.assert_array_equal(full[0, 1], a01)
+    np.testing.assert_array_equal(full[1, 0], a10)
+
+
+# ----------------------------------------------------------------------------
+# live pass: exact special cases
+# ----------------------------------------------------------------------------
+def test_zero_noise_benign_is_fp16_of_reference(orc):
+    a = _ref(orc)
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0)
+    np.testing.assert_array_equal(h, _f16(a))
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, benign_mode=NOISE_BLOCK, bscale=0.0)
+    np.testing.assert_array_equal(h, _f16(a))
+
+
+def test_full_sign_flip_is_negated_reference(orc):
+    a = _ref(orc)
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True, tamper=T_FLIP,
+                      flip_p=1.0)
+    np.testing.assert_array_equal(h, _f16(-a))
+    assert abs(_rel(h, a) - 2.0) < 1e-3  # tau(v) = -v gives m = 2
+
+
+def test_power_of_two_rescale(orc):
+    a = _ref(orc)
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True, tamper=T_SCALE,
+                      scale=2.0)
+    np.testing.assert_array_equal(h, _f16(2.0 * a))
+
+
+def test_clean_base_ignores_benign_noise(orc):
+    a = _ref(orc)
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.5, malicious=True, tamper=T_SCALE,
+                      scale=1.0, tamper_base=BASE_CLEAN)
+    np.testing.assert_array_equal(h, _f16(a))
+    # ... while a benign shard in the same call is noisy
+    hb = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.5)
+    assert not np.array_equal(hb, _f16(a))
+
+
+def test_benign_shard_ignores_tamper_settings(orc):
+    a = _ref(orc)
+    kw = dict(seed=1, cfg_id=4, sigma_b=1e-3)
+    h0 = orc.sim_block(0, 0, a, **kw)
+    h1 = orc.sim_block(0, 0, a, malicious=False, tamper=T_ADD | T_FLIP | T_SCALE, tscale=5.0,
+                       flip_p=1.0, scale=3.0, **kw)
+    np.testing.assert_array_equal(h0, h1)
+
+
+def test_noise_is_keyed_by_config_block_and_seed(orc):
+    a = _ref(orc, T=8, H=64)
+    base = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=1e-2)
+    np.testing.assert_array_equal(base, orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=1e-2))
+    for kw in (dict(seed=2, cfg_id=0), dict(seed=1, cfg_id=1)):
+        assert not np.array_equal(base, orc.sim_block(0, 0, a, sigma_b=1e-2, **kw))
+    assert not np.array_equal(base, orc.sim_block(1, 0, a, seed=1, cfg_id=0, sigma_b=1e-2))
+    assert not np.array_equal(base, orc.sim_block(0, 1, a, seed=1, cfg_id=0, sigma_b=1e-2))
+
+
+# ----------------------------------------------------------------------------
+# live pass: magnitudes fixed by Eqs. 2-4
+# ----------------------------------------------------------------------------
+def test_elementwise_benign_noise_scale(orc):
+    """delta ~ N(0, (sigma |a|)^2): m^2 = sigma^2 E[a^2 z^2]/E[a^2] = sigma^2
+    (plus the fp16 rounding floor, negligible at sigma = 1e-2)."""
+    a = _ref(orc, T=256, H=512)
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=1e-2)
+    m = _rel(h, a)
+    assert abs(m / 1e-2 - 1.0) < 0.01
+    # the relative displacement has unit variance and no bias
+    ok = np.abs(a) > 1.0  # fp16 rounding is small against the noise there
+    r = (_h(h)[ok] - a[ok]) / (1e-2 * np.abs(a[ok].astype(np.float64)))
+    assert abs(r.mean()) < 0.01 and abs(r.std() - 1.0) < 0.02
+
+
+def test_block_benign_noise_scale(orc):
+    """Eq. 2 proper: delta ~ N(0, sigma^2 mu^2), mu the mean |a| of the block,
+    so m = sigma mu / rms(a) (about sigma sqrt(2/pi) for normal activations)."""
+    a = _ref(orc, T=256, H=512)
+    q, mu_sum = orc.ref_stats_block(a)
+    n = a.size
+    _, bs = orc.block_scales(256, 512, np.array([q]), np.array([mu_sum]), 0.0, 1e-2)
+    assert bs[0] == np.float32(1e-2 * (mu_sum / n))
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, benign_mode=NOISE_BLOCK, bscale=bs[0])
+    m = _rel(h, a)
+    rms = math.sqrt(q / n)
+    assert abs(m / (1e-2 * (mu_sum / n) / rms) - 1.0) < 0.01
+    assert abs((mu_sum / n) / rms - math.sqrt(2 / math.pi)) < 0.02
+    # additive noise of constant scale: (h - a) / bscale has unit variance
+    r = (_h(h) - a) / float(bs[0])
+    assert abs(r.std() - 1.0) < 0.02
+
+
+def test_student_t_noise(orc):
+    """Heavy-tailed benign noise: unit-variance Student-t with 3 degrees of
+    freedom.  Its median |t| and tail mass match the t(3) law / sqrt(3)."""
+    T, H = 512, 512
+    a = np.full((T, H), 1.0, np.float32)  # |a| = 1: the noise is read off directly
+    h = orc.sim_block(0, 0, a, seed=2, cfg_id=0, benign_dist=DIST_T3, sigma_b=0.25)
+    # fp16 spacing near 1 is 2^-10 (2^-11 just below 1): small against 0.25
+    t = (_h(h) - 1.0) / 0.25 * math.sqrt(3.0)
+    med = np.median(np.abs(t))
+    assert abs(med - stats.t(3).ppf(0.75)) < 0.02
+    tail = (np.abs(t) > stats.t(3).ppf(0.995)).mean()
+    assert 0.007 < tail < 0.013
+    # Gaussian noise on the same input has a much lighter tail
+    hg = orc.sim_block(0, 0, a, seed=2, cfg_id=0, sigma_b=0.25)
+    tg = (_h(hg) - 1.0) / 0.25 * math.sqrt(3.0)
+    assert (np.abs(tg) > stats.t(3).ppf(0.995)).mean() < 0.002
+
+
+def test_gaussian_tamper_magnitude(orc):
+    """m = ||eps rms(a) z|| / ||a|| = eps (the paper: m ~ eps)."""
+    a = _ref(orc, T=256, H=512)
+    q, s = orc.ref_stats_block(a)
+    ts, _ = orc.block_scales(256, 512, np.array([q]), np.array([s]), 0.05, 0.0)
+    assert ts[0] == np.float32(0.05 * math.sqrt(q / a.size))
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True, tamper=T_ADD,
+                      tscale=ts[0])
+    assert abs(_rel(h, a) / 0.05 - 1.0) < 0.01
+    # with benign noise underneath: m^2 = eps^2 + sigma^2
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.02, malicious=True, tamper=T_ADD,
+                      tscale=ts[0])
+    assert abs(_rel(h, a) / math.sqrt(0.05**2 + 0.02**2) - 1.0) < 0.01
+
+
+@pytest.mark.parametrize("p", [0.001, 0.01, 0.25])
+def test_partial_sign_flip(orc, p):
+    """Each element flips with probability p; m = 2 sqrt(p)."""
+    a = _ref(orc, T=512, H=512)
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True, tamper=T_FLIP,
+                      flip_p=p, tamper_base=BASE_CLEAN)
+    flipped = ((h ^ _f16(a)) & 0x8000) != 0  # sign bit differs from fp16(a)
+    n = a.size
+    frac = flipped.mean()
+    assert abs(frac - p) < 6 * math.sqrt(p * (1 - p) / n)
+    # unflipped elements are exactly fp16(a), flipped ones exactly fp16(-a)
+    np.testing.assert_array_equal(h[~flipped], _f16(a)[~flipped])
+    np.testing.assert_array_equal(h[flipped], _f16(-a)[flipped])
+    assert abs(_rel(h, a) / (2 * math.sqrt(p)) - 1.0) < 0.1
+
+
+def test_flip_probability_zero(orc):
+    a = _ref(orc)
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True, tamper=T_FLIP,
+                      flip_p=0.0)
+    np.testing.assert_array_equal(h, _f16(a))
+
+
+def test_rescale_magnitude(orc):
+    """tau(v) = (1 + alpha) v gives m = alpha (Section 4.4 rescale)."""
+    a = _ref(orc, T=128, H=512)
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True, tamper=T_SCALE,
+                      scale=1.10)
+    assert abs(_rel(h, a) - 0.10) < 5e-4
+
+
+def test_mixed_tamper_order(orc):
+    """Mixed = Gaussian, then sign flip, then rescale.  A full flip after the
+    Gaussian step gives exactly -(a + tscale z) (the other order would give
+    -a + tscale z); a power-of-two rescale after both doubles that (exact in
+    fp16 away from the subnormal range)."""
+    a = _ref(orc)
+    add_only = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True,
+                             tamper=T_ADD, tscale=0.1)
+    flip_after = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True,
+                               tamper=T_ADD | T_FLIP | T_SCALE, tscale=0.1, flip_p=1.0,
+                               scale=1.0)
+    np.testing.assert_array_equal(flip_after, add_only ^ np.uint16(0x8000))
+    mixed = orc.sim_block(0, 0, a, seed=1, cfg_id=0, sigma_b=0.0, malicious=True,
+                          tamper=T_ADD | T_FLIP | T_SCALE, tscale=0.1, flip_p=1.0, scale=2.0)
+    normal = np.abs(_h(add_only)) >= 2.0**-13
+    assert normal.mean() > 0.99
+    np.testing.assert_array_equal(_h(mixed)[normal], -2.0 * _h(add_only)[normal])
+
+
+def test_canary_sim_array_layout(orc):
+    S, C, T, H = 3, 2, 4, 16
+    ref = orc.ref_synth(S, C, T, H, 9, 1, np.ones(H, np.float32))
+    ts = np.full((S, C), 0.07, np.float32)
+    h = orc.canary_sim(ref, seed=9, cfg_id=5, sigma_b=1e-3, mal_mask=0b010, tamper=T_ADD,
+                       tscale=ts)
+    for s in range(S):
+        for c in range(C):
+            want = orc.sim_block(s, c, ref[s, c], seed=9, cfg_id=5, sigma_b=1e-3,
+                                 malicious=(s == 1), tamper=T_ADD, tscale=0.07)
+            np.testing.assert_array_equal(h[s, c], want)
+
+
+def test_block_scales_closed_form(orc):
+    """A block of constant magnitude c has rms = mu = c."""
+    T, H = 4, 8
+    a = np.full(T * H, -3.0, np.float32)
+    q, s = orc.ref_stats_block(a)
+    assert q == 9.0 * T * H and s == 3.0 * T * H
+    ts, bs = orc.block_scales(T, H, np.array([q]), np.array([s]), 0.5, 0.25)
+    assert ts[0] == 1.5 and bs[0] == 0.75
