@@ -1,0 +1,334 @@
+"""Benchmark of the canary-versus-reference drift detector on one MI355X.
+
+A step is one pass of the detector's hot path over the workload: for every
+run (tamper setting) of the workload, simulate the live fp16 activations
+(canary_sim), score every (shard, canary) block by Eq. 4 (drift_score), then
+rank all runs in one batched AUROC launch (Eqs. 5-6, scrambled-label control
+and pooled Mann-Whitney).  The fp32 references and their block statistics
+are the verifier's offline precomputation and are built before timing.
+
+Default workload: Llama-70B-shaped, 16 shards x 256 canaries x 256 tokens x
+hidden 8192 (48 GiB of activations), three runs: additive Gaussian eps 0.05,
+sign flip of 0.1% of elements, uniform rescale by 1.05.
+
+Prints one JSON line.  `value` is drift-scored activation bytes (2 B fp16 +
+4 B fp32 per element, each read once) per second of the whole step; the
+`roofline` object reports the drift kernel alone against the 8 TB/s HBM peak;
+`sweep` reports the 216-run factorial in configurations per second;
+`cpu_baseline` times the CPU oracle on a bounded sample of the same step.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+DRIFT_BYTES_PER_ELEM = 6      # fp16 h + fp32 a, each read once
+DRIFT_BYTES_PER_BLOCK = 4     # one fp32 score written
+SIM_BYTES_PER_ELEM = 6        # fp32 a read + fp16 h written
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="llama70b")
+    p.add_argument("--no-sweep", action="store_true")
+    p.add_argument("--sweep-reps", type=int, default=3)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-canaries", type=int, default=1,
+                   help="canaries (all shards each) in the CPU oracle sample")
+    return p.parse_args()
+
+
+class Prepared:
+    """Device-resident inputs of one workload (built before timing)."""
+
+    def __init__(self, torch, cdt, W, wl, rs, h_buf=None):
+        self.rs = rs
+        S, C, T, H = rs.S, rs.C, rs.T, rs.H
+        self.gain = cdt.outlier_gain(H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
+        self.ref = cdt.ref_synth(S, C, T, H, wl.seed, rs.ref_set_id, self.gain)
+        self.ws = cdt.workspace(S, C, T, H, self.ref)
+        self.sumsq, self.sumabs = cdt.ref_stats(self.ref, ws=self.ws)
+        n = S * C * T * H
+        if h_buf is None:
+            self.h = torch.empty((S, C, T, H), dtype=torch.float16, device="cuda")
+        else:
+            self.h = h_buf[:n].view(S, C, T, H)
+        self.scales = []
+        for run in rs.runs:
+            ts, bs = cdt.block_scales(self.sumsq, self.sumabs, T, H, run.eps, run.sigma_b)
+            self.scales.append((ts, bs))
+
+
+def sim_kwargs(wl, rs, run, ts, bs):
+    return dict(seed=wl.seed, cfg_id=run.cfg_id, benign_mode=run.benign_mode,
+                benign_dist=run.benign_dist, sigma_b=run.sigma_b, mal_mask=rs.mal_mask,
+                tamper=run.tamper, tamper_base=run.tamper_base, flip_p=run.flip_p,
+                scale=run.scale, bscale=bs, tscale=ts)
+
+
+def gpu_step(torch, cdt, wl, preps, scores, score_views, cfgs, auroc_ws, counts, pooled,
+             drift_ev=None, sim_ev=None):
+    k = 0
+    for prep in preps:
+        rs = prep.rs
+        for r, run in enumerate(rs.runs):
+            ts, bs = prep.scales[r]
+            if sim_ev is not None:
+                sim_ev[k][0].record()
+            cdt.canary_sim(prep.ref, out=prep.h, **sim_kwargs(wl, rs, run, ts, bs))
+            if sim_ev is not None:
+                sim_ev[k][1].record()
+                drift_ev[k][0].record()
+            cdt.drift_score(prep.h, prep.ref, out=score_views[k], ws=prep.ws)
+            if drift_ev is not None:
+                drift_ev[k][1].record()
+            k += 1
+    cdt.auroc(cfgs, scores, seed=wl.seed, flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED,
+              counts=counts, pooled=pooled, ws=auroc_ws)
+
+
+def setup_batch(torch, cdt, wl, preps):
+    """Scores slab for every run of the workload plus the batched AUROC table."""
+    views, cfgs, off = [], [], 0
+    total = sum(p.rs.C * p.rs.S * len(p.rs.runs) for p in preps)
+    scores = torch.empty((total,), dtype=torch.float32, device="cuda")
+    for prep in preps:
+        rs = prep.rs
+        for run in rs.runs:
+            n = rs.C * rs.S
+            views.append(scores[off:off + n].view(rs.C, rs.S))
+            cfgs.append((rs.S, rs.C, off, rs.mal_mask, run.cfg_id))
+            off += n
+    ncfg = len(cfgs)
+    counts = torch.empty((ncfg, 6), dtype=torch.int64, device="cuda")
+    pooled = torch.empty((ncfg, 3), dtype=torch.int64, device="cuda")
+    auroc_ws = torch.empty((max(16, cdt.lib().cdt_auroc_workspace_bytes(ncfg)),),
+                           dtype=torch.uint8, device="cuda")
+    return scores, views, cfgs, counts, pooled, auroc_ws
+
+
+def run_main(torch, cdt, W, args):
+    wl = W.get(args.workload)
+    log(f"workload {wl.name}: preparing references")
+    preps = [Prepared(torch, cdt, W, wl, rs) for rs in wl.ref_sets]
+    scores, views, cfgs, counts, pooled, auroc_ws = setup_batch(torch, cdt, wl, preps)
+    torch.cuda.synchronize()
+    nrun = len(cfgs)
+    log(f"{nrun} runs; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled)
+    torch.cuda.synchronize()
+
+    E = torch.cuda.Event
+    drift_ev = [[(E(enable_timing=True), E(enable_timing=True)) for _ in range(nrun)]
+                for _ in range(args.steps)]
+    sim_ev = [[(E(enable_timing=True), E(enable_timing=True)) for _ in range(nrun)]
+              for _ in range(args.steps)]
+    t0, t1 = E(enable_timing=True), E(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for s in range(args.steps):
+        gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled,
+                 drift_ev[s], sim_ev[s])
+    t1.record()
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    ms_step = ms_total / args.steps
+    drift_ms = [a.elapsed_time(b) for st in drift_ev for (a, b) in st]
+    sim_ms = [a.elapsed_time(b) for st in sim_ev for (a, b) in st]
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
+
+    elems_per_step = sum(len(p.rs.runs) * p.rs.elems for p in preps)
+    blocks_per_step = sum(len(p.rs.runs) * p.rs.S * p.rs.C for p in preps)
+    scored_bytes = elems_per_step * DRIFT_BYTES_PER_ELEM + blocks_per_step * DRIFT_BYTES_PER_BLOCK
+    value = scored_bytes / (ms_step * 1e-3) / 1e9
+
+    # dominant kernel: drift_score of the largest reference set
+    big = max(preps, key=lambda p: p.rs.elems)
+    per_launch = big.rs.elems * DRIFT_BYTES_PER_ELEM + big.rs.S * big.rs.C * DRIFT_BYTES_PER_BLOCK
+    k0 = sum(len(p.rs.runs) for p in preps[:preps.index(big)])
+    big_ms = [drift_ms[s * nrun + k0 + r] for s in range(args.steps) for r in range(len(big.rs.runs))]
+    big_sim = [sim_ms[s * nrun + k0 + r] for s in range(args.steps) for r in range(len(big.rs.runs))]
+    drift_avg = sum(big_ms) / len(big_ms)
+    sim_avg = sum(big_sim) / len(big_sim)
+    achieved = per_launch / (drift_avg * 1e-3) / 1e9
+    sim_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (sim_avg * 1e-3) / 1e9
+
+    res = {
+        "metric": "drift-scored activation GB/s",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "shape_SxCxTxH": [big.rs.S, big.rs.C, big.rs.T, big.rs.H],
+            "runs": [r.label for p in preps for r in p.rs.runs],
+            "inputs": "fp16 live activations vs fp32 references, sums in fp64",
+            "step": "canary_sim + drift_score per run, one batched auroc",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "drift_score (drift_partial_kernel + drift_combine_kernel)",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "bytes_per_launch": per_launch,
+            "avg_launch_ms": round(drift_avg, 4),
+        },
+        "canary_sim": {
+            "avg_launch_ms": round(sim_avg, 4),
+            "GBps": round(sim_gbps, 1),
+            "frac_of_hbm_peak": round(sim_gbps / HBM_PEAK_GBPS, 4),
+        },
+    }
+    c = cdt.u64(counts)
+    res["detection"] = {r.label: round(cdt.strict_auroc(c[i]), 4)
+                        for i, r in enumerate([r for p in preps for r in p.rs.runs])}
+    res["control"] = {r.label: round(int(c[i][3]) / max(1, int(c[i][5])), 4)
+                      for i, r in enumerate([r for p in preps for r in p.rs.runs])}
+    del preps, scores, views
+    torch.cuda.empty_cache()
+    return res, elems_per_step
+
+
+def run_sweep(torch, cdt, W, reps):
+    wl = W.sweep()
+    log("sweep: preparing 9 reference sets")
+    max_elems = max(rs.elems for rs in wl.ref_sets)
+    h_buf = torch.empty((max_elems,), dtype=torch.float16, device="cuda")
+    preps = [Prepared(torch, cdt, W, wl, rs, h_buf=h_buf) for rs in wl.ref_sets]
+    scores, views, cfgs, counts, pooled, auroc_ws = setup_batch(torch, cdt, wl, preps)
+    gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled)  # warmup
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    times.sort()
+    ms = times[len(times) // 2]
+    # auroc alone
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    cdt.auroc(cfgs, scores, seed=wl.seed, flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED,
+              counts=counts, pooled=pooled, ws=auroc_ws)
+    b.record()
+    torch.cuda.synchronize()
+    auroc_ms = a.elapsed_time(b)
+    c = cdt.u64(counts)
+    strict = [int(x[0]) / int(x[2]) for x in c]
+    ctrl = sum(int(x[3]) for x in c) / sum(int(x[5]) for x in c)
+    ctrl_mean = sum(int(x[3]) / int(x[5]) for x in c) / len(c)
+    log(f"sweep: {ms:.2f} ms for {len(cfgs)} configs")
+    out = {
+        "configs": len(cfgs),
+        "ms": round(ms, 3),
+        "configs_per_s": round(len(cfgs) / (ms * 1e-3), 1),
+        "auroc_only_ms": round(auroc_ms, 4),
+        "auroc_only_configs_per_s": round(len(cfgs) / (auroc_ms * 1e-3), 1),
+        "auroc_min": round(min(strict), 4),
+        "configs_at_auroc_1": sum(1 for x in strict if x == 1.0),
+        "control_pooled_mean": round(ctrl_mean, 4),
+        "control_pooled_pairs": round(ctrl, 4),
+    }
+    del preps, h_buf, scores
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline(W, args):
+    """The CPU oracle (untuned, one thread) on a bounded sample of the same
+    step: every shard of the first `cpu_canaries` canaries, all runs."""
+    import numpy as np
+
+    import oracle
+
+    wl = W.get(args.workload)
+    rs = max(wl.ref_sets, key=lambda r: r.elems)
+    Cs = min(args.cpu_canaries, rs.C)
+    gain = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
+    refs = np.stack([np.stack([oracle.ref_block(s, c, rs.T, rs.H, wl.seed, rs.ref_set_id, gain)
+                               for c in range(Cs)]) for s in range(rs.S)])
+    sumsq, sumabs = oracle.ref_stats(refs)
+    t0 = time.perf_counter()
+    elems = 0
+    for run in rs.runs:
+        ts, bs = oracle.block_scales(rs.T, rs.H, sumsq, sumabs, run.eps, run.sigma_b)
+        h = np.empty(refs.shape, np.uint16)
+        for s in range(rs.S):
+            for c in range(Cs):
+                h[s, c] = oracle.sim_block(s, c, refs[s, c], seed=wl.seed, cfg_id=run.cfg_id,
+                                           benign_mode=run.benign_mode,
+                                           benign_dist=run.benign_dist, sigma_b=run.sigma_b,
+                                           bscale=bs[s, c], malicious=s in rs.mal_shards,
+                                           tamper=run.tamper, tamper_base=run.tamper_base,
+                                           tscale=ts[s, c], flip_p=run.flip_p, scale=run.scale)
+        _, s32, _ = oracle.drift_score(h, refs)
+        oracle.auroc_config(s32, rs.mal_mask, seed=wl.seed, cfg_id=run.cfg_id)
+        elems += h.size
+    dt = time.perf_counter() - t0
+    nbytes = elems * DRIFT_BYTES_PER_ELEM + len(rs.runs) * rs.S * Cs * DRIFT_BYTES_PER_BLOCK
+    return {
+        "value": round(nbytes / dt / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{rs.S} shards x {Cs} canary(ies) x {rs.T} x {rs.H}, {len(rs.runs)} runs "
+                  f"(canary_sim + drift + auroc), {dt:.1f} s",
+        "seconds": round(dt, 2),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus above 1 is not supported"}))
+        sys.exit(2)
+    import torch
+
+    from paper_2607_19490_amd import cdt
+    from paper_2607_19490_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    cdt.lib()
+    torch.cuda.set_device(0)
+    res, _ = run_main(torch, cdt, W, args)
+    if not args.no_sweep:
+        res["sweep"] = run_sweep(torch, cdt, W, args.sweep_reps)
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        res["cpu_baseline"] = cpu_baseline(W, args)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,213 @@
+/*
+ * cdt.h -- C ABI of libcdt, the canary-versus-reference activation drift
+ * detector of "Integrity of peer-to-peer distributed LLM inference under
+ * malicious nodes" (Cihangiroglu & Nocera), on AMD Instinct MI355X (gfx950).
+ *
+ * Vocabulary (Section 3): a pipeline of k stages ("shards", S here) hands
+ * T x d activations (d = H here) from stage to stage; the verifier holds fp32
+ * reference activations a*_i for n canaries (C here) and compares the fp16
+ * activations h_i each stage returns for them.  A block is one (shard,
+ * canary) pair: T*H elements.
+ *
+ * Layouts (row-major, contiguous):
+ *   activations  ref[S][C][T][H] fp32,  h[S][C][T][H] fp16 (as uint16 bits)
+ *   per block    [S][C]  (block statistics and scales)
+ *   scores       [C][S]  (one canary's k mismatches adjacent, as Eq. 5 ranks)
+ *
+ * Conventions for every call:
+ *   - Array pointers are DEVICE pointers (hipMalloc or torch allocations)
+ *     owned by the caller, unless a comment says "host".  The library never
+ *     allocates or frees memory.
+ *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*,
+ *     NULL = the default stream); nothing synchronises implicitly.
+ *   - Arguments are validated before any device work; on failure nothing is
+ *     launched and an error code is returned.  cdt_last_error() gives a
+ *     per-thread description of the last failure.
+ *   - Results are deterministic: fixed reduction orders, no atomics.
+ *   - activations need H % 8 == 0, T*H < 2^32, and 16-byte aligned
+ *     pointers; S <= 64 wherever a shard bit mask is involved.
+ *   - Empty shapes (S, C, T or H zero) are valid and do no work, except
+ *     that drift scores of empty blocks are written as 0.
+ */
+#ifndef CDT_H
+#define CDT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define CDT_OK 0
+#define CDT_EINVAL 1  /* null pointer, bad enum, bad size or workspace too small */
+#define CDT_EALIGN 2  /* array pointer not 16-byte aligned                       */
+#define CDT_ELIMIT 3  /* shape beyond a documented limit                          */
+#define CDT_EDEVICE 4 /* HIP launch or runtime error                             */
+
+/* Random streams (fourth Philox counter word = stream << 24 | id). */
+#define CDT_STREAM_REF 0
+#define CDT_STREAM_BENIGN 1
+#define CDT_STREAM_T12 2
+#define CDT_STREAM_T3 3
+#define CDT_STREAM_TAMPER_ADD 4
+#define CDT_STREAM_TAMPER_FLIP 5
+#define CDT_STREAM_SCRAMBLE 6
+#define CDT_STREAM_RANDOM 7
+#define CDT_STREAM_OUTLIER 8
+#define CDT_STREAM_ALT 9
+
+/* Interface version; changes whenever a layout or generator rule changes. */
+int cdt_version(void);
+
+/* Description of the last error on the calling thread ("" if none). */
+const char* cdt_last_error(void);
+
+/* ------------------------------------------------------------------------ */
+/* Synthetic references (the verifier's offline fp32 pass, Eq. 1 and        */
+/* Section 3.3; no model weights, so a seeded stand-in)                     */
+/* ------------------------------------------------------------------------ */
+
+/* Outlier channel gains gain[H] (fp32, device): the n_out channels j with the
+ * smallest (w_j, j), w_j = Philox4x32-10 word 0 of counter
+ * (j, 0, 0, OUTLIER<<24 | ref_set_id) under key (lo32 seed, hi32 seed), get
+ * gain `big`; every other channel gets 1.  Needs n_out <= H <= 32768 and
+ * ref_set_id < 2^24. */
+int cdt_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed, uint32_t ref_set_id,
+                     float* gain, void* stream);
+
+/* ref[s][c][t][j] = fp32(z * gain[j]) with z the unit normal of element
+ * e = t*H + j drawn from stream REF (id = ref_set_id): Philox call
+ * q = e/2 of counter (q, c, s, REF<<24 | ref_set_id), words 0-1 for even e
+ * and 2-3 for odd e, made into z by the Irwin-Hall rule
+ *   n = sum of the four 16-bit halves of the two words - 131070,
+ *   z = fp32(n) * fp32(sqrt(3 / (2^32 - 1))).
+ * gain: [H] fp32 (device). */
+int cdt_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
+                  uint32_t ref_set_id, const float* gain, float* ref, void* stream);
+
+/* Workspace (device bytes) needed by cdt_ref_stats and cdt_drift_score for
+ * this shape: per-block partial sums of a fixed chunking. */
+size_t cdt_reduce_workspace_bytes(uint32_t S, uint32_t C, uint32_t T, uint32_t H);
+
+/* Per-block reference statistics in fp64: sumsq[s][c] = sum a^2 and
+ * sumabs[s][c] = sum |a| over the block (mu_i of Eq. 2 is sumabs / (T H)).
+ * ws: device workspace of at least cdt_reduce_workspace_bytes bytes. */
+int cdt_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,
+                  double* sumsq, double* sumabs, void* ws, size_t ws_bytes, void* stream);
+
+/* Per-block scales, each computed in fp64 and rounded once to fp32:
+ *   tscale[b] = eps * sqrt(sumsq[b] / (T H))       (Gaussian tamper: eps rms)
+ *   bscale[b] = sigma_b * (sumabs[b] / (T H))      (Eq. 2: sigma_hw mu_i)
+ * Either output may be NULL.  nblocks = S*C. */
+int cdt_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const double* sumsq,
+                     const double* sumabs, double eps, double sigma_b, float* tscale,
+                     float* bscale, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Live pass simulation (Eqs. 2-3)                                           */
+/* ------------------------------------------------------------------------ */
+#define CDT_NOISE_ELEMENTWISE 0 /* delta ~ N(0, (sigma_b |a|)^2) per element      */
+#define CDT_NOISE_BLOCK 1       /* delta ~ N(0, bscale^2): Eq. 2, sigma_hw mu_i    */
+#define CDT_DIST_GAUSS 0        /* unit normal (Irwin-Hall stand-in)              */
+#define CDT_DIST_T3 1           /* unit-variance Student-t, 3 degrees of freedom  */
+#define CDT_T_ADD 1             /* Gaussian tamper: v + tscale * z                */
+#define CDT_T_FLIP 2            /* sign flip of a selected fraction (all: -v)     */
+#define CDT_T_SCALE 4           /* rescale: (1 + alpha) v                         */
+#define CDT_BASE_BENIGN 0       /* tamper the benign output a + delta             */
+#define CDT_BASE_CLEAN 1        /* tamper the clean a (Eq. 3 read literally)      */
+
+typedef struct cdt_sim_params {
+    uint64_t seed;          /* Philox key (lo32, hi32)                            */
+    uint32_t cfg_id;        /* counter id of the noise streams, < 2^24             */
+    uint32_t benign_mode;   /* CDT_NOISE_*                                         */
+    uint32_t benign_dist;   /* CDT_DIST_*                                          */
+    uint32_t tamper;        /* OR of CDT_T_* (all three: Gaussian, flip, rescale) */
+    uint32_t tamper_base;   /* CDT_BASE_*                                          */
+    uint32_t reserved;      /* must be 0                                           */
+    uint64_t mal_mask;      /* bit s set: shard s is malicious (tampers)           */
+    double sigma_b;         /* ELEMENTWISE noise level (used as fp32(sigma_b))     */
+    double flip_p;          /* flip probability in [0, 1]; 1 flips every element   */
+    double scale;           /* rescale factor 1 + alpha (used as fp32(scale))      */
+    const float* bscale;    /* device [S][C], BLOCK mode, else may be NULL         */
+    const float* tscale;    /* device [S][C], needed with CDT_T_ADD                */
+} cdt_sim_params;
+
+/* h = fp16_rne(v) for every element, with (one fp32 operation per step, in
+ * this order, no fused multiply-add):
+ *   sc = fp32(sigma_b) * |a|  (ELEMENTWISE)   or  bscale[s][c]  (BLOCK)
+ *   zb = z_BENIGN, or for T3: q = (z1*z1 + z2*z2) + z3*z3 with z1, z2 from
+ *        one T12 call (q = e) and z3 from stream T3, zb = q == 0 ? 0 :
+ *        z_BENIGN / sqrt(q)
+ *   v  = a + sc * zb
+ * and on malicious shards, starting from v (BENIGN base) or a (CLEAN base):
+ *   ADD   v = v + tscale[s][c] * z_TAMPER_ADD
+ *   FLIP  v = -v if flip_p >= 1 or u < floor(flip_p 2^32), u = word e%4 of
+ *         TAMPER_FLIP call q = e/4
+ *   SCALE v = fp32(scale) * v
+ * One-normal streams use call q = e/2 like cdt_ref_synth; every counter is
+ * (q, c, s, stream<<24 | cfg_id).  p: host struct, read during the call.
+ * Needs S <= 64. */
+int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
+                   const float* ref, uint16_t* h, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Relative-L2 mismatch, Eq. 4                                               */
+/* ------------------------------------------------------------------------ */
+
+/* score[c][s] = fp32( sqrt( sum (h - a)^2 / sum a^2 ) ) over block (s, c), the
+ * sums accumulated in fp64 from the exactly widened fp16 h and fp32 a; a
+ * block with sum a^2 = 0 scores 0 if h = a there and +inf otherwise.
+ * num_den: optional device [C][S][2] fp64 (sum (h-a)^2, sum a^2), or NULL.
+ * ws: device workspace of at least cdt_reduce_workspace_bytes bytes.
+ * h and ref are read once each; nothing else touches HBM in bulk. */
+int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                    const float* ref, float* score, double* num_den, void* ws, size_t ws_bytes,
+                    void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Detection AUROC, Eqs. 5-6, the Mann-Whitney form and the scrambled-label  */
+/* control of Section 4.5, batched over configurations                       */
+/* ------------------------------------------------------------------------ */
+#define CDT_AUROC_CONTROL 1     /* also count the scrambled-label control        */
+#define CDT_AUROC_POOLED 2      /* also rank all C*S scores of a config together  */
+#define CDT_CTRL_INCLUDE_TRUE 4 /* control keeps the true malicious shards as negatives */
+
+typedef struct cdt_auroc_cfg {
+    uint32_t S, C;       /* shards (<= 64) and canaries of this configuration     */
+    uint64_t score_off;  /* element offset of its [C][S] table in `scores`       */
+    uint64_t pos_mask;   /* malicious shards (the positives of the ranking)      */
+    uint32_t cfg_id;     /* counter id of the SCRAMBLE stream (< 2^24)            */
+    uint32_t reserved;   /* must be 0                                             */
+} cdt_auroc_cfg;
+
+/* Bytes of device workspace cdt_auroc needs for n_cfg configurations. */
+size_t cdt_auroc_workspace_bytes(uint32_t n_cfg);
+
+/* For each configuration g (cfgs: HOST array of n_cfg entries, validated and
+ * copied into ws during the call):
+ *   counts[g][0..2] = G, E, pairs with G = #{(t, i in M, j not in M):
+ *       m_ti > m_tj}, E the ties (Eq. 5 summed over canaries; Eq. 6 as
+ *       printed is G / pairs, the Mann-Whitney value (G + E/2) / pairs);
+ *   counts[g][3..5] = the same for the scrambled-label control (if
+ *       CDT_AUROC_CONTROL, else 0): per canary t a benign shard j*, the
+ *       (u mod B)-th benign shard in increasing order, u = Philox word 0 of
+ *       counter (t, 0, 0, SCRAMBLE<<24 | cfg_id), B the number of benign
+ *       shards, ranked against the benign shards other than j* (all other
+ *       shards with CDT_CTRL_INCLUDE_TRUE);
+ *   pooled[g][0..2] = G, E, pairs over every positive score against every
+ *       negative score of the configuration (if CDT_AUROC_POOLED; needs
+ *       C*S <= 16384; pooled may be NULL otherwise).
+ * Score order: NaN below every number, NaN ties NaN, -0 ties +0.
+ * counts: device [n_cfg][6] uint64; scores: device fp32; n_scores bounds
+ * every configuration's table. */
+int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, uint64_t n_scores,
+              uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled, void* ws,
+              size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CDT_H */

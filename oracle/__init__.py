@@ -56,6 +56,9 @@ _SIGS = {
     "orc_f16_rne_range": ([_u64, _u64, _u16p], None),
     "orc_f16_rne_array": ([_u64, _f32p, _u16p], None),
     "orc_outlier_gain": ([_u32, _u32, _f, _u64, _u32, _f32p], _i),
+    "orc_ref_range": ([_u32, _u32, _u32, _u64, _u64, _u64, _u32, _f32p, _f32p], None),
+    "orc_sim_range": ([_u32, _u32, _u64, _u64, _u64, _u32, _i, _i, _d, _f, _i, _u32, _i, _f,
+                       _d, _d, _f32p, _u16p], _i),
     "orc_ref_block": ([_u32, _u32, _u32, _u32, _u64, _u32, _f32p, _f32p], None),
     "orc_ref_synth": ([_u32, _u32, _u32, _u32, _u64, _u32, _f32p, _f32p], None),
     "orc_ref_stats_block": ([_u64, _f32p, _f64p, _f64p], None),
@@ -154,6 +157,15 @@ def ref_block(s, c, T, H, seed, ref_set_id, gain):
     return out.reshape(T, H)
 
 
+def ref_range(s, c, H, e0, count, seed, ref_set_id, gain):
+    """Elements [e0, e0 + count) of reference block (s, c) (flat, e = t*H + j)."""
+    gain = _c(gain, np.float32)
+    out = np.empty(count, np.float32)
+    lib().orc_ref_range(s, c, H, e0, count, seed, ref_set_id, _p(gain, ctypes.c_float),
+                        _p(out, ctypes.c_float))
+    return out
+
+
 def ref_synth(S, C, T, H, seed, ref_set_id, gain):
     gain = _c(gain, np.float32)
     out = np.empty((S, C, T, H), np.float32)
@@ -199,6 +211,18 @@ def sim_block(s, c, ref_block_arr, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWIS
     T, H = a.shape
     h = np.empty((T, H), np.uint16)
     lib().orc_sim_block(s, c, T, H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
+                        float(bscale), int(bool(malicious)), tamper, tamper_base, float(tscale),
+                        flip_p, scale, _p(a, ctypes.c_float), _p(h, ctypes.c_uint16))
+    return h
+
+
+def sim_range(s, c, e0, ref_part, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE,
+              benign_dist=DIST_GAUSS, sigma_b=1e-3, bscale=0.0, malicious=False, tamper=0,
+              tamper_base=BASE_BENIGN, tscale=0.0, flip_p=0.0, scale=1.0):
+    """Live fp16 bits of elements [e0, e0 + len(ref_part)) of block (s, c)."""
+    a = _c(ref_part, np.float32).ravel()
+    h = np.empty(a.size, np.uint16)
+    lib().orc_sim_range(s, c, e0, a.size, seed, cfg_id, benign_mode, benign_dist, sigma_b,
                         float(bscale), int(bool(malicious)), tamper, tamper_base, float(tscale),
                         flip_p, scale, _p(a, ctypes.c_float), _p(h, ctypes.c_uint16))
     return h

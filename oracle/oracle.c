@@ -259,15 +259,22 @@ int orc_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed, uint3
     return 0;
 }
 
+/* Elements [e0, e0 + count) of block (s, c), element e = t*H + j. */
+void orc_ref_range(uint32_t s, uint32_t c, uint32_t H, uint64_t e0, uint64_t count,
+                   uint64_t seed, uint32_t ref_set_id, const float* gain, float* out)
+{
+    for (uint64_t k = 0; k < count; ++k) {
+        uint32_t e = (uint32_t)(e0 + k);
+        uint32_t j = e % H;
+        float z = normal1(seed, ST_REF, ref_set_id, s, c, e);
+        out[k] = r32((double)z * (double)gain[j]);
+    }
+}
+
 void orc_ref_block(uint32_t s, uint32_t c, uint32_t T, uint32_t H, uint64_t seed,
                    uint32_t ref_set_id, const float* gain, float* out)
 {
-    for (uint32_t t = 0; t < T; ++t)
-        for (uint32_t j = 0; j < H; ++j) {
-            uint32_t e = t * H + j;
-            float z = normal1(seed, ST_REF, ref_set_id, s, c, e);
-            out[e] = r32((double)z * (double)gain[j]);
-        }
+    orc_ref_range(s, c, H, 0, (uint64_t)T * H, seed, ref_set_id, gain, out);
 }
 
 /* Whole reference array [S][C][T][H]. */
@@ -352,51 +359,61 @@ static int flip_selected(double p, uint32_t u)
     return (double)u < thr;
 }
 
+/* Elements [e0, e0 + count) of block (s, c); ref and h hold just that range. */
+int orc_sim_range(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t seed,
+                  uint32_t cfg_id, int benign_mode, int benign_dist, double sigma_b, float bscale,
+                  int malicious, uint32_t tamper, int tamper_base, float tscale, double flip_p,
+                  double scale, const float* ref, uint16_t* h)
+{
+    float sigma_f = r32(sigma_b);
+    float scale_f = r32(scale);
+    for (uint64_t k = 0; k < count; ++k) {
+        uint32_t e = (uint32_t)(e0 + k);
+        float a = ref[k];
+
+        /* benign hardware noise, Eq. 2 */
+        float sc = (benign_mode == ORC_NOISE_BLOCK) ? bscale : r32((double)sigma_f * fabs((double)a));
+        float zb = normal1(seed, ST_BENIGN, cfg_id, s, c, e);
+        if (benign_dist == ORC_DIST_T3) {
+            float z1, z2;
+            normal2(seed, ST_T12, cfg_id, s, c, e, &z1, &z2);
+            float z3 = normal1(seed, ST_T3, cfg_id, s, c, e);
+            float q = r32((double)r32((double)r32((double)z1 * z1) + (double)r32((double)z2 * z2)) +
+                          (double)r32((double)z3 * z3));
+            zb = (q == 0.0f) ? 0.0f : r32((double)zb / (double)r32(sqrt((double)q)));
+        }
+        float benign = r32((double)a + (double)r32((double)sc * (double)zb));
+        float v = benign;
+
+        /* tampering, Eq. 3 */
+        if (malicious) {
+            if (tamper_base == ORC_BASE_CLEAN)
+                v = a;
+            if (tamper & ORC_T_ADD) {
+                float zt = normal1(seed, ST_TADD, cfg_id, s, c, e);
+                v = r32((double)v + (double)r32((double)tscale * (double)zt));
+            }
+            if (tamper & ORC_T_FLIP) {
+                uint32_t u = word1(seed, ST_TFLIP, cfg_id, s, c, e);
+                if (flip_selected(flip_p, u))
+                    v = -v;
+            }
+            if (tamper & ORC_T_SCALE)
+                v = r32((double)scale_f * (double)v);
+        }
+        h[k] = orc_f16_rne(v);
+    }
+    return 0;
+}
+
 int orc_sim_block(uint32_t s, uint32_t c, uint32_t T, uint32_t H, uint64_t seed, uint32_t cfg_id,
                   int benign_mode, int benign_dist, double sigma_b, float bscale, int malicious,
                   uint32_t tamper, int tamper_base, float tscale, double flip_p, double scale,
                   const float* ref, uint16_t* h)
 {
-    float sigma_f = r32(sigma_b);
-    float scale_f = r32(scale);
-    for (uint32_t t = 0; t < T; ++t)
-        for (uint32_t j = 0; j < H; ++j) {
-            uint32_t e = t * H + j;
-            float a = ref[e];
-
-            /* benign hardware noise, Eq. 2 */
-            float sc = (benign_mode == ORC_NOISE_BLOCK) ? bscale : r32((double)sigma_f * fabs((double)a));
-            float zb = normal1(seed, ST_BENIGN, cfg_id, s, c, e);
-            if (benign_dist == ORC_DIST_T3) {
-                float z1, z2;
-                normal2(seed, ST_T12, cfg_id, s, c, e, &z1, &z2);
-                float z3 = normal1(seed, ST_T3, cfg_id, s, c, e);
-                float q = r32((double)r32((double)r32((double)z1 * z1) + (double)r32((double)z2 * z2)) +
-                              (double)r32((double)z3 * z3));
-                zb = (q == 0.0f) ? 0.0f : r32((double)zb / (double)r32(sqrt((double)q)));
-            }
-            float benign = r32((double)a + (double)r32((double)sc * (double)zb));
-            float v = benign;
-
-            /* tampering, Eq. 3 */
-            if (malicious) {
-                if (tamper_base == ORC_BASE_CLEAN)
-                    v = a;
-                if (tamper & ORC_T_ADD) {
-                    float zt = normal1(seed, ST_TADD, cfg_id, s, c, e);
-                    v = r32((double)v + (double)r32((double)tscale * (double)zt));
-                }
-                if (tamper & ORC_T_FLIP) {
-                    uint32_t u = word1(seed, ST_TFLIP, cfg_id, s, c, e);
-                    if (flip_selected(flip_p, u))
-                        v = -v;
-                }
-                if (tamper & ORC_T_SCALE)
-                    v = r32((double)scale_f * (double)v);
-            }
-            h[e] = orc_f16_rne(v);
-        }
-    return 0;
+    return orc_sim_range(s, c, 0, (uint64_t)T * H, seed, cfg_id, benign_mode, benign_dist,
+                         sigma_b, bscale, malicious, tamper, tamper_base, tscale, flip_p, scale,
+                         ref, h);
 }
 
 /* Whole live array [S][C][T][H].  tscale and bscale are [S][C] (may be NULL

@@ -1,0 +1,292 @@
+"""Thin Python binding of libcdt (declared in include/cdt.h).
+
+Argument marshalling only: every function checks the torch tensors it is
+given (device, dtype, contiguity, shape), passes their device pointers and
+the current HIP stream to the C ABI, and raises CdtError on a non-zero
+return.  All arithmetic runs in the HIP kernels.  If libcdt.so has not been
+built, loading fails loudly; there is no fallback path.
+
+fp16 activations travel as torch.float16 tensors (their bits are the
+uint16 words of the C ABI).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcdt.so")
+
+OK, EINVAL, EALIGN, ELIMIT, EDEVICE = 0, 1, 2, 3, 4
+NOISE_ELEMENTWISE, NOISE_BLOCK = 0, 1
+DIST_GAUSS, DIST_T3 = 0, 1
+T_ADD, T_FLIP, T_SCALE = 1, 2, 4
+BASE_BENIGN, BASE_CLEAN = 0, 1
+AUROC_CONTROL, AUROC_POOLED, CTRL_INCLUDE_TRUE = 1, 2, 4
+
+
+class CdtError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+class SimParams(ctypes.Structure):
+    _fields_ = [
+        ("seed", ctypes.c_uint64),
+        ("cfg_id", ctypes.c_uint32),
+        ("benign_mode", ctypes.c_uint32),
+        ("benign_dist", ctypes.c_uint32),
+        ("tamper", ctypes.c_uint32),
+        ("tamper_base", ctypes.c_uint32),
+        ("reserved", ctypes.c_uint32),
+        ("mal_mask", ctypes.c_uint64),
+        ("sigma_b", ctypes.c_double),
+        ("flip_p", ctypes.c_double),
+        ("scale", ctypes.c_double),
+        ("bscale", ctypes.c_void_p),
+        ("tscale", ctypes.c_void_p),
+    ]
+
+
+class AurocCfg(ctypes.Structure):
+    _fields_ = [
+        ("S", ctypes.c_uint32),
+        ("C", ctypes.c_uint32),
+        ("score_off", ctypes.c_uint64),
+        ("pos_mask", ctypes.c_uint64),
+        ("cfg_id", ctypes.c_uint32),
+        ("reserved", ctypes.c_uint32),
+    ]
+
+
+_u32, _u64, _f, _d, _vp, _sz = (ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float, ctypes.c_double,
+                                ctypes.c_void_p, ctypes.c_size_t)
+_SIGS = {
+    "cdt_version": ([], ctypes.c_int),
+    "cdt_last_error": ([], ctypes.c_char_p),
+    "cdt_outlier_gain": ([_u32, _u32, _f, _u64, _u32, _vp, _vp], ctypes.c_int),
+    "cdt_ref_synth": ([_u32, _u32, _u32, _u32, _u64, _u32, _vp, _vp, _vp], ctypes.c_int),
+    "cdt_reduce_workspace_bytes": ([_u32, _u32, _u32, _u32], _sz),
+    "cdt_ref_stats": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "cdt_block_scales": ([_u64, _u32, _u32, _vp, _vp, _d, _d, _vp, _vp, _vp], ctypes.c_int),
+    "cdt_canary_sim": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp],
+                       ctypes.c_int),
+    "cdt_drift_score": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "cdt_auroc_workspace_bytes": ([_u32], _sz),
+    "cdt_auroc": ([_u32, ctypes.POINTER(AurocCfg), _vp, _u64, _u64, _u32, _vp, _vp, _vp, _sz, _vp],
+                  ctypes.c_int),
+}
+
+_LIB = None
+
+
+def lib():
+    """Load libcdt.so (built by paper_2607_19490_amd.build); raises if absent."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libcdt.so is not built ({LIB_PATH}); run __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _LIB = L
+    return _LIB
+
+
+def exported_symbols():
+    return list(_SIGS)
+
+
+def _check(rc):
+    if rc != OK:
+        raise CdtError(rc, lib().cdt_last_error().decode())
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream():
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _need(t, name, dtype, shape=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must live on the GPU")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _empty(shape, dtype, like=None):
+    torch = _torch()
+    dev = like.device if like is not None else torch.device("cuda", torch.cuda.current_device())
+    return torch.empty(shape, dtype=dtype, device=dev)
+
+
+def version():
+    return lib().cdt_version()
+
+
+def last_error():
+    return lib().cdt_last_error().decode()
+
+
+# ---------------------------------------------------------------------------
+def outlier_gain(H, n_out, big, seed, ref_set_id, out=None):
+    torch = _torch()
+    out = _empty((H,), torch.float32) if out is None else out
+    _need(out, "gain", torch.float32, (H,))
+    _check(lib().cdt_outlier_gain(H, n_out, big, seed, ref_set_id, _ptr(out), _stream()))
+    return out
+
+
+def ref_synth(S, C, T, H, seed, ref_set_id, gain, out=None):
+    torch = _torch()
+    _need(gain, "gain", torch.float32, (H,))
+    out = _empty((S, C, T, H), torch.float32, gain) if out is None else out
+    _need(out, "ref", torch.float32, (S, C, T, H))
+    _check(lib().cdt_ref_synth(S, C, T, H, seed, ref_set_id, _ptr(gain), _ptr(out), _stream()))
+    return out
+
+
+def reduce_workspace_bytes(S, C, T, H):
+    return lib().cdt_reduce_workspace_bytes(S, C, T, H)
+
+
+def workspace(S, C, T, H, like=None):
+    torch = _torch()
+    n = max(16, reduce_workspace_bytes(S, C, T, H))
+    return _empty((n,), torch.uint8, like)
+
+
+def _ws_arg(ws, S, C, T, H, like):
+    if ws is None:
+        ws = workspace(S, C, T, H, like)
+    return ws, ctypes.c_size_t(ws.numel() * ws.element_size())
+
+
+def ref_stats(ref, ws=None):
+    torch = _torch()
+    _need(ref, "ref", torch.float32)
+    S, C, T, H = ref.shape
+    sumsq = _empty((S, C), torch.float64, ref)
+    sumabs = _empty((S, C), torch.float64, ref)
+    ws, nbytes = _ws_arg(ws, S, C, T, H, ref)
+    _check(lib().cdt_ref_stats(S, C, T, H, _ptr(ref), _ptr(sumsq), _ptr(sumabs), _ptr(ws), nbytes,
+                               _stream()))
+    return sumsq, sumabs
+
+
+def block_scales(sumsq, sumabs, T, H, eps, sigma_b, tscale=None, bscale=None):
+    torch = _torch()
+    _need(sumsq, "sumsq", torch.float64)
+    _need(sumabs, "sumabs", torch.float64, tuple(sumsq.shape))
+    tscale = _empty(tuple(sumsq.shape), torch.float32, sumsq) if tscale is None else tscale
+    bscale = _empty(tuple(sumsq.shape), torch.float32, sumsq) if bscale is None else bscale
+    _need(tscale, "tscale", torch.float32, tuple(sumsq.shape))
+    _need(bscale, "bscale", torch.float32, tuple(sumsq.shape))
+    _check(lib().cdt_block_scales(sumsq.numel(), T, H, _ptr(sumsq), _ptr(sumabs), eps, sigma_b,
+                                  _ptr(tscale), _ptr(bscale), _stream()))
+    return tscale, bscale
+
+
+def sim_params(*, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE, benign_dist=DIST_GAUSS,
+               sigma_b=1e-3, mal_mask=0, tamper=0, tamper_base=BASE_BENIGN, flip_p=0.0,
+               scale=1.0, bscale=None, tscale=None):
+    return SimParams(seed, cfg_id, benign_mode, benign_dist, tamper, tamper_base, 0, mal_mask,
+                     sigma_b, flip_p, scale,
+                     None if bscale is None else bscale.data_ptr(),
+                     None if tscale is None else tscale.data_ptr())
+
+
+def canary_sim(ref, out=None, *, bscale=None, tscale=None, **kw):
+    """ref [S][C][T][H] fp32 -> h [S][C][T][H] fp16.  Keywords as sim_params."""
+    torch = _torch()
+    _need(ref, "ref", torch.float32)
+    S, C, T, H = ref.shape
+    for name, t in (("bscale", bscale), ("tscale", tscale)):
+        if t is not None:
+            _need(t, name, torch.float32, (S, C))
+    out = _empty((S, C, T, H), torch.float16, ref) if out is None else out
+    _need(out, "h", torch.float16, (S, C, T, H))
+    p = sim_params(bscale=bscale, tscale=tscale, **kw)
+    _check(lib().cdt_canary_sim(S, C, T, H, ctypes.byref(p), _ptr(ref), _ptr(out), _stream()))
+    return out
+
+
+def drift_score(h, ref, out=None, num_den=None, ws=None):
+    """Eq. 4 per block -> scores [C][S] fp32 (and optional [C][S][2] fp64)."""
+    torch = _torch()
+    _need(ref, "ref", torch.float32)
+    S, C, T, H = ref.shape
+    _need(h, "h", torch.float16, (S, C, T, H))
+    out = _empty((C, S), torch.float32, ref) if out is None else out
+    _need(out, "score", torch.float32, (C, S))
+    if num_den is not None:
+        _need(num_den, "num_den", torch.float64, (C, S, 2))
+    ws, nbytes = _ws_arg(ws, S, C, T, H, ref)
+    _check(lib().cdt_drift_score(S, C, T, H, _ptr(h), _ptr(ref), _ptr(out), _ptr(num_den),
+                                 _ptr(ws), nbytes, _stream()))
+    return out
+
+
+def auroc_cfg_array(cfgs):
+    """cfgs: iterable of (S, C, score_off, pos_mask, cfg_id) -> ctypes array."""
+    cfgs = list(cfgs)
+    arr = (AurocCfg * max(1, len(cfgs)))()
+    for i, (S, C, off, mask, cid) in enumerate(cfgs):
+        arr[i] = AurocCfg(S, C, off, mask, cid, 0)
+    return arr, len(cfgs)
+
+
+def auroc(cfgs, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_POOLED, counts=None, pooled=None,
+          ws=None):
+    """Batched AUROC counts.  cfgs: iterable of (S, C, score_off, pos_mask,
+    cfg_id); scores: flat (or any contiguous) fp32 device tensor.
+    Returns (counts [n][6] uint64-as-int64, pooled [n][3] or None)."""
+    torch = _torch()
+    _need(scores, "scores", torch.float32)
+    arr, n = auroc_cfg_array(cfgs)
+    counts = _empty((n, 6), torch.int64, scores) if counts is None else counts
+    _need(counts, "counts", torch.int64, (n, 6))
+    if flags & AUROC_POOLED:
+        pooled = _empty((n, 3), torch.int64, scores) if pooled is None else pooled
+        _need(pooled, "pooled", torch.int64, (n, 3))
+    if ws is None:
+        ws = _empty((max(16, lib().cdt_auroc_workspace_bytes(n)),), torch.uint8, scores)
+    _check(lib().cdt_auroc(n, arr, _ptr(scores), scores.numel(), seed, flags, _ptr(counts),
+                           _ptr(pooled), _ptr(ws), ws.numel(), _stream()))
+    return counts, (pooled if flags & AUROC_POOLED else None)
+
+
+def strict_auroc(counts_row):
+    """Eq. 6 as printed (ties count 0) from one counts row (G, E, pairs)."""
+    G, E, N = (int(x) for x in counts_row[:3])
+    return G / N if N else float("nan")
+
+
+def mw_auroc(counts_row):
+    """Mann-Whitney normalisation (ties count one half)."""
+    G, E, N = (int(x) for x in counts_row[:3])
+    return (G + 0.5 * E) / N if N else float("nan")
+
+
+def u64(counts):
+    """View int64 count tensors (copied to host) as uint64 numpy arrays."""
+    return counts.cpu().numpy().view(np.uint64)

@@ -1,0 +1,250 @@
+// C ABI of libcdt: argument validation, workspace sizing, launches and
+// error reporting.  Every check runs on the host before any HIP call, so a
+// rejected call touches no device state.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/cdt.h"
+#include "cdt_launch.hpp"
+
+namespace {
+
+thread_local char g_error[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_error, sizeof(g_error), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_error[0] = '\0';
+    return CDT_OK;
+}
+
+int device_status(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(CDT_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr uint64_t kMaxBlockElems = 1ull << 32;  // element index e must fit 32 bits
+constexpr uint32_t kMaxId = 1u << 24;            // counter id field
+constexpr uint32_t kMaxOutlierH = 32768;
+constexpr uint32_t kMaxPooled = 16384;
+
+// Shape checks common to every activation call.
+int check_shape(const char* fn, uint32_t S, uint32_t C, uint32_t T, uint32_t H) {
+    (void)S;
+    (void)C;
+    if (H % 8 != 0) return fail(CDT_EINVAL, "%s: H=%u must be a multiple of 8", fn, H);
+    const uint64_t n = static_cast<uint64_t>(T) * H;
+    if (n >= kMaxBlockElems)
+        return fail(CDT_ELIMIT, "%s: T*H=%llu must be below 2^32", fn,
+                    static_cast<unsigned long long>(n));
+    return CDT_OK;
+}
+
+bool empty(uint32_t S, uint32_t C, uint32_t T, uint32_t H) {
+    return static_cast<uint64_t>(S) * C * T * H == 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cdt_version(void) { return 1; }
+
+const char* cdt_last_error(void) { return g_error; }
+
+int cdt_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed, uint32_t ref_set_id,
+                     float* gain, void* stream) {
+    if (H > kMaxOutlierH) return fail(CDT_ELIMIT, "cdt_outlier_gain: H=%u above %u", H, kMaxOutlierH);
+    if (n_out > H) return fail(CDT_EINVAL, "cdt_outlier_gain: n_out=%u above H=%u", n_out, H);
+    if (ref_set_id >= kMaxId) return fail(CDT_ELIMIT, "cdt_outlier_gain: ref_set_id >= 2^24");
+    if (!isfinite(big)) return fail(CDT_EINVAL, "cdt_outlier_gain: gain must be finite");
+    if (H == 0) return ok();
+    if (!gain) return fail(CDT_EINVAL, "cdt_outlier_gain: gain is NULL");
+    return device_status(cdt::launch_outlier_gain(H, n_out, big, seed, ref_set_id, gain,
+                                                  static_cast<hipStream_t>(stream)),
+                         "cdt_outlier_gain");
+}
+
+int cdt_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
+                  uint32_t ref_set_id, const float* gain, float* ref, void* stream) {
+    int rc = check_shape("cdt_ref_synth", S, C, T, H);
+    if (rc) return rc;
+    if (ref_set_id >= kMaxId) return fail(CDT_ELIMIT, "cdt_ref_synth: ref_set_id >= 2^24");
+    if (empty(S, C, T, H)) return ok();
+    if (!gain || !ref) return fail(CDT_EINVAL, "cdt_ref_synth: NULL array");
+    if (!aligned16(gain) || !aligned16(ref))
+        return fail(CDT_EALIGN, "cdt_ref_synth: arrays must be 16-byte aligned");
+    return device_status(cdt::launch_ref_synth(S, C, T, H, seed, ref_set_id, gain, ref,
+                                               static_cast<hipStream_t>(stream)),
+                         "cdt_ref_synth");
+}
+
+size_t cdt_reduce_workspace_bytes(uint32_t S, uint32_t C, uint32_t T, uint32_t H) {
+    const uint64_t n = static_cast<uint64_t>(T) * H;
+    const uint64_t cpb = cdt::reduce_chunks_per_block(n);
+    return static_cast<size_t>(cpb * S * C * 2 * sizeof(double));
+}
+
+int cdt_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,
+                  double* sumsq, double* sumabs, void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_shape("cdt_ref_stats", S, C, T, H);
+    if (rc) return rc;
+    if (static_cast<uint64_t>(S) * C == 0) return ok();
+    if (!sumsq || !sumabs) return fail(CDT_EINVAL, "cdt_ref_stats: NULL output");
+    const size_t need = cdt_reduce_workspace_bytes(S, C, T, H);
+    if (static_cast<uint64_t>(T) * H > 0) {
+        if (!ref) return fail(CDT_EINVAL, "cdt_ref_stats: ref is NULL");
+        if (!aligned16(ref)) return fail(CDT_EALIGN, "cdt_ref_stats: ref must be 16-byte aligned");
+    }
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(CDT_EINVAL, "cdt_ref_stats: workspace of %zu bytes needed, %zu given", need,
+                    ws ? ws_bytes : 0);
+    if (ws && !aligned16(ws)) return fail(CDT_EALIGN, "cdt_ref_stats: ws must be 16-byte aligned");
+    return device_status(cdt::launch_ref_stats(S, C, T, H, ref, sumsq, sumabs, ws,
+                                               static_cast<hipStream_t>(stream)),
+                         "cdt_ref_stats");
+}
+
+int cdt_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const double* sumsq,
+                     const double* sumabs, double eps, double sigma_b, float* tscale,
+                     float* bscale, void* stream) {
+    if (!(eps >= 0.0) || !isfinite(eps) || !(sigma_b >= 0.0) || !isfinite(sigma_b))
+        return fail(CDT_EINVAL, "cdt_block_scales: eps and sigma_b must be finite and >= 0");
+    if (nblocks == 0 || (!tscale && !bscale)) return ok();
+    if (tscale && !sumsq) return fail(CDT_EINVAL, "cdt_block_scales: tscale needs sumsq");
+    if (bscale && !sumabs) return fail(CDT_EINVAL, "cdt_block_scales: bscale needs sumabs");
+    if (nblocks > (1ull << 40)) return fail(CDT_ELIMIT, "cdt_block_scales: too many blocks");
+    return device_status(cdt::launch_block_scales(nblocks, T, H, sumsq, sumabs, eps, sigma_b,
+                                                  tscale, bscale,
+                                                  static_cast<hipStream_t>(stream)),
+                         "cdt_block_scales");
+}
+
+int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
+                   const float* ref, uint16_t* h, void* stream) {
+    int rc = check_shape("cdt_canary_sim", S, C, T, H);
+    if (rc) return rc;
+    if (!p) return fail(CDT_EINVAL, "cdt_canary_sim: params is NULL");
+    if (S > 64) return fail(CDT_ELIMIT, "cdt_canary_sim: S=%u above 64", S);
+    if (p->cfg_id >= kMaxId) return fail(CDT_ELIMIT, "cdt_canary_sim: cfg_id >= 2^24");
+    if (p->benign_mode > CDT_NOISE_BLOCK) return fail(CDT_EINVAL, "cdt_canary_sim: bad benign_mode");
+    if (p->benign_dist > CDT_DIST_T3) return fail(CDT_EINVAL, "cdt_canary_sim: bad benign_dist");
+    if (p->tamper & ~7u) return fail(CDT_EINVAL, "cdt_canary_sim: bad tamper flags");
+    if (p->tamper_base > CDT_BASE_CLEAN) return fail(CDT_EINVAL, "cdt_canary_sim: bad tamper_base");
+    if (p->reserved != 0) return fail(CDT_EINVAL, "cdt_canary_sim: reserved must be 0");
+    if (!(p->sigma_b >= 0.0) || !isfinite(p->sigma_b))
+        return fail(CDT_EINVAL, "cdt_canary_sim: sigma_b must be finite and >= 0");
+    if (!(p->flip_p >= 0.0 && p->flip_p <= 1.0))
+        return fail(CDT_EINVAL, "cdt_canary_sim: flip_p must lie in [0, 1]");
+    if (!isfinite(p->scale)) return fail(CDT_EINVAL, "cdt_canary_sim: scale must be finite");
+    if (empty(S, C, T, H)) return ok();
+    if (!ref || !h) return fail(CDT_EINVAL, "cdt_canary_sim: NULL array");
+    if (!aligned16(ref) || !aligned16(h))
+        return fail(CDT_EALIGN, "cdt_canary_sim: arrays must be 16-byte aligned");
+    const uint64_t mal = p->mal_mask & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
+    if (p->benign_mode == CDT_NOISE_BLOCK && !p->bscale)
+        return fail(CDT_EINVAL, "cdt_canary_sim: BLOCK noise needs bscale");
+    if (mal && (p->tamper & CDT_T_ADD) && !p->tscale)
+        return fail(CDT_EINVAL, "cdt_canary_sim: Gaussian tamper needs tscale");
+
+    cdt::SimLaunch L;
+    L.S = S;
+    L.C = C;
+    L.T = T;
+    L.H = H;
+    L.seed = p->seed;
+    L.cfg_id = p->cfg_id;
+    L.benign_mode = p->benign_mode;
+    L.benign_dist = p->benign_dist;
+    L.tamper = p->tamper;
+    L.tamper_base = p->tamper_base;
+    L.mal_mask = mal;
+    L.sigma_b = static_cast<float>(p->sigma_b);
+    // Flip selection: u < floor(p 2^32) with p < 1 (so the threshold fits 32
+    // bits); p == 1 flips every element.
+    L.flip_all = p->flip_p >= 1.0;
+    L.flip_thr = L.flip_all ? 0u : static_cast<uint32_t>(floor(p->flip_p * 4294967296.0));
+    L.scale = static_cast<float>(p->scale);
+    L.bscale = p->bscale;
+    L.tscale = p->tscale;
+    return device_status(cdt::launch_canary_sim(L, ref, h, static_cast<hipStream_t>(stream)),
+                         "cdt_canary_sim");
+}
+
+int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                    const float* ref, float* score, double* num_den, void* ws, size_t ws_bytes,
+                    void* stream) {
+    int rc = check_shape("cdt_drift_score", S, C, T, H);
+    if (rc) return rc;
+    if (static_cast<uint64_t>(S) * C == 0) return ok();
+    if (!score) return fail(CDT_EINVAL, "cdt_drift_score: score is NULL");
+    if (static_cast<uint64_t>(T) * H > 0) {
+        if (!h || !ref) return fail(CDT_EINVAL, "cdt_drift_score: NULL array");
+        if (!aligned16(h) || !aligned16(ref))
+            return fail(CDT_EALIGN, "cdt_drift_score: arrays must be 16-byte aligned");
+    }
+    const size_t need = cdt_reduce_workspace_bytes(S, C, T, H);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(CDT_EINVAL, "cdt_drift_score: workspace of %zu bytes needed, %zu given", need,
+                    ws ? ws_bytes : 0);
+    if (ws && !aligned16(ws)) return fail(CDT_EALIGN, "cdt_drift_score: ws must be 16-byte aligned");
+    return device_status(cdt::launch_drift_score(S, C, T, H, h, ref, score, num_den, ws,
+                                                 static_cast<hipStream_t>(stream)),
+                         "cdt_drift_score");
+}
+
+size_t cdt_auroc_workspace_bytes(uint32_t n_cfg) {
+    return static_cast<size_t>(n_cfg) * sizeof(cdt_auroc_cfg);
+}
+
+int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, uint64_t n_scores,
+              uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled, void* ws,
+              size_t ws_bytes, void* stream) {
+    static_assert(sizeof(cdt_auroc_cfg) == sizeof(cdt::AurocCfgDev), "cfg layout");
+    if (flags & ~7u) return fail(CDT_EINVAL, "cdt_auroc: bad flags");
+    if (n_cfg == 0) return ok();
+    if (!cfgs || !counts) return fail(CDT_EINVAL, "cdt_auroc: NULL cfgs or counts");
+    if ((flags & CDT_AUROC_POOLED) && !pooled)
+        return fail(CDT_EINVAL, "cdt_auroc: pooled counts requested but pooled is NULL");
+    if (n_cfg > (1u << 24)) return fail(CDT_ELIMIT, "cdt_auroc: n_cfg above 2^24");
+    for (uint32_t g = 0; g < n_cfg; ++g) {
+        const cdt_auroc_cfg& c = cfgs[g];
+        if (c.S > 64) return fail(CDT_ELIMIT, "cdt_auroc: cfg %u has S=%u above 64", g, c.S);
+        if (c.cfg_id >= kMaxId) return fail(CDT_ELIMIT, "cdt_auroc: cfg %u cfg_id >= 2^24", g);
+        if (c.reserved != 0) return fail(CDT_EINVAL, "cdt_auroc: cfg %u reserved must be 0", g);
+        const uint64_t len = static_cast<uint64_t>(c.S) * c.C;
+        if ((flags & CDT_AUROC_POOLED) && len > kMaxPooled)
+            return fail(CDT_ELIMIT, "cdt_auroc: cfg %u has C*S=%llu above %u for pooled ranking",
+                        g, static_cast<unsigned long long>(len), kMaxPooled);
+        if (c.C > (1u << 30)) return fail(CDT_ELIMIT, "cdt_auroc: cfg %u C above 2^30", g);
+        if (c.score_off > n_scores || len > n_scores - c.score_off)
+            return fail(CDT_EINVAL, "cdt_auroc: cfg %u table [%llu, +%llu) outside %llu scores", g,
+                        static_cast<unsigned long long>(c.score_off),
+                        static_cast<unsigned long long>(len),
+                        static_cast<unsigned long long>(n_scores));
+        if (len > 0 && !scores) return fail(CDT_EINVAL, "cdt_auroc: scores is NULL");
+    }
+    const size_t need = cdt_auroc_workspace_bytes(n_cfg);
+    if (!ws || ws_bytes < need)
+        return fail(CDT_EINVAL, "cdt_auroc: workspace of %zu bytes needed, %zu given", need,
+                    ws ? ws_bytes : 0);
+    if (!aligned16(ws)) return fail(CDT_EALIGN, "cdt_auroc: ws must be 16-byte aligned");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(ws, cfgs, need, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return device_status(e, "cdt_auroc: config upload");
+    return device_status(cdt::launch_auroc(n_cfg, static_cast<const cdt::AurocCfgDev*>(ws),
+                                           scores, seed, flags, counts, pooled, st),
+                         "cdt_auroc");
+}
+
+}  // extern "C"

@@ -1,0 +1,112 @@
+// Device-side building blocks shared by the libcdt kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cdt {
+
+constexpr int kWave = 64;
+
+// Native 16-byte vectors (usable with the nontemporal load/store builtins).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Random stream ids (fourth counter word = stream << 24 | id).
+enum : uint32_t {
+    kStreamRef = 0,
+    kStreamBenign = 1,
+    kStreamT12 = 2,
+    kStreamT3 = 3,
+    kStreamTamperAdd = 4,
+    kStreamTamperFlip = 5,
+    kStreamScramble = 6,
+    kStreamRandom = 7,
+    kStreamOutlier = 8,
+    kStreamAlt = 9,
+};
+
+struct Words4 {
+    uint32_t x, y, z, w;
+};
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 32x32->64 multiplies on counter words 0 and 2, XOR of the high halves into
+// words 1 and 3 with the round key, and a word permutation; the key advances
+// by the two Weyl increments between rounds.  The multiplies lower to
+// v_mad_u64_u32; when a counter word is wave-uniform the first round's
+// product stays on the scalar unit.
+__device__ __forceinline__ Words4 philox10(Words4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t p0 = static_cast<uint64_t>(0xD2511F53u) * c.x;
+        const uint64_t p1 = static_cast<uint64_t>(0xCD9E8D57u) * c.z;
+        Words4 n;
+        n.x = static_cast<uint32_t>(p1 >> 32) ^ c.y ^ k0;
+        n.y = static_cast<uint32_t>(p1);
+        n.z = static_cast<uint32_t>(p0 >> 32) ^ c.w ^ k1;
+        n.w = static_cast<uint32_t>(p0);
+        c = n;
+        k0 += 0x9E3779B9u;
+        k1 += 0xBB67AE85u;
+    }
+    return c;
+}
+
+struct Key {
+    uint32_t k0, k1;
+};
+
+__device__ __forceinline__ Key make_key(uint64_t seed) {
+    return Key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)};
+}
+
+__device__ __forceinline__ Words4 draw(Key k, uint32_t q, uint32_t c, uint32_t s, uint32_t tag) {
+    return philox10(Words4{q, c, s, tag}, k.k0, k.k1);
+}
+
+__host__ __device__ constexpr uint32_t stream_tag(uint32_t stream, uint32_t id) {
+    return (stream << 24) | (id & 0xFFFFFFu);
+}
+
+// Unit normal stand-in: the Irwin-Hall sum of the four 16-bit halves of two
+// Philox words, centred (4 * 32767.5) and scaled by fp32(sqrt(3/(2^32-1))).
+__device__ __forceinline__ float irwin_hall4(uint32_t w0, uint32_t w1) {
+    const int n = static_cast<int>(w0 & 0xFFFFu) + static_cast<int>(w0 >> 16) +
+                  static_cast<int>(w1 & 0xFFFFu) + static_cast<int>(w1 >> 16) - 131070;
+    return static_cast<float>(n) * 0x1.bb67aep-16f;
+}
+
+// fp32 -> fp16 bits, IEEE round to nearest even (v_cvt_f16_f32 under the
+// default round-to-nearest mode; fp16 subnormals are kept).
+__device__ __forceinline__ uint16_t to_half_bits(float v) {
+    const _Float16 h = static_cast<_Float16>(v);
+    return __builtin_bit_cast(uint16_t, h);
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t bits16) {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
+}
+
+// Order-preserving key of a score: NaN lowest, -0 == +0, numeric otherwise.
+__device__ __forceinline__ uint32_t order_key(float x) {
+    if (x != x) return 0u;
+    uint32_t u = __float_as_uint(x);
+    if (x == 0.0f) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Wave-wide sums (wave64, butterfly through ds_swizzle/DPP lowering).
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+    return v;
+}
+
+__device__ __forceinline__ unsigned long long wave_sum(unsigned long long v) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+    return v;
+}
+
+}  // namespace cdt

@@ -1,0 +1,71 @@
+// Internal launch interface between the C ABI layer and the kernel files.
+// Arguments reaching these functions have been validated by the ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace cdt {
+
+// Elementwise kernels: a thread owns groups of 8 consecutive elements (one
+// 16-byte fp16 vector, two 16-byte fp32 vectors); a 256-thread workgroup
+// covers kGenItems groups per thread of one block per chunk.
+constexpr int kGenThreads = 256;
+constexpr int kGenItems = 4;
+constexpr uint32_t kGenChunkGroups = kGenThreads * kGenItems;
+
+// Block reductions: a workgroup reduces kReduceChunkElems elements of one
+// block to a pair of fp64 partial sums; a second kernel adds the partials of
+// a block in chunk order.
+constexpr int kReduceThreads = 256;
+constexpr int kReduceUnroll = 4;
+constexpr uint64_t kReduceChunkElems = 32768;
+
+inline uint64_t reduce_chunks_per_block(uint64_t n) {
+    return (n + kReduceChunkElems - 1) / kReduceChunkElems;
+}
+
+struct SimLaunch {
+    uint32_t S, C, T, H;
+    uint64_t seed;
+    uint32_t cfg_id;
+    uint32_t benign_mode, benign_dist, tamper, tamper_base;
+    uint64_t mal_mask;
+    float sigma_b;       // fp32(sigma_b)
+    uint32_t flip_thr;   // floor(p 2^32) (p < 1)
+    uint32_t flip_all;   // p >= 1
+    float scale;         // fp32(scale)
+    const float* bscale;
+    const float* tscale;
+};
+
+struct AurocCfgDev {
+    uint32_t S, C;
+    uint64_t score_off;
+    uint64_t pos_mask;
+    uint32_t cfg_id;
+    uint32_t reserved;
+};
+static_assert(sizeof(AurocCfgDev) == 32, "cfg layout must match cdt_auroc_cfg");
+
+hipError_t launch_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed,
+                               uint32_t ref_set_id, float* gain, hipStream_t st);
+hipError_t launch_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
+                            uint32_t ref_set_id, const float* gain, float* ref, hipStream_t st);
+hipError_t launch_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const double* sumsq,
+                               const double* sumabs, double eps, double sigma_b, float* tscale,
+                               float* bscale, hipStream_t st);
+hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, hipStream_t st);
+
+hipError_t launch_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,
+                            double* sumsq, double* sumabs, void* ws, hipStream_t st);
+hipError_t launch_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                              const float* ref, float* score, double* num_den, void* ws,
+                              hipStream_t st);
+
+hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float* scores,
+                        uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
+                        hipStream_t st);
+
+}  // namespace cdt

@@ -1,0 +1,290 @@
+// Generator kernels: synthetic fp32 references (stand-in for the verifier's
+// offline pass of Eq. 1), per-block scales, and the simulated live pass of
+// Eqs. 2-3 (benign hardware noise, tampering, fp16 hand-off).
+//
+// Every random number comes from Philox4x32-10 evaluated in registers from
+// its counter, so noise and tamper directions never touch HBM: a thread
+// reads 8 fp32 references (two 16-byte loads) and writes 8 fp16 activations
+// (one 16-byte store).  All fp32 arithmetic is written one operation per
+// step with FMA contraction off, so results are reproducible bit for bit.
+#include <math.h>
+
+#include "cdt_device.hpp"
+#include "cdt_launch.hpp"
+
+#pragma clang fp contract(off)
+
+namespace cdt {
+namespace {
+
+constexpr uint32_t kMaxOutlierH = 32768;
+
+// ---------------------------------------------------------------------------
+// Outlier channels: every workgroup draws all H channel words into LDS, then
+// each thread ranks one channel against all of them.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void outlier_gain_kernel(uint32_t H, uint32_t n_out, float big,
+                                                           Key key, uint32_t tag,
+                                                           float* __restrict__ gain) {
+    __shared__ uint32_t words[kMaxOutlierH];
+    for (uint32_t j = threadIdx.x; j < H; j += blockDim.x) words[j] = draw(key, j, 0, 0, tag).x;
+    __syncthreads();
+    const uint32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= H) return;
+    const uint32_t wj = words[j];
+    uint32_t rank = 0;
+    for (uint32_t i = 0; i < H; ++i) {
+        const uint32_t wi = words[i];
+        rank += (wi < wj) || (wi == wj && i < j);
+    }
+    gain[j] = rank < n_out ? big : 1.0f;
+}
+
+// ---------------------------------------------------------------------------
+// Chunk walk shared by the elementwise kernels: chunk -> (block, first group).
+// ---------------------------------------------------------------------------
+struct ChunkPos {
+    uint64_t block;
+    uint32_t s, c;
+    uint32_t g0;  // first 8-element group of this chunk inside the block
+};
+
+__device__ __forceinline__ ChunkPos chunk_pos(uint64_t chunk, uint64_t chunks_per_block,
+                                              uint32_t C) {
+    ChunkPos p;
+    p.block = chunk / chunks_per_block;
+    p.g0 = static_cast<uint32_t>(chunk - p.block * chunks_per_block) * kGenChunkGroups;
+    p.s = static_cast<uint32_t>(p.block / C);
+    p.c = static_cast<uint32_t>(p.block - static_cast<uint64_t>(p.s) * C);
+    return p;
+}
+
+// Eight unit normals of one stream for elements e0..e0+7 (e0 % 8 == 0):
+// Philox calls q = e0/2 .. e0/2+3, words (x, y) -> even element, (z, w) -> odd.
+__device__ __forceinline__ void normals8(Key key, uint32_t e0, uint32_t c, uint32_t s,
+                                         uint32_t tag, float z[8]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const Words4 w = draw(key, (e0 >> 1) + k, c, s, tag);
+        z[2 * k] = irwin_hall4(w.x, w.y);
+        z[2 * k + 1] = irwin_hall4(w.z, w.w);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Synthetic references: ref = fp32(z_REF * gain[j]).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kGenThreads) void ref_synth_kernel(
+    uint32_t C, uint32_t H, uint32_t n8, uint64_t chunks_per_block, uint64_t total_chunks,
+    Key key, uint32_t tag, const float* __restrict__ gain, float* __restrict__ ref) {
+    const uint64_t n = static_cast<uint64_t>(n8) * 8;
+    for (uint64_t chunk = blockIdx.x; chunk < total_chunks; chunk += gridDim.x) {
+        const ChunkPos p = chunk_pos(chunk, chunks_per_block, C);
+        float4* out = reinterpret_cast<float4*>(ref + p.block * n);
+#pragma unroll
+        for (int it = 0; it < kGenItems; ++it) {
+            const uint32_t g = p.g0 + it * kGenThreads + threadIdx.x;
+            if (g >= n8) break;
+            const uint32_t e0 = g * 8;
+            const uint32_t j0 = e0 % H;
+            const float4 g_lo = *reinterpret_cast<const float4*>(gain + j0);
+            const float4 g_hi = *reinterpret_cast<const float4*>(gain + j0 + 4);
+            float z[8];
+            normals8(key, e0, p.c, p.s, tag, z);
+            out[2 * g] = make_float4(z[0] * g_lo.x, z[1] * g_lo.y, z[2] * g_lo.z, z[3] * g_lo.w);
+            out[2 * g + 1] =
+                make_float4(z[4] * g_hi.x, z[5] * g_hi.y, z[6] * g_hi.z, z[7] * g_hi.w);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Per-block scales (fp64, rounded once to fp32).
+// ---------------------------------------------------------------------------
+__global__ void block_scales_kernel(uint64_t nblocks, double n, const double* __restrict__ sumsq,
+                                    const double* __restrict__ sumabs, double eps, double sigma_b,
+                                    float* __restrict__ tscale, float* __restrict__ bscale) {
+    const uint64_t b = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (b >= nblocks) return;
+    if (tscale) {
+        const double rms = n > 0 ? sqrt(sumsq[b] / n) : 0.0;
+        tscale[b] = static_cast<float>(eps * rms);
+    }
+    if (bscale) {
+        const double mu = n > 0 ? sumabs[b] / n : 0.0;
+        bscale[b] = static_cast<float>(sigma_b * mu);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Live pass (Eqs. 2-3) -> fp16.
+// ---------------------------------------------------------------------------
+struct SimArgs {
+    uint32_t C, n8;
+    uint64_t chunks_per_block, total_chunks;
+    Key key;
+    uint32_t tag_benign, tag_t12, tag_t3, tag_add, tag_flip;
+    uint32_t block_mode, t3, tamper, clean;
+    uint64_t mal_mask;
+    float sigma_b;
+    uint32_t flip_thr, flip_all;
+    float scale;
+    const float* bscale;
+    const float* tscale;
+};
+
+__global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
+                                                                 const float* __restrict__ ref,
+                                                                 uint16_t* __restrict__ h) {
+    const uint64_t n = static_cast<uint64_t>(A.n8) * 8;
+    for (uint64_t chunk = blockIdx.x; chunk < A.total_chunks; chunk += gridDim.x) {
+        const ChunkPos p = chunk_pos(chunk, A.chunks_per_block, A.C);
+        const bool mal = (A.mal_mask >> p.s) & 1u;
+        const float bsc = A.block_mode ? A.bscale[p.block] : 0.0f;
+        const float tsc = (mal && (A.tamper & 1u)) ? A.tscale[p.block] : 0.0f;
+        const float4* in = reinterpret_cast<const float4*>(ref + p.block * n);
+        uint4* out = reinterpret_cast<uint4*>(h + p.block * n);
+#pragma unroll 1
+        for (int it = 0; it < kGenItems; ++it) {
+            const uint32_t g = p.g0 + it * kGenThreads + threadIdx.x;
+            if (g >= A.n8) break;
+            const uint32_t e0 = g * 8;
+            const float4 a_lo = in[2 * g];
+            const float4 a_hi = in[2 * g + 1];
+            const float a[8] = {a_lo.x, a_lo.y, a_lo.z, a_lo.w, a_hi.x, a_hi.y, a_hi.z, a_hi.w};
+
+            // Eq. 2: benign hardware noise.
+            float zb[8];
+            normals8(A.key, e0, p.c, p.s, A.tag_benign, zb);
+            if (A.t3) {
+                float z3[8];
+                normals8(A.key, e0, p.c, p.s, A.tag_t3, z3);
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const Words4 w = draw(A.key, e0 + k, p.c, p.s, A.tag_t12);
+                    const float z1 = irwin_hall4(w.x, w.y);
+                    const float z2 = irwin_hall4(w.z, w.w);
+                    const float q = (z1 * z1 + z2 * z2) + z3[k] * z3[k];
+                    zb[k] = (q == 0.0f) ? 0.0f : zb[k] / sqrtf(q);
+                }
+            }
+            float v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const float sc = A.block_mode ? bsc : A.sigma_b * fabsf(a[k]);
+                v[k] = a[k] + sc * zb[k];
+            }
+
+            // Eq. 3: tampering on malicious shards.
+            if (mal) {
+                if (A.clean) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) v[k] = a[k];
+                }
+                if (A.tamper & 1u) {
+                    float zt[8];
+                    normals8(A.key, e0, p.c, p.s, A.tag_add, zt);
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) v[k] = v[k] + tsc * zt[k];
+                }
+                if (A.tamper & 2u) {
+                    const Words4 u0 = draw(A.key, e0 >> 2, p.c, p.s, A.tag_flip);
+                    const Words4 u1 = draw(A.key, (e0 >> 2) + 1, p.c, p.s, A.tag_flip);
+                    const uint32_t u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        if (A.flip_all || u[k] < A.flip_thr) v[k] = -v[k];
+                }
+                if (A.tamper & 4u) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) v[k] = A.scale * v[k];
+                }
+            }
+
+            uint4 o;
+            o.x = to_half_bits(v[0]) | (static_cast<uint32_t>(to_half_bits(v[1])) << 16);
+            o.y = to_half_bits(v[2]) | (static_cast<uint32_t>(to_half_bits(v[3])) << 16);
+            o.z = to_half_bits(v[4]) | (static_cast<uint32_t>(to_half_bits(v[5])) << 16);
+            o.w = to_half_bits(v[6]) | (static_cast<uint32_t>(to_half_bits(v[7])) << 16);
+            out[g] = o;
+        }
+    }
+}
+
+// Grid for a chunked elementwise walk: enough workgroups to fill 256 CUs
+// several times over; larger jobs loop.
+inline uint32_t gen_grid(uint64_t total_chunks) {
+    const uint64_t cap = 256ull * 64;
+    return static_cast<uint32_t>(total_chunks < cap ? total_chunks : cap);
+}
+
+}  // namespace
+
+hipError_t launch_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed,
+                               uint32_t ref_set_id, float* gain, hipStream_t st) {
+    if (H == 0) return hipSuccess;
+    const uint32_t grid = (H + 255) / 256;
+    hipLaunchKernelGGL(outlier_gain_kernel, dim3(grid), dim3(256), 0, st, H, n_out, big,
+                       Key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)},
+                       stream_tag(kStreamOutlier, ref_set_id), gain);
+    return hipGetLastError();
+}
+
+hipError_t launch_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
+                            uint32_t ref_set_id, const float* gain, float* ref, hipStream_t st) {
+    const uint64_t n = static_cast<uint64_t>(T) * H;
+    const uint64_t nblocks = static_cast<uint64_t>(S) * C;
+    if (n == 0 || nblocks == 0) return hipSuccess;
+    const uint32_t n8 = static_cast<uint32_t>(n / 8);
+    const uint64_t cpb = (n8 + kGenChunkGroups - 1) / kGenChunkGroups;
+    const uint64_t total = cpb * nblocks;
+    hipLaunchKernelGGL(ref_synth_kernel, dim3(gen_grid(total)), dim3(kGenThreads), 0, st, C, H,
+                       n8, cpb, total,
+                       Key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)},
+                       stream_tag(kStreamRef, ref_set_id), gain, ref);
+    return hipGetLastError();
+}
+
+hipError_t launch_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const double* sumsq,
+                               const double* sumabs, double eps, double sigma_b, float* tscale,
+                               float* bscale, hipStream_t st) {
+    if (nblocks == 0) return hipSuccess;
+    const uint64_t grid = (nblocks + 255) / 256;
+    hipLaunchKernelGGL(block_scales_kernel, dim3(static_cast<uint32_t>(grid)), dim3(256), 0, st,
+                       nblocks, static_cast<double>(T) * static_cast<double>(H), sumsq, sumabs,
+                       eps, sigma_b, tscale, bscale);
+    return hipGetLastError();
+}
+
+hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, hipStream_t st) {
+    const uint64_t n = static_cast<uint64_t>(p.T) * p.H;
+    const uint64_t nblocks = static_cast<uint64_t>(p.S) * p.C;
+    if (n == 0 || nblocks == 0) return hipSuccess;
+    SimArgs A;
+    A.C = p.C;
+    A.n8 = static_cast<uint32_t>(n / 8);
+    A.chunks_per_block = (A.n8 + kGenChunkGroups - 1) / kGenChunkGroups;
+    A.total_chunks = A.chunks_per_block * nblocks;
+    A.key = Key{static_cast<uint32_t>(p.seed), static_cast<uint32_t>(p.seed >> 32)};
+    A.tag_benign = stream_tag(kStreamBenign, p.cfg_id);
+    A.tag_t12 = stream_tag(kStreamT12, p.cfg_id);
+    A.tag_t3 = stream_tag(kStreamT3, p.cfg_id);
+    A.tag_add = stream_tag(kStreamTamperAdd, p.cfg_id);
+    A.tag_flip = stream_tag(kStreamTamperFlip, p.cfg_id);
+    A.block_mode = p.benign_mode == 1;
+    A.t3 = p.benign_dist == 1;
+    A.tamper = p.tamper;
+    A.clean = p.tamper_base == 1;
+    A.mal_mask = p.mal_mask;
+    A.sigma_b = p.sigma_b;
+    A.flip_thr = p.flip_thr;
+    A.flip_all = p.flip_all;
+    A.scale = p.scale;
+    A.bscale = p.bscale;
+    A.tscale = p.tscale;
+    hipLaunchKernelGGL(canary_sim_kernel, dim3(gen_grid(A.total_chunks)), dim3(kGenThreads), 0,
+                       st, A, ref, h);
+    return hipGetLastError();
+}
+
+}  // namespace cdt

@@ -1,0 +1,231 @@
+// Detection AUROC (Eqs. 5-6), its Mann-Whitney form and the scrambled-label
+// control of Section 4.5, batched over configurations.
+//
+// Per-canary counts: one workgroup per configuration; each wave takes one
+// canary at a time with lane s holding shard s's score as an order key
+// (S <= 64 = one wave).  Every positive lane compares itself with every
+// negative shard through wave shuffles; integer counts are summed over waves
+// in a fixed order.
+//
+// Pooled Mann-Whitney: one 1024-thread workgroup per configuration sorts the
+// C*S (key, label) pairs with an LDS bitonic network, scans the negatives in
+// sorted order, and for each positive binary-searches its tie group: it beats
+// the negatives before the group and ties those inside it.
+#include "cdt_device.hpp"
+#include "cdt_launch.hpp"
+
+namespace cdt {
+namespace {
+
+constexpr int kCountThreads = 256;
+constexpr int kCountWaves = kCountThreads / kWave;
+constexpr int kPoolThreads = 1024;
+constexpr uint32_t kPoolMax = 16384;
+
+__device__ __forceinline__ uint64_t shard_mask(uint32_t S) {
+    return S >= 64 ? ~0ull : ((1ull << S) - 1ull);
+}
+
+// r-th set bit (0-based) of m; m has more than r bits set.
+__device__ __forceinline__ uint32_t nth_set_bit(uint64_t m, uint32_t r) {
+    for (uint32_t i = 0; i < r; ++i) m &= m - 1;
+    return static_cast<uint32_t>(__builtin_ctzll(m));
+}
+
+__global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
+    const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, Key key,
+    uint32_t flags, unsigned long long* __restrict__ counts) {
+    const AurocCfgDev cfg = cfgs[blockIdx.x];
+    const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const uint64_t all = shard_mask(cfg.S);
+    const uint64_t pos = cfg.pos_mask & all;
+    const uint64_t neg = all & ~pos;
+    const bool lane_in = lane < cfg.S;
+    const bool lane_pos = lane_in && ((pos >> lane) & 1u);
+    const bool control = flags & 1u;
+    const bool include_true = flags & 4u;
+    const uint32_t n_benign = __builtin_popcountll(neg);
+    const uint32_t tag = stream_tag(kStreamScramble, cfg.cfg_id);
+
+    unsigned long long g = 0, e = 0, gc = 0, ec = 0;
+    for (uint32_t t = wave; t < cfg.C; t += kCountWaves) {
+        const float* row = scores + cfg.score_off + static_cast<uint64_t>(t) * cfg.S;
+        const uint32_t k = lane_in ? order_key(row[lane]) : 0u;
+        for (uint32_t j = 0; j < cfg.S; ++j) {
+            const uint32_t kj = __shfl(k, j, kWave);
+            if (lane_pos && ((neg >> j) & 1u)) {
+                g += k > kj;
+                e += k == kj;
+            }
+        }
+        if (control && n_benign > 0) {
+            const uint32_t u = draw(key, t, 0, 0, tag).x;
+            const uint32_t js = nth_set_bit(neg, u % n_benign);
+            const uint32_t kjs = __shfl(k, js, kWave);
+            const bool counted =
+                lane_in && lane != js && (include_true || !((pos >> lane) & 1u));
+            if (counted) {
+                gc += kjs > k;
+                ec += kjs == k;
+            }
+        }
+    }
+
+    __shared__ unsigned long long lds[4][kCountWaves];
+    g = wave_sum(g);
+    e = wave_sum(e);
+    gc = wave_sum(gc);
+    ec = wave_sum(ec);
+    if (lane == 0) {
+        lds[0][wave] = g;
+        lds[1][wave] = e;
+        lds[2][wave] = gc;
+        lds[3][wave] = ec;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long tot[4] = {0, 0, 0, 0};
+        for (int q = 0; q < 4; ++q)
+            for (int w = 0; w < kCountWaves; ++w) tot[q] += lds[q][w];
+        const unsigned long long n_pos = __builtin_popcountll(pos);
+        unsigned long long* out = counts + 6ull * blockIdx.x;
+        out[0] = tot[0];
+        out[1] = tot[1];
+        out[2] = static_cast<unsigned long long>(cfg.C) * n_pos * n_benign;
+        unsigned long long n_ctrl = 0;
+        if (control && n_benign > 0) n_ctrl = include_true ? cfg.S - 1 : n_benign - 1;
+        out[3] = control ? tot[2] : 0;
+        out[4] = control ? tot[3] : 0;
+        out[5] = static_cast<unsigned long long>(cfg.C) * n_ctrl;
+    }
+}
+
+// Element layout in the pooled sort: key << 32 | label (label 1 = positive);
+// after the negative scan: key << 32 | negatives_before << 1 | label.
+__global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
+    const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores,
+    unsigned long long* __restrict__ pooled) {
+    __shared__ uint64_t v[kPoolMax];
+    __shared__ uint32_t scan[kPoolThreads];
+    __shared__ unsigned long long red[2][kPoolThreads / kWave];
+    const AurocCfgDev cfg = cfgs[blockIdx.x];
+    const uint32_t n = cfg.S * cfg.C;
+    uint32_t P2 = 1;
+    while (P2 < n) P2 <<= 1;
+    const uint64_t pos = cfg.pos_mask & shard_mask(cfg.S);
+    const float* tab = scores + cfg.score_off;
+
+    for (uint32_t i = threadIdx.x; i < P2; i += kPoolThreads) {
+        if (i < n) {
+            const uint32_t s = i % cfg.S;
+            v[i] = (static_cast<uint64_t>(order_key(tab[i])) << 32) | ((pos >> s) & 1u);
+        } else {
+            v[i] = ~0ull;  // padding sorts last
+        }
+    }
+    __syncthreads();
+
+    // Bitonic sort, ascending.
+    for (uint32_t k = 2; k <= P2; k <<= 1) {
+        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+            for (uint32_t p = threadIdx.x; p < P2 / 2; p += kPoolThreads) {
+                const uint32_t i = 2 * p - (p & (j - 1));
+                const uint32_t l = i + j;
+                const uint64_t x = v[i], y = v[l];
+                const bool up = (i & k) == 0;
+                if ((x > y) == up) {
+                    v[i] = y;
+                    v[l] = x;
+                }
+            }
+            __syncthreads();
+        }
+    }
+
+    // Exclusive scan of negatives over the sorted order: each thread owns a
+    // contiguous run of `per` elements.
+    const uint32_t per = (n + kPoolThreads - 1) / kPoolThreads;
+    const uint32_t lo = threadIdx.x * per;
+    const uint32_t hi = min(lo + per, n);
+    uint32_t cnt = 0;
+    for (uint32_t i = lo; i < hi; ++i) cnt += !(v[i] & 1u);
+    scan[threadIdx.x] = cnt;
+    __syncthreads();
+    for (uint32_t off = 1; off < kPoolThreads; off <<= 1) {
+        const uint32_t add = threadIdx.x >= off ? scan[threadIdx.x - off] : 0u;
+        __syncthreads();
+        scan[threadIdx.x] += add;
+        __syncthreads();
+    }
+    const uint32_t n_neg = scan[kPoolThreads - 1];
+    uint32_t before = scan[threadIdx.x] - cnt;
+    for (uint32_t i = lo; i < hi; ++i) {
+        const uint64_t x = v[i];
+        v[i] = (x & ~0xFFFFFFFFull) | (static_cast<uint64_t>(before) << 1) | (x & 1u);
+        before += !(x & 1u);
+    }
+    __syncthreads();
+
+    // Positives: negatives strictly below the key, and inside its tie group.
+    unsigned long long gp = 0, ep = 0;
+    for (uint32_t i = threadIdx.x; i < n; i += kPoolThreads) {
+        const uint64_t x = v[i];
+        if (!(x & 1u)) continue;
+        const uint32_t key = static_cast<uint32_t>(x >> 32);
+        uint32_t a = 0, b = n;  // first index with key >= this key
+        while (a < b) {
+            const uint32_t m = (a + b) >> 1;
+            if (static_cast<uint32_t>(v[m] >> 32) < key) a = m + 1; else b = m;
+        }
+        const uint32_t first = a;
+        a = first;
+        b = n;  // first index with key > this key
+        while (a < b) {
+            const uint32_t m = (a + b) >> 1;
+            if (static_cast<uint32_t>(v[m] >> 32) <= key) a = m + 1; else b = m;
+        }
+        const uint32_t last = a;
+        const uint32_t neg_lt = first < n ? static_cast<uint32_t>((v[first] >> 1) & 0x7FFFFFFFu) : n_neg;
+        const uint32_t neg_le = last < n ? static_cast<uint32_t>((v[last] >> 1) & 0x7FFFFFFFu) : n_neg;
+        gp += neg_lt;
+        ep += neg_le - neg_lt;
+    }
+    gp = wave_sum(gp);
+    ep = wave_sum(ep);
+    const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    if (lane == 0) {
+        red[0][wave] = gp;
+        red[1][wave] = ep;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long G = 0, E = 0;
+        for (int w = 0; w < kPoolThreads / kWave; ++w) {
+            G += red[0][w];
+            E += red[1][w];
+        }
+        const unsigned long long n_pos = static_cast<unsigned long long>(n) - n_neg;
+        unsigned long long* out = pooled + 3ull * blockIdx.x;
+        out[0] = G;
+        out[1] = E;
+        out[2] = n_pos * n_neg;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float* scores,
+                        uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
+                        hipStream_t st) {
+    if (n_cfg == 0) return hipSuccess;
+    const Key key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)};
+    hipLaunchKernelGGL(auroc_counts_kernel, dim3(n_cfg), dim3(kCountThreads), 0, st, cfgs_dev,
+                       scores, key, flags, reinterpret_cast<unsigned long long*>(counts));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !(flags & 2u)) return e;
+    hipLaunchKernelGGL(auroc_pooled_kernel, dim3(n_cfg), dim3(kPoolThreads), 0, st, cfgs_dev,
+                       scores, reinterpret_cast<unsigned long long*>(pooled));
+    return hipGetLastError();
+}
+
+}  // namespace cdt

@@ -1,0 +1,143 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments before any device work."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from tests.conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "cdt.h")
+
+
+@pytest.fixture(scope="module")
+def cdt():
+    from paper_2607_19490_amd import build, cdt as binding
+    if not os.path.exists(binding.LIB_PATH):
+        build.build()
+    binding.lib()
+    return binding
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cdt_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declarations_are_exported(cdt):
+    names = _declared()
+    assert "cdt_drift_score" in names and "cdt_canary_sim" in names and "cdt_auroc" in names
+    L = cdt.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(names) == sorted(cdt.exported_symbols())
+
+
+def test_version_and_sizes(cdt):
+    L = cdt.lib()
+    assert L.cdt_version() == 1
+    assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 16
+    assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 16
+    assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
+    assert L.cdt_auroc_workspace_bytes(216) == 216 * 32
+
+
+def test_struct_layouts_match_the_header(cdt, tmp_path):
+    """Compile the header with the host C compiler and compare every field
+    offset and struct size with the ctypes mirrors of the binding."""
+    src = tmp_path / "layout.c"
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "cdt.h"', "int main(void){"]
+    for cname, py in (("cdt_sim_params", cdt.SimParams), ("cdt_auroc_cfg", cdt.AurocCfg)):
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in py._fields_:
+            lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines.append("return 0;}")
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out.strip().splitlines()}
+    for cname, py in (("cdt_sim_params", cdt.SimParams), ("cdt_auroc_cfg", cdt.AurocCfg)):
+        assert got[(cname, "size")] == ctypes.sizeof(py)
+        for f, _ in py._fields_:
+            assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
+
+
+def _err(cdt):
+    return cdt.lib().cdt_last_error().decode()
+
+
+def test_shape_and_pointer_validation(cdt):
+    L = cdt.lib()
+    assert L.cdt_drift_score(2, 2, 3, 12, None, None, None, None, None, 0, None) == cdt.EINVAL
+    assert "multiple of 8" in _err(cdt)
+    assert L.cdt_drift_score(2, 2, 1 << 16, 1 << 16, 16, 16, 16, None, 16, 1 << 40, None) == cdt.ELIMIT
+    assert L.cdt_drift_score(2, 2, 3, 16, None, None, 16, None, 16, 1 << 20, None) == cdt.EINVAL
+    assert L.cdt_drift_score(2, 2, 3, 16, 8, 16, 16, None, 16, 1 << 20, None) == cdt.EALIGN
+    # workspace too small
+    assert L.cdt_drift_score(2, 2, 3, 16, 16, 16, 16, None, 16, 15, None) == cdt.EINVAL
+    assert "workspace" in _err(cdt)
+    # empty shapes are accepted without touching the device
+    assert L.cdt_drift_score(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
+    assert L.cdt_ref_synth(2, 0, 3, 16, 0, 0, None, None, None) == cdt.OK
+    assert L.cdt_ref_synth(2, 2, 3, 16, 0, 1 << 24, 16, 16, None) == cdt.ELIMIT
+
+
+def test_sim_param_validation(cdt):
+    L = cdt.lib()
+
+    def call(S=4, **kw):
+        base = dict(seed=0, cfg_id=0, sigma_b=1e-3)
+        base.update(kw)
+        tscale = base.pop("tscale_ptr", 16)
+        p = cdt.sim_params(**base)
+        p.tscale = tscale
+        return L.cdt_canary_sim(S, 2, 2, 16, ctypes.byref(p), 16, 16, None)
+
+    assert call(S=65) == cdt.ELIMIT
+    assert call(cfg_id=1 << 24) == cdt.ELIMIT
+    assert call(benign_mode=2) == cdt.EINVAL
+    assert call(benign_dist=2) == cdt.EINVAL
+    assert call(tamper=8) == cdt.EINVAL
+    assert call(sigma_b=-1.0) == cdt.EINVAL
+    assert call(sigma_b=float("nan")) == cdt.EINVAL
+    assert call(flip_p=1.5) == cdt.EINVAL
+    assert call(scale=float("inf")) == cdt.EINVAL
+    assert call(benign_mode=1) == cdt.EINVAL  # BLOCK noise without bscale
+    assert "bscale" in _err(cdt)
+    assert call(mal_mask=1, tamper=1, tscale_ptr=None) == cdt.EINVAL
+    p = cdt.sim_params(seed=0, cfg_id=0)
+    p.reserved = 1
+    assert L.cdt_canary_sim(4, 2, 2, 16, ctypes.byref(p), 16, 16, None) == cdt.EINVAL
+    assert L.cdt_canary_sim(4, 2, 2, 16, None, 16, 16, None) == cdt.EINVAL
+
+
+def test_auroc_validation(cdt):
+    L = cdt.lib()
+    arr, n = cdt.auroc_cfg_array([(65, 4, 0, 1, 0)])
+    assert L.cdt_auroc(n, arr, 16, 1000, 0, 0, 16, None, 16, 64, None) == cdt.ELIMIT
+    arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0), (8, 4, 30, 1, 1)])
+    assert L.cdt_auroc(n, arr, 16, 60, 0, 0, 16, None, 16, 64, None) == cdt.EINVAL
+    assert "outside" in _err(cdt)
+    arr, n = cdt.auroc_cfg_array([(64, 300, 0, 1, 0)])
+    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 2, 16, 16, 16, 64, None) == cdt.ELIMIT
+    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 2, 16, None, 16, 64, None) == cdt.EINVAL
+    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 8, 16, None, 16, 64, None) == cdt.EINVAL
+    arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0)])
+    assert L.cdt_auroc(n, arr, 16, 32, 0, 0, 16, None, 16, 31, None) == cdt.EINVAL
+    assert L.cdt_auroc(0, arr, None, 0, 0, 0, None, None, None, 0, None) == cdt.OK
+
+
+def test_scale_and_outlier_validation(cdt):
+    L = cdt.lib()
+    assert L.cdt_block_scales(4, 2, 8, 16, 16, -1.0, 0.0, 16, 16, None) == cdt.EINVAL
+    assert L.cdt_block_scales(4, 2, 8, None, 16, 0.1, 0.0, 16, None, None) == cdt.EINVAL
+    assert L.cdt_block_scales(0, 2, 8, None, None, 0.1, 0.0, 16, None, None) == cdt.OK
+    assert L.cdt_outlier_gain(40000, 1, 20.0, 0, 0, 16, None) == cdt.ELIMIT
+    assert L.cdt_outlier_gain(16, 17, 20.0, 0, 0, 16, None) == cdt.EINVAL
+    assert L.cdt_outlier_gain(16, 1, 20.0, 0, 0, None, None) == cdt.EINVAL
+    assert L.cdt_outlier_gain(0, 0, 20.0, 0, 0, None, None) == cdt.OK

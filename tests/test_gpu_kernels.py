@@ -1,0 +1,239 @@
+"""GPU parity of every libcdt kernel against the CPU oracle, through the C ABI.
+
+Bar: bit-exact for generated activations (fp32 references, fp16 live
+activations), outlier channels and AUROC counts; 1e-5 relative for drift
+scores (Eq. 4); the fp64 sums within the bound of two n-term fp64 sums.  Shapes span several
+chunks, ragged tails, single-element blocks and empty inputs.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_19490_amd import inputs
+from tests.gpu_util import announce, h_bits, rel_err, require_gpu, to_dev, ulp_diff_f32
+
+pytestmark = pytest.mark.gpu
+
+DRIFT_RTOL = 1e-5  # tolerance stated for drift scores
+
+# (S, C, T, H): tiny, ragged (T*H not a multiple of any chunk), multi-chunk
+# with a partial last chunk, and single-group blocks
+SHAPES = [(4, 8, 16, 256), (3, 5, 7, 264), (2, 3, 41, 1000), (5, 2, 1, 8), (1, 1, 130, 8192)]
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    return require_gpu()
+
+
+# ----------------------------------------------------------------------------
+# generator
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("H,n_out", [(8, 1), (256, 0), (264, 3), (4096, 41), (8192, 82)])
+def test_outlier_gain(gpu, H, n_out):
+    torch, cdt = gpu
+    announce(f"outlier_gain H={H} n_out={n_out}")
+    g = cdt.outlier_gain(H, n_out, 20.0, 7, 3)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(g.cpu().numpy(), oracle.outlier_gain(H, n_out, 20.0, 7, 3))
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_ref_synth(gpu, shape):
+    torch, cdt = gpu
+    S, C, T, H = shape
+    announce(f"ref_synth {shape}")
+    gain = oracle.outlier_gain(H, max(1, H // 100), 20.0, 1, 2)
+    ref = cdt.ref_synth(S, C, T, H, 11, 2, to_dev(torch, gain))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ref.cpu().numpy(), oracle.ref_synth(S, C, T, H, 11, 2, gain))
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_ref_stats_and_block_scales(gpu, shape):
+    torch, cdt = gpu
+    S, C, T, H = shape
+    announce(f"ref_stats {shape}")
+    ref = oracle.ref_synth(S, C, T, H, 5, 0, oracle.outlier_gain(H, 1, 20.0, 5, 0))
+    q, m = cdt.ref_stats(to_dev(torch, ref))
+    torch.cuda.synchronize()
+    q_o, m_o = oracle.ref_stats(ref)
+    tol = max(1e-14, 2 * T * H * 2.0**-53)  # two fp64 sums of n non-negative terms
+    assert rel_err(q.cpu().numpy(), q_o) < tol
+    assert rel_err(m.cpu().numpy(), m_o) < tol
+    # block scales from identical fp64 statistics: same fp32 result
+    ts, bs = cdt.block_scales(to_dev(torch, q_o), to_dev(torch, m_o), T, H, 0.05, 2e-3)
+    torch.cuda.synchronize()
+    ts_o, bs_o = oracle.block_scales(T, H, q_o, m_o, 0.05, 2e-3)
+    assert ulp_diff_f32(ts.cpu().numpy(), ts_o).max() == 0
+    assert ulp_diff_f32(bs.cpu().numpy(), bs_o).max() == 0
+
+
+SIM_CASES = {
+    "gauss_add": dict(sigma_b=1e-3, tamper=1, eps=0.05),
+    "t3_flip": dict(benign_dist=1, sigma_b=2e-2, tamper=2, flip_p=0.3),
+    "block_scale": dict(benign_mode=1, sigma_b=2e-3, tamper=4, scale=1.05),
+    "mixed": dict(sigma_b=1e-4, tamper=7, eps=0.1, flip_p=0.1, scale=1.1),
+    "mixed_clean": dict(sigma_b=1e-2, tamper=7, eps=0.02, flip_p=0.02, scale=1.02,
+                        tamper_base=1),
+    "full_flip": dict(benign_mode=1, sigma_b=2e-3, tamper=2, flip_p=1.0),
+    "t3_block_add": dict(benign_mode=1, benign_dist=1, sigma_b=0.1, tamper=1, eps=0.2),
+    "no_noise": dict(sigma_b=0.0, tamper=0),
+}
+
+
+@pytest.mark.parametrize("case", sorted(SIM_CASES))
+@pytest.mark.parametrize("shape", SHAPES[:3] + [(64, 2, 3, 16)])
+def test_canary_sim(gpu, case, shape):
+    torch, cdt = gpu
+    S, C, T, H = shape
+    kw = dict(SIM_CASES[case])
+    announce(f"canary_sim {case} {shape}")
+    eps = kw.pop("eps", 0.0)
+    gain = oracle.outlier_gain(H, max(1, H // 100), 20.0, 3, 1)
+    ref = oracle.ref_synth(S, C, T, H, 3, 1, gain)
+    q, m = oracle.ref_stats(ref)
+    ts, bs = oracle.block_scales(T, H, q, m, eps, kw.get("sigma_b", 0.0))
+    mal = (1 << (S // 2)) | (1 << (S - 1))  # two colluders
+    h = cdt.canary_sim(to_dev(torch, ref), seed=0xDEADBEEF12345, cfg_id=77, mal_mask=mal,
+                       bscale=to_dev(torch, bs), tscale=to_dev(torch, ts), **kw)
+    torch.cuda.synchronize()
+    want = oracle.canary_sim(ref, seed=0xDEADBEEF12345, cfg_id=77, mal_mask=mal, bscale=bs,
+                             tscale=ts, **kw)
+    got = h_bits(h)
+    bad = int((got != want).sum())
+    assert bad == 0, f"{bad} of {want.size} fp16 words differ"
+
+
+# ----------------------------------------------------------------------------
+# Eq. 4
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("shape", SHAPES + [(16, 4, 4, 32768)])
+def test_drift_score(gpu, shape):
+    torch, cdt = gpu
+    S, C, T, H = shape
+    announce(f"drift_score {shape}")
+    a = inputs.ref_normal(shape, seed=S * 1000 + H, outlier_frac=0.01)
+    h = inputs.live_near(a, seed=7, rel=1e-3, flip_frac=0.001)
+    nd = torch.empty((C, S, 2), dtype=torch.float64, device="cuda")
+    sc = cdt.drift_score(to_dev(torch, h).view(torch.float16), to_dev(torch, a), num_den=nd)
+    torch.cuda.synchronize()
+    s64, s32, nd_o = oracle.drift_score(h, a)
+    assert rel_err(sc.cpu().numpy(), s64) < DRIFT_RTOL
+    # both sides add n non-negative fp64 terms (in different orders): each
+    # sum is within (n - 1) 2^-53 of the exact one, relative
+    assert rel_err(nd.cpu().numpy(), nd_o) < max(1e-14, 2 * T * H * 2.0**-53)
+    assert ulp_diff_f32(sc.cpu().numpy(), s32).max() <= 1
+
+
+def test_drift_exact_special_cases(gpu):
+    """h = a gives 0, h = -a gives 2, h = 2a gives 1, h = 0 gives 1, exactly."""
+    torch, cdt = gpu
+    S, C, T, H = 4, 3, 33, 72
+    announce("drift exact cases")
+    a16 = inputs.fp16_bits(inputs.ref_normal((1, C, T, H), seed=1))
+    a = a16.view(np.float16).astype(np.float32)
+    ref = np.concatenate([a] * S)
+    h = np.concatenate([a16, inputs.fp16_bits(-a), inputs.fp16_bits(2 * a),
+                        np.zeros_like(a16)])
+    sc = cdt.drift_score(to_dev(torch, h).view(torch.float16), to_dev(torch, ref))
+    torch.cuda.synchronize()
+    got = sc.cpu().numpy()
+    np.testing.assert_array_equal(got, np.tile(np.array([0.0, 2.0, 1.0, 1.0], np.float32), (C, 1)))
+
+
+def test_drift_degenerate_and_empty(gpu):
+    torch, cdt = gpu
+    announce("drift degenerate")
+    # all-zero reference blocks: 0 when h = 0 too, +inf otherwise
+    ref = np.zeros((2, 2, 1, 8), np.float32)
+    h = np.zeros((2, 2, 1, 8), np.uint16)
+    h[1, 0, 0, 3] = inputs.fp16_bits(np.float32(0.5))
+    sc = cdt.drift_score(to_dev(torch, h).view(torch.float16), to_dev(torch, ref))
+    torch.cuda.synchronize()
+    got = sc.cpu().numpy()
+    assert got[0, 1] == np.inf and got[0, 0] == 0 and got[1, 0] == 0 and got[1, 1] == 0
+    # empty blocks (T = 0) score 0; empty shard/canary sets write nothing
+    sc = cdt.drift_score(torch.empty((3, 2, 0, 16), dtype=torch.float16, device="cuda"),
+                         torch.empty((3, 2, 0, 16), dtype=torch.float32, device="cuda"))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(sc.cpu().numpy(), np.zeros((2, 3), np.float32))
+    sc = cdt.drift_score(torch.empty((0, 2, 4, 16), dtype=torch.float16, device="cuda"),
+                         torch.empty((0, 2, 4, 16), dtype=torch.float32, device="cuda"))
+    torch.cuda.synchronize()
+    assert sc.shape == (2, 0)
+
+
+def test_drift_deterministic(gpu):
+    """No atomics: two runs give bitwise-equal scores and sums."""
+    torch, cdt = gpu
+    announce("drift determinism")
+    shape = (8, 16, 64, 4096)
+    a = to_dev(torch, inputs.ref_normal(shape, seed=3, outlier_frac=0.01))
+    h = to_dev(torch, inputs.live_near(a.cpu().numpy(), seed=4)).view(torch.float16)
+    nd1 = torch.empty((16, 8, 2), dtype=torch.float64, device="cuda")
+    nd2 = torch.empty_like(nd1)
+    s1 = cdt.drift_score(h, a, num_den=nd1)
+    s2 = cdt.drift_score(h, a, num_den=nd2)
+    torch.cuda.synchronize()
+    assert torch.equal(s1, s2) and torch.equal(nd1, nd2)
+
+
+# ----------------------------------------------------------------------------
+# Eqs. 5-6
+# ----------------------------------------------------------------------------
+def _auroc_batch():
+    """A batch of score tables: ties, NaNs, S = 1 and 64, colluders, C = 0."""
+    cases = [
+        (8, 32, (4,), dict(gap=0.3)),
+        (16, 64, (8,), dict(gap=0.0, tie_levels=6)),
+        (64, 256, (3, 17, 40, 63), dict(gap=0.05, nan_frac=0.02)),
+        (32, 32, (16,), dict(gap=1.0)),
+        (1, 5, (0,), dict()),
+        (5, 0, (2,), dict()),
+        (12, 100, (5,), dict(gap=-0.2, tie_levels=3)),
+        (4, 7, (), dict()),
+        (64, 16, tuple(range(64)), dict()),
+    ]
+    tables, cfgs, off = [], [], 0
+    for k, (S, C, pos, kw) in enumerate(cases):
+        t = inputs.scores(C, S, seed=100 + k, mal=pos, **kw)
+        mask = 0
+        for s in pos:
+            mask |= 1 << s
+        tables.append(t)
+        cfgs.append((S, C, off, mask, 1000 + k))
+        off += t.size
+    return tables, cfgs
+
+
+@pytest.mark.parametrize("flags", [0, 1, 3, 7])
+def test_auroc_counts(gpu, flags):
+    torch, cdt = gpu
+    announce(f"auroc flags={flags}")
+    tables, cfgs = _auroc_batch()
+    flat = np.concatenate([t.ravel() for t in tables]).astype(np.float32)
+    counts, pooled = cdt.auroc(cfgs, to_dev(torch, flat), seed=42, flags=flags)
+    torch.cuda.synchronize()
+    got = cdt.u64(counts)
+    got_p = cdt.u64(pooled) if pooled is not None else None
+    for g, (t, (S, C, off, mask, cid)) in enumerate(zip(tables, cfgs)):
+        want, want_p = oracle.auroc_config(t, mask, seed=42, cfg_id=cid, flags=flags)
+        np.testing.assert_array_equal(got[g], want, err_msg=f"cfg {g} S={S} C={C}")
+        if flags & 2:
+            np.testing.assert_array_equal(got_p[g], want_p, err_msg=f"pooled cfg {g}")
+
+
+def test_auroc_pooled_at_capacity(gpu):
+    torch, cdt = gpu
+    announce("auroc pooled 64x256")
+    S, C = 64, 256
+    t = inputs.scores(C, S, seed=9, mal=(10, 20), gap=0.01, tie_levels=50)
+    counts, pooled = cdt.auroc([(S, C, 0, (1 << 10) | (1 << 20), 3)], to_dev(torch, t.ravel()),
+                               seed=1, flags=3)
+    torch.cuda.synchronize()
+    want, want_p = oracle.auroc_config(t, (1 << 10) | (1 << 20), seed=1, cfg_id=3, flags=3)
+    np.testing.assert_array_equal(cdt.u64(counts)[0], want)
+    np.testing.assert_array_equal(cdt.u64(pooled)[0], want_p)

@@ -1,0 +1,306 @@
+"""The detector end to end at the workloads' full sizes, in the launch
+configuration the benchmark times, checked against the CPU oracle.
+
+At sizes the oracle cannot regenerate whole, sampled (shard, canary) blocks
+are regenerated one by one and compared bit for bit (references, block
+scales, live fp16 activations) and within 1e-5 (drift scores); AUROC counts
+are checked by properties that hold at any size (pair counts, the detector
+at 1.0 where the tamper dwarfs the noise floor, the scrambled-label control
+inside the pre-registered window).  Small configurations of the sweep and
+the paper's own shape are compared whole, counts included.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_19490_amd import workloads as W
+from tests.gpu_util import announce, h_bits, rel_err, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+DRIFT_RTOL = 1e-5
+NEAR_TIE = 2e-5
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    return require_gpu()
+
+
+@pytest.fixture(scope="module")
+def gold():
+    with open(os.path.join(GOLDEN, "paper_outcomes.json")) as f:
+        return json.load(f)
+
+
+class GpuSet:
+    """One reference set on the device, as the benchmark prepares it."""
+
+    def __init__(self, torch, cdt, wl, rs, h=None):
+        self.torch, self.cdt, self.wl, self.rs = torch, cdt, wl, rs
+        S, C, T, H = rs.S, rs.C, rs.T, rs.H
+        self.gain = cdt.outlier_gain(H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
+        self.ref = cdt.ref_synth(S, C, T, H, wl.seed, rs.ref_set_id, self.gain)
+        self.ws = cdt.workspace(S, C, T, H, self.ref)
+        self.sumsq, self.sumabs = cdt.ref_stats(self.ref, ws=self.ws)
+        self.h = torch.empty((S, C, T, H), dtype=torch.float16, device="cuda") if h is None else h
+
+    def run(self, run, score=None):
+        ts, bs = self.cdt.block_scales(self.sumsq, self.sumabs, self.rs.T, self.rs.H, run.eps,
+                                       run.sigma_b)
+        self.cdt.canary_sim(self.ref, out=self.h, seed=self.wl.seed, cfg_id=run.cfg_id,
+                            benign_mode=run.benign_mode, benign_dist=run.benign_dist,
+                            sigma_b=run.sigma_b, mal_mask=self.rs.mal_mask, tamper=run.tamper,
+                            tamper_base=run.tamper_base, flip_p=run.flip_p, scale=run.scale,
+                            bscale=bs, tscale=ts)
+        score = self.cdt.drift_score(self.h, self.ref, out=score, ws=self.ws)
+        return score, ts, bs
+
+
+def sample_blocks(rs, k=4, seed=0):
+    g = np.random.default_rng(seed + rs.S * 7 + rs.H)
+    shards = sorted({0, rs.S - 1, *rs.mal_shards, int(g.integers(rs.S))})
+    blocks = []
+    for i, s in enumerate(shards[:k]):
+        c = int(g.integers(rs.C)) if i else rs.C - 1
+        blocks.append((s, c))
+    return blocks
+
+
+def check_blocks(gs, run, score, ts, bs, blocks, gain_o):
+    """Regenerate sampled blocks with the oracle and compare."""
+    torch, rs, wl = gs.torch, gs.rs, gs.wl
+    sc = score.cpu().numpy()
+    ts_d, bs_d = ts.cpu().numpy(), bs.cpu().numpy()
+    for s, c in blocks:
+        announce(f"{wl.name} run {run.label} block ({s},{c})")
+        ref_o = oracle.ref_block(s, c, rs.T, rs.H, wl.seed, rs.ref_set_id, gain_o)
+        np.testing.assert_array_equal(gs.ref[s, c].cpu().numpy(), ref_o)
+        q, m = oracle.ref_stats_block(ref_o)
+        ts_o, bs_o = oracle.block_scales(rs.T, rs.H, np.array([q]), np.array([m]), run.eps,
+                                         run.sigma_b)
+        assert ts_d[s, c] == ts_o[0] and bs_d[s, c] == bs_o[0]
+        h_o = oracle.sim_block(s, c, ref_o, seed=wl.seed, cfg_id=run.cfg_id,
+                               benign_mode=run.benign_mode, benign_dist=run.benign_dist,
+                               sigma_b=run.sigma_b, bscale=bs_o[0],
+                               malicious=s in rs.mal_shards, tamper=run.tamper,
+                               tamper_base=run.tamper_base, tscale=ts_o[0], flip_p=run.flip_p,
+                               scale=run.scale)
+        got = gs.h[s, c].cpu().numpy().view(np.uint16)
+        assert int((got != h_o).sum()) == 0
+        m_o, _, _ = oracle.drift_block(h_o, ref_o)
+        assert rel_err(sc[c, s], m_o) < DRIFT_RTOL
+
+
+def counts_match(got, scores64, mask, seed, cfg_id):
+    """End-to-end count parity: exact, except for pairs whose oracle scores
+    lie within NEAR_TIE of each other (where fp32 rounding may order them
+    either way)."""
+    want, want_p = oracle.auroc_config(scores64.astype(np.float32), mask, seed=seed, cfg_id=cfg_id)
+    if np.array_equal(got[:6], want):
+        return True
+    C, S = scores64.shape
+    amb = 0
+    for t in range(C):
+        row = scores64[t]
+        for i in range(S):
+            for j in range(i + 1, S):
+                if abs(row[i] - row[j]) <= NEAR_TIE * max(abs(row[i]), abs(row[j])):
+                    amb += 1
+    diff = int(np.abs(got[:6].astype(np.int64) - want.astype(np.int64)).sum())
+    return diff <= 2 * amb
+
+
+def detector_properties(cdt, counts, cfgs):
+    c = cdt.u64(counts)
+    for g, (S, C, off, mask, cid) in enumerate(cfgs):
+        n_pos = bin(mask).count("1")
+        assert int(c[g][2]) == C * n_pos * (S - n_pos)
+        assert int(c[g][5]) == C * (S - n_pos - 1)
+        assert int(c[g][0]) + int(c[g][1]) <= int(c[g][2])
+    return c
+
+
+# ----------------------------------------------------------------------------
+def _single_set_workload(gpu, name, nsample=4):
+    torch, cdt = gpu
+    wl = W.get(name)
+    rs = wl.ref_sets[0]
+    announce(f"{name}: preparing {rs.S}x{rs.C}x{rs.T}x{rs.H}")
+    gs = GpuSet(torch, cdt, wl, rs)
+    gain_o = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
+    np.testing.assert_array_equal(gs.gain.cpu().numpy(), gain_o)
+    scores, cfgs = [], []
+    for k, run in enumerate(rs.runs):
+        score, ts, bs = gs.run(run)
+        torch.cuda.synchronize()
+        if k < 6 or k % 10 == 0 or k == len(rs.runs) - 1:
+            check_blocks(gs, run, score, ts, bs, sample_blocks(rs, nsample, k), gain_o)
+        scores.append(score)
+        cfgs.append((rs.S, rs.C, k * rs.C * rs.S, rs.mal_mask, run.cfg_id))
+    flat = torch.cat([s.reshape(-1) for s in scores])
+    counts, pooled = cdt.auroc(cfgs, flat, seed=wl.seed)
+    torch.cuda.synchronize()
+    c = detector_properties(cdt, counts, cfgs)
+    del gs, flat, scores
+    torch.cuda.empty_cache()
+    return wl, rs, c, cdt.u64(pooled)
+
+
+def test_llama7b(gpu):
+    wl, rs, c, _ = _single_set_workload(gpu, "llama7b")
+    for g in range(len(rs.runs)):
+        assert int(c[g][0]) == int(c[g][2]), rs.runs[g].label  # detector at 1.0
+
+
+def test_llama70b(gpu):
+    wl, rs, c, pooled = _single_set_workload(gpu, "llama70b")
+    for g, run in enumerate(rs.runs):
+        assert int(c[g][0]) == int(c[g][2]), run.label
+        a_ctrl = int(c[g][3]) / int(c[g][5])
+        # per canary the scrambled stage's rank among the B benign stages is
+        # uniform, so A_ctrl(t) is uniform on {0, 1/(B-1), ..., 1}: variance
+        # (B^2 - 1) / (12 (B - 1)^2); five standard deviations of the mean
+        B = rs.S - len(rs.mal_shards)
+        sd = math.sqrt((B * B - 1) / 12.0) / (B - 1) / math.sqrt(rs.C)
+        assert abs(a_ctrl - 0.5) < 5 * sd, a_ctrl
+        assert int(pooled[g][0]) == int(pooled[g][2])  # pooled ranking separates fully too
+
+
+def test_snr_curve(gpu):
+    wl, rs, c, _ = _single_set_workload(gpu, "snr", nsample=2)
+    auc = [(int(x[0]) + 0.5 * int(x[1])) / int(x[2]) for x in c]
+    gauss = auc[0::2]
+    t3 = auc[1::2]
+    assert gauss[0] == 1.0 and t3[0] == 1.0  # noise floor far below the tamper
+    assert gauss[-1] < gauss[0] and t3[-1] < t3[0]  # the floor crosses the tamper
+    assert min(auc) >= 0.0 and max(auc) <= 1.0
+
+
+def test_sweep(gpu, gold):
+    """All 216 runs as the benchmark launches them; three small runs compared
+    whole with the oracle (scores and counts), a large one by sampled blocks;
+    the pre-registered criteria on the batch."""
+    torch, cdt = gpu
+    wl = W.sweep()
+    max_elems = max(rs.elems for rs in wl.ref_sets)
+    h_buf = torch.empty((max_elems,), dtype=torch.float16, device="cuda")
+    scores, cfgs, off = [], [], 0
+    whole = {0, 13, 23}  # add/flip/scale/mixed mix on the smallest set
+    whole_scores = {}
+    for rs in wl.ref_sets:
+        announce(f"sweep set {rs.ref_set_id}: {rs.S}x{rs.C}x{rs.T}x{rs.H}")
+        gs = GpuSet(torch, cdt, wl, rs, h=h_buf[:rs.elems].view(rs.S, rs.C, rs.T, rs.H))
+        gain_o = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
+        ref_o = oracle.ref_synth(rs.S, rs.C, rs.T, rs.H, wl.seed, rs.ref_set_id, gain_o) \
+            if rs.ref_set_id == 0 else None
+        for run in rs.runs:
+            score, ts, bs = gs.run(run)
+            torch.cuda.synchronize()
+            if run.cfg_id in whole:
+                announce(f"sweep cfg {run.cfg_id} whole")
+                q, m = oracle.ref_stats(ref_o)
+                ts_o, bs_o = oracle.block_scales(rs.T, rs.H, q, m, run.eps, run.sigma_b)
+                h_o = oracle.canary_sim(ref_o, seed=wl.seed, cfg_id=run.cfg_id,
+                                        sigma_b=run.sigma_b, mal_mask=rs.mal_mask,
+                                        tamper=run.tamper, tscale=ts_o, flip_p=run.flip_p,
+                                        scale=run.scale)
+                assert np.array_equal(gs.h.cpu().numpy().view(np.uint16), h_o)
+                s64, _, _ = oracle.drift_score(h_o, ref_o)
+                assert rel_err(score.cpu().numpy(), s64) < DRIFT_RTOL
+                whole_scores[run.cfg_id] = s64
+            if rs.ref_set_id == len(wl.ref_sets) - 1 and run.cfg_id % 24 in (3, 14):
+                check_blocks(gs, run, score, ts, bs, sample_blocks(rs, 2, run.cfg_id), gain_o)
+            scores.append(score.clone())
+            cfgs.append((rs.S, rs.C, off, rs.mal_mask, run.cfg_id))
+            off += rs.S * rs.C
+        del gs
+    flat = torch.cat([s.reshape(-1) for s in scores])
+    counts, _ = cdt.auroc(cfgs, flat, seed=wl.seed)
+    torch.cuda.synchronize()
+    c = detector_properties(cdt, counts, cfgs)
+    for cid, s64 in whole_scores.items():
+        g = [k for k, x in enumerate(cfgs) if x[4] == cid][0]
+        assert counts_match(c[g], s64, cfgs[g][3], wl.seed, cid), cid
+    strict = [int(x[0]) / int(x[2]) for x in c]
+    assert min(strict) >= gold["success_auroc"]["value"]
+    assert sum(1 for a in strict if a == 1.0) == len(strict)
+    ctrl = np.mean([int(x[3]) / int(x[5]) for x in c])
+    lo, hi = gold["control_window"]["value"]
+    assert lo <= ctrl <= hi
+    del h_buf, flat, scores
+    torch.cuda.empty_cache()
+
+
+def test_paper_shape(gpu, gold):
+    """12 stages x 100 canaries x 48 tokens x d = 768 with block-scaled noise
+    at sigma_hw = 0.002: every one of the six attacks at AUROC 1.0, the
+    Gaussian 0.02 run compared whole with the oracle, counts included."""
+    torch, cdt = gpu
+    wl = W.paper()
+    rs = wl.ref_sets[0]
+    gs = GpuSet(torch, cdt, wl, rs)
+    gain_o = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
+    ref_o = oracle.ref_synth(rs.S, rs.C, rs.T, rs.H, wl.seed, rs.ref_set_id, gain_o)
+    np.testing.assert_array_equal(gs.ref.cpu().numpy(), ref_o)
+    q, m = oracle.ref_stats(ref_o)
+    for k, run in enumerate(rs.runs):
+        announce(f"paper run {run.label}")
+        score, ts, bs = gs.run(run)
+        counts, _ = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, run.cfg_id)], score, seed=wl.seed)
+        torch.cuda.synchronize()
+        c = cdt.u64(counts)[0]
+        assert int(c[0]) == int(c[2]) == rs.C * (rs.S - 1), run.label
+        if k == 0:
+            ts_o, bs_o = oracle.block_scales(rs.T, rs.H, q, m, run.eps, run.sigma_b)
+            h_o = oracle.canary_sim(ref_o, seed=wl.seed, cfg_id=run.cfg_id,
+                                    benign_mode=run.benign_mode, sigma_b=run.sigma_b, bscale=bs_o,
+                                    mal_mask=rs.mal_mask, tamper=run.tamper, tscale=ts_o)
+            assert np.array_equal(gs.h.cpu().numpy().view(np.uint16), h_o)
+            s64, _, _ = oracle.drift_score(h_o, ref_o)
+            assert rel_err(score.cpu().numpy(), s64) < DRIFT_RTOL
+            assert counts_match(c, s64, rs.mal_mask, wl.seed, run.cfg_id)
+        else:
+            check_blocks(gs, run, score, ts, bs, sample_blocks(rs, 2, k), gain_o)
+    del gs
+    torch.cuda.empty_cache()
+
+
+def test_largest_block(gpu):
+    """One block of T*H = 2^32 - 2^19 elements (just under the 2^32 limit):
+    generated elements past 2^31 match the oracle, and Eq. 4 on a block whose
+    difference is known exactly gives the exact sums."""
+    torch, cdt = gpu
+    T, H = 1 << 16, (1 << 16) - 8
+    n = T * H
+    announce(f"largest block n={n}")
+    gain = torch.ones((H,), dtype=torch.float32, device="cuda")
+    ref = cdt.ref_synth(1, 1, T, H, 5, 9, gain)
+    h = cdt.canary_sim(ref, seed=5, cfg_id=9, sigma_b=1e-2, mal_mask=1, tamper=2, flip_p=0.25)
+    torch.cuda.synchronize()
+    ones = np.ones(H, np.float32)
+    for e0 in (0, (1 << 31) - 3 * 8, (1 << 31) + 1000 * 8, n - 4096):
+        ref_o = oracle.ref_range(0, 0, H, e0, 4096, 5, 9, ones)
+        np.testing.assert_array_equal(ref.view(-1)[e0:e0 + 4096].cpu().numpy(), ref_o)
+        h_o = oracle.sim_range(0, 0, e0, ref_o, seed=5, cfg_id=9, sigma_b=1e-2, malicious=True,
+                               tamper=2, flip_p=0.25)
+        np.testing.assert_array_equal(h.view(-1)[e0:e0 + 4096].cpu().numpy().view(np.uint16), h_o)
+    # exact drift: a = 1 everywhere, h = 1 except k scattered elements = 2
+    ref.fill_(1.0)
+    h.fill_(1.0)
+    idx = torch.tensor([0, 12345, (1 << 31) - 1, 1 << 31, (1 << 31) + 77, n - 9, n - 1],
+                       dtype=torch.int64, device="cuda")
+    h.view(-1)[idx] = 2.0
+    nd = torch.empty((1, 1, 2), dtype=torch.float64, device="cuda")
+    sc = cdt.drift_score(h, ref, num_den=nd)
+    torch.cuda.synchronize()
+    D, R = nd.cpu().numpy().ravel()
+    assert D == float(idx.numel()) and R == float(n)
+    assert sc.item() == np.float32(math.sqrt(idx.numel() / n))
+    del ref, h
+    torch.cuda.empty_cache()
