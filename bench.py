@@ -34,8 +34,33 @@ DRIFT_BYTES_PER_BLOCK = 4     # one fp32 score written
 SIM_BYTES_PER_ELEM = 6        # fp32 a read + fp16 h written
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "drift_score_llama70b_hbm_traffic.md")
+DRIFT_SOURCES = ("reduce.hip", "cdt_device.hpp", "cdt_launch.hpp")
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def measured_traffic(workload):
+    """HBM bytes per drift_score launch from the committed rocprofv3 FETCH_SIZE
+    and WRITE_SIZE passes (scaled by a plain copy of known size), or None if
+    they were taken on another workload or on different kernel sources."""
+    import hashlib
+    if workload != "llama70b" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and line.startswith("drift_score_"):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for f in DRIFT_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_19490_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if fields.get("drift_score_source_sha256") != h.hexdigest():
+        return None
+    return int(fields["drift_score_traffic_bytes_per_launch"])
 
 
 def parse():
@@ -47,8 +72,11 @@ def parse():
     p.add_argument("--no-sweep", action="store_true")
     p.add_argument("--sweep-reps", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-canaries", type=int, default=1,
+    p.add_argument("--cpu-canaries", type=int, default=4,
                    help="canaries (all shards each) in the CPU oracle sample")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="first run one plain 4 GiB device copy (torch), the known-size "
+                        "kernel that scales HBM byte counters")
     return p.parse_args()
 
 
@@ -195,7 +223,7 @@ def run_main(torch, cdt, W, args):
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(wl.name),
             "bytes_per_launch": per_launch,
             "avg_launch_ms": round(drift_avg, 4),
         },
@@ -321,6 +349,14 @@ def main():
         sys.exit(1)
     cdt.lib()
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        x = torch.ones((1 << 30,), dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        torch.cuda.synchronize()
+        y.copy_(x)  # reads 4 GiB, writes 4 GiB
+        torch.cuda.synchronize()
+        del x, y
+        log("copy calibration: 4 GiB read + 4 GiB written")
     res, _ = run_main(torch, cdt, W, args)
     if not args.no_sweep:
         res["sweep"] = run_sweep(torch, cdt, W, args.sweep_reps)

@@ -6,7 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
-#include "../../include/cdt.h"
+#include "cdt.h"
 #include "cdt_launch.hpp"
 
 namespace {

@@ -8,6 +8,20 @@ namespace cdt {
 
 constexpr int kWave = 64;
 
+// MI355X has 8 accelerator complex dies (XCDs), each with its own L2;
+// consecutive workgroup ids are dispatched round-robin over them.
+constexpr uint32_t kXcds = 8;
+
+// Remap a work index so that each XCD walks one contiguous range of
+// [0, total): index `it` runs on XCD it % 8 (true when the grid stride is a
+// multiple of 8 or the grid covers all of [0, total) once).  A bijection of
+// [0, total) for every total.
+__device__ __forceinline__ uint64_t xcd_contiguous(uint64_t it, uint64_t total) {
+    const uint64_t x = it % kXcds, local = it / kXcds;
+    const uint64_t base = total / kXcds, rem = total % kXcds;
+    return x * base + (x < rem ? x : rem) + local;
+}
+
 // Native 16-byte vectors (usable with the nontemporal load/store builtins).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -33,18 +47,23 @@ struct Words4 {
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
 // 32x32->64 multiplies on counter words 0 and 2, XOR of the high halves into
 // words 1 and 3 with the round key, and a word permutation; the key advances
-// by the two Weyl increments between rounds.  The multiplies lower to
-// v_mad_u64_u32; when a counter word is wave-uniform the first round's
-// product stays on the scalar unit.
+// by the two Weyl increments between rounds.  Each round is two
+// v_mad_u64_u32 and two 3-input XORs (v_bitop3_b32, truth table 0x96 =
+// a ^ b ^ c); while a counter word is wave-uniform (the canary, shard and
+// stream words are) the product stays on the scalar unit.
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
 __device__ __forceinline__ Words4 philox10(Words4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
         const uint64_t p0 = static_cast<uint64_t>(0xD2511F53u) * c.x;
         const uint64_t p1 = static_cast<uint64_t>(0xCD9E8D57u) * c.z;
         Words4 n;
-        n.x = static_cast<uint32_t>(p1 >> 32) ^ c.y ^ k0;
+        n.x = xor3(static_cast<uint32_t>(p1 >> 32), c.y, k0);
         n.y = static_cast<uint32_t>(p1);
-        n.z = static_cast<uint32_t>(p0 >> 32) ^ c.w ^ k1;
+        n.z = xor3(static_cast<uint32_t>(p0 >> 32), c.w, k1);
         n.w = static_cast<uint32_t>(p0);
         c = n;
         k0 += 0x9E3779B9u;
@@ -71,10 +90,12 @@ __host__ __device__ constexpr uint32_t stream_tag(uint32_t stream, uint32_t id) 
 
 // Unit normal stand-in: the Irwin-Hall sum of the four 16-bit halves of two
 // Philox words, centred (4 * 32767.5) and scaled by fp32(sqrt(3/(2^32-1))).
+// v_sad_u16(w, 0, acc) adds both 16-bit halves of w to acc; starting the
+// accumulator at -131070 (mod 2^32) leaves the centred sum n as an int32.
 __device__ __forceinline__ float irwin_hall4(uint32_t w0, uint32_t w1) {
-    const int n = static_cast<int>(w0 & 0xFFFFu) + static_cast<int>(w0 >> 16) +
-                  static_cast<int>(w1 & 0xFFFFu) + static_cast<int>(w1 >> 16) - 131070;
-    return static_cast<float>(n) * 0x1.bb67aep-16f;
+    const uint32_t centred =
+        __builtin_amdgcn_sad_u16(w0, 0u, __builtin_amdgcn_sad_u16(w1, 0u, 0u - 131070u));
+    return static_cast<float>(static_cast<int>(centred)) * 0x1.bb67aep-16f;
 }
 
 // fp32 -> fp16 bits, IEEE round to nearest even (v_cvt_f16_f32 under the

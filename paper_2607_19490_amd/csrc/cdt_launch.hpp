@@ -17,9 +17,11 @@ constexpr uint32_t kGenChunkGroups = kGenThreads * kGenItems;
 
 // Block reductions: a workgroup reduces kReduceChunkElems elements of one
 // block to a pair of fp64 partial sums; a second kernel adds the partials of
-// a block in chunk order.
-constexpr int kReduceThreads = 256;
-constexpr int kReduceUnroll = 4;
+// a block in chunk order.  1024 threads with two 8-element groups in flight
+// each measured fastest on the 16 x 256 x 256 x 8192 stream (85% of the HBM
+// peak against 84% for 256 x 4 and 80% for 1024 x 4).
+constexpr int kReduceThreads = 1024;
+constexpr int kReduceUnroll = 2;
 constexpr uint64_t kReduceChunkElems = 32768;
 
 inline uint64_t reduce_chunks_per_block(uint64_t n) {

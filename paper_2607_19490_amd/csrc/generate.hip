@@ -41,6 +41,16 @@ __global__ __launch_bounds__(256) void outlier_gain_kernel(uint32_t H, uint32_t 
 }
 
 // ---------------------------------------------------------------------------
+// Streamed loads and stores of the elementwise kernels (each byte is touched
+// once per launch).  The fp16 output is stored nontemporally: it leaves no
+// dirty lines behind in L2 / the Infinity Cache for the next kernel to evict.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ f32x4 load_stream(const f32x4* p) { return *p; }
+__device__ __forceinline__ void store_stream(u32x4* p, u32x4 v) {
+    __builtin_nontemporal_store(v, p);
+}
+
+// ---------------------------------------------------------------------------
 // Chunk walk shared by the elementwise kernels: chunk -> (block, first group).
 // ---------------------------------------------------------------------------
 struct ChunkPos {
@@ -78,12 +88,12 @@ __global__ __launch_bounds__(kGenThreads) void ref_synth_kernel(
     uint32_t C, uint32_t H, uint32_t n8, uint64_t chunks_per_block, uint64_t total_chunks,
     Key key, uint32_t tag, const float* __restrict__ gain, float* __restrict__ ref) {
     const uint64_t n = static_cast<uint64_t>(n8) * 8;
-    for (uint64_t chunk = blockIdx.x; chunk < total_chunks; chunk += gridDim.x) {
-        const ChunkPos p = chunk_pos(chunk, chunks_per_block, C);
+    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
+        const ChunkPos p = chunk_pos(xcd_contiguous(it, total_chunks), chunks_per_block, C);
         float4* out = reinterpret_cast<float4*>(ref + p.block * n);
 #pragma unroll
-        for (int it = 0; it < kGenItems; ++it) {
-            const uint32_t g = p.g0 + it * kGenThreads + threadIdx.x;
+        for (int item = 0; item < kGenItems; ++item) {
+            const uint32_t g = p.g0 + item * kGenThreads + threadIdx.x;
             if (g >= n8) break;
             const uint32_t e0 = g * 8;
             const uint32_t j0 = e0 % H;
@@ -137,20 +147,31 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
                                                                  const float* __restrict__ ref,
                                                                  uint16_t* __restrict__ h) {
     const uint64_t n = static_cast<uint64_t>(A.n8) * 8;
-    for (uint64_t chunk = blockIdx.x; chunk < A.total_chunks; chunk += gridDim.x) {
-        const ChunkPos p = chunk_pos(chunk, A.chunks_per_block, A.C);
+    for (uint64_t it = blockIdx.x; it < A.total_chunks; it += gridDim.x) {
+        const ChunkPos p = chunk_pos(xcd_contiguous(it, A.total_chunks), A.chunks_per_block, A.C);
         const bool mal = (A.mal_mask >> p.s) & 1u;
         const float bsc = A.block_mode ? A.bscale[p.block] : 0.0f;
         const float tsc = (mal && (A.tamper & 1u)) ? A.tscale[p.block] : 0.0f;
-        const float4* in = reinterpret_cast<const float4*>(ref + p.block * n);
-        uint4* out = reinterpret_cast<uint4*>(h + p.block * n);
+        const f32x4* in = reinterpret_cast<const f32x4*>(ref + p.block * n);
+        u32x4* out = reinterpret_cast<u32x4*>(h + p.block * n);
+        // Double buffer: the next group's reference loads are issued before
+        // the Philox work on the current group, so loads overlap the ALU work.
+        uint32_t g = p.g0 + threadIdx.x;
+        f32x4 nxt_lo = f32x4{0.f, 0.f, 0.f, 0.f}, nxt_hi = nxt_lo;
+        if (g < A.n8) {
+            nxt_lo = load_stream(in + 2 * g);
+            nxt_hi = load_stream(in + 2 * g + 1);
+        }
 #pragma unroll 1
-        for (int it = 0; it < kGenItems; ++it) {
-            const uint32_t g = p.g0 + it * kGenThreads + threadIdx.x;
+        for (int item = 0; item < kGenItems; ++item, g += kGenThreads) {
             if (g >= A.n8) break;
+            const f32x4 a_lo = nxt_lo, a_hi = nxt_hi;
+            const uint32_t g_next = g + kGenThreads;
+            if (item + 1 < kGenItems && g_next < A.n8) {
+                nxt_lo = load_stream(in + 2 * g_next);
+                nxt_hi = load_stream(in + 2 * g_next + 1);
+            }
             const uint32_t e0 = g * 8;
-            const float4 a_lo = in[2 * g];
-            const float4 a_hi = in[2 * g + 1];
             const float a[8] = {a_lo.x, a_lo.y, a_lo.z, a_lo.w, a_hi.x, a_hi.y, a_hi.z, a_hi.w};
 
             // Eq. 2: benign hardware noise.
@@ -201,18 +222,19 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
                 }
             }
 
-            uint4 o;
+            u32x4 o;
             o.x = to_half_bits(v[0]) | (static_cast<uint32_t>(to_half_bits(v[1])) << 16);
             o.y = to_half_bits(v[2]) | (static_cast<uint32_t>(to_half_bits(v[3])) << 16);
             o.z = to_half_bits(v[4]) | (static_cast<uint32_t>(to_half_bits(v[5])) << 16);
             o.w = to_half_bits(v[6]) | (static_cast<uint32_t>(to_half_bits(v[7])) << 16);
-            out[g] = o;
+            store_stream(out + g, o);
         }
     }
 }
 
 // Grid for a chunked elementwise walk: enough workgroups to fill 256 CUs
-// several times over; larger jobs loop.
+// several times over; larger jobs loop with a stride (16384) that is a
+// multiple of the XCD count, as xcd_contiguous needs.
 inline uint32_t gen_grid(uint64_t total_chunks) {
     const uint64_t cap = 256ull * 64;
     return static_cast<uint32_t>(total_chunks < cap ? total_chunks : cap);

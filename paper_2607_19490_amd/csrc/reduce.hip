@@ -6,10 +6,12 @@
 //   * a block (shard, canary) of n = T*H elements is cut into chunks of
 //     kReduceChunkElems; one 256-thread workgroup reduces one chunk;
 //   * each thread streams groups of 8 elements (one 16-byte h load, two
-//     16-byte a loads), kReduceUnroll groups in flight before any use;
+//     16-byte a loads), kReduceUnroll groups in flight before any use; the
+//     loads are nontemporal (read once, no reuse);
+//   * chunks are handed out so that each XCD streams one contiguous range;
 //   * the squares are accumulated in fp64 from the exactly widened operands
 //     (h - a is exact in fp64), so the partial sums carry no cancellation;
-//   * wave butterfly sums, then an LDS pass over the 4 waves, give one
+//   * wave butterfly sums, then an LDS pass over the waves, give one
 //     (D, R) pair per chunk in a fixed order (no atomics);
 //   * a combine kernel adds a block's chunk partials in chunk order and
 //     forms m = sqrt(D / R).
@@ -76,7 +78,8 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
     const uint16_t* __restrict__ h, const float* __restrict__ ref, uint32_t n8,
     uint64_t chunks_per_block, uint64_t total_chunks, double2* __restrict__ partial) {
     const uint64_t n = static_cast<uint64_t>(n8) * 8;
-    for (uint64_t chunk = blockIdx.x; chunk < total_chunks; chunk += gridDim.x) {
+    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
+        const uint64_t chunk = xcd_contiguous(it, total_chunks);
         const uint64_t b = chunk / chunks_per_block;
         const uint32_t g0 = static_cast<uint32_t>(chunk - b * chunks_per_block) * kChunkGroups;
         const uint32_t g_end = min(g0 + kChunkGroups, n8);
@@ -173,6 +176,8 @@ __global__ void ref_stats_combine_kernel(const double2* __restrict__ partial,
     sumabs[b] = M;
 }
 
+// One workgroup per chunk up to 2^20 chunks, then a grid-stride walk whose
+// stride (2^20) is a multiple of the XCD count, as xcd_contiguous needs.
 inline uint32_t reduce_grid(uint64_t total_chunks) {
     const uint64_t cap = 1ull << 20;
     return static_cast<uint32_t>(total_chunks < cap ? total_chunks : cap);
