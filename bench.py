@@ -72,6 +72,8 @@ def parse():
     p.add_argument("--no-sweep", action="store_true")
     p.add_argument("--sweep-reps", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-ablations", action="store_true",
+                   help="skip the ablation kernels and the Table 1 reproduction")
     p.add_argument("--cpu-canaries", type=int, default=4,
                    help="canaries (all shards each) in the CPU oracle sample")
     p.add_argument("--copy-calibration", action="store_true",
@@ -238,9 +240,120 @@ def run_main(torch, cdt, W, args):
                         for i, r in enumerate([r for p in preps for r in p.rs.runs])}
     res["control"] = {r.label: round(int(c[i][3]) / max(1, int(c[i][5])), 4)
                       for i, r in enumerate([r for p in preps for r in p.rs.runs])}
+    if not args.no_ablations:
+        res["ablation_kernels"] = ablation_kernels(torch, cdt, wl, big)
     del preps, scores, views
     torch.cuda.empty_cache()
     return res, elems_per_step
+
+
+def time_ms(torch, fn, reps=5):
+    """Median time of fn() over reps launches (HIP events on the current stream)."""
+    fn()
+    torch.cuda.synchronize()
+    t = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        torch.cuda.synchronize()
+        t.append(a.elapsed_time(b))
+    t.sort()
+    return t[len(t) // 2]
+
+
+def auroc_row(cdt, torch, score, rs, cfg_id, seed, flags):
+    counts, _, base = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, cfg_id)], score.reshape(-1),
+                                seed=seed, flags=flags)
+    torch.cuda.synchronize()
+    c = cdt.u64(counts)[0]
+    out = {"auroc": round(cdt.strict_auroc(c), 4), "auroc_mw": round(cdt.mw_auroc(c), 4),
+           "control": round(int(c[3]) / max(1, int(c[5])), 4)}
+    if base is not None:
+        out["random_baseline"] = round(cdt.strict_auroc(cdt.u64(base)[0]), 4)
+    return out
+
+
+def ablation_kernels(torch, cdt, wl, prep):
+    """The reference conditions and ablations of Sections 4.4-4.5 on the
+    largest workload: an independent benign recompute (redraw) of every
+    stage, Eq. 4 against it (recompute ceiling / noisy reference), and the
+    cosine mismatch against the fp32 reference and against the recompute.
+    Timed per launch, with their detection AUROC on the last run."""
+    rs = prep.rs
+    run = rs.runs[-1]
+    ts, bs = prep.scales[-1]
+    elems = rs.elems
+    blocks = rs.S * rs.C
+    kw = sim_kwargs(wl, rs, run, ts, bs)
+    cdt.canary_sim(prep.ref, out=prep.h, **kw)
+    r = torch.empty_like(prep.h)
+    kw_r = dict(kw, mal_mask=0, redraw=True)
+    sim_ms = time_ms(torch, lambda: cdt.canary_sim(prep.ref, out=r, **kw_r))
+    out = {}
+    score = torch.empty((rs.C, rs.S), dtype=torch.float32, device="cuda")
+    cases = (
+        ("drift_score_f16ref", lambda: cdt.drift_score_f16ref(prep.h, r, out=score, ws=prep.ws), 4),
+        ("cosine_score", lambda: cdt.cosine_score(prep.h, prep.ref, out=score, ws=prep.ws), 6),
+        ("cosine_score_f16ref",
+         lambda: cdt.cosine_score_f16ref(prep.h, r, out=score, ws=prep.ws), 4),
+    )
+    flags = cdt.AUROC_CONTROL | cdt.AUROC_RANDOM
+    for name, fn, bpe in cases:
+        ms = time_ms(torch, fn)
+        nbytes = elems * bpe + blocks * DRIFT_BYTES_PER_BLOCK
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        row = {"ms": round(ms, 4), "GBps": round(gbps, 1),
+               "frac_of_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+        row.update(auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags))
+        out[name] = row
+    out["redraw_canary_sim"] = {"ms": round(sim_ms, 4),
+                                "GBps": round(elems * SIM_BYTES_PER_ELEM / (sim_ms * 1e-3) / 1e9, 1)}
+    out["run"] = run.label
+    del r
+    return out
+
+
+def table1(torch, cdt, W):
+    """The structure of Table 1 on the paper's own shape (12 stages, 100
+    canaries, 48 tokens, d = 768, block noise sigma_hw = 0.002, six attacks):
+    detector settings x (AUROC, random baseline, scrambled control, recompute
+    ceiling).  With independent stages the noisy-reference ablation and the
+    recompute ceiling compare the live output with the same independent
+    benign pass."""
+    wl = W.paper()
+    rs = wl.ref_sets[0]
+    prep = Prepared(torch, cdt, W, wl, rs)
+    r = torch.empty_like(prep.h)
+    score = torch.empty((rs.C, rs.S), dtype=torch.float32, device="cuda")
+    flags = cdt.AUROC_CONTROL | cdt.AUROC_RANDOM
+    rows = {"full_detector": {}, "noisy_reference": {}, "cosine_metric": {}}
+    for k, run in enumerate(rs.runs):
+        ts, bs = prep.scales[k]
+        kw = sim_kwargs(wl, rs, run, ts, bs)
+        cdt.canary_sim(prep.ref, out=prep.h, **kw)
+        cdt.canary_sim(prep.ref, out=r, **dict(kw, mal_mask=0, redraw=True))
+        cdt.drift_score(prep.h, prep.ref, out=score, ws=prep.ws)
+        full = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
+        cdt.drift_score_f16ref(prep.h, r, out=score, ws=prep.ws)
+        ceil = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
+        cdt.cosine_score(prep.h, prep.ref, out=score, ws=prep.ws)
+        cos = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
+        cdt.cosine_score_f16ref(prep.h, r, out=score, ws=prep.ws)
+        cos_ceil = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
+        rows["full_detector"][run.label] = dict(full, ceiling=ceil["auroc"])
+        rows["noisy_reference"][run.label] = dict(ceil, ceiling=ceil["auroc"])
+        rows["cosine_metric"][run.label] = dict(cos, ceiling=cos_ceil["auroc"])
+    summary = {}
+    for name, per in rows.items():
+        vals = list(per.values())
+        summary[name] = {key: round(sum(v[key] for v in vals) / len(vals), 4)
+                         for key in ("auroc", "random_baseline", "control", "ceiling")}
+    del prep, r
+    torch.cuda.empty_cache()
+    return {"workload": "paper 12x100x48x768, block noise sigma_hw 0.002",
+            "mean_over_six_attacks": summary, "per_attack": rows}
 
 
 def run_sweep(torch, cdt, W, reps):
@@ -360,6 +473,9 @@ def main():
     res, _ = run_main(torch, cdt, W, args)
     if not args.no_sweep:
         res["sweep"] = run_sweep(torch, cdt, W, args.sweep_reps)
+    if not args.no_ablations:
+        log("table 1 structure on the paper's shape")
+        res["table1"] = table1(torch, cdt, W)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(W, args)

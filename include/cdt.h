@@ -57,6 +57,8 @@ extern "C" {
 #define CDT_STREAM_RANDOM 7
 #define CDT_STREAM_OUTLIER 8
 #define CDT_STREAM_ALT 9
+#define CDT_STREAM_ALT_T12 10
+#define CDT_STREAM_ALT_T3 11
 
 /* Interface version; changes whenever a layout or generator rule changes. */
 int cdt_version(void);
@@ -87,8 +89,10 @@ int cdt_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed, uint3
 int cdt_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
                   uint32_t ref_set_id, const float* gain, float* ref, void* stream);
 
-/* Workspace (device bytes) needed by cdt_ref_stats and cdt_drift_score for
- * this shape: per-block partial sums of a fixed chunking. */
+/* Workspace (device bytes) needed by cdt_ref_stats and the four block
+ * reductions (cdt_drift_score, cdt_drift_score_f16ref, cdt_cosine_score,
+ * cdt_cosine_score_f16ref) for this shape: per-block partial sums (up to
+ * three fp64 per chunk) of a fixed chunking. */
 size_t cdt_reduce_workspace_bytes(uint32_t S, uint32_t C, uint32_t T, uint32_t H);
 
 /* Per-block reference statistics in fp64: sumsq[s][c] = sum a^2 and
@@ -125,7 +129,10 @@ typedef struct cdt_sim_params {
     uint32_t benign_dist;   /* CDT_DIST_*                                          */
     uint32_t tamper;        /* OR of CDT_T_* (all three: Gaussian, flip, rescale) */
     uint32_t tamper_base;   /* CDT_BASE_*                                          */
-    uint32_t reserved;      /* must be 0                                           */
+    uint32_t redraw;        /* 0: benign noise from BENIGN/T12/T3; 1: from ALT/    */
+                            /* ALT_T12/ALT_T3, an independent benign recompute of  */
+                            /* the same stage (Section 4.5: recompute ceiling and  */
+                            /* noisy-reference ablation)                           */
     uint64_t mal_mask;      /* bit s set: shard s is malicious (tampers)           */
     double sigma_b;         /* ELEMENTWISE noise level (used as fp32(sigma_b))     */
     double flip_p;          /* flip probability in [0, 1]; 1 flips every element   */
@@ -166,6 +173,34 @@ int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16
                     const float* ref, float* score, double* num_den, void* ws, size_t ws_bytes,
                     void* stream);
 
+/* Relative-L2 mismatch against an fp16 reference r (Eq. 4 with the stored
+ * fp32 reference replaced by a second live pass, Section 4.5: the
+ * noisy-reference ablation and the redundant-recompute ceiling):
+ * score[c][s] = fp32( sqrt( sum (h - r)^2 / sum r^2 ) ), sums in fp64.
+ * r: device [S][C][T][H] fp16 bits.  Otherwise as cdt_drift_score. */
+int cdt_drift_score_f16ref(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                           const uint16_t* r, float* score, double* num_den, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/* Cosine mismatch, the metric ablation of Section 4.4:
+ * score[c][s] = fp32(1 - h.a / (||h|| ||a||)).  With d = h - a, A = sum a^2,
+ * P = sum a d, D = sum d^2 (fp64, from exactly widened operands) and
+ * Hn = A + 2P + D = ||h||^2, it is evaluated as
+ *   (A D - P^2) / (sqrt(A Hn) (sqrt(A Hn) + A + P))      when A + P > 0,
+ *   1 - (A + P) / sqrt(A Hn)                              otherwise,
+ * the same value without the cancellation of 1 - cos near 0.  A block with
+ * h or a all zero scores 0 if both are zero, else 1.
+ * sums: optional device [C][S][3] fp64 (D, A, P), or NULL. */
+int cdt_cosine_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                     const float* ref, float* score, double* sums, void* ws, size_t ws_bytes,
+                     void* stream);
+
+/* The cosine mismatch against an fp16 reference r (a second live pass, as
+ * in cdt_drift_score_f16ref): the cosine row of the recompute ceiling. */
+int cdt_cosine_score_f16ref(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                            const uint16_t* r, float* score, double* sums, void* ws,
+                            size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Detection AUROC, Eqs. 5-6, the Mann-Whitney form and the scrambled-label  */
 /* control of Section 4.5, batched over configurations                       */
@@ -173,6 +208,7 @@ int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16
 #define CDT_AUROC_CONTROL 1     /* also count the scrambled-label control        */
 #define CDT_AUROC_POOLED 2      /* also rank all C*S scores of a config together  */
 #define CDT_CTRL_INCLUDE_TRUE 4 /* control keeps the true malicious shards as negatives */
+#define CDT_AUROC_RANDOM 8      /* also count the random baseline                  */
 
 typedef struct cdt_auroc_cfg {
     uint32_t S, C;       /* shards (<= 64) and canaries of this configuration     */
@@ -198,13 +234,17 @@ size_t cdt_auroc_workspace_bytes(uint32_t n_cfg);
  *       shards with CDT_CTRL_INCLUDE_TRUE);
  *   pooled[g][0..2] = G, E, pairs over every positive score against every
  *       negative score of the configuration (if CDT_AUROC_POOLED; needs
- *       C*S <= 16384; pooled may be NULL otherwise).
+ *       C*S <= 16384; pooled may be NULL otherwise);
+ *   baseline[g][0..2] = G, E, pairs of Eq. 5 with every score replaced by
+ *       the random-baseline score of Section 4.5, u(t, s) = (w >> 8) 2^-24,
+ *       w = Philox word 0 of counter (t, s, 0, RANDOM<<24 | cfg_id) (if
+ *       CDT_AUROC_RANDOM; baseline may be NULL otherwise).
  * Score order: NaN below every number, NaN ties NaN, -0 ties +0.
  * counts: device [n_cfg][6] uint64; scores: device fp32; n_scores bounds
  * every configuration's table. */
 int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, uint64_t n_scores,
-              uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled, void* ws,
-              size_t ws_bytes, void* stream);
+              uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
+              uint64_t* baseline, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

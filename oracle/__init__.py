@@ -34,6 +34,7 @@ BASE_CLEAN = 1
 AUROC_CONTROL = 1
 AUROC_POOLED = 2
 CTRL_INCLUDE_TRUE = 4
+AUROC_RANDOM = 8
 
 _u16p = ctypes.POINTER(ctypes.c_uint16)
 _u32p = ctypes.POINTER(ctypes.c_uint32)
@@ -59,6 +60,14 @@ _SIGS = {
     "orc_ref_range": ([_u32, _u32, _u32, _u64, _u64, _u64, _u32, _f32p, _f32p], None),
     "orc_sim_range": ([_u32, _u32, _u64, _u64, _u64, _u32, _i, _i, _d, _f, _i, _u32, _i, _f,
                        _d, _d, _f32p, _u16p], _i),
+    "orc_sim_range_ex": ([_u32, _u32, _u64, _u64, _u64, _u32, _i, _i, _d, _f, _i, _u32, _i, _f,
+                          _d, _d, _i, _f32p, _u16p], _i),
+    "orc_drift_block_f16ref": ([_u64, _u16p, _u16p, _f64p, _f64p], _d),
+    "orc_drift_score_f16ref": ([_u32, _u32, _u32, _u32, _u16p, _u16p, _f64p, _f32p], None),
+    "orc_cosine_block": ([_u64, _u16p, _f32p], _d),
+    "orc_cosine_block_f16ref": ([_u64, _u16p, _u16p], _d),
+    "orc_cosine_score": ([_u32, _u32, _u32, _u32, _u16p, _f32p, _f64p, _f32p], None),
+    "orc_random_score": ([_u64, _u32, _u32, _u32], _f),
     "orc_ref_block": ([_u32, _u32, _u32, _u32, _u64, _u32, _f32p, _f32p], None),
     "orc_ref_synth": ([_u32, _u32, _u32, _u32, _u64, _u32, _f32p, _f32p], None),
     "orc_ref_stats_block": ([_u64, _f32p, _f64p, _f64p], None),
@@ -67,12 +76,12 @@ _SIGS = {
     "orc_sim_block": ([_u32, _u32, _u32, _u32, _u64, _u32, _i, _i, _d, _f, _i, _u32, _i, _f,
                        _d, _d, _f32p, _u16p], _i),
     "orc_canary_sim": ([_u32, _u32, _u32, _u32, _u64, _u32, _i, _i, _d, _f32p, _u64, _u32, _i,
-                        _f32p, _d, _d, _f32p, _u16p], _i),
+                        _f32p, _d, _d, _i, _f32p, _u16p], _i),
     "orc_drift_block": ([_u64, _u16p, _f32p, _f64p, _f64p], _d),
     "orc_drift_score": ([_u32, _u32, _u32, _u32, _u16p, _f32p, _f64p, _f32p, _f64p], None),
     "orc_score_cmp": ([_f, _f], _i),
     "orc_scramble_jstar": ([_u32, _u64, _u64, _u32, _u32], _i),
-    "orc_auroc_config": ([_u32, _u32, _f32p, _u64, _u64, _u32, _u32, _u64p, _u64p], _i),
+    "orc_auroc_config": ([_u32, _u32, _f32p, _u64, _u64, _u32, _u32, _u64p, _u64p, _u64p], _i),
 }
 
 
@@ -206,13 +215,14 @@ def block_scales(T, H, sumsq, sumabs, eps, sigma_b):
 
 def sim_block(s, c, ref_block_arr, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE,
               benign_dist=DIST_GAUSS, sigma_b=1e-3, bscale=0.0, malicious=False, tamper=0,
-              tamper_base=BASE_BENIGN, tscale=0.0, flip_p=0.0, scale=1.0):
+              tamper_base=BASE_BENIGN, tscale=0.0, flip_p=0.0, scale=1.0, redraw=False):
     a = _c(ref_block_arr, np.float32)
     T, H = a.shape
     h = np.empty((T, H), np.uint16)
-    lib().orc_sim_block(s, c, T, H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
-                        float(bscale), int(bool(malicious)), tamper, tamper_base, float(tscale),
-                        flip_p, scale, _p(a, ctypes.c_float), _p(h, ctypes.c_uint16))
+    lib().orc_sim_range_ex(s, c, 0, T * H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
+                           float(bscale), int(bool(malicious)), tamper, tamper_base,
+                           float(tscale), flip_p, scale, int(bool(redraw)),
+                           _p(a, ctypes.c_float), _p(h, ctypes.c_uint16))
     return h
 
 
@@ -230,7 +240,7 @@ def sim_range(s, c, e0, ref_part, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE
 
 def canary_sim(ref, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE, benign_dist=DIST_GAUSS,
                sigma_b=1e-3, bscale=None, mal_mask=0, tamper=0, tamper_base=BASE_BENIGN,
-               tscale=None, flip_p=0.0, scale=1.0):
+               tscale=None, flip_p=0.0, scale=1.0, redraw=False):
     """ref [S][C][T][H] fp32 -> h [S][C][T][H] fp16 bit patterns (uint16)."""
     ref = _c(ref, np.float32)
     S, C, T, H = ref.shape
@@ -239,8 +249,8 @@ def canary_sim(ref, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE, benign_dist=
     h = np.empty((S, C, T, H), np.uint16)
     lib().orc_canary_sim(S, C, T, H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
                          _p(bs, ctypes.c_float), mal_mask, tamper, tamper_base,
-                         _p(ts, ctypes.c_float), flip_p, scale, _p(ref, ctypes.c_float),
-                         _p(h, ctypes.c_uint16))
+                         _p(ts, ctypes.c_float), flip_p, scale, int(bool(redraw)),
+                         _p(ref, ctypes.c_float), _p(h, ctypes.c_uint16))
     return h
 
 
@@ -275,6 +285,70 @@ def drift_score(h_bits, ref):
     return s64, s32, nd
 
 
+def drift_block_f16ref(h_bits, r_bits):
+    """Eq. 4 against an fp16 reference (second live pass): (m, D, R)."""
+    h = _c(h_bits, np.uint16).ravel()
+    r = _c(r_bits, np.uint16).ravel()
+    assert h.size == r.size
+    D = ctypes.c_double()
+    R = ctypes.c_double()
+    m = lib().orc_drift_block_f16ref(h.size, _p(h, ctypes.c_uint16), _p(r, ctypes.c_uint16),
+                                     ctypes.byref(D), ctypes.byref(R))
+    return m, D.value, R.value
+
+
+def drift_score_f16ref(h_bits, r_bits):
+    """h, r [S][C][T][H] fp16 bits -> (score64 [C][S], score32 [C][S])."""
+    h = _c(h_bits, np.uint16)
+    r = _c(r_bits, np.uint16)
+    S, C, T, H = h.shape
+    assert r.shape == h.shape
+    s64 = np.empty((C, S), np.float64)
+    s32 = np.empty((C, S), np.float32)
+    lib().orc_drift_score_f16ref(S, C, T, H, _p(h, ctypes.c_uint16), _p(r, ctypes.c_uint16),
+                                 _p(s64, ctypes.c_double), _p(s32, ctypes.c_float))
+    return s64, s32
+
+
+def cosine_block(h_bits, a):
+    """Cosine mismatch 1 - h.a / (|h| |a|) of one block (Section 4.4 ablation)."""
+    h = _c(h_bits, np.uint16).ravel()
+    a = _c(a, np.float32).ravel()
+    assert h.size == a.size
+    return lib().orc_cosine_block(h.size, _p(h, ctypes.c_uint16), _p(a, ctypes.c_float))
+
+
+def cosine_block_f16ref(h_bits, r_bits):
+    """Cosine mismatch against an fp16 reference (second live pass)."""
+    h = _c(h_bits, np.uint16).ravel()
+    r = _c(r_bits, np.uint16).ravel()
+    assert h.size == r.size
+    return lib().orc_cosine_block_f16ref(h.size, _p(h, ctypes.c_uint16), _p(r, ctypes.c_uint16))
+
+
+def cosine_score_f16ref(h_bits, r_bits):
+    """h, r [S][C][T][H] fp16 bits -> cosine mismatch [C][S] (fp64)."""
+    h = _c(h_bits, np.uint16)
+    r = _c(r_bits, np.uint16)
+    S, C = h.shape[:2]
+    out = np.empty((C, S), np.float64)
+    for s in range(S):
+        for c in range(C):
+            out[c, s] = cosine_block_f16ref(h[s, c], r[s, c])
+    return out
+
+
+def cosine_score(h_bits, ref):
+    h = _c(h_bits, np.uint16)
+    ref = _c(ref, np.float32)
+    S, C, T, H = ref.shape
+    s64 = np.empty((C, S), np.float64)
+    s32 = np.empty((C, S), np.float32)
+    lib().orc_cosine_score(S, C, T, H, _p(h, ctypes.c_uint16), _p(ref, ctypes.c_float),
+                           _p(s64, ctypes.c_double), _p(s32, ctypes.c_float))
+    return s64, s32
+
+
 # ---------------------------------------------------------------------------
 # Eqs. 5-6
 # ---------------------------------------------------------------------------
@@ -294,10 +368,28 @@ def auroc_config(scores, pos_mask, *, seed=0, cfg_id=0, flags=AUROC_CONTROL | AU
     counts = np.zeros(6, np.uint64)
     pooled = np.zeros(3, np.uint64)
     rc = lib().orc_auroc_config(S, C, _p(sc, ctypes.c_float), pos_mask, seed, cfg_id, flags,
-                                _p(counts, ctypes.c_uint64), _p(pooled, ctypes.c_uint64))
+                                _p(counts, ctypes.c_uint64), _p(pooled, ctypes.c_uint64), None)
     if rc:
         raise ValueError(f"orc_auroc_config failed ({rc})")
     return counts, pooled
+
+
+def random_score(seed, cfg_id, t, s):
+    return np.float32(lib().orc_random_score(seed, cfg_id, t, s))
+
+
+def random_baseline(C, S, pos_mask, *, seed=0, cfg_id=0):
+    """Eq. 5 counts (G, E, pairs) with every score replaced by Uniform[0,1)
+    (the random baseline of Section 4.5)."""
+    counts = np.zeros(6, np.uint64)
+    base = np.zeros(3, np.uint64)
+    dummy = np.zeros((max(C, 1), max(S, 1)), np.float32)
+    rc = lib().orc_auroc_config(S, C, _p(dummy, ctypes.c_float), pos_mask, seed, cfg_id,
+                                AUROC_RANDOM, _p(counts, ctypes.c_uint64), None,
+                                _p(base, ctypes.c_uint64))
+    if rc:
+        raise ValueError(f"orc_auroc_config failed ({rc})")
+    return base
 
 
 def auroc_strict(counts):

@@ -84,7 +84,9 @@ enum {
     ST_SCRAMBLE = 6, /* scrambled-label stage j* (Section 4.5)            */
     ST_RANDOM = 7,   /* random-baseline scores (Section 4.5)              */
     ST_OUTLIER = 8,  /* outlier channel choice of the synthetic reference */
-    ST_ALT = 9       /* independent benign redraw (Section 4.5 ceiling)   */
+    ST_ALT = 9,      /* independent benign redraw (Section 4.5 ceiling)   */
+    ST_ALT_T12 = 10, /* ... its Student-t chi-square normals 1, 2          */
+    ST_ALT_T3 = 11   /* ... and normal 3                                   */
 };
 
 static void philox_at(uint64_t seed, uint32_t w0, uint32_t w1, uint32_t w2,
@@ -360,24 +362,30 @@ static int flip_selected(double p, uint32_t u)
 }
 
 /* Elements [e0, e0 + count) of block (s, c); ref and h hold just that range. */
-int orc_sim_range(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t seed,
-                  uint32_t cfg_id, int benign_mode, int benign_dist, double sigma_b, float bscale,
-                  int malicious, uint32_t tamper, int tamper_base, float tscale, double flip_p,
-                  double scale, const float* ref, uint16_t* h)
+/* redraw != 0 draws the benign noise from the ALT streams: an independent
+ * benign recompute of the same stage (Section 4.5, recompute ceiling and
+ * noisy-reference ablation). */
+int orc_sim_range_ex(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t seed,
+                     uint32_t cfg_id, int benign_mode, int benign_dist, double sigma_b,
+                     float bscale, int malicious, uint32_t tamper, int tamper_base, float tscale,
+                     double flip_p, double scale, int redraw, const float* ref, uint16_t* h)
 {
     float sigma_f = r32(sigma_b);
     float scale_f = r32(scale);
+    uint32_t st_benign = redraw ? ST_ALT : ST_BENIGN;
+    uint32_t st_t12 = redraw ? ST_ALT_T12 : ST_T12;
+    uint32_t st_t3 = redraw ? ST_ALT_T3 : ST_T3;
     for (uint64_t k = 0; k < count; ++k) {
         uint32_t e = (uint32_t)(e0 + k);
         float a = ref[k];
 
         /* benign hardware noise, Eq. 2 */
         float sc = (benign_mode == ORC_NOISE_BLOCK) ? bscale : r32((double)sigma_f * fabs((double)a));
-        float zb = normal1(seed, ST_BENIGN, cfg_id, s, c, e);
+        float zb = normal1(seed, st_benign, cfg_id, s, c, e);
         if (benign_dist == ORC_DIST_T3) {
             float z1, z2;
-            normal2(seed, ST_T12, cfg_id, s, c, e, &z1, &z2);
-            float z3 = normal1(seed, ST_T3, cfg_id, s, c, e);
+            normal2(seed, st_t12, cfg_id, s, c, e, &z1, &z2);
+            float z3 = normal1(seed, st_t3, cfg_id, s, c, e);
             float q = r32((double)r32((double)r32((double)z1 * z1) + (double)r32((double)z2 * z2)) +
                           (double)r32((double)z3 * z3));
             zb = (q == 0.0f) ? 0.0f : r32((double)zb / (double)r32(sqrt((double)q)));
@@ -406,6 +414,16 @@ int orc_sim_range(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t 
     return 0;
 }
 
+int orc_sim_range(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t seed,
+                  uint32_t cfg_id, int benign_mode, int benign_dist, double sigma_b, float bscale,
+                  int malicious, uint32_t tamper, int tamper_base, float tscale, double flip_p,
+                  double scale, const float* ref, uint16_t* h)
+{
+    return orc_sim_range_ex(s, c, e0, count, seed, cfg_id, benign_mode, benign_dist, sigma_b,
+                            bscale, malicious, tamper, tamper_base, tscale, flip_p, scale, 0, ref,
+                            h);
+}
+
 int orc_sim_block(uint32_t s, uint32_t c, uint32_t T, uint32_t H, uint64_t seed, uint32_t cfg_id,
                   int benign_mode, int benign_dist, double sigma_b, float bscale, int malicious,
                   uint32_t tamper, int tamper_base, float tscale, double flip_p, double scale,
@@ -421,16 +439,17 @@ int orc_sim_block(uint32_t s, uint32_t c, uint32_t T, uint32_t H, uint64_t seed,
 int orc_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed, uint32_t cfg_id,
                    int benign_mode, int benign_dist, double sigma_b, const float* bscale,
                    uint64_t mal_mask, uint32_t tamper, int tamper_base, const float* tscale,
-                   double flip_p, double scale, const float* ref, uint16_t* h)
+                   double flip_p, double scale, int redraw, const float* ref, uint16_t* h)
 {
     uint64_t n = (uint64_t)T * H;
     for (uint32_t s = 0; s < S; ++s)
         for (uint32_t c = 0; c < C; ++c) {
             uint64_t b = (uint64_t)s * C + c;
             int mal = s < 64 && ((mal_mask >> s) & 1u);
-            orc_sim_block(s, c, T, H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
-                          bscale ? bscale[b] : 0.0f, mal, tamper, tamper_base,
-                          tscale ? tscale[b] : 0.0f, flip_p, scale, ref + b * n, h + b * n);
+            orc_sim_range_ex(s, c, 0, n, seed, cfg_id, benign_mode, benign_dist, sigma_b,
+                             bscale ? bscale[b] : 0.0f, mal, tamper, tamper_base,
+                             tscale ? tscale[b] : 0.0f, flip_p, scale, redraw, ref + b * n,
+                             h + b * n);
         }
     return 0;
 }
@@ -483,6 +502,97 @@ void orc_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint1
         }
 }
 
+/* Relative-L2 mismatch against an fp16 reference r (Eq. 4 with the stored
+ * fp32 reference replaced by a second live pass: the noisy-reference
+ * ablation and the redundant-recompute ceiling of Section 4.5). */
+double orc_drift_block_f16ref(uint64_t n, const uint16_t* h, const uint16_t* r, double* D_out,
+                              double* R_out)
+{
+    double D = 0.0, R = 0.0;
+    for (uint64_t e = 0; e < n; ++e) {
+        double hv = orc_f16_value(h[e]);
+        double rv = orc_f16_value(r[e]);
+        double d = hv - rv;
+        D += d * d;
+        R += rv * rv;
+    }
+    if (D_out)
+        *D_out = D;
+    if (R_out)
+        *R_out = R;
+    if (R == 0.0)
+        return D == 0.0 ? 0.0 : INFINITY;
+    return sqrt(D / R);
+}
+
+void orc_drift_score_f16ref(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                            const uint16_t* r, double* score64, float* score32)
+{
+    uint64_t n = (uint64_t)T * H;
+    for (uint32_t s = 0; s < S; ++s)
+        for (uint32_t c = 0; c < C; ++c) {
+            uint64_t b = (uint64_t)s * C + c;
+            double m = orc_drift_block_f16ref(n, h + b * n, r + b * n, NULL, NULL);
+            uint64_t o = (uint64_t)c * S + s;
+            if (score64)
+                score64[o] = m;
+            if (score32)
+                score32[o] = r32(m);
+        }
+}
+
+/* Cosine mismatch, the metric ablation of Section 4.4:
+ *   m~ = 1 - (h . a) / (||h|| ||a||),
+ * with the three sums in extended precision (long double) from exact
+ * products.  A block where h or a is all zero has no angle; it scores 0 when
+ * both are zero and 1 otherwise. */
+double orc_cosine_block(uint64_t n, const uint16_t* h, const float* a)
+{
+    long double hh = 0.0L, aa = 0.0L, ha = 0.0L;
+    for (uint64_t e = 0; e < n; ++e) {
+        long double hv = (long double)orc_f16_value(h[e]);
+        long double av = (long double)a[e];
+        hh += hv * hv;
+        aa += av * av;
+        ha += hv * av;
+    }
+    if (hh == 0.0L || aa == 0.0L)
+        return (hh == 0.0L && aa == 0.0L) ? 0.0 : 1.0;
+    return (double)(1.0L - ha / sqrtl(hh * aa));
+}
+
+/* The same against an fp16 reference r (a second live pass). */
+double orc_cosine_block_f16ref(uint64_t n, const uint16_t* h, const uint16_t* r)
+{
+    long double hh = 0.0L, rr = 0.0L, hr = 0.0L;
+    for (uint64_t e = 0; e < n; ++e) {
+        long double hv = (long double)orc_f16_value(h[e]);
+        long double rv = (long double)orc_f16_value(r[e]);
+        hh += hv * hv;
+        rr += rv * rv;
+        hr += hv * rv;
+    }
+    if (hh == 0.0L || rr == 0.0L)
+        return (hh == 0.0L && rr == 0.0L) ? 0.0 : 1.0;
+    return (double)(1.0L - hr / sqrtl(hh * rr));
+}
+
+void orc_cosine_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                      const float* ref, double* score64, float* score32)
+{
+    uint64_t n = (uint64_t)T * H;
+    for (uint32_t s = 0; s < S; ++s)
+        for (uint32_t c = 0; c < C; ++c) {
+            uint64_t b = (uint64_t)s * C + c;
+            double m = orc_cosine_block(n, h + b * n, ref + b * n);
+            uint64_t o = (uint64_t)c * S + s;
+            if (score64)
+                score64[o] = m;
+            if (score32)
+                score32[o] = r32(m);
+        }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Detection AUROC.                                                          */
 /* Score order: NaN below every number, NaN ties NaN, -0 ties +0, otherwise  */
@@ -502,7 +612,17 @@ static int score_cmp(float x, float y)
 
 int orc_score_cmp(float x, float y) { return score_cmp(x, y); }
 
-enum { ORC_AUROC_CONTROL = 1, ORC_AUROC_POOLED = 2, ORC_CTRL_INCLUDE_TRUE = 4 };
+enum { ORC_AUROC_CONTROL = 1, ORC_AUROC_POOLED = 2, ORC_CTRL_INCLUDE_TRUE = 4, ORC_AUROC_RANDOM = 8 };
+
+/* Random-baseline score of (canary t, stage s) (Section 4.5): Uniform[0, 1)
+ * with 24 random bits, u = (w >> 8) 2^-24, w = Philox word 0 of counter
+ * (t, s, 0, RANDOM|cfg_id). */
+float orc_random_score(uint64_t seed, uint32_t cfg_id, uint32_t t, uint32_t s)
+{
+    uint32_t w[4];
+    philox_at(seed, t, s, 0, ST_RANDOM, cfg_id, w);
+    return (float)((double)(w[0] >> 8) * 0x1p-24);
+}
 
 /* Scrambled-label stage for canary t (Section 4.5): a uniformly chosen
  * benign stage j* != i*.  With benign stages b_0 < b_1 < ... < b_{B-1},
@@ -530,7 +650,7 @@ int orc_scramble_jstar(uint32_t S, uint64_t pos_mask, uint64_t seed, uint32_t cf
  *   configuration (the Mann-Whitney U of all C*S scores pooled). */
 int orc_auroc_config(uint32_t S, uint32_t C, const float* scores, uint64_t pos_mask,
                      uint64_t seed, uint32_t cfg_id, uint32_t flags, uint64_t* counts,
-                     uint64_t* pooled)
+                     uint64_t* pooled, uint64_t* baseline)
 {
     if (S > 64)
         return 1;
@@ -539,6 +659,9 @@ int orc_auroc_config(uint32_t S, uint32_t C, const float* scores, uint64_t pos_m
     if (pooled)
         for (int k = 0; k < 3; ++k)
             pooled[k] = 0;
+    if (baseline)
+        for (int k = 0; k < 3; ++k)
+            baseline[k] = 0;
 
     for (uint32_t t = 0; t < C; ++t) {
         const float* m = scores + (uint64_t)t * S;
@@ -569,6 +692,24 @@ int orc_auroc_config(uint32_t S, uint32_t C, const float* scores, uint64_t pos_m
                 }
             }
         }
+    }
+
+    /* Random baseline: Eq. 5 counts with every score replaced by a uniform. */
+    if (baseline && (flags & ORC_AUROC_RANDOM)) {
+        for (uint32_t t = 0; t < C; ++t)
+            for (uint32_t i = 0; i < S; ++i) {
+                if (!((pos_mask >> i) & 1u))
+                    continue;
+                float ui = orc_random_score(seed, cfg_id, t, i);
+                for (uint32_t j = 0; j < S; ++j) {
+                    if ((pos_mask >> j) & 1u)
+                        continue;
+                    int r = score_cmp(ui, orc_random_score(seed, cfg_id, t, j));
+                    baseline[0] += (r > 0);
+                    baseline[1] += (r == 0);
+                    baseline[2] += 1;
+                }
+            }
     }
 
     if (pooled && (flags & ORC_AUROC_POOLED)) {

@@ -22,7 +22,7 @@ NOISE_ELEMENTWISE, NOISE_BLOCK = 0, 1
 DIST_GAUSS, DIST_T3 = 0, 1
 T_ADD, T_FLIP, T_SCALE = 1, 2, 4
 BASE_BENIGN, BASE_CLEAN = 0, 1
-AUROC_CONTROL, AUROC_POOLED, CTRL_INCLUDE_TRUE = 1, 2, 4
+AUROC_CONTROL, AUROC_POOLED, CTRL_INCLUDE_TRUE, AUROC_RANDOM = 1, 2, 4, 8
 
 
 class CdtError(RuntimeError):
@@ -39,7 +39,7 @@ class SimParams(ctypes.Structure):
         ("benign_dist", ctypes.c_uint32),
         ("tamper", ctypes.c_uint32),
         ("tamper_base", ctypes.c_uint32),
-        ("reserved", ctypes.c_uint32),
+        ("redraw", ctypes.c_uint32),
         ("mal_mask", ctypes.c_uint64),
         ("sigma_b", ctypes.c_double),
         ("flip_p", ctypes.c_double),
@@ -73,9 +73,14 @@ _SIGS = {
     "cdt_canary_sim": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp],
                        ctypes.c_int),
     "cdt_drift_score": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "cdt_drift_score_f16ref": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+                               ctypes.c_int),
+    "cdt_cosine_score": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "cdt_cosine_score_f16ref": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+                                ctypes.c_int),
     "cdt_auroc_workspace_bytes": ([_u32], _sz),
-    "cdt_auroc": ([_u32, ctypes.POINTER(AurocCfg), _vp, _u64, _u64, _u32, _vp, _vp, _vp, _sz, _vp],
-                  ctypes.c_int),
+    "cdt_auroc": ([_u32, ctypes.POINTER(AurocCfg), _vp, _u64, _u64, _u32, _vp, _vp, _vp, _vp, _sz,
+                   _vp], ctypes.c_int),
 }
 
 _LIB = None
@@ -208,9 +213,9 @@ def block_scales(sumsq, sumabs, T, H, eps, sigma_b, tscale=None, bscale=None):
 
 def sim_params(*, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE, benign_dist=DIST_GAUSS,
                sigma_b=1e-3, mal_mask=0, tamper=0, tamper_base=BASE_BENIGN, flip_p=0.0,
-               scale=1.0, bscale=None, tscale=None):
-    return SimParams(seed, cfg_id, benign_mode, benign_dist, tamper, tamper_base, 0, mal_mask,
-                     sigma_b, flip_p, scale,
+               scale=1.0, bscale=None, tscale=None, redraw=False):
+    return SimParams(seed, cfg_id, benign_mode, benign_dist, tamper, tamper_base, int(redraw),
+                     mal_mask, sigma_b, flip_p, scale,
                      None if bscale is None else bscale.data_ptr(),
                      None if tscale is None else tscale.data_ptr())
 
@@ -230,20 +235,39 @@ def canary_sim(ref, out=None, *, bscale=None, tscale=None, **kw):
     return out
 
 
+def _drift(fn, h, ref, ref_dtype, out, sums, nsums, ws):
+    torch = _torch()
+    _need(h, "h", torch.float16)
+    S, C, T, H = h.shape
+    _need(ref, "ref", ref_dtype, (S, C, T, H))
+    out = _empty((C, S), torch.float32, h) if out is None else out
+    _need(out, "score", torch.float32, (C, S))
+    if sums is not None:
+        _need(sums, "sums", torch.float64, (C, S, nsums))
+    ws, nbytes = _ws_arg(ws, S, C, T, H, h)
+    _check(fn(S, C, T, H, _ptr(h), _ptr(ref), _ptr(out), _ptr(sums), _ptr(ws), nbytes,
+              _stream()))
+    return out
+
+
 def drift_score(h, ref, out=None, num_den=None, ws=None):
     """Eq. 4 per block -> scores [C][S] fp32 (and optional [C][S][2] fp64)."""
-    torch = _torch()
-    _need(ref, "ref", torch.float32)
-    S, C, T, H = ref.shape
-    _need(h, "h", torch.float16, (S, C, T, H))
-    out = _empty((C, S), torch.float32, ref) if out is None else out
-    _need(out, "score", torch.float32, (C, S))
-    if num_den is not None:
-        _need(num_den, "num_den", torch.float64, (C, S, 2))
-    ws, nbytes = _ws_arg(ws, S, C, T, H, ref)
-    _check(lib().cdt_drift_score(S, C, T, H, _ptr(h), _ptr(ref), _ptr(out), _ptr(num_den),
-                                 _ptr(ws), nbytes, _stream()))
-    return out
+    return _drift(lib().cdt_drift_score, h, ref, _torch().float32, out, num_den, 2, ws)
+
+
+def drift_score_f16ref(h, r, out=None, num_den=None, ws=None):
+    """Eq. 4 against an fp16 reference (a second live pass) -> [C][S] fp32."""
+    return _drift(lib().cdt_drift_score_f16ref, h, r, _torch().float16, out, num_den, 2, ws)
+
+
+def cosine_score(h, ref, out=None, sums=None, ws=None):
+    """Cosine mismatch 1 - cos(h, a) per block -> [C][S] fp32 (sums: [C][S][3])."""
+    return _drift(lib().cdt_cosine_score, h, ref, _torch().float32, out, sums, 3, ws)
+
+
+def cosine_score_f16ref(h, r, out=None, sums=None, ws=None):
+    """Cosine mismatch against an fp16 reference (a second live pass)."""
+    return _drift(lib().cdt_cosine_score_f16ref, h, r, _torch().float16, out, sums, 3, ws)
 
 
 def auroc_cfg_array(cfgs):
@@ -256,10 +280,11 @@ def auroc_cfg_array(cfgs):
 
 
 def auroc(cfgs, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_POOLED, counts=None, pooled=None,
-          ws=None):
+          baseline=None, ws=None):
     """Batched AUROC counts.  cfgs: iterable of (S, C, score_off, pos_mask,
     cfg_id); scores: flat (or any contiguous) fp32 device tensor.
-    Returns (counts [n][6] uint64-as-int64, pooled [n][3] or None)."""
+    Returns (counts [n][6], pooled [n][3] or None, baseline [n][3] or None),
+    uint64 counts held in int64 tensors."""
     torch = _torch()
     _need(scores, "scores", torch.float32)
     arr, n = auroc_cfg_array(cfgs)
@@ -268,11 +293,15 @@ def auroc(cfgs, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_POOLED, counts=No
     if flags & AUROC_POOLED:
         pooled = _empty((n, 3), torch.int64, scores) if pooled is None else pooled
         _need(pooled, "pooled", torch.int64, (n, 3))
+    if flags & AUROC_RANDOM:
+        baseline = _empty((n, 3), torch.int64, scores) if baseline is None else baseline
+        _need(baseline, "baseline", torch.int64, (n, 3))
     if ws is None:
         ws = _empty((max(16, lib().cdt_auroc_workspace_bytes(n)),), torch.uint8, scores)
     _check(lib().cdt_auroc(n, arr, _ptr(scores), scores.numel(), seed, flags, _ptr(counts),
-                           _ptr(pooled), _ptr(ws), ws.numel(), _stream()))
-    return counts, (pooled if flags & AUROC_POOLED else None)
+                           _ptr(pooled), _ptr(baseline), _ptr(ws), ws.numel(), _stream()))
+    return (counts, pooled if flags & AUROC_POOLED else None,
+            baseline if flags & AUROC_RANDOM else None)
 
 
 def strict_auroc(counts_row):

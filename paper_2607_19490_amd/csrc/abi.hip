@@ -58,7 +58,7 @@ bool empty(uint32_t S, uint32_t C, uint32_t T, uint32_t H) {
 
 extern "C" {
 
-int cdt_version(void) { return 1; }
+int cdt_version(void) { return 2; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -92,7 +92,7 @@ int cdt_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
 size_t cdt_reduce_workspace_bytes(uint32_t S, uint32_t C, uint32_t T, uint32_t H) {
     const uint64_t n = static_cast<uint64_t>(T) * H;
     const uint64_t cpb = cdt::reduce_chunks_per_block(n);
-    return static_cast<size_t>(cpb * S * C * 2 * sizeof(double));
+    return static_cast<size_t>(cpb * S * C * cdt::kReduceMaxSums * sizeof(double));
 }
 
 int cdt_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,
@@ -141,7 +141,7 @@ int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim
     if (p->benign_dist > CDT_DIST_T3) return fail(CDT_EINVAL, "cdt_canary_sim: bad benign_dist");
     if (p->tamper & ~7u) return fail(CDT_EINVAL, "cdt_canary_sim: bad tamper flags");
     if (p->tamper_base > CDT_BASE_CLEAN) return fail(CDT_EINVAL, "cdt_canary_sim: bad tamper_base");
-    if (p->reserved != 0) return fail(CDT_EINVAL, "cdt_canary_sim: reserved must be 0");
+    if (p->redraw > 1) return fail(CDT_EINVAL, "cdt_canary_sim: redraw must be 0 or 1");
     if (!(p->sigma_b >= 0.0) || !isfinite(p->sigma_b))
         return fail(CDT_EINVAL, "cdt_canary_sim: sigma_b must be finite and >= 0");
     if (!(p->flip_p >= 0.0 && p->flip_p <= 1.0))
@@ -168,6 +168,7 @@ int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim
     L.benign_dist = p->benign_dist;
     L.tamper = p->tamper;
     L.tamper_base = p->tamper_base;
+    L.redraw = p->redraw;
     L.mal_mask = mal;
     L.sigma_b = static_cast<float>(p->sigma_b);
     // Flip selection: u < floor(p 2^32) with p < 1 (so the threshold fits 32
@@ -181,26 +182,58 @@ int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim
                          "cdt_canary_sim");
 }
 
-int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
-                    const float* ref, float* score, double* num_den, void* ws, size_t ws_bytes,
-                    void* stream) {
-    int rc = check_shape("cdt_drift_score", S, C, T, H);
+namespace {
+
+int drift_common(const char* fn, cdt::DriftMetric metric, uint32_t S, uint32_t C, uint32_t T,
+                 uint32_t H, const uint16_t* h, const void* ref, float* score, double* sums,
+                 void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_shape(fn, S, C, T, H);
     if (rc) return rc;
     if (static_cast<uint64_t>(S) * C == 0) return ok();
-    if (!score) return fail(CDT_EINVAL, "cdt_drift_score: score is NULL");
+    if (!score) return fail(CDT_EINVAL, "%s: score is NULL", fn);
     if (static_cast<uint64_t>(T) * H > 0) {
-        if (!h || !ref) return fail(CDT_EINVAL, "cdt_drift_score: NULL array");
+        if (!h || !ref) return fail(CDT_EINVAL, "%s: NULL array", fn);
         if (!aligned16(h) || !aligned16(ref))
-            return fail(CDT_EALIGN, "cdt_drift_score: arrays must be 16-byte aligned");
+            return fail(CDT_EALIGN, "%s: arrays must be 16-byte aligned", fn);
     }
     const size_t need = cdt_reduce_workspace_bytes(S, C, T, H);
     if (need > 0 && (!ws || ws_bytes < need))
-        return fail(CDT_EINVAL, "cdt_drift_score: workspace of %zu bytes needed, %zu given", need,
+        return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
                     ws ? ws_bytes : 0);
-    if (ws && !aligned16(ws)) return fail(CDT_EALIGN, "cdt_drift_score: ws must be 16-byte aligned");
-    return device_status(cdt::launch_drift_score(S, C, T, H, h, ref, score, num_den, ws,
-                                                 static_cast<hipStream_t>(stream)),
-                         "cdt_drift_score");
+    if (ws && !aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
+    return device_status(cdt::launch_drift(metric, S, C, T, H, h, ref, score, sums, ws,
+                                           static_cast<hipStream_t>(stream)),
+                         fn);
+}
+
+}  // namespace
+
+int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                    const float* ref, float* score, double* num_den, void* ws, size_t ws_bytes,
+                    void* stream) {
+    return drift_common("cdt_drift_score", cdt::DriftMetric::kL2, S, C, T, H, h, ref, score,
+                        num_den, ws, ws_bytes, stream);
+}
+
+int cdt_drift_score_f16ref(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                           const uint16_t* r, float* score, double* num_den, void* ws,
+                           size_t ws_bytes, void* stream) {
+    return drift_common("cdt_drift_score_f16ref", cdt::DriftMetric::kL2HalfRef, S, C, T, H, h, r,
+                        score, num_den, ws, ws_bytes, stream);
+}
+
+int cdt_cosine_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                     const float* ref, float* score, double* sums, void* ws, size_t ws_bytes,
+                     void* stream) {
+    return drift_common("cdt_cosine_score", cdt::DriftMetric::kCosine, S, C, T, H, h, ref, score,
+                        sums, ws, ws_bytes, stream);
+}
+
+int cdt_cosine_score_f16ref(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                            const uint16_t* r, float* score, double* sums, void* ws,
+                            size_t ws_bytes, void* stream) {
+    return drift_common("cdt_cosine_score_f16ref", cdt::DriftMetric::kCosineHalfRef, S, C, T, H,
+                        h, r, score, sums, ws, ws_bytes, stream);
 }
 
 size_t cdt_auroc_workspace_bytes(uint32_t n_cfg) {
@@ -208,14 +241,16 @@ size_t cdt_auroc_workspace_bytes(uint32_t n_cfg) {
 }
 
 int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, uint64_t n_scores,
-              uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled, void* ws,
-              size_t ws_bytes, void* stream) {
+              uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
+              uint64_t* baseline, void* ws, size_t ws_bytes, void* stream) {
     static_assert(sizeof(cdt_auroc_cfg) == sizeof(cdt::AurocCfgDev), "cfg layout");
-    if (flags & ~7u) return fail(CDT_EINVAL, "cdt_auroc: bad flags");
+    if (flags & ~15u) return fail(CDT_EINVAL, "cdt_auroc: bad flags");
     if (n_cfg == 0) return ok();
     if (!cfgs || !counts) return fail(CDT_EINVAL, "cdt_auroc: NULL cfgs or counts");
     if ((flags & CDT_AUROC_POOLED) && !pooled)
         return fail(CDT_EINVAL, "cdt_auroc: pooled counts requested but pooled is NULL");
+    if ((flags & CDT_AUROC_RANDOM) && !baseline)
+        return fail(CDT_EINVAL, "cdt_auroc: baseline counts requested but baseline is NULL");
     if (n_cfg > (1u << 24)) return fail(CDT_ELIMIT, "cdt_auroc: n_cfg above 2^24");
     for (uint32_t g = 0; g < n_cfg; ++g) {
         const cdt_auroc_cfg& c = cfgs[g];
@@ -243,7 +278,7 @@ int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, ui
     hipError_t e = hipMemcpyAsync(ws, cfgs, need, hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return device_status(e, "cdt_auroc: config upload");
     return device_status(cdt::launch_auroc(n_cfg, static_cast<const cdt::AurocCfgDev*>(ws),
-                                           scores, seed, flags, counts, pooled, st),
+                                           scores, seed, flags, counts, pooled, baseline, st),
                          "cdt_auroc");
 }
 

@@ -38,6 +38,8 @@ enum : uint32_t {
     kStreamRandom = 7,
     kStreamOutlier = 8,
     kStreamAlt = 9,
+    kStreamAltT12 = 10,
+    kStreamAltT3 = 11,
 };
 
 struct Words4 {

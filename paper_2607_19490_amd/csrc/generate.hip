@@ -143,6 +143,9 @@ struct SimArgs {
     const float* tscale;
 };
 
+// Specialised on the two launch-uniform noise modes so that the common
+// (Gaussian, elementwise) path carries no Student-t or block-scale code.
+template <bool kT3, bool kBlock>
 __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
                                                                  const float* __restrict__ ref,
                                                                  uint16_t* __restrict__ h) {
@@ -150,7 +153,7 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
     for (uint64_t it = blockIdx.x; it < A.total_chunks; it += gridDim.x) {
         const ChunkPos p = chunk_pos(xcd_contiguous(it, A.total_chunks), A.chunks_per_block, A.C);
         const bool mal = (A.mal_mask >> p.s) & 1u;
-        const float bsc = A.block_mode ? A.bscale[p.block] : 0.0f;
+        const float bsc = kBlock ? A.bscale[p.block] : 0.0f;
         const float tsc = (mal && (A.tamper & 1u)) ? A.tscale[p.block] : 0.0f;
         const f32x4* in = reinterpret_cast<const f32x4*>(ref + p.block * n);
         u32x4* out = reinterpret_cast<u32x4*>(h + p.block * n);
@@ -177,7 +180,7 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
             // Eq. 2: benign hardware noise.
             float zb[8];
             normals8(A.key, e0, p.c, p.s, A.tag_benign, zb);
-            if (A.t3) {
+            if (kT3) {
                 float z3[8];
                 normals8(A.key, e0, p.c, p.s, A.tag_t3, z3);
 #pragma unroll
@@ -192,7 +195,7 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
             float v[8];
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
-                const float sc = A.block_mode ? bsc : A.sigma_b * fabsf(a[k]);
+                const float sc = kBlock ? bsc : A.sigma_b * fabsf(a[k]);
                 v[k] = a[k] + sc * zb[k];
             }
 
@@ -232,9 +235,9 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
     }
 }
 
-// Grid for a chunked elementwise walk: enough workgroups to fill 256 CUs
-// several times over; larger jobs loop with a stride (16384) that is a
-// multiple of the XCD count, as xcd_contiguous needs.
+// Grid for a chunked elementwise walk: 64 workgroups per CU; larger jobs
+// loop with a stride (16384) that is a multiple of the XCD count, as
+// xcd_contiguous needs.
 inline uint32_t gen_grid(uint64_t total_chunks) {
     const uint64_t cap = 256ull * 64;
     return static_cast<uint32_t>(total_chunks < cap ? total_chunks : cap);
@@ -288,9 +291,10 @@ hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, 
     A.chunks_per_block = (A.n8 + kGenChunkGroups - 1) / kGenChunkGroups;
     A.total_chunks = A.chunks_per_block * nblocks;
     A.key = Key{static_cast<uint32_t>(p.seed), static_cast<uint32_t>(p.seed >> 32)};
-    A.tag_benign = stream_tag(kStreamBenign, p.cfg_id);
-    A.tag_t12 = stream_tag(kStreamT12, p.cfg_id);
-    A.tag_t3 = stream_tag(kStreamT3, p.cfg_id);
+    // An independent benign recompute draws its noise from the ALT streams.
+    A.tag_benign = stream_tag(p.redraw ? kStreamAlt : kStreamBenign, p.cfg_id);
+    A.tag_t12 = stream_tag(p.redraw ? kStreamAltT12 : kStreamT12, p.cfg_id);
+    A.tag_t3 = stream_tag(p.redraw ? kStreamAltT3 : kStreamT3, p.cfg_id);
     A.tag_add = stream_tag(kStreamTamperAdd, p.cfg_id);
     A.tag_flip = stream_tag(kStreamTamperFlip, p.cfg_id);
     A.block_mode = p.benign_mode == 1;
@@ -304,8 +308,15 @@ hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, 
     A.scale = p.scale;
     A.bscale = p.bscale;
     A.tscale = p.tscale;
-    hipLaunchKernelGGL(canary_sim_kernel, dim3(gen_grid(A.total_chunks)), dim3(kGenThreads), 0,
-                       st, A, ref, h);
+    const dim3 grid(gen_grid(A.total_chunks)), block(kGenThreads);
+    if (A.t3 && A.block_mode)
+        hipLaunchKernelGGL((canary_sim_kernel<true, true>), grid, block, 0, st, A, ref, h);
+    else if (A.t3)
+        hipLaunchKernelGGL((canary_sim_kernel<true, false>), grid, block, 0, st, A, ref, h);
+    else if (A.block_mode)
+        hipLaunchKernelGGL((canary_sim_kernel<false, true>), grid, block, 0, st, A, ref, h);
+    else
+        hipLaunchKernelGGL((canary_sim_kernel<false, false>), grid, block, 0, st, A, ref, h);
     return hipGetLastError();
 }
 

@@ -32,9 +32,16 @@ __device__ __forceinline__ uint32_t nth_set_bit(uint64_t m, uint32_t r) {
     return static_cast<uint32_t>(__builtin_ctzll(m));
 }
 
+// Random-baseline score of (canary t, shard s): 24 random bits scaled into
+// [0, 1), exact in fp32.
+__device__ __forceinline__ float random_score(Key key, uint32_t t, uint32_t s, uint32_t tag) {
+    return static_cast<float>(draw(key, t, s, 0, tag).x >> 8) * 0x1p-24f;
+}
+
 __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
     const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, Key key,
-    uint32_t flags, unsigned long long* __restrict__ counts) {
+    uint32_t flags, unsigned long long* __restrict__ counts,
+    unsigned long long* __restrict__ baseline) {
     const AurocCfgDev cfg = cfgs[blockIdx.x];
     const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const uint64_t all = shard_mask(cfg.S);
@@ -44,10 +51,12 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
     const bool lane_pos = lane_in && ((pos >> lane) & 1u);
     const bool control = flags & 1u;
     const bool include_true = flags & 4u;
+    const bool random = flags & 8u;
     const uint32_t n_benign = __builtin_popcountll(neg);
     const uint32_t tag = stream_tag(kStreamScramble, cfg.cfg_id);
+    const uint32_t tag_random = stream_tag(kStreamRandom, cfg.cfg_id);
 
-    unsigned long long g = 0, e = 0, gc = 0, ec = 0;
+    unsigned long long g = 0, e = 0, gc = 0, ec = 0, gr = 0, er = 0;
     for (uint32_t t = wave; t < cfg.C; t += kCountWaves) {
         const float* row = scores + cfg.score_off + static_cast<uint64_t>(t) * cfg.S;
         const uint32_t k = lane_in ? order_key(row[lane]) : 0u;
@@ -56,6 +65,16 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
             if (lane_pos && ((neg >> j) & 1u)) {
                 g += k > kj;
                 e += k == kj;
+            }
+        }
+        if (random) {
+            const uint32_t kr = lane_in ? order_key(random_score(key, t, lane, tag_random)) : 0u;
+            for (uint32_t j = 0; j < cfg.S; ++j) {
+                const uint32_t kj = __shfl(kr, j, kWave);
+                if (lane_pos && ((neg >> j) & 1u)) {
+                    gr += kr > kj;
+                    er += kr == kj;
+                }
             }
         }
         if (control && n_benign > 0) {
@@ -71,21 +90,18 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
         }
     }
 
-    __shared__ unsigned long long lds[4][kCountWaves];
-    g = wave_sum(g);
-    e = wave_sum(e);
-    gc = wave_sum(gc);
-    ec = wave_sum(ec);
+    __shared__ unsigned long long lds[6][kCountWaves];
+    unsigned long long part[6] = {g, e, gc, ec, gr, er};
+#pragma unroll
+    for (int q = 0; q < 6; ++q) part[q] = wave_sum(part[q]);
     if (lane == 0) {
-        lds[0][wave] = g;
-        lds[1][wave] = e;
-        lds[2][wave] = gc;
-        lds[3][wave] = ec;
+#pragma unroll
+        for (int q = 0; q < 6; ++q) lds[q][wave] = part[q];
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        unsigned long long tot[4] = {0, 0, 0, 0};
-        for (int q = 0; q < 4; ++q)
+        unsigned long long tot[6] = {0, 0, 0, 0, 0, 0};
+        for (int q = 0; q < 6; ++q)
             for (int w = 0; w < kCountWaves; ++w) tot[q] += lds[q][w];
         const unsigned long long n_pos = __builtin_popcountll(pos);
         unsigned long long* out = counts + 6ull * blockIdx.x;
@@ -97,6 +113,12 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
         out[3] = control ? tot[2] : 0;
         out[4] = control ? tot[3] : 0;
         out[5] = static_cast<unsigned long long>(cfg.C) * n_ctrl;
+        if (random) {
+            unsigned long long* rb = baseline + 3ull * blockIdx.x;
+            rb[0] = tot[4];
+            rb[1] = tot[5];
+            rb[2] = out[2];
+        }
     }
 }
 
@@ -216,11 +238,12 @@ __global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
 
 hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float* scores,
                         uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
-                        hipStream_t st) {
+                        uint64_t* baseline, hipStream_t st) {
     if (n_cfg == 0) return hipSuccess;
     const Key key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)};
     hipLaunchKernelGGL(auroc_counts_kernel, dim3(n_cfg), dim3(kCountThreads), 0, st, cfgs_dev,
-                       scores, key, flags, reinterpret_cast<unsigned long long*>(counts));
+                       scores, key, flags, reinterpret_cast<unsigned long long*>(counts),
+                       reinterpret_cast<unsigned long long*>(baseline));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !(flags & 2u)) return e;
     hipLaunchKernelGGL(auroc_pooled_kernel, dim3(n_cfg), dim3(kPoolThreads), 0, st, cfgs_dev,

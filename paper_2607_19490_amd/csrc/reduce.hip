@@ -28,55 +28,75 @@ namespace {
 constexpr uint32_t kChunkGroups = static_cast<uint32_t>(kReduceChunkElems / 8);
 constexpr int kWavesPerGroup = kReduceThreads / kWave;
 
-struct Pair {
-    double a, b;
-};
-
-// Sum a per-thread pair over the workgroup; thread 0 gets the result.
-__device__ __forceinline__ Pair block_sum(Pair v) {
-    __shared__ double lds[2][kWavesPerGroup];
-    v.a = wave_sum(v.a);
-    v.b = wave_sum(v.b);
+// Sum kN per-thread values over the workgroup; thread 0 gets the result.
+template <int kN>
+__device__ __forceinline__ void block_sum(double (&v)[kN]) {
+    __shared__ double lds[kN][kWavesPerGroup];
+#pragma unroll
+    for (int k = 0; k < kN; ++k) v[k] = wave_sum(v[k]);
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     if (lane == 0) {
-        lds[0][wave] = v.a;
-        lds[1][wave] = v.b;
+#pragma unroll
+        for (int k = 0; k < kN; ++k) lds[k][wave] = v[k];
     }
     __syncthreads();
-    Pair r{0.0, 0.0};
     if (threadIdx.x == 0) {
 #pragma unroll
-        for (int w = 0; w < kWavesPerGroup; ++w) {
-            r.a += lds[0][w];
-            r.b += lds[1][w];
+        for (int k = 0; k < kN; ++k) {
+            double t = 0.0;
+            for (int w = 0; w < kWavesPerGroup; ++w) t += lds[k][w];
+            v[k] = t;
         }
     }
     __syncthreads();
-    return r;
 }
 
-__device__ __forceinline__ void accumulate8(const u32x4& hv, const f32x4& a0, const f32x4& a1,
-                                            double& D, double& R) {
+// Per-metric element step.  h and the reference are widened exactly to
+// fp64, so d = h - a is exact and the sums carry no cancellation.
+template <DriftMetric kM>
+struct DriftTraits {
+    static constexpr bool kHalfRef =
+        kM == DriftMetric::kL2HalfRef || kM == DriftMetric::kCosineHalfRef;
+    static constexpr bool kCos = kM == DriftMetric::kCosine || kM == DriftMetric::kCosineHalfRef;
+    static constexpr int kSums = kCos ? 3 : 2;
+
+    __device__ static __forceinline__ void add(double hv, double av, double (&acc)[kSums]) {
+        const double d = hv - av;
+        acc[0] = fma(d, d, acc[0]);      // D = sum d^2
+        acc[1] = fma(av, av, acc[1]);    // R = A = sum a^2
+        if constexpr (kSums == 3) acc[2] = fma(av, d, acc[2]);  // P = sum a d
+    }
+};
+
+template <DriftMetric kM>
+__device__ __forceinline__ void accumulate8(const u32x4& hv, const u32x4& r_half,
+                                            const f32x4& a0, const f32x4& a1,
+                                            double (&acc)[DriftTraits<kM>::kSums]) {
     const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
+    const uint32_t rw[4] = {r_half.x, r_half.y, r_half.z, r_half.w};
     const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const double h_lo = static_cast<double>(half_bits_to_float(hw[k] & 0xFFFFu));
         const double h_hi = static_cast<double>(half_bits_to_float(hw[k] >> 16));
-        const double a_lo = static_cast<double>(av[2 * k]);
-        const double a_hi = static_cast<double>(av[2 * k + 1]);
-        const double d_lo = h_lo - a_lo;
-        const double d_hi = h_hi - a_hi;
-        D = fma(d_lo, d_lo, D);
-        R = fma(a_lo, a_lo, R);
-        D = fma(d_hi, d_hi, D);
-        R = fma(a_hi, a_hi, R);
+        double a_lo, a_hi;
+        if constexpr (DriftTraits<kM>::kHalfRef) {
+            a_lo = static_cast<double>(half_bits_to_float(rw[k] & 0xFFFFu));
+            a_hi = static_cast<double>(half_bits_to_float(rw[k] >> 16));
+        } else {
+            a_lo = static_cast<double>(av[2 * k]);
+            a_hi = static_cast<double>(av[2 * k + 1]);
+        }
+        DriftTraits<kM>::add(h_lo, a_lo, acc);
+        DriftTraits<kM>::add(h_hi, a_hi, acc);
     }
 }
 
+template <DriftMetric kM>
 __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
-    const uint16_t* __restrict__ h, const float* __restrict__ ref, uint32_t n8,
-    uint64_t chunks_per_block, uint64_t total_chunks, double2* __restrict__ partial) {
+    const uint16_t* __restrict__ h, const void* __restrict__ ref, uint32_t n8,
+    uint64_t chunks_per_block, uint64_t total_chunks, double* __restrict__ partial) {
+    using Tr = DriftTraits<kM>;
     const uint64_t n = static_cast<uint64_t>(n8) * 8;
     for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
         const uint64_t chunk = xcd_contiguous(it, total_chunks);
@@ -84,54 +104,89 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
         const uint32_t g0 = static_cast<uint32_t>(chunk - b * chunks_per_block) * kChunkGroups;
         const uint32_t g_end = min(g0 + kChunkGroups, n8);
         const u32x4* hb = reinterpret_cast<const u32x4*>(h + b * n);
-        const f32x4* ab = reinterpret_cast<const f32x4*>(ref + b * n);
-        double D = 0.0, R = 0.0;
+        const f32x4* ab = nullptr;  // fp32 reference block
+        const u32x4* rb = nullptr;  // fp16 reference block
+        if constexpr (Tr::kHalfRef)
+            rb = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(ref) + b * n);
+        else
+            ab = reinterpret_cast<const f32x4*>(static_cast<const float*>(ref) + b * n);
+        double acc[Tr::kSums];
+#pragma unroll
+        for (int k = 0; k < Tr::kSums; ++k) acc[k] = 0.0;
         for (uint32_t base = g0; base < g_end; base += kReduceThreads * kReduceUnroll) {
-            u32x4 hv[kReduceUnroll];
+            u32x4 hv[kReduceUnroll], rv[kReduceUnroll];
             f32x4 a0[kReduceUnroll], a1[kReduceUnroll];
 #pragma unroll
             for (int u = 0; u < kReduceUnroll; ++u) {
                 const uint32_t g = base + u * kReduceThreads + threadIdx.x;
+                hv[u] = u32x4{0u, 0u, 0u, 0u};
+                rv[u] = hv[u];
+                a0[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+                a1[u] = a0[u];
                 if (g < g_end) {
                     hv[u] = __builtin_nontemporal_load(hb + g);
-                    a0[u] = __builtin_nontemporal_load(ab + 2 * g);
-                    a1[u] = __builtin_nontemporal_load(ab + 2 * g + 1);
-                } else {
-                    hv[u] = u32x4{0u, 0u, 0u, 0u};
-                    a0[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-                    a1[u] = a0[u];
+                    if constexpr (Tr::kHalfRef) {
+                        rv[u] = __builtin_nontemporal_load(rb + g);
+                    } else {
+                        a0[u] = __builtin_nontemporal_load(ab + 2 * g);
+                        a1[u] = __builtin_nontemporal_load(ab + 2 * g + 1);
+                    }
                 }
             }
 #pragma unroll
-            for (int u = 0; u < kReduceUnroll; ++u) accumulate8(hv[u], a0[u], a1[u], D, R);
+            for (int u = 0; u < kReduceUnroll; ++u) accumulate8<kM>(hv[u], rv[u], a0[u], a1[u], acc);
         }
-        const Pair s = block_sum(Pair{D, R});
-        if (threadIdx.x == 0) partial[chunk] = make_double2(s.a, s.b);
+        block_sum<Tr::kSums>(acc);
+        if (threadIdx.x == 0) {
+#pragma unroll
+            for (int k = 0; k < Tr::kSums; ++k) partial[chunk * Tr::kSums + k] = acc[k];
+        }
     }
 }
 
-__global__ void drift_combine_kernel(const double2* __restrict__ partial, uint64_t chunks_per_block,
+// Eq. 4 from the block sums: m = sqrt(D / R); R = 0 gives 0 (D = 0) or +inf.
+__device__ __forceinline__ double relative_l2(double D, double R) {
+    if (R == 0.0) return (D == 0.0) ? 0.0 : static_cast<double>(INFINITY);
+    return sqrt(D / R);
+}
+
+// 1 - cos(h, a) from D = |h-a|^2, A = |a|^2, P = a.(h-a): with |h|^2 = A + 2P + D
+// and h.a = A + P, 1 - cos = (A D - P^2) / (sqrt(A |h|^2) (sqrt(A |h|^2) + A + P)),
+// which keeps full relative accuracy as the angle goes to 0.
+__device__ __forceinline__ double cosine_mismatch(double D, double A, double P) {
+    const double hn = A + 2.0 * P + D;
+    if (A == 0.0 || hn <= 0.0) return (A == 0.0 && hn <= 0.0) ? 0.0 : 1.0;
+    const double g = sqrt(A * hn);
+    const double dot = A + P;
+    if (dot > 0.0) return (A * D - P * P) / (g * (g + dot));
+    return 1.0 - dot / g;
+}
+
+template <DriftMetric kM>
+__global__ void drift_combine_kernel(const double* __restrict__ partial, uint64_t chunks_per_block,
                                      uint64_t nblocks, uint32_t S, uint32_t C,
-                                     float* __restrict__ score, double* __restrict__ num_den) {
+                                     float* __restrict__ score, double* __restrict__ sums) {
+    using Tr = DriftTraits<kM>;
     const uint64_t b = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (b >= nblocks) return;
-    double D = 0.0, R = 0.0;
+    double acc[Tr::kSums];
+#pragma unroll
+    for (int k = 0; k < Tr::kSums; ++k) acc[k] = 0.0;
     for (uint64_t i = 0; i < chunks_per_block; ++i) {
-        const double2 p = partial[b * chunks_per_block + i];
-        D += p.x;
-        R += p.y;
+#pragma unroll
+        for (int k = 0; k < Tr::kSums; ++k) acc[k] += partial[(b * chunks_per_block + i) * Tr::kSums + k];
     }
     double m;
-    if (R == 0.0)
-        m = (D == 0.0) ? 0.0 : static_cast<double>(INFINITY);
+    if constexpr (Tr::kCos)
+        m = cosine_mismatch(acc[0], acc[1], acc[2]);
     else
-        m = sqrt(D / R);
+        m = relative_l2(acc[0], acc[1]);
     const uint64_t s = b / C, c = b - s * C;
     const uint64_t o = c * S + s;
     score[o] = static_cast<float>(m);
-    if (num_den) {
-        num_den[2 * o] = D;
-        num_den[2 * o + 1] = R;
+    if (sums) {
+#pragma unroll
+        for (int k = 0; k < Tr::kSums; ++k) sums[Tr::kSums * o + k] = acc[k];
     }
 }
 
@@ -156,8 +211,9 @@ __global__ __launch_bounds__(kReduceThreads) void ref_stats_partial_kernel(
                 M += fabs(x);
             }
         }
-        const Pair s = block_sum(Pair{Q, M});
-        if (threadIdx.x == 0) partial[chunk] = make_double2(s.a, s.b);
+        double acc[2] = {Q, M};
+        block_sum<2>(acc);
+        if (threadIdx.x == 0) partial[chunk] = make_double2(acc[0], acc[1]);
     }
 }
 
@@ -185,25 +241,44 @@ inline uint32_t reduce_grid(uint64_t total_chunks) {
 
 }  // namespace
 
-hipError_t launch_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
-                              const float* ref, float* score, double* num_den, void* ws,
-                              hipStream_t st) {
+template <DriftMetric kM>
+hipError_t launch_drift_t(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                          const void* ref, float* score, double* sums, void* ws, hipStream_t st) {
     const uint64_t n = static_cast<uint64_t>(T) * H;
     const uint64_t nblocks = static_cast<uint64_t>(S) * C;
     if (nblocks == 0) return hipSuccess;
     const uint64_t cpb = reduce_chunks_per_block(n);
     const uint64_t total = cpb * nblocks;
-    double2* partial = static_cast<double2*>(ws);
+    double* partial = static_cast<double*>(ws);
     if (total > 0) {
-        hipLaunchKernelGGL(drift_partial_kernel, dim3(reduce_grid(total)), dim3(kReduceThreads), 0,
-                           st, h, ref, static_cast<uint32_t>(n / 8), cpb, total, partial);
+        hipLaunchKernelGGL(drift_partial_kernel<kM>, dim3(reduce_grid(total)),
+                           dim3(kReduceThreads), 0, st, h, ref, static_cast<uint32_t>(n / 8), cpb,
+                           total, partial);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     const uint64_t grid = (nblocks + 255) / 256;
-    hipLaunchKernelGGL(drift_combine_kernel, dim3(static_cast<uint32_t>(grid)), dim3(256), 0, st,
-                       partial, cpb, nblocks, S, C, score, num_den);
+    hipLaunchKernelGGL(drift_combine_kernel<kM>, dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
+                       st, partial, cpb, nblocks, S, C, score, sums);
     return hipGetLastError();
+}
+
+hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                        const uint16_t* h, const void* ref, float* score, double* sums, void* ws,
+                        hipStream_t st) {
+    switch (metric) {
+        case DriftMetric::kL2:
+            return launch_drift_t<DriftMetric::kL2>(S, C, T, H, h, ref, score, sums, ws, st);
+        case DriftMetric::kL2HalfRef:
+            return launch_drift_t<DriftMetric::kL2HalfRef>(S, C, T, H, h, ref, score, sums, ws,
+                                                           st);
+        case DriftMetric::kCosine:
+            return launch_drift_t<DriftMetric::kCosine>(S, C, T, H, h, ref, score, sums, ws, st);
+        case DriftMetric::kCosineHalfRef:
+            return launch_drift_t<DriftMetric::kCosineHalfRef>(S, C, T, H, h, ref, score, sums,
+                                                               ws, st);
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,

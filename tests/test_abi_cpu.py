@@ -38,9 +38,9 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 1
-    assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 16
-    assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 16
+    assert L.cdt_version() == 2
+    assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
+    assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
     assert L.cdt_auroc_workspace_bytes(216) == 216 * 32
 
@@ -81,6 +81,11 @@ def test_shape_and_pointer_validation(cdt):
     # workspace too small
     assert L.cdt_drift_score(2, 2, 3, 16, 16, 16, 16, None, 16, 15, None) == cdt.EINVAL
     assert "workspace" in _err(cdt)
+    for fn in (L.cdt_drift_score_f16ref, L.cdt_cosine_score):
+        assert fn(2, 2, 3, 12, None, None, None, None, None, 0, None) == cdt.EINVAL
+        assert fn(2, 2, 3, 16, 8, 16, 16, None, 16, 1 << 20, None) == cdt.EALIGN
+        assert fn(2, 2, 3, 16, 16, 16, 16, None, 16, 15, None) == cdt.EINVAL
+        assert fn(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
     # empty shapes are accepted without touching the device
     assert L.cdt_drift_score(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
     assert L.cdt_ref_synth(2, 0, 3, 16, 0, 0, None, None, None) == cdt.OK
@@ -111,7 +116,7 @@ def test_sim_param_validation(cdt):
     assert "bscale" in _err(cdt)
     assert call(mal_mask=1, tamper=1, tscale_ptr=None) == cdt.EINVAL
     p = cdt.sim_params(seed=0, cfg_id=0)
-    p.reserved = 1
+    p.redraw = 2
     assert L.cdt_canary_sim(4, 2, 2, 16, ctypes.byref(p), 16, 16, None) == cdt.EINVAL
     assert L.cdt_canary_sim(4, 2, 2, 16, None, 16, 16, None) == cdt.EINVAL
 
@@ -119,17 +124,21 @@ def test_sim_param_validation(cdt):
 def test_auroc_validation(cdt):
     L = cdt.lib()
     arr, n = cdt.auroc_cfg_array([(65, 4, 0, 1, 0)])
-    assert L.cdt_auroc(n, arr, 16, 1000, 0, 0, 16, None, 16, 64, None) == cdt.ELIMIT
+    assert L.cdt_auroc(n, arr, 16, 1000, 0, 0, 16, None, None, 16, 64, None) == cdt.ELIMIT
     arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0), (8, 4, 30, 1, 1)])
-    assert L.cdt_auroc(n, arr, 16, 60, 0, 0, 16, None, 16, 64, None) == cdt.EINVAL
+    assert L.cdt_auroc(n, arr, 16, 60, 0, 0, 16, None, None, 16, 64, None) == cdt.EINVAL
     assert "outside" in _err(cdt)
     arr, n = cdt.auroc_cfg_array([(64, 300, 0, 1, 0)])
-    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 2, 16, 16, 16, 64, None) == cdt.ELIMIT
-    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 2, 16, None, 16, 64, None) == cdt.EINVAL
-    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 8, 16, None, 16, 64, None) == cdt.EINVAL
+    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 2, 16, 16, None, 16, 64, None) == cdt.ELIMIT
+    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 2, 16, None, None, 16, 64, None) == cdt.EINVAL
+    assert L.cdt_auroc(n, arr, 16, 64 * 300, 0, 8, 16, None, None, 16, 64, None) == cdt.EINVAL
     arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0)])
-    assert L.cdt_auroc(n, arr, 16, 32, 0, 0, 16, None, 16, 31, None) == cdt.EINVAL
-    assert L.cdt_auroc(0, arr, None, 0, 0, 0, None, None, None, 0, None) == cdt.OK
+    assert L.cdt_auroc(n, arr, 16, 32, 0, 0, 16, None, None, 16, 31, None) == cdt.EINVAL
+    assert L.cdt_auroc(0, arr, None, 0, 0, 0, None, None, None, None, 0, None) == cdt.OK
+    arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0)])
+    assert L.cdt_auroc(n, arr, 16, 32, 0, 8, 16, None, None, 16, 64, None) == cdt.EINVAL
+    assert "baseline" in _err(cdt)
+    assert L.cdt_auroc(n, arr, 16, 32, 0, 16, 16, None, None, 16, 64, None) == cdt.EINVAL
 
 
 def test_scale_and_outlier_validation(cdt):

@@ -215,7 +215,7 @@ def test_auroc_counts(gpu, flags):
     announce(f"auroc flags={flags}")
     tables, cfgs = _auroc_batch()
     flat = np.concatenate([t.ravel() for t in tables]).astype(np.float32)
-    counts, pooled = cdt.auroc(cfgs, to_dev(torch, flat), seed=42, flags=flags)
+    counts, pooled, _ = cdt.auroc(cfgs, to_dev(torch, flat), seed=42, flags=flags)
     torch.cuda.synchronize()
     got = cdt.u64(counts)
     got_p = cdt.u64(pooled) if pooled is not None else None
@@ -231,7 +231,7 @@ def test_auroc_pooled_at_capacity(gpu):
     announce("auroc pooled 64x256")
     S, C = 64, 256
     t = inputs.scores(C, S, seed=9, mal=(10, 20), gap=0.01, tie_levels=50)
-    counts, pooled = cdt.auroc([(S, C, 0, (1 << 10) | (1 << 20), 3)], to_dev(torch, t.ravel()),
+    counts, pooled, _ = cdt.auroc([(S, C, 0, (1 << 10) | (1 << 20), 3)], to_dev(torch, t.ravel()),
                                seed=1, flags=3)
     torch.cuda.synchronize()
     want, want_p = oracle.auroc_config(t, (1 << 10) | (1 << 20), seed=1, cfg_id=3, flags=3)

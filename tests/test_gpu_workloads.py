@@ -144,7 +144,7 @@ def _single_set_workload(gpu, name, nsample=4):
         scores.append(score)
         cfgs.append((rs.S, rs.C, k * rs.C * rs.S, rs.mal_mask, run.cfg_id))
     flat = torch.cat([s.reshape(-1) for s in scores])
-    counts, pooled = cdt.auroc(cfgs, flat, seed=wl.seed)
+    counts, pooled, _ = cdt.auroc(cfgs, flat, seed=wl.seed)
     torch.cuda.synchronize()
     c = detector_properties(cdt, counts, cfgs)
     del gs, flat, scores
@@ -221,7 +221,7 @@ def test_sweep(gpu, gold):
             off += rs.S * rs.C
         del gs
     flat = torch.cat([s.reshape(-1) for s in scores])
-    counts, _ = cdt.auroc(cfgs, flat, seed=wl.seed)
+    counts, _, _ = cdt.auroc(cfgs, flat, seed=wl.seed)
     torch.cuda.synchronize()
     c = detector_properties(cdt, counts, cfgs)
     for cid, s64 in whole_scores.items():
@@ -252,7 +252,7 @@ def test_paper_shape(gpu, gold):
     for k, run in enumerate(rs.runs):
         announce(f"paper run {run.label}")
         score, ts, bs = gs.run(run)
-        counts, _ = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, run.cfg_id)], score, seed=wl.seed)
+        counts, _, _ = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, run.cfg_id)], score, seed=wl.seed)
         torch.cuda.synchronize()
         c = cdt.u64(counts)[0]
         assert int(c[0]) == int(c[2]) == rs.C * (rs.S - 1), run.label
@@ -304,3 +304,27 @@ def test_largest_block(gpu):
     assert sc.item() == np.float32(math.sqrt(idx.numel() / n))
     del ref, h
     torch.cuda.empty_cache()
+
+
+def test_table1_structure(gpu, gold):
+    """Table 1 on the paper's shape: the full detector, the recompute
+    ceiling and the noisy-reference ablation at 1.0 on all six attacks; the
+    random baseline and the scrambled control at chance; the cosine metric
+    blind to the pure rescale only (Section 5.2)."""
+    torch, cdt = gpu
+    import bench
+    announce("table 1 structure")
+    t = bench.table1(torch, cdt, W)
+    lo, hi = gold["control_window"]["value"]
+    for label, row in t["per_attack"]["full_detector"].items():
+        assert row["auroc"] == 1.0 and row["ceiling"] == 1.0, label
+    for label, row in t["per_attack"]["noisy_reference"].items():
+        assert row["auroc"] == 1.0, label
+    for label, row in t["per_attack"]["cosine_metric"].items():
+        if label.startswith("rescale"):
+            assert row["auroc"] < 0.75, row  # a rescale keeps the angle
+        else:
+            assert row["auroc"] == 1.0, (label, row)
+    for name, summ in t["mean_over_six_attacks"].items():
+        assert lo <= summ["random_baseline"] <= hi, (name, summ)
+        assert lo <= summ["control"] <= hi, (name, summ)
