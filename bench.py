@@ -111,12 +111,20 @@ def sim_kwargs(wl, rs, run, ts, bs):
 
 
 def gpu_step(torch, cdt, wl, preps, scores, score_views, cfgs, auroc_ws, counts, pooled,
-             drift_ev=None, sim_ev=None):
+             drift_ev=None, sim_ev=None, fused=False):
+    """One pass of the hot path.  fused=True runs the live pass and Eq. 4 as
+    one launch per run (cdt_sim_score, activations not stored), the
+    simulation study's fast path; the scores are bitwise the same."""
     k = 0
     for prep in preps:
         rs = prep.rs
         for r, run in enumerate(rs.runs):
             ts, bs = prep.scales[r]
+            if fused:
+                cdt.sim_score(prep.ref, out=score_views[k], ws=prep.ws,
+                              **sim_kwargs(wl, rs, run, ts, bs))
+                k += 1
+                continue
             if sim_ev is not None:
                 sim_ev[k][0].record()
             cdt.canary_sim(prep.ref, out=prep.h, **sim_kwargs(wl, rs, run, ts, bs))
@@ -240,6 +248,18 @@ def run_main(torch, cdt, W, args):
                         for i, r in enumerate([r for p in preps for r in p.rs.runs])}
     res["control"] = {r.label: round(int(c[i][3]) / max(1, int(c[i][5])), 4)
                       for i, r in enumerate([r for p in preps for r in p.rs.runs])}
+    # the fused live-pass-and-score path on the same workload
+    fused_ms = time_ms(torch, lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs,
+                                               auroc_ws, counts, pooled, fused=True))
+    ck = cdt.u64(counts)
+    res["fused_step"] = {
+        "ms_per_step": round(fused_ms, 4),
+        "value": round(scored_bytes / (fused_ms * 1e-3) / 1e9, 2),
+        "unit": "GB/s of drift-scored activations (one cdt_sim_score launch per run)",
+        "reference_read_GBps": round(elems_per_step * 4 / (fused_ms * 1e-3) / 1e9, 1),
+        "detection": {r.label: round(cdt.strict_auroc(ck[i]), 4)
+                      for i, r in enumerate([r for p in preps for r in p.rs.runs])},
+    }
     if not args.no_ablations:
         res["ablation_kernels"] = ablation_kernels(torch, cdt, wl, big)
     del preps, scores, views
@@ -375,6 +395,8 @@ def run_sweep(torch, cdt, W, reps):
         times.append(a.elapsed_time(b))
     times.sort()
     ms = times[len(times) // 2]
+    fused_ms = time_ms(torch, lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs,
+                                               auroc_ws, counts, pooled, fused=True), reps)
     # auroc alone
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
@@ -392,6 +414,8 @@ def run_sweep(torch, cdt, W, reps):
         "configs": len(cfgs),
         "ms": round(ms, 3),
         "configs_per_s": round(len(cfgs) / (ms * 1e-3), 1),
+        "fused_ms": round(fused_ms, 3),
+        "fused_configs_per_s": round(len(cfgs) / (fused_ms * 1e-3), 1),
         "auroc_only_ms": round(auroc_ms, 4),
         "auroc_only_configs_per_s": round(len(cfgs) / (auroc_ms * 1e-3), 1),
         "auroc_min": round(min(strict), 4),

@@ -159,6 +159,17 @@ typedef struct cdt_sim_params {
 int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
                    const float* ref, uint16_t* h, void* stream);
 
+/* The live pass and Eq. 4 in one launch (the simulation study's fast path):
+ * every reference element is read once, its live fp16 value formed exactly
+ * as cdt_canary_sim forms it, and scored at once as cdt_drift_score scores
+ * it.  score / num_den are bitwise those of cdt_canary_sim followed by
+ * cdt_drift_score.  h: device [S][C][T][H] fp16 bits written as well, or
+ * NULL to skip the store.  ws: cdt_reduce_workspace_bytes bytes.
+ * Needs S <= 64. */
+int cdt_sim_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
+                  const float* ref, uint16_t* h, float* score, double* num_den, void* ws,
+                  size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Relative-L2 mismatch, Eq. 4                                               */
 /* ------------------------------------------------------------------------ */

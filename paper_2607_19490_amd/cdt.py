@@ -72,6 +72,8 @@ _SIGS = {
     "cdt_block_scales": ([_u64, _u32, _u32, _vp, _vp, _d, _d, _vp, _vp, _vp], ctypes.c_int),
     "cdt_canary_sim": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp],
                        ctypes.c_int),
+    "cdt_sim_score": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp, _vp, _vp,
+                       _sz, _vp], ctypes.c_int),
     "cdt_drift_score": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
     "cdt_drift_score_f16ref": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
                                ctypes.c_int),
@@ -232,6 +234,29 @@ def canary_sim(ref, out=None, *, bscale=None, tscale=None, **kw):
     _need(out, "h", torch.float16, (S, C, T, H))
     p = sim_params(bscale=bscale, tscale=tscale, **kw)
     _check(lib().cdt_canary_sim(S, C, T, H, ctypes.byref(p), _ptr(ref), _ptr(out), _stream()))
+    return out
+
+
+def sim_score(ref, h=None, out=None, num_den=None, ws=None, *, bscale=None, tscale=None, **kw):
+    """Live pass and Eq. 4 in one launch: ref [S][C][T][H] fp32 -> scores
+    [C][S] fp32, bitwise those of canary_sim then drift_score.  h (fp16,
+    optional) also receives the live activations.  Keywords as sim_params."""
+    torch = _torch()
+    _need(ref, "ref", torch.float32)
+    S, C, T, H = ref.shape
+    for name, t in (("bscale", bscale), ("tscale", tscale)):
+        if t is not None:
+            _need(t, name, torch.float32, (S, C))
+    if h is not None:
+        _need(h, "h", torch.float16, (S, C, T, H))
+    out = _empty((C, S), torch.float32, ref) if out is None else out
+    _need(out, "score", torch.float32, (C, S))
+    if num_den is not None:
+        _need(num_den, "num_den", torch.float64, (C, S, 2))
+    ws, nbytes = _ws_arg(ws, S, C, T, H, ref)
+    p = sim_params(bscale=bscale, tscale=tscale, **kw)
+    _check(lib().cdt_sim_score(S, C, T, H, ctypes.byref(p), _ptr(ref), _ptr(h), _ptr(out),
+                               _ptr(num_den), _ptr(ws), nbytes, _stream()))
     return out
 
 

@@ -130,56 +130,93 @@ int cdt_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const double* sum
                          "cdt_block_scales");
 }
 
+namespace {
+
+// Validation of the live-pass parameters shared by cdt_canary_sim and
+// cdt_sim_score; fills the launch description on success.
+int check_sim(const char* fn, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+              const cdt_sim_params* p, cdt::SimLaunch* L) {
+    int rc = check_shape(fn, S, C, T, H);
+    if (rc) return rc;
+    if (!p) return fail(CDT_EINVAL, "%s: params is NULL", fn);
+    if (S > 64) return fail(CDT_ELIMIT, "%s: S=%u above 64", fn, S);
+    if (p->cfg_id >= kMaxId) return fail(CDT_ELIMIT, "%s: cfg_id >= 2^24", fn);
+    if (p->benign_mode > CDT_NOISE_BLOCK) return fail(CDT_EINVAL, "%s: bad benign_mode", fn);
+    if (p->benign_dist > CDT_DIST_T3) return fail(CDT_EINVAL, "%s: bad benign_dist", fn);
+    if (p->tamper & ~7u) return fail(CDT_EINVAL, "%s: bad tamper flags", fn);
+    if (p->tamper_base > CDT_BASE_CLEAN) return fail(CDT_EINVAL, "%s: bad tamper_base", fn);
+    if (p->redraw > 1) return fail(CDT_EINVAL, "%s: redraw must be 0 or 1", fn);
+    if (!(p->sigma_b >= 0.0) || !isfinite(p->sigma_b))
+        return fail(CDT_EINVAL, "%s: sigma_b must be finite and >= 0", fn);
+    if (!(p->flip_p >= 0.0 && p->flip_p <= 1.0))
+        return fail(CDT_EINVAL, "%s: flip_p must lie in [0, 1]", fn);
+    if (!isfinite(p->scale)) return fail(CDT_EINVAL, "%s: scale must be finite", fn);
+    const uint64_t mal = p->mal_mask & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
+    if (!empty(S, C, T, H)) {
+        if (p->benign_mode == CDT_NOISE_BLOCK && !p->bscale)
+            return fail(CDT_EINVAL, "%s: BLOCK noise needs bscale", fn);
+        if (mal && (p->tamper & CDT_T_ADD) && !p->tscale)
+            return fail(CDT_EINVAL, "%s: Gaussian tamper needs tscale", fn);
+    }
+    L->S = S;
+    L->C = C;
+    L->T = T;
+    L->H = H;
+    L->seed = p->seed;
+    L->cfg_id = p->cfg_id;
+    L->benign_mode = p->benign_mode;
+    L->benign_dist = p->benign_dist;
+    L->tamper = p->tamper;
+    L->tamper_base = p->tamper_base;
+    L->redraw = p->redraw;
+    L->mal_mask = mal;
+    L->sigma_b = static_cast<float>(p->sigma_b);
+    // Flip selection: u < floor(p 2^32) with p < 1 (so the threshold fits 32
+    // bits); p == 1 flips every element.
+    L->flip_all = p->flip_p >= 1.0;
+    L->flip_thr = L->flip_all ? 0u : static_cast<uint32_t>(floor(p->flip_p * 4294967296.0));
+    L->scale = static_cast<float>(p->scale);
+    L->bscale = p->bscale;
+    L->tscale = p->tscale;
+    return CDT_OK;
+}
+
+}  // namespace
+
 int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
                    const float* ref, uint16_t* h, void* stream) {
-    int rc = check_shape("cdt_canary_sim", S, C, T, H);
+    cdt::SimLaunch L;
+    int rc = check_sim("cdt_canary_sim", S, C, T, H, p, &L);
     if (rc) return rc;
-    if (!p) return fail(CDT_EINVAL, "cdt_canary_sim: params is NULL");
-    if (S > 64) return fail(CDT_ELIMIT, "cdt_canary_sim: S=%u above 64", S);
-    if (p->cfg_id >= kMaxId) return fail(CDT_ELIMIT, "cdt_canary_sim: cfg_id >= 2^24");
-    if (p->benign_mode > CDT_NOISE_BLOCK) return fail(CDT_EINVAL, "cdt_canary_sim: bad benign_mode");
-    if (p->benign_dist > CDT_DIST_T3) return fail(CDT_EINVAL, "cdt_canary_sim: bad benign_dist");
-    if (p->tamper & ~7u) return fail(CDT_EINVAL, "cdt_canary_sim: bad tamper flags");
-    if (p->tamper_base > CDT_BASE_CLEAN) return fail(CDT_EINVAL, "cdt_canary_sim: bad tamper_base");
-    if (p->redraw > 1) return fail(CDT_EINVAL, "cdt_canary_sim: redraw must be 0 or 1");
-    if (!(p->sigma_b >= 0.0) || !isfinite(p->sigma_b))
-        return fail(CDT_EINVAL, "cdt_canary_sim: sigma_b must be finite and >= 0");
-    if (!(p->flip_p >= 0.0 && p->flip_p <= 1.0))
-        return fail(CDT_EINVAL, "cdt_canary_sim: flip_p must lie in [0, 1]");
-    if (!isfinite(p->scale)) return fail(CDT_EINVAL, "cdt_canary_sim: scale must be finite");
     if (empty(S, C, T, H)) return ok();
     if (!ref || !h) return fail(CDT_EINVAL, "cdt_canary_sim: NULL array");
     if (!aligned16(ref) || !aligned16(h))
         return fail(CDT_EALIGN, "cdt_canary_sim: arrays must be 16-byte aligned");
-    const uint64_t mal = p->mal_mask & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
-    if (p->benign_mode == CDT_NOISE_BLOCK && !p->bscale)
-        return fail(CDT_EINVAL, "cdt_canary_sim: BLOCK noise needs bscale");
-    if (mal && (p->tamper & CDT_T_ADD) && !p->tscale)
-        return fail(CDT_EINVAL, "cdt_canary_sim: Gaussian tamper needs tscale");
-
-    cdt::SimLaunch L;
-    L.S = S;
-    L.C = C;
-    L.T = T;
-    L.H = H;
-    L.seed = p->seed;
-    L.cfg_id = p->cfg_id;
-    L.benign_mode = p->benign_mode;
-    L.benign_dist = p->benign_dist;
-    L.tamper = p->tamper;
-    L.tamper_base = p->tamper_base;
-    L.redraw = p->redraw;
-    L.mal_mask = mal;
-    L.sigma_b = static_cast<float>(p->sigma_b);
-    // Flip selection: u < floor(p 2^32) with p < 1 (so the threshold fits 32
-    // bits); p == 1 flips every element.
-    L.flip_all = p->flip_p >= 1.0;
-    L.flip_thr = L.flip_all ? 0u : static_cast<uint32_t>(floor(p->flip_p * 4294967296.0));
-    L.scale = static_cast<float>(p->scale);
-    L.bscale = p->bscale;
-    L.tscale = p->tscale;
     return device_status(cdt::launch_canary_sim(L, ref, h, static_cast<hipStream_t>(stream)),
                          "cdt_canary_sim");
+}
+
+int cdt_sim_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
+                  const float* ref, uint16_t* h, float* score, double* num_den, void* ws,
+                  size_t ws_bytes, void* stream) {
+    cdt::SimLaunch L;
+    int rc = check_sim("cdt_sim_score", S, C, T, H, p, &L);
+    if (rc) return rc;
+    if (static_cast<uint64_t>(S) * C == 0) return ok();
+    if (!score) return fail(CDT_EINVAL, "cdt_sim_score: score is NULL");
+    if (static_cast<uint64_t>(T) * H > 0) {
+        if (!ref) return fail(CDT_EINVAL, "cdt_sim_score: ref is NULL");
+        if (!aligned16(ref) || (h && !aligned16(h)))
+            return fail(CDT_EALIGN, "cdt_sim_score: arrays must be 16-byte aligned");
+    }
+    const size_t need = cdt_reduce_workspace_bytes(S, C, T, H);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(CDT_EINVAL, "cdt_sim_score: workspace of %zu bytes needed, %zu given", need,
+                    ws ? ws_bytes : 0);
+    if (ws && !aligned16(ws)) return fail(CDT_EALIGN, "cdt_sim_score: ws must be 16-byte aligned");
+    return device_status(cdt::launch_sim_score(L, ref, h, score, num_den, ws,
+                                               static_cast<hipStream_t>(stream)),
+                         "cdt_sim_score");
 }
 
 namespace {

@@ -76,6 +76,10 @@ hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, 
                         const uint16_t* h, const void* ref, float* score, double* sums, void* ws,
                         hipStream_t st);
 
+// Live pass and Eq. 4 in one kernel (h may be NULL: not stored).
+hipError_t launch_sim_score(const SimLaunch& p, const float* ref, uint16_t* h, float* score,
+                            double* num_den, void* ws, hipStream_t st);
+
 hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float* scores,
                         uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
                         uint64_t* baseline, hipStream_t st);

@@ -1,0 +1,152 @@
+// The simulated live pass of Eqs. 2-3 for one group of 8 consecutive
+// elements, shared by the canary_sim kernel and the fused sim-and-score
+// kernel.  Every fp32 step is one rounded operation in the written order
+// (FMA contraction is off in every file that includes this header).
+#pragma once
+
+#include <math.h>
+
+#include "cdt_device.hpp"
+#include "cdt_launch.hpp"
+
+#pragma clang fp contract(off)
+
+namespace cdt {
+
+// Eight unit normals of one stream for elements e0..e0+7 (e0 % 8 == 0):
+// Philox calls q = e0/2 .. e0/2+3, words (x, y) -> even element, (z, w) -> odd.
+__device__ __forceinline__ void normals8(Key key, uint32_t e0, uint32_t c, uint32_t s,
+                                         uint32_t tag, float z[8]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const Words4 w = draw(key, (e0 >> 1) + k, c, s, tag);
+        z[2 * k] = irwin_hall4(w.x, w.y);
+        z[2 * k + 1] = irwin_hall4(w.z, w.w);
+    }
+}
+
+// Launch-uniform parameters of the live pass.
+struct SimArgs {
+    uint32_t C, n8;
+    uint64_t chunks_per_block, total_chunks;
+    Key key;
+    uint32_t tag_benign, tag_t12, tag_t3, tag_add, tag_flip;
+    uint32_t block_mode, t3, tamper, clean;
+    uint64_t mal_mask;
+    float sigma_b;
+    uint32_t flip_thr, flip_all;
+    float scale;
+    const float* bscale;
+    const float* tscale;
+};
+
+inline SimArgs make_sim_args(const SimLaunch& p, uint64_t chunks_per_block,
+                             uint64_t total_chunks) {
+    SimArgs A;
+    A.C = p.C;
+    A.n8 = static_cast<uint32_t>(static_cast<uint64_t>(p.T) * p.H / 8);
+    A.chunks_per_block = chunks_per_block;
+    A.total_chunks = total_chunks;
+    A.key = Key{static_cast<uint32_t>(p.seed), static_cast<uint32_t>(p.seed >> 32)};
+    // An independent benign recompute draws its noise from the ALT streams.
+    A.tag_benign = stream_tag(p.redraw ? kStreamAlt : kStreamBenign, p.cfg_id);
+    A.tag_t12 = stream_tag(p.redraw ? kStreamAltT12 : kStreamT12, p.cfg_id);
+    A.tag_t3 = stream_tag(p.redraw ? kStreamAltT3 : kStreamT3, p.cfg_id);
+    A.tag_add = stream_tag(kStreamTamperAdd, p.cfg_id);
+    A.tag_flip = stream_tag(kStreamTamperFlip, p.cfg_id);
+    A.block_mode = p.benign_mode == 1;
+    A.t3 = p.benign_dist == 1;
+    A.tamper = p.tamper;
+    A.clean = p.tamper_base == 1;
+    A.mal_mask = p.mal_mask;
+    A.sigma_b = p.sigma_b;
+    A.flip_thr = p.flip_thr;
+    A.flip_all = p.flip_all;
+    A.scale = p.scale;
+    A.bscale = p.bscale;
+    A.tscale = p.tscale;
+    return A;
+}
+
+// Block-uniform state: which (shard, canary) and its scales.
+struct SimBlock {
+    uint32_t s, c;
+    bool mal;
+    float bsc;  // Eq. 2 block noise scale (BLOCK mode)
+    float tsc;  // Gaussian tamper scale
+};
+
+template <bool kBlock>
+__device__ __forceinline__ SimBlock sim_block(const SimArgs& A, uint64_t block) {
+    SimBlock B;
+    B.s = static_cast<uint32_t>(block / A.C);
+    B.c = static_cast<uint32_t>(block - static_cast<uint64_t>(B.s) * A.C);
+    B.mal = (A.mal_mask >> B.s) & 1u;
+    B.bsc = kBlock ? A.bscale[block] : 0.0f;
+    B.tsc = (B.mal && (A.tamper & 1u)) ? A.tscale[block] : 0.0f;
+    return B;
+}
+
+// Live fp16 activations of elements e0..e0+7 from their references.
+template <bool kT3, bool kBlock>
+__device__ __forceinline__ u32x4 sim_group8(const SimArgs& A, const SimBlock& B, uint32_t e0,
+                                            const f32x4& a_lo, const f32x4& a_hi) {
+    const float a[8] = {a_lo.x, a_lo.y, a_lo.z, a_lo.w, a_hi.x, a_hi.y, a_hi.z, a_hi.w};
+
+    // Eq. 2: benign hardware noise.
+    float zb[8];
+    normals8(A.key, e0, B.c, B.s, A.tag_benign, zb);
+    if (kT3) {
+        float z3[8];
+        normals8(A.key, e0, B.c, B.s, A.tag_t3, z3);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const Words4 w = draw(A.key, e0 + k, B.c, B.s, A.tag_t12);
+            const float z1 = irwin_hall4(w.x, w.y);
+            const float z2 = irwin_hall4(w.z, w.w);
+            const float q = (z1 * z1 + z2 * z2) + z3[k] * z3[k];
+            zb[k] = (q == 0.0f) ? 0.0f : zb[k] / sqrtf(q);
+        }
+    }
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const float sc = kBlock ? B.bsc : A.sigma_b * fabsf(a[k]);
+        v[k] = a[k] + sc * zb[k];
+    }
+
+    // Eq. 3: tampering on malicious shards.
+    if (B.mal) {
+        if (A.clean) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = a[k];
+        }
+        if (A.tamper & 1u) {
+            float zt[8];
+            normals8(A.key, e0, B.c, B.s, A.tag_add, zt);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = v[k] + B.tsc * zt[k];
+        }
+        if (A.tamper & 2u) {
+            const Words4 u0 = draw(A.key, e0 >> 2, B.c, B.s, A.tag_flip);
+            const Words4 u1 = draw(A.key, (e0 >> 2) + 1, B.c, B.s, A.tag_flip);
+            const uint32_t u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                if (A.flip_all || u[k] < A.flip_thr) v[k] = -v[k];
+        }
+        if (A.tamper & 4u) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = A.scale * v[k];
+        }
+    }
+
+    u32x4 o;
+    o.x = to_half_bits(v[0]) | (static_cast<uint32_t>(to_half_bits(v[1])) << 16);
+    o.y = to_half_bits(v[2]) | (static_cast<uint32_t>(to_half_bits(v[3])) << 16);
+    o.z = to_half_bits(v[4]) | (static_cast<uint32_t>(to_half_bits(v[5])) << 16);
+    o.w = to_half_bits(v[6]) | (static_cast<uint32_t>(to_half_bits(v[7])) << 16);
+    return o;
+}
+
+}  // namespace cdt

@@ -11,6 +11,7 @@
 
 #include "cdt_device.hpp"
 #include "cdt_launch.hpp"
+#include "cdt_sim.hpp"
 
 #pragma clang fp contract(off)
 
@@ -69,18 +70,6 @@ __device__ __forceinline__ ChunkPos chunk_pos(uint64_t chunk, uint64_t chunks_pe
     return p;
 }
 
-// Eight unit normals of one stream for elements e0..e0+7 (e0 % 8 == 0):
-// Philox calls q = e0/2 .. e0/2+3, words (x, y) -> even element, (z, w) -> odd.
-__device__ __forceinline__ void normals8(Key key, uint32_t e0, uint32_t c, uint32_t s,
-                                         uint32_t tag, float z[8]) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const Words4 w = draw(key, (e0 >> 1) + k, c, s, tag);
-        z[2 * k] = irwin_hall4(w.x, w.y);
-        z[2 * k + 1] = irwin_hall4(w.z, w.w);
-    }
-}
-
 // ---------------------------------------------------------------------------
 // Synthetic references: ref = fp32(z_REF * gain[j]).
 // ---------------------------------------------------------------------------
@@ -129,20 +118,6 @@ __global__ void block_scales_kernel(uint64_t nblocks, double n, const double* __
 // ---------------------------------------------------------------------------
 // Live pass (Eqs. 2-3) -> fp16.
 // ---------------------------------------------------------------------------
-struct SimArgs {
-    uint32_t C, n8;
-    uint64_t chunks_per_block, total_chunks;
-    Key key;
-    uint32_t tag_benign, tag_t12, tag_t3, tag_add, tag_flip;
-    uint32_t block_mode, t3, tamper, clean;
-    uint64_t mal_mask;
-    float sigma_b;
-    uint32_t flip_thr, flip_all;
-    float scale;
-    const float* bscale;
-    const float* tscale;
-};
-
 // Specialised on the two launch-uniform noise modes so that the common
 // (Gaussian, elementwise) path carries no Student-t or block-scale code.
 template <bool kT3, bool kBlock>
@@ -152,9 +127,7 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
     const uint64_t n = static_cast<uint64_t>(A.n8) * 8;
     for (uint64_t it = blockIdx.x; it < A.total_chunks; it += gridDim.x) {
         const ChunkPos p = chunk_pos(xcd_contiguous(it, A.total_chunks), A.chunks_per_block, A.C);
-        const bool mal = (A.mal_mask >> p.s) & 1u;
-        const float bsc = kBlock ? A.bscale[p.block] : 0.0f;
-        const float tsc = (mal && (A.tamper & 1u)) ? A.tscale[p.block] : 0.0f;
+        const SimBlock B = sim_block<kBlock>(A, p.block);
         const f32x4* in = reinterpret_cast<const f32x4*>(ref + p.block * n);
         u32x4* out = reinterpret_cast<u32x4*>(h + p.block * n);
         // Double buffer: the next group's reference loads are issued before
@@ -174,63 +147,7 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
                 nxt_lo = load_stream(in + 2 * g_next);
                 nxt_hi = load_stream(in + 2 * g_next + 1);
             }
-            const uint32_t e0 = g * 8;
-            const float a[8] = {a_lo.x, a_lo.y, a_lo.z, a_lo.w, a_hi.x, a_hi.y, a_hi.z, a_hi.w};
-
-            // Eq. 2: benign hardware noise.
-            float zb[8];
-            normals8(A.key, e0, p.c, p.s, A.tag_benign, zb);
-            if (kT3) {
-                float z3[8];
-                normals8(A.key, e0, p.c, p.s, A.tag_t3, z3);
-#pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const Words4 w = draw(A.key, e0 + k, p.c, p.s, A.tag_t12);
-                    const float z1 = irwin_hall4(w.x, w.y);
-                    const float z2 = irwin_hall4(w.z, w.w);
-                    const float q = (z1 * z1 + z2 * z2) + z3[k] * z3[k];
-                    zb[k] = (q == 0.0f) ? 0.0f : zb[k] / sqrtf(q);
-                }
-            }
-            float v[8];
-#pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const float sc = kBlock ? bsc : A.sigma_b * fabsf(a[k]);
-                v[k] = a[k] + sc * zb[k];
-            }
-
-            // Eq. 3: tampering on malicious shards.
-            if (mal) {
-                if (A.clean) {
-#pragma unroll
-                    for (int k = 0; k < 8; ++k) v[k] = a[k];
-                }
-                if (A.tamper & 1u) {
-                    float zt[8];
-                    normals8(A.key, e0, p.c, p.s, A.tag_add, zt);
-#pragma unroll
-                    for (int k = 0; k < 8; ++k) v[k] = v[k] + tsc * zt[k];
-                }
-                if (A.tamper & 2u) {
-                    const Words4 u0 = draw(A.key, e0 >> 2, p.c, p.s, A.tag_flip);
-                    const Words4 u1 = draw(A.key, (e0 >> 2) + 1, p.c, p.s, A.tag_flip);
-                    const uint32_t u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-#pragma unroll
-                    for (int k = 0; k < 8; ++k)
-                        if (A.flip_all || u[k] < A.flip_thr) v[k] = -v[k];
-                }
-                if (A.tamper & 4u) {
-#pragma unroll
-                    for (int k = 0; k < 8; ++k) v[k] = A.scale * v[k];
-                }
-            }
-
-            u32x4 o;
-            o.x = to_half_bits(v[0]) | (static_cast<uint32_t>(to_half_bits(v[1])) << 16);
-            o.y = to_half_bits(v[2]) | (static_cast<uint32_t>(to_half_bits(v[3])) << 16);
-            o.z = to_half_bits(v[4]) | (static_cast<uint32_t>(to_half_bits(v[5])) << 16);
-            o.w = to_half_bits(v[6]) | (static_cast<uint32_t>(to_half_bits(v[7])) << 16);
-            store_stream(out + g, o);
+            store_stream(out + g, sim_group8<kT3, kBlock>(A, B, g * 8, a_lo, a_hi));
         }
     }
 }
@@ -285,29 +202,9 @@ hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, 
     const uint64_t n = static_cast<uint64_t>(p.T) * p.H;
     const uint64_t nblocks = static_cast<uint64_t>(p.S) * p.C;
     if (n == 0 || nblocks == 0) return hipSuccess;
-    SimArgs A;
-    A.C = p.C;
-    A.n8 = static_cast<uint32_t>(n / 8);
-    A.chunks_per_block = (A.n8 + kGenChunkGroups - 1) / kGenChunkGroups;
-    A.total_chunks = A.chunks_per_block * nblocks;
-    A.key = Key{static_cast<uint32_t>(p.seed), static_cast<uint32_t>(p.seed >> 32)};
-    // An independent benign recompute draws its noise from the ALT streams.
-    A.tag_benign = stream_tag(p.redraw ? kStreamAlt : kStreamBenign, p.cfg_id);
-    A.tag_t12 = stream_tag(p.redraw ? kStreamAltT12 : kStreamT12, p.cfg_id);
-    A.tag_t3 = stream_tag(p.redraw ? kStreamAltT3 : kStreamT3, p.cfg_id);
-    A.tag_add = stream_tag(kStreamTamperAdd, p.cfg_id);
-    A.tag_flip = stream_tag(kStreamTamperFlip, p.cfg_id);
-    A.block_mode = p.benign_mode == 1;
-    A.t3 = p.benign_dist == 1;
-    A.tamper = p.tamper;
-    A.clean = p.tamper_base == 1;
-    A.mal_mask = p.mal_mask;
-    A.sigma_b = p.sigma_b;
-    A.flip_thr = p.flip_thr;
-    A.flip_all = p.flip_all;
-    A.scale = p.scale;
-    A.bscale = p.bscale;
-    A.tscale = p.tscale;
+    const uint64_t n8 = n / 8;
+    const uint64_t cpb = (n8 + kGenChunkGroups - 1) / kGenChunkGroups;
+    const SimArgs A = make_sim_args(p, cpb, cpb * nblocks);
     const dim3 grid(gen_grid(A.total_chunks)), block(kGenThreads);
     if (A.t3 && A.block_mode)
         hipLaunchKernelGGL((canary_sim_kernel<true, true>), grid, block, 0, st, A, ref, h);

@@ -19,6 +19,7 @@
 
 #include "cdt_device.hpp"
 #include "cdt_launch.hpp"
+#include "cdt_sim.hpp"
 
 #pragma clang fp contract(off)
 
@@ -140,6 +141,57 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
         if (threadIdx.x == 0) {
 #pragma unroll
             for (int k = 0; k < Tr::kSums; ++k) partial[chunk * Tr::kSums + k] = acc[k];
+        }
+    }
+}
+
+// Fused live pass and Eq. 4: each group of 8 references is read once, turned
+// into fp16 live activations in registers (exactly as canary_sim does), and
+// scored at once.  Same chunking, thread mapping and accumulation order as
+// drift_partial_kernel<kL2>, so the block sums are bitwise those of
+// canary_sim followed by drift_score.  kStoreH also writes the activations.
+template <bool kT3, bool kBlock, bool kStoreH>
+__global__ __launch_bounds__(kReduceThreads) void sim_score_partial_kernel(
+    SimArgs A, const float* __restrict__ ref, uint16_t* __restrict__ h,
+    double* __restrict__ partial) {
+    constexpr DriftMetric kM = DriftMetric::kL2;
+    const uint64_t n = static_cast<uint64_t>(A.n8) * 8;
+    for (uint64_t it = blockIdx.x; it < A.total_chunks; it += gridDim.x) {
+        const uint64_t chunk = xcd_contiguous(it, A.total_chunks);
+        const uint64_t b = chunk / A.chunks_per_block;
+        const uint32_t g0 = static_cast<uint32_t>(chunk - b * A.chunks_per_block) * kChunkGroups;
+        const uint32_t g_end = min(g0 + kChunkGroups, A.n8);
+        const SimBlock B = sim_block<kBlock>(A, b);
+        const f32x4* ab = reinterpret_cast<const f32x4*>(ref + b * n);
+        u32x4* hb = reinterpret_cast<u32x4*>(h + b * n);
+        double acc[2] = {0.0, 0.0};
+        for (uint32_t base = g0; base < g_end; base += kReduceThreads * kReduceUnroll) {
+            f32x4 a0[kReduceUnroll], a1[kReduceUnroll];
+#pragma unroll
+            for (int u = 0; u < kReduceUnroll; ++u) {
+                const uint32_t g = base + u * kReduceThreads + threadIdx.x;
+                a0[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+                a1[u] = a0[u];
+                if (g < g_end) {
+                    a0[u] = __builtin_nontemporal_load(ab + 2 * g);
+                    a1[u] = __builtin_nontemporal_load(ab + 2 * g + 1);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kReduceUnroll; ++u) {
+                const uint32_t g = base + u * kReduceThreads + threadIdx.x;
+                u32x4 hv = u32x4{0u, 0u, 0u, 0u};
+                if (g < g_end) {
+                    hv = sim_group8<kT3, kBlock>(A, B, g * 8, a0[u], a1[u]);
+                    if constexpr (kStoreH) __builtin_nontemporal_store(hv, hb + g);
+                }
+                accumulate8<kM>(hv, hv, a0[u], a1[u], acc);
+            }
+        }
+        block_sum<2>(acc);
+        if (threadIdx.x == 0) {
+            partial[chunk * 2] = acc[0];
+            partial[chunk * 2 + 1] = acc[1];
         }
     }
 }
@@ -279,6 +331,45 @@ hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, 
                                                                ws, st);
     }
     return hipErrorInvalidValue;
+}
+
+template <bool kT3, bool kBlock>
+void launch_sim_score_t(const SimArgs& A, dim3 grid, const float* ref, uint16_t* h,
+                        double* partial, hipStream_t st) {
+    if (h)
+        hipLaunchKernelGGL((sim_score_partial_kernel<kT3, kBlock, true>), grid,
+                           dim3(kReduceThreads), 0, st, A, ref, h, partial);
+    else
+        hipLaunchKernelGGL((sim_score_partial_kernel<kT3, kBlock, false>), grid,
+                           dim3(kReduceThreads), 0, st, A, ref, h, partial);
+}
+
+hipError_t launch_sim_score(const SimLaunch& p, const float* ref, uint16_t* h, float* score,
+                            double* num_den, void* ws, hipStream_t st) {
+    const uint64_t n = static_cast<uint64_t>(p.T) * p.H;
+    const uint64_t nblocks = static_cast<uint64_t>(p.S) * p.C;
+    if (nblocks == 0) return hipSuccess;
+    const uint64_t cpb = reduce_chunks_per_block(n);
+    const uint64_t total = cpb * nblocks;
+    double* partial = static_cast<double*>(ws);
+    if (total > 0) {
+        const SimArgs A = make_sim_args(p, cpb, total);
+        const dim3 grid(reduce_grid(total));
+        if (A.t3 && A.block_mode)
+            launch_sim_score_t<true, true>(A, grid, ref, h, partial, st);
+        else if (A.t3)
+            launch_sim_score_t<true, false>(A, grid, ref, h, partial, st);
+        else if (A.block_mode)
+            launch_sim_score_t<false, true>(A, grid, ref, h, partial, st);
+        else
+            launch_sim_score_t<false, false>(A, grid, ref, h, partial, st);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const uint64_t grid = (nblocks + 255) / 256;
+    hipLaunchKernelGGL(drift_combine_kernel<DriftMetric::kL2>, dim3(static_cast<uint32_t>(grid)),
+                       dim3(256), 0, st, partial, cpb, nblocks, p.S, p.C, score, num_den);
+    return hipGetLastError();
 }
 
 hipError_t launch_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,

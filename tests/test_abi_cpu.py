@@ -115,6 +115,17 @@ def test_sim_param_validation(cdt):
     assert call(benign_mode=1) == cdt.EINVAL  # BLOCK noise without bscale
     assert "bscale" in _err(cdt)
     assert call(mal_mask=1, tamper=1, tscale_ptr=None) == cdt.EINVAL
+    # the fused launch validates the same parameters
+    p = cdt.sim_params(seed=0, cfg_id=1 << 24)
+    assert L.cdt_sim_score(4, 2, 2, 16, ctypes.byref(p), 16, None, 16, None, 16, 1 << 20,
+                           None) == cdt.ELIMIT
+    p = cdt.sim_params(seed=0, cfg_id=0)
+    assert L.cdt_sim_score(4, 2, 2, 16, ctypes.byref(p), 16, None, None, None, 16, 1 << 20,
+                           None) == cdt.EINVAL
+    assert L.cdt_sim_score(4, 2, 2, 16, ctypes.byref(p), 16, 8, 16, None, 16, 1 << 20,
+                           None) == cdt.EALIGN
+    assert L.cdt_sim_score(4, 2, 2, 16, ctypes.byref(p), 16, None, 16, None, 16, 1,
+                           None) == cdt.EINVAL
     p = cdt.sim_params(seed=0, cfg_id=0)
     p.redraw = 2
     assert L.cdt_canary_sim(4, 2, 2, 16, ctypes.byref(p), 16, 16, None) == cdt.EINVAL
