@@ -100,6 +100,12 @@ class Prepared:
         self.scales = []
         for run in rs.runs:
             ts, bs = cdt.block_scales(self.sumsq, self.sumabs, T, H, run.eps, run.sigma_b)
+            if run.exact_norm:
+                ts = cdt.tamper_scale_exact(self.ref, run.eps, ws=self.ws, bscale=bs,
+                                            seed=wl.seed, cfg_id=run.cfg_id,
+                                            benign_mode=run.benign_mode,
+                                            benign_dist=run.benign_dist, sigma_b=run.sigma_b,
+                                            tamper_base=run.tamper_base)
             self.scales.append((ts, bs))
 
 

@@ -159,6 +159,20 @@ typedef struct cdt_sim_params {
 int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
                    const float* ref, uint16_t* h, void* stream);
 
+/* Per-block scale of the exact-norm Gaussian tamper of Section 3.2,
+ * tau(v) = v + eps ||v||_F N / ||N||_F: with v the untampered output of the
+ * block (a + delta, formed exactly as cdt_canary_sim forms it, or a itself
+ * for the clean base) and N its TAMPER_ADD normals,
+ *   tscale[s][c] = fp32( eps * sqrt( sum v^2 / sum N^2 ) )   (fp64 sums),
+ * so that cdt_canary_sim's Gaussian tamper, given this tscale, adds a
+ * perturbation of norm eps ||v|| (up to rounding).  p gives the benign
+ * settings, seed and cfg_id of the run (its tamper fields are ignored).
+ * norms: optional device [S][C][2] fp64 (sum v^2, sum N^2), or NULL.
+ * ws: cdt_reduce_workspace_bytes bytes. */
+int cdt_tamper_scale_exact(uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                           const cdt_sim_params* p, const float* ref, double eps, float* tscale,
+                           double* norms, void* ws, size_t ws_bytes, void* stream);
+
 /* The live pass and Eq. 4 in one launch (the simulation study's fast path):
  * every reference element is read once, its live fp16 value formed exactly
  * as cdt_canary_sim forms it, and scored at once as cdt_drift_score scores

@@ -62,6 +62,8 @@ _SIGS = {
                        _d, _d, _f32p, _u16p], _i),
     "orc_sim_range_ex": ([_u32, _u32, _u64, _u64, _u64, _u32, _i, _i, _d, _f, _i, _u32, _i, _f,
                           _d, _d, _i, _f32p, _u16p], _i),
+    "orc_tamper_scale_exact_block": ([_u32, _u32, _u32, _u32, _u64, _u32, _i, _i, _d, _f, _i, _i,
+                                      _d, _f32p, _f64p, _f64p], _f),
     "orc_drift_block_f16ref": ([_u64, _u16p, _u16p, _f64p, _f64p], _d),
     "orc_drift_score_f16ref": ([_u32, _u32, _u32, _u32, _u16p, _u16p, _f64p, _f32p], None),
     "orc_cosine_block": ([_u64, _u16p, _f32p], _d),
@@ -236,6 +238,41 @@ def sim_range(s, c, e0, ref_part, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE
                         float(bscale), int(bool(malicious)), tamper, tamper_base, float(tscale),
                         flip_p, scale, _p(a, ctypes.c_float), _p(h, ctypes.c_uint16))
     return h
+
+
+def tamper_scale_exact_block(s, c, ref_block_arr, eps, *, seed, cfg_id,
+                             benign_mode=NOISE_ELEMENTWISE, benign_dist=DIST_GAUSS, sigma_b=1e-3,
+                             bscale=0.0, tamper_base=BASE_BENIGN, redraw=False):
+    """Exact-norm Gaussian tamper scale of one block: (tscale, sum v^2, sum N^2)."""
+    a = _c(ref_block_arr, np.float32)
+    T, H = a.shape
+    vv = ctypes.c_double()
+    zz = ctypes.c_double()
+    ts = lib().orc_tamper_scale_exact_block(s, c, T, H, seed, cfg_id, benign_mode, benign_dist,
+                                            sigma_b, float(bscale), tamper_base,
+                                            int(bool(redraw)), eps, _p(a, ctypes.c_float),
+                                            ctypes.byref(vv), ctypes.byref(zz))
+    return np.float32(ts), vv.value, zz.value
+
+
+def tamper_scale_exact(ref, eps, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE,
+                       benign_dist=DIST_GAUSS, sigma_b=1e-3, bscale=None,
+                       tamper_base=BASE_BENIGN, redraw=False):
+    """[S][C] exact-norm tamper scales (and the [S][C][2] norms) of a whole array."""
+    ref = _c(ref, np.float32)
+    S, C = ref.shape[:2]
+    ts = np.empty((S, C), np.float32)
+    norms = np.empty((S, C, 2), np.float64)
+    for s in range(S):
+        for c in range(C):
+            t, vv, zz = tamper_scale_exact_block(
+                s, c, ref[s, c], eps, seed=seed, cfg_id=cfg_id, benign_mode=benign_mode,
+                benign_dist=benign_dist, sigma_b=sigma_b,
+                bscale=0.0 if bscale is None else bscale[s, c], tamper_base=tamper_base,
+                redraw=redraw)
+            ts[s, c] = t
+            norms[s, c] = (vv, zz)
+    return ts, norms
 
 
 def canary_sim(ref, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE, benign_dist=DIST_GAUSS,

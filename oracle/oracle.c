@@ -362,9 +362,30 @@ static int flip_selected(double p, uint32_t u)
 }
 
 /* Elements [e0, e0 + count) of block (s, c); ref and h hold just that range. */
-/* redraw != 0 draws the benign noise from the ALT streams: an independent
- * benign recompute of the same stage (Section 4.5, recompute ceiling and
+/* Eq. 2: the benign output v = a + sc * zb of element e of block (s, c).
+ * redraw != 0 draws the noise from the ALT streams: an independent benign
+ * recompute of the same stage (Section 4.5, recompute ceiling and
  * noisy-reference ablation). */
+static float benign_value(uint32_t s, uint32_t c, uint32_t e, uint64_t seed, uint32_t cfg_id,
+                          int benign_mode, int benign_dist, float sigma_f, float bscale,
+                          int redraw, float a)
+{
+    uint32_t st_benign = redraw ? ST_ALT : ST_BENIGN;
+    uint32_t st_t12 = redraw ? ST_ALT_T12 : ST_T12;
+    uint32_t st_t3 = redraw ? ST_ALT_T3 : ST_T3;
+    float sc = (benign_mode == ORC_NOISE_BLOCK) ? bscale : r32((double)sigma_f * fabs((double)a));
+    float zb = normal1(seed, st_benign, cfg_id, s, c, e);
+    if (benign_dist == ORC_DIST_T3) {
+        float z1, z2;
+        normal2(seed, st_t12, cfg_id, s, c, e, &z1, &z2);
+        float z3 = normal1(seed, st_t3, cfg_id, s, c, e);
+        float q = r32((double)r32((double)r32((double)z1 * z1) + (double)r32((double)z2 * z2)) +
+                      (double)r32((double)z3 * z3));
+        zb = (q == 0.0f) ? 0.0f : r32((double)zb / (double)r32(sqrt((double)q)));
+    }
+    return r32((double)a + (double)r32((double)sc * (double)zb));
+}
+
 int orc_sim_range_ex(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t seed,
                      uint32_t cfg_id, int benign_mode, int benign_dist, double sigma_b,
                      float bscale, int malicious, uint32_t tamper, int tamper_base, float tscale,
@@ -372,26 +393,11 @@ int orc_sim_range_ex(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64
 {
     float sigma_f = r32(sigma_b);
     float scale_f = r32(scale);
-    uint32_t st_benign = redraw ? ST_ALT : ST_BENIGN;
-    uint32_t st_t12 = redraw ? ST_ALT_T12 : ST_T12;
-    uint32_t st_t3 = redraw ? ST_ALT_T3 : ST_T3;
     for (uint64_t k = 0; k < count; ++k) {
         uint32_t e = (uint32_t)(e0 + k);
         float a = ref[k];
-
-        /* benign hardware noise, Eq. 2 */
-        float sc = (benign_mode == ORC_NOISE_BLOCK) ? bscale : r32((double)sigma_f * fabs((double)a));
-        float zb = normal1(seed, st_benign, cfg_id, s, c, e);
-        if (benign_dist == ORC_DIST_T3) {
-            float z1, z2;
-            normal2(seed, st_t12, cfg_id, s, c, e, &z1, &z2);
-            float z3 = normal1(seed, st_t3, cfg_id, s, c, e);
-            float q = r32((double)r32((double)r32((double)z1 * z1) + (double)r32((double)z2 * z2)) +
-                          (double)r32((double)z3 * z3));
-            zb = (q == 0.0f) ? 0.0f : r32((double)zb / (double)r32(sqrt((double)q)));
-        }
-        float benign = r32((double)a + (double)r32((double)sc * (double)zb));
-        float v = benign;
+        float v = benign_value(s, c, e, seed, cfg_id, benign_mode, benign_dist, sigma_f, bscale,
+                               redraw, a);
 
         /* tampering, Eq. 3 */
         if (malicious) {
@@ -412,6 +418,36 @@ int orc_sim_range_ex(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64
         h[k] = orc_f16_rne(v);
     }
     return 0;
+}
+
+/* Exact-norm Gaussian tamper of Section 3.2, tau(v) = v + eps ||v|| N / ||N||,
+ * for block (s, c): vv = sum v^2 over the untampered output (the benign
+ * a + delta, or a for the clean base) and zz = sum z^2 over the TAMPER_ADD
+ * normals, in fp64; the scale of those normals is fp32(eps sqrt(vv / zz)). */
+float orc_tamper_scale_exact_block(uint32_t s, uint32_t c, uint32_t T, uint32_t H, uint64_t seed,
+                                   uint32_t cfg_id, int benign_mode, int benign_dist,
+                                   double sigma_b, float bscale, int tamper_base, int redraw,
+                                   double eps, const float* ref, double* vv_out, double* zz_out)
+{
+    float sigma_f = r32(sigma_b);
+    double vv = 0.0, zz = 0.0;
+    uint64_t n = (uint64_t)T * H;
+    for (uint64_t k = 0; k < n; ++k) {
+        uint32_t e = (uint32_t)k;
+        float a = ref[k];
+        float v = (tamper_base == ORC_BASE_CLEAN)
+                      ? a
+                      : benign_value(s, c, e, seed, cfg_id, benign_mode, benign_dist, sigma_f,
+                                     bscale, redraw, a);
+        float z = normal1(seed, ST_TADD, cfg_id, s, c, e);
+        vv += (double)v * (double)v;
+        zz += (double)z * (double)z;
+    }
+    if (vv_out)
+        *vv_out = vv;
+    if (zz_out)
+        *zz_out = zz;
+    return zz > 0.0 ? r32(eps * sqrt(vv / zz)) : 0.0f;
 }
 
 int orc_sim_range(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t seed,

@@ -72,6 +72,8 @@ _SIGS = {
     "cdt_block_scales": ([_u64, _u32, _u32, _vp, _vp, _d, _d, _vp, _vp, _vp], ctypes.c_int),
     "cdt_canary_sim": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp],
                        ctypes.c_int),
+    "cdt_tamper_scale_exact": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _d, _vp,
+                                _vp, _vp, _sz, _vp], ctypes.c_int),
     "cdt_sim_score": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp, _vp, _vp,
                        _sz, _vp], ctypes.c_int),
     "cdt_drift_score": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
@@ -234,6 +236,25 @@ def canary_sim(ref, out=None, *, bscale=None, tscale=None, **kw):
     _need(out, "h", torch.float16, (S, C, T, H))
     p = sim_params(bscale=bscale, tscale=tscale, **kw)
     _check(lib().cdt_canary_sim(S, C, T, H, ctypes.byref(p), _ptr(ref), _ptr(out), _stream()))
+    return out
+
+
+def tamper_scale_exact(ref, eps, norms=None, ws=None, *, bscale=None, **kw):
+    """Per-block scale [S][C] fp32 of the exact-norm Gaussian tamper
+    (eps ||v|| N / ||N||) for the run described by the keywords (as
+    sim_params); norms (optional, [S][C][2] fp64) receives sum v^2, sum N^2."""
+    torch = _torch()
+    _need(ref, "ref", torch.float32)
+    S, C, T, H = ref.shape
+    if bscale is not None:
+        _need(bscale, "bscale", torch.float32, (S, C))
+    if norms is not None:
+        _need(norms, "norms", torch.float64, (S, C, 2))
+    out = _empty((S, C), torch.float32, ref)
+    ws, nbytes = _ws_arg(ws, S, C, T, H, ref)
+    p = sim_params(bscale=bscale, **kw)
+    _check(lib().cdt_tamper_scale_exact(S, C, T, H, ctypes.byref(p), _ptr(ref), eps, _ptr(out),
+                                        _ptr(norms), _ptr(ws), nbytes, _stream()))
     return out
 
 

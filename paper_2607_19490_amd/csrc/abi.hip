@@ -219,6 +219,35 @@ int cdt_sim_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_
                          "cdt_sim_score");
 }
 
+int cdt_tamper_scale_exact(uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                           const cdt_sim_params* p, const float* ref, double eps, float* tscale,
+                           double* norms, void* ws, size_t ws_bytes, void* stream) {
+    const char* fn = "cdt_tamper_scale_exact";
+    if (!p) return fail(CDT_EINVAL, "%s: params is NULL", fn);
+    if (!(eps >= 0.0) || !isfinite(eps)) return fail(CDT_EINVAL, "%s: eps must be finite and >= 0", fn);
+    // The tamper settings do not enter the norms (tscale is this call's output).
+    cdt_sim_params q = *p;
+    q.tamper = 0;
+    q.tscale = nullptr;
+    cdt::SimLaunch L;
+    int rc = check_sim(fn, S, C, T, H, &q, &L);
+    if (rc) return rc;
+    if (static_cast<uint64_t>(S) * C == 0) return ok();
+    if (!tscale) return fail(CDT_EINVAL, "%s: tscale is NULL", fn);
+    if (static_cast<uint64_t>(T) * H > 0) {
+        if (!ref) return fail(CDT_EINVAL, "%s: ref is NULL", fn);
+        if (!aligned16(ref)) return fail(CDT_EALIGN, "%s: ref must be 16-byte aligned", fn);
+    }
+    const size_t need = cdt_reduce_workspace_bytes(S, C, T, H);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                    ws ? ws_bytes : 0);
+    if (ws && !aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
+    return device_status(cdt::launch_tamper_scale_exact(L, ref, eps, tscale, norms, ws,
+                                                        static_cast<hipStream_t>(stream)),
+                         fn);
+}
+
 namespace {
 
 int drift_common(const char* fn, cdt::DriftMetric metric, uint32_t S, uint32_t C, uint32_t T,

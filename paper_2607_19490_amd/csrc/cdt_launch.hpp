@@ -80,6 +80,10 @@ hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, 
 hipError_t launch_sim_score(const SimLaunch& p, const float* ref, uint16_t* h, float* score,
                             double* num_den, void* ws, hipStream_t st);
 
+// Per-block scale of the exact-norm Gaussian tamper (and its two norms).
+hipError_t launch_tamper_scale_exact(const SimLaunch& p, const float* ref, double eps,
+                                     float* tscale, double* norms, void* ws, hipStream_t st);
+
 hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float* scores,
                         uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
                         uint64_t* baseline, hipStream_t st);

@@ -87,13 +87,10 @@ __device__ __forceinline__ SimBlock sim_block(const SimArgs& A, uint64_t block) 
     return B;
 }
 
-// Live fp16 activations of elements e0..e0+7 from their references.
+// Eq. 2: the benign output v = a + sc * zb of elements e0..e0+7.
 template <bool kT3, bool kBlock>
-__device__ __forceinline__ u32x4 sim_group8(const SimArgs& A, const SimBlock& B, uint32_t e0,
-                                            const f32x4& a_lo, const f32x4& a_hi) {
-    const float a[8] = {a_lo.x, a_lo.y, a_lo.z, a_lo.w, a_hi.x, a_hi.y, a_hi.z, a_hi.w};
-
-    // Eq. 2: benign hardware noise.
+__device__ __forceinline__ void benign8(const SimArgs& A, const SimBlock& B, uint32_t e0,
+                                        const float a[8], float v[8]) {
     float zb[8];
     normals8(A.key, e0, B.c, B.s, A.tag_benign, zb);
     if (kT3) {
@@ -108,39 +105,49 @@ __device__ __forceinline__ u32x4 sim_group8(const SimArgs& A, const SimBlock& B,
             zb[k] = (q == 0.0f) ? 0.0f : zb[k] / sqrtf(q);
         }
     }
-    float v[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
         const float sc = kBlock ? B.bsc : A.sigma_b * fabsf(a[k]);
         v[k] = a[k] + sc * zb[k];
     }
+}
 
-    // Eq. 3: tampering on malicious shards.
-    if (B.mal) {
-        if (A.clean) {
+// Eq. 3: the tampering of a malicious shard, in place on v (which holds the
+// benign output; the clean base replaces it by a first).
+__device__ __forceinline__ void tamper8(const SimArgs& A, const SimBlock& B, uint32_t e0,
+                                        const float a[8], float v[8]) {
+    if (A.clean) {
 #pragma unroll
-            for (int k = 0; k < 8; ++k) v[k] = a[k];
-        }
-        if (A.tamper & 1u) {
-            float zt[8];
-            normals8(A.key, e0, B.c, B.s, A.tag_add, zt);
-#pragma unroll
-            for (int k = 0; k < 8; ++k) v[k] = v[k] + B.tsc * zt[k];
-        }
-        if (A.tamper & 2u) {
-            const Words4 u0 = draw(A.key, e0 >> 2, B.c, B.s, A.tag_flip);
-            const Words4 u1 = draw(A.key, (e0 >> 2) + 1, B.c, B.s, A.tag_flip);
-            const uint32_t u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-#pragma unroll
-            for (int k = 0; k < 8; ++k)
-                if (A.flip_all || u[k] < A.flip_thr) v[k] = -v[k];
-        }
-        if (A.tamper & 4u) {
-#pragma unroll
-            for (int k = 0; k < 8; ++k) v[k] = A.scale * v[k];
-        }
+        for (int k = 0; k < 8; ++k) v[k] = a[k];
     }
+    if (A.tamper & 1u) {
+        float zt[8];
+        normals8(A.key, e0, B.c, B.s, A.tag_add, zt);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = v[k] + B.tsc * zt[k];
+    }
+    if (A.tamper & 2u) {
+        const Words4 u0 = draw(A.key, e0 >> 2, B.c, B.s, A.tag_flip);
+        const Words4 u1 = draw(A.key, (e0 >> 2) + 1, B.c, B.s, A.tag_flip);
+        const uint32_t u[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+            if (A.flip_all || u[k] < A.flip_thr) v[k] = -v[k];
+    }
+    if (A.tamper & 4u) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = A.scale * v[k];
+    }
+}
 
+// Live fp16 activations of elements e0..e0+7 from their references.
+template <bool kT3, bool kBlock>
+__device__ __forceinline__ u32x4 sim_group8(const SimArgs& A, const SimBlock& B, uint32_t e0,
+                                            const f32x4& a_lo, const f32x4& a_hi) {
+    const float a[8] = {a_lo.x, a_lo.y, a_lo.z, a_lo.w, a_hi.x, a_hi.y, a_hi.z, a_hi.w};
+    float v[8];
+    benign8<kT3, kBlock>(A, B, e0, a, v);
+    if (B.mal) tamper8(A, B, e0, a, v);
     u32x4 o;
     o.x = to_half_bits(v[0]) | (static_cast<uint32_t>(to_half_bits(v[1])) << 16);
     o.y = to_half_bits(v[2]) | (static_cast<uint32_t>(to_half_bits(v[3])) << 16);

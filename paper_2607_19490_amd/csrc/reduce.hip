@@ -196,6 +196,67 @@ __global__ __launch_bounds__(kReduceThreads) void sim_score_partial_kernel(
     }
 }
 
+// Norms for the exact-norm Gaussian tamper of Section 3.2, tau(v) = v +
+// eps ||v|| N / ||N||: per block vv = sum v^2 over the untampered output (the
+// benign a + delta, or a itself for the clean base) and zz = sum z^2 over
+// the TAMPER_ADD normals, both in fp64.  A scale c = eps sqrt(vv / zz) on
+// those normals adds a perturbation of norm eps ||v||.
+template <bool kT3, bool kBlock>
+__global__ __launch_bounds__(kReduceThreads) void tamper_norms_partial_kernel(
+    SimArgs A, const float* __restrict__ ref, double* __restrict__ partial) {
+    const uint64_t n = static_cast<uint64_t>(A.n8) * 8;
+    for (uint64_t it = blockIdx.x; it < A.total_chunks; it += gridDim.x) {
+        const uint64_t chunk = xcd_contiguous(it, A.total_chunks);
+        const uint64_t b = chunk / A.chunks_per_block;
+        const uint32_t g0 = static_cast<uint32_t>(chunk - b * A.chunks_per_block) * kChunkGroups;
+        const uint32_t g_end = min(g0 + kChunkGroups, A.n8);
+        const SimBlock B = sim_block<kBlock>(A, b);
+        const f32x4* ab = reinterpret_cast<const f32x4*>(ref + b * n);
+        double acc[2] = {0.0, 0.0};
+        for (uint32_t g = g0 + threadIdx.x; g < g_end; g += kReduceThreads) {
+            const f32x4 lo = ab[2 * g], hi = ab[2 * g + 1];
+            const float a[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+            float v[8], z[8];
+            if (A.clean) {
+#pragma unroll
+                for (int k = 0; k < 8; ++k) v[k] = a[k];
+            } else {
+                benign8<kT3, kBlock>(A, B, g * 8, a, v);
+            }
+            normals8(A.key, g * 8, B.c, B.s, A.tag_add, z);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const double vd = static_cast<double>(v[k]), zd = static_cast<double>(z[k]);
+                acc[0] = fma(vd, vd, acc[0]);
+                acc[1] = fma(zd, zd, acc[1]);
+            }
+        }
+        block_sum<2>(acc);
+        if (threadIdx.x == 0) {
+            partial[chunk * 2] = acc[0];
+            partial[chunk * 2 + 1] = acc[1];
+        }
+    }
+}
+
+__global__ void tamper_scale_combine_kernel(const double* __restrict__ partial,
+                                            uint64_t chunks_per_block, uint64_t nblocks,
+                                            double eps, float* __restrict__ tscale,
+                                            double* __restrict__ norms) {
+    const uint64_t b = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (b >= nblocks) return;
+    double vv = 0.0, zz = 0.0;
+    for (uint64_t i = 0; i < chunks_per_block; ++i) {
+        vv += partial[(b * chunks_per_block + i) * 2];
+        zz += partial[(b * chunks_per_block + i) * 2 + 1];
+    }
+    tscale[b] = zz > 0.0 ? static_cast<float>(eps * sqrt(vv / zz)) : 0.0f;
+    if (norms) {
+        norms[2 * b] = vv;
+        norms[2 * b + 1] = zz;
+    }
+}
+
 // Eq. 4 from the block sums: m = sqrt(D / R); R = 0 gives 0 (D = 0) or +inf.
 __device__ __forceinline__ double relative_l2(double D, double R) {
     if (R == 0.0) return (D == 0.0) ? 0.0 : static_cast<double>(INFINITY);
@@ -369,6 +430,38 @@ hipError_t launch_sim_score(const SimLaunch& p, const float* ref, uint16_t* h, f
     const uint64_t grid = (nblocks + 255) / 256;
     hipLaunchKernelGGL(drift_combine_kernel<DriftMetric::kL2>, dim3(static_cast<uint32_t>(grid)),
                        dim3(256), 0, st, partial, cpb, nblocks, p.S, p.C, score, num_den);
+    return hipGetLastError();
+}
+
+hipError_t launch_tamper_scale_exact(const SimLaunch& p, const float* ref, double eps,
+                                     float* tscale, double* norms, void* ws, hipStream_t st) {
+    const uint64_t n = static_cast<uint64_t>(p.T) * p.H;
+    const uint64_t nblocks = static_cast<uint64_t>(p.S) * p.C;
+    if (nblocks == 0) return hipSuccess;
+    const uint64_t cpb = reduce_chunks_per_block(n);
+    const uint64_t total = cpb * nblocks;
+    double* partial = static_cast<double*>(ws);
+    if (total > 0) {
+        const SimArgs A = make_sim_args(p, cpb, total);
+        const dim3 grid(reduce_grid(total)), block(kReduceThreads);
+        if (A.t3 && A.block_mode)
+            hipLaunchKernelGGL((tamper_norms_partial_kernel<true, true>), grid, block, 0, st, A,
+                               ref, partial);
+        else if (A.t3)
+            hipLaunchKernelGGL((tamper_norms_partial_kernel<true, false>), grid, block, 0, st, A,
+                               ref, partial);
+        else if (A.block_mode)
+            hipLaunchKernelGGL((tamper_norms_partial_kernel<false, true>), grid, block, 0, st, A,
+                               ref, partial);
+        else
+            hipLaunchKernelGGL((tamper_norms_partial_kernel<false, false>), grid, block, 0, st, A,
+                               ref, partial);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const uint64_t grid = (nblocks + 255) / 256;
+    hipLaunchKernelGGL(tamper_scale_combine_kernel, dim3(static_cast<uint32_t>(grid)), dim3(256),
+                       0, st, partial, cpb, nblocks, eps, tscale, norms);
     return hipGetLastError();
 }
 

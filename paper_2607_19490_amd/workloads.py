@@ -48,6 +48,7 @@ class Run:
     flip_p: float = 0.0     # sign-flip fraction (1.0 = the paper's full flip)
     scale: float = 1.0      # rescale factor 1 + alpha
     tamper_base: int = BASE_BENIGN
+    exact_norm: bool = False  # Gaussian tamper scaled to exactly eps ||v|| (Section 3.2)
     label: str = ""
 
 
@@ -166,12 +167,13 @@ def snr() -> Workload:
 def paper() -> Workload:
     """The paper's own pipeline shape: 12 stages, 100 canaries of 48 tokens,
     d = 768, malicious stage floor(k/2) = 6 counted from 1 (index 5 here),
-    block-scaled benign noise at sigma_hw = 0.002 and the six attacks."""
+    block-scaled benign noise at sigma_hw = 0.002 and the six attacks, the
+    Gaussian ones with the exact norm eps ||v||."""
     S, H = 12, 768
     runs = []
     for eps in (0.02, 0.05, 0.10, 0.20):
         runs.append(Run(len(runs), benign_mode=NOISE_BLOCK, sigma_b=0.002, tamper=T_ADD,
-                        eps=eps, label=f"gauss{eps:g}"))
+                        eps=eps, exact_norm=True, label=f"gauss{eps:g}"))
     runs.append(Run(len(runs), benign_mode=NOISE_BLOCK, sigma_b=0.002, tamper=T_FLIP,
                     flip_p=1.0, label="signflip"))
     runs.append(Run(len(runs), benign_mode=NOISE_BLOCK, sigma_b=0.002, tamper=T_SCALE,

@@ -237,3 +237,27 @@ def test_auroc_pooled_at_capacity(gpu):
     want, want_p = oracle.auroc_config(t, (1 << 10) | (1 << 20), seed=1, cfg_id=3, flags=3)
     np.testing.assert_array_equal(cdt.u64(counts)[0], want)
     np.testing.assert_array_equal(cdt.u64(pooled)[0], want_p)
+
+
+@pytest.mark.parametrize("kw", [dict(sigma_b=1e-3), dict(benign_dist=1, sigma_b=2e-2),
+                                dict(benign_mode=1, sigma_b=2e-3), dict(sigma_b=0.1, tamper_base=1),
+                                dict(sigma_b=1e-2, redraw=True)],
+                         ids=["gauss", "t3", "block", "clean", "redraw"])
+@pytest.mark.parametrize("shape", SHAPES[:3] + [(1, 1, 130, 8192)])
+def test_tamper_scale_exact(gpu, kw, shape):
+    """Exact-norm Gaussian tamper scale (Section 3.2): the two fp64 norms
+    within the bound of n-term fp64 sums, the fp32 scale within one ulp."""
+    torch, cdt = gpu
+    S, C, T, H = shape
+    announce(f"tamper_scale_exact {kw} {shape}")
+    ref = oracle.ref_synth(S, C, T, H, 6, 0, oracle.outlier_gain(H, 1, 20.0, 6, 0))
+    q, m = oracle.ref_stats(ref)
+    _, bs = oracle.block_scales(T, H, q, m, 0.0, kw.get("sigma_b", 0.0))
+    norms = torch.empty((S, C, 2), dtype=torch.float64, device="cuda")
+    ts = cdt.tamper_scale_exact(to_dev(torch, ref), 0.05, norms=norms, bscale=to_dev(torch, bs),
+                                seed=8, cfg_id=21, **kw)
+    torch.cuda.synchronize()
+    ts_o, norms_o = oracle.tamper_scale_exact(ref, 0.05, seed=8, cfg_id=21, bscale=bs, **kw)
+    assert rel_err(norms.cpu().numpy(), norms_o) < max(1e-14, 2 * T * H * 2.0**-53)
+    d = ulp_diff_f32(ts.cpu().numpy(), ts_o)
+    assert d.max() <= 1 and (d == 0).mean() > 0.9

@@ -18,7 +18,7 @@ import pytest
 
 import oracle
 from paper_2607_19490_amd import workloads as W
-from tests.gpu_util import announce, h_bits, rel_err, require_gpu
+from tests.gpu_util import announce, h_bits, rel_err, require_gpu, ulp_diff_f32
 
 pytestmark = pytest.mark.gpu
 
@@ -53,6 +53,12 @@ class GpuSet:
     def run(self, run, score=None):
         ts, bs = self.cdt.block_scales(self.sumsq, self.sumabs, self.rs.T, self.rs.H, run.eps,
                                        run.sigma_b)
+        if run.exact_norm:
+            ts = self.cdt.tamper_scale_exact(self.ref, run.eps, ws=self.ws, bscale=bs,
+                                             seed=self.wl.seed, cfg_id=run.cfg_id,
+                                             benign_mode=run.benign_mode,
+                                             benign_dist=run.benign_dist, sigma_b=run.sigma_b,
+                                             tamper_base=run.tamper_base)
         self.cdt.canary_sim(self.ref, out=self.h, seed=self.wl.seed, cfg_id=run.cfg_id,
                             benign_mode=run.benign_mode, benign_dist=run.benign_dist,
                             sigma_b=run.sigma_b, mal_mask=self.rs.mal_mask, tamper=run.tamper,
@@ -84,7 +90,19 @@ def check_blocks(gs, run, score, ts, bs, blocks, gain_o):
         q, m = oracle.ref_stats_block(ref_o)
         ts_o, bs_o = oracle.block_scales(rs.T, rs.H, np.array([q]), np.array([m]), run.eps,
                                          run.sigma_b)
-        assert ts_d[s, c] == ts_o[0] and bs_d[s, c] == bs_o[0]
+        same_scale = True
+        if run.exact_norm:
+            # the scale comes from fp64 sums taken in different orders: it may
+            # round one fp32 ulp apart (then h is compared through the score)
+            ts_o[0], _, _ = oracle.tamper_scale_exact_block(
+                s, c, ref_o, run.eps, seed=wl.seed, cfg_id=run.cfg_id,
+                benign_mode=run.benign_mode, benign_dist=run.benign_dist, sigma_b=run.sigma_b,
+                bscale=bs_o[0], tamper_base=run.tamper_base)
+            assert ulp_diff_f32(ts_d[s, c], ts_o[0]) <= 1
+            same_scale = ts_d[s, c] == ts_o[0]
+        else:
+            assert ts_d[s, c] == ts_o[0]
+        assert bs_d[s, c] == bs_o[0]
         h_o = oracle.sim_block(s, c, ref_o, seed=wl.seed, cfg_id=run.cfg_id,
                                benign_mode=run.benign_mode, benign_dist=run.benign_dist,
                                sigma_b=run.sigma_b, bscale=bs_o[0],
@@ -92,7 +110,8 @@ def check_blocks(gs, run, score, ts, bs, blocks, gain_o):
                                tamper_base=run.tamper_base, tscale=ts_o[0], flip_p=run.flip_p,
                                scale=run.scale)
         got = gs.h[s, c].cpu().numpy().view(np.uint16)
-        assert int((got != h_o).sum()) == 0
+        if same_scale:
+            assert int((got != h_o).sum()) == 0
         m_o, _, _ = oracle.drift_block(h_o, ref_o)
         assert rel_err(sc[c, s], m_o) < DRIFT_RTOL
 
@@ -258,10 +277,19 @@ def test_paper_shape(gpu, gold):
         assert int(c[0]) == int(c[2]) == rs.C * (rs.S - 1), run.label
         if k == 0:
             ts_o, bs_o = oracle.block_scales(rs.T, rs.H, q, m, run.eps, run.sigma_b)
+            assert run.exact_norm
+            ts_o, norms_o = oracle.tamper_scale_exact(ref_o, run.eps, seed=wl.seed,
+                                                      cfg_id=run.cfg_id,
+                                                      benign_mode=run.benign_mode,
+                                                      sigma_b=run.sigma_b, bscale=bs_o)
+            ts_d = ts.cpu().numpy()
+            assert ulp_diff_f32(ts_d, ts_o).max() <= 1
+            same = ts_d == ts_o  # blocks whose scales rounded alike: h bit-exact
             h_o = oracle.canary_sim(ref_o, seed=wl.seed, cfg_id=run.cfg_id,
                                     benign_mode=run.benign_mode, sigma_b=run.sigma_b, bscale=bs_o,
                                     mal_mask=rs.mal_mask, tamper=run.tamper, tscale=ts_o)
-            assert np.array_equal(gs.h.cpu().numpy().view(np.uint16), h_o)
+            h_d = gs.h.cpu().numpy().view(np.uint16)
+            assert np.array_equal(h_d[same], h_o[same]) and same.mean() > 0.99
             s64, _, _ = oracle.drift_score(h_o, ref_o)
             assert rel_err(score.cpu().numpy(), s64) < DRIFT_RTOL
             assert counts_match(c, s64, rs.mal_mask, wl.seed, run.cfg_id)

@@ -286,3 +286,40 @@ def test_block_scales_closed_form(orc):
     assert q == 9.0 * T * H and s == 3.0 * T * H
     ts, bs = orc.block_scales(T, H, np.array([q]), np.array([s]), 0.5, 0.25)
     assert ts[0] == 1.5 and bs[0] == 0.75
+
+
+# ----------------------------------------------------------------------------
+# exact-norm Gaussian tamper (Section 3.2: v + eps ||v|| N / ||N||)
+# ----------------------------------------------------------------------------
+def test_exact_norm_tamper_has_norm_eps_times_v(orc):
+    """On the clean base the added perturbation has norm eps ||a|| exactly
+    (up to rounding), where the per-element form only matches it on average."""
+    a = _ref(orc, T=16, H=256)  # a small block: per-element fluctuation is visible
+    eps = 0.05
+    ts, vv, zz = orc.tamper_scale_exact_block(0, 0, a, eps, seed=1, cfg_id=3, sigma_b=0.0,
+                                              tamper_base=BASE_CLEAN)
+    q, _ = orc.ref_stats_block(a)
+    assert vv == q  # clean base: sum v^2 is sum a^2
+    h = orc.sim_block(0, 0, a, seed=1, cfg_id=3, sigma_b=0.0, malicious=True, tamper=T_ADD,
+                      tscale=ts, tamper_base=BASE_CLEAN)
+    m = _rel(h, a)
+    assert abs(m / eps - 1.0) < 2e-4
+    # the per-element form at the same eps misses eps by the sampling error of ||N||
+    ts_el, _ = orc.block_scales(16, 256, np.array([q]), np.array([0.0]), eps, 0.0)
+    h_el = orc.sim_block(0, 0, a, seed=1, cfg_id=3, sigma_b=0.0, malicious=True, tamper=T_ADD,
+                         tscale=ts_el[0], tamper_base=BASE_CLEAN)
+    assert abs(_rel(h_el, a) / eps - 1.0) > 10 * abs(m / eps - 1.0)
+
+
+def test_exact_norm_tamper_on_benign_output(orc):
+    """On the benign base the perturbation is eps ||a + delta||: m^2 = eps^2
+    ||v||^2 / ||a||^2 + sigma^2, with ||v|| = ||a|| (1 + O(sigma^2))."""
+    a = _ref(orc, T=64, H=512)
+    eps, sigma = 0.05, 0.01
+    ts, vv, zz = orc.tamper_scale_exact_block(0, 0, a, eps, seed=2, cfg_id=1, sigma_b=sigma)
+    q, _ = orc.ref_stats_block(a)
+    assert abs(vv / q - 1.0) < 5 * sigma**2
+    assert abs(zz / a.size - 1.0) < 0.05  # unit-variance normals
+    h = orc.sim_block(0, 0, a, seed=2, cfg_id=1, sigma_b=sigma, malicious=True, tamper=T_ADD,
+                      tscale=ts)
+    assert abs(_rel(h, a) / math.sqrt(eps**2 + sigma**2) - 1.0) < 0.01

@@ -30,6 +30,10 @@ def test_paper_shape_six_attacks(orc):
     margins = {}
     for run in rs.runs:
         ts, bs = orc.block_scales(rs.T, rs.H, sumsq, sumabs, run.eps, run.sigma_b)
+        if run.exact_norm:
+            ts, _ = orc.tamper_scale_exact(ref, run.eps, seed=wl.seed, cfg_id=run.cfg_id,
+                                           benign_mode=run.benign_mode, sigma_b=run.sigma_b,
+                                           bscale=bs)
         h = orc.canary_sim(ref, seed=wl.seed, cfg_id=run.cfg_id, benign_mode=run.benign_mode,
                            sigma_b=run.sigma_b, bscale=bs, mal_mask=rs.mal_mask,
                            tamper=run.tamper, tscale=ts, flip_p=run.flip_p, scale=run.scale)
