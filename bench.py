@@ -113,7 +113,7 @@ def sim_kwargs(wl, rs, run, ts, bs):
     return dict(seed=wl.seed, cfg_id=run.cfg_id, benign_mode=run.benign_mode,
                 benign_dist=run.benign_dist, sigma_b=run.sigma_b, mal_mask=rs.mal_mask,
                 tamper=run.tamper, tamper_base=run.tamper_base, flip_p=run.flip_p,
-                scale=run.scale, bscale=bs, tscale=ts)
+                scale=run.scale, bscale=bs, tscale=ts, carry=run.carry)
 
 
 def gpu_step(torch, cdt, wl, preps, scores, score_views, cfgs, auroc_ws, counts, pooled,
@@ -295,7 +295,7 @@ def auroc_row(cdt, torch, score, rs, cfg_id, seed, flags):
     torch.cuda.synchronize()
     c = cdt.u64(counts)[0]
     out = {"auroc": round(cdt.strict_auroc(c), 4), "auroc_mw": round(cdt.mw_auroc(c), 4),
-           "control": round(int(c[3]) / max(1, int(c[5])), 4)}
+           "control": round(int(c[3]) / int(c[5]), 4) if int(c[5]) else None}
     if base is not None:
         out["random_baseline"] = round(cdt.strict_auroc(cdt.u64(base)[0]), 4)
     return out
@@ -336,6 +336,12 @@ def ablation_kernels(torch, cdt, wl, prep):
         out[name] = row
     out["redraw_canary_sim"] = {"ms": round(sim_ms, 4),
                                 "GBps": round(elems * SIM_BYTES_PER_ELEM / (sim_ms * 1e-3) / 1e9, 1)}
+    # the propagation model: stages in order per canary, live error carried
+    kw_c = dict(kw, carry=0.7)
+    chain_ms = time_ms(torch, lambda: cdt.canary_sim(prep.ref, out=r, **kw_c))
+    out["chain_canary_sim"] = {"ms": round(chain_ms, 4), "carry": 0.7,
+                               "GBps": round(elems * SIM_BYTES_PER_ELEM / (chain_ms * 1e-3) / 1e9,
+                                             1)}
     out["run"] = run.label
     del r
     return out
@@ -375,11 +381,46 @@ def table1(torch, cdt, W):
     for name, per in rows.items():
         vals = list(per.values())
         summary[name] = {key: round(sum(v[key] for v in vals) / len(vals), 4)
-                         for key in ("auroc", "random_baseline", "control", "ceiling")}
+                         for key in ("auroc", "random_baseline", "control", "ceiling")
+                         if all(v[key] is not None for v in vals)}
     del prep, r
     torch.cuda.empty_cache()
     return {"workload": "paper 12x100x48x768, block noise sigma_hw 0.002",
             "mean_over_six_attacks": summary, "per_attack": rows}
+
+
+def substudies(torch, cdt, W):
+    """Depth, position, collusion and frontier substudies (Sections 4.4 and
+    5.3-5.5) on the paper's shape with the live error carried between
+    stages: detection AUROC per configuration."""
+    wl = W.substudies()
+    out = {}
+    cache = {}
+    score_all = []
+    for rs in wl.ref_sets:
+        key = (rs.S, rs.ref_set_id)
+        if key not in cache:
+            cache.clear()
+            cache[key] = Prepared(torch, cdt, W, wl, rs)
+        prep = cache[key]
+        run = rs.runs[0]
+        ts, bs = cdt.block_scales(prep.sumsq, prep.sumabs, rs.T, rs.H, run.eps, run.sigma_b)
+        cdt.canary_sim(prep.ref, out=prep.h, **sim_kwargs(wl, rs, run, ts, bs))
+        score = cdt.drift_score(prep.h, prep.ref, ws=prep.ws)
+        row = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed,
+                        cdt.AUROC_CONTROL | cdt.AUROC_RANDOM)
+        import numpy as np
+        sc = score.cpu().numpy()
+        mal = list(rs.mal_shards)
+        ben = [s for s in range(rs.S) if s not in mal]
+        row["median_m_malicious"] = float(f"{np.median(sc[:, mal]):.4g}")
+        row["max_m_benign"] = float(f"{sc[:, ben].max():.4g}")
+        study, name = run.label.split(":")
+        out.setdefault(study, {})[name] = row
+    cache.clear()
+    torch.cuda.empty_cache()
+    return {"carry": W.SUBSTUDY_CARRY, "shape": "k x 100 x 48 x 768, block noise 0.002",
+            "studies": out}
 
 
 def run_sweep(torch, cdt, W, reps):
@@ -506,6 +547,8 @@ def main():
     if not args.no_ablations:
         log("table 1 structure on the paper's shape")
         res["table1"] = table1(torch, cdt, W)
+        log("substudies (depth, position, collusion, frontier)")
+        res["substudies"] = substudies(torch, cdt, W)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(W, args)

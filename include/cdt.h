@@ -139,6 +139,8 @@ typedef struct cdt_sim_params {
     double scale;           /* rescale factor 1 + alpha (used as fp32(scale))      */
     const float* bscale;    /* device [S][C], BLOCK mode, else may be NULL         */
     const float* tscale;    /* device [S][C], needed with CDT_T_ADD                */
+    double carry;           /* propagation gain g in [0, 1] (used as fp32(g)); 0:  */
+                            /* independent stages                                  */
 } cdt_sim_params;
 
 /* h = fp16_rne(v) for every element, with (one fp32 operation per step, in
@@ -155,7 +157,15 @@ typedef struct cdt_sim_params {
  *   SCALE v = fp32(scale) * v
  * One-normal streams use call q = e/2 like cdt_ref_synth; every counter is
  * (q, c, s, stream<<24 | cfg_id).  p: host struct, read during the call.
- * Needs S <= 64. */
+ * Needs S <= 64.
+ *
+ * Propagation model (carry g > 0; the depth, position, collusion and
+ * frontier substudies of Sections 4.4 and 5.3-5.5): stage s sees the live
+ * error of stage s-1, d = fp32(h_{s-1} - a_{s-1}), as the paper's Eq. 2
+ * feeds f_i the live h_{i-1}.  Its noise-free output is u = fp32(a +
+ * fp32(g * d)) (u = a for stage 0); the benign step is v = u + sc * zb (sc
+ * still from |a|), the clean base is u, and the tamper follows as above.
+ * g = 0 gives the independent stages exactly. */
 int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
                    const float* ref, uint16_t* h, void* stream);
 

@@ -368,7 +368,7 @@ static int flip_selected(double p, uint32_t u)
  * noisy-reference ablation). */
 static float benign_value(uint32_t s, uint32_t c, uint32_t e, uint64_t seed, uint32_t cfg_id,
                           int benign_mode, int benign_dist, float sigma_f, float bscale,
-                          int redraw, float a)
+                          int redraw, float a, float base)
 {
     uint32_t st_benign = redraw ? ST_ALT : ST_BENIGN;
     uint32_t st_t12 = redraw ? ST_ALT_T12 : ST_T12;
@@ -383,7 +383,30 @@ static float benign_value(uint32_t s, uint32_t c, uint32_t e, uint64_t seed, uin
                       (double)r32((double)z3 * z3));
         zb = (q == 0.0f) ? 0.0f : r32((double)zb / (double)r32(sqrt((double)q)));
     }
-    return r32((double)a + (double)r32((double)sc * (double)zb));
+    return r32((double)base + (double)r32((double)sc * (double)zb));
+}
+
+/* Eq. 3: the tampering of a malicious stage applied to its benign output v,
+ * or to the noise-free output `base` for the clean base, in this order:
+ * Gaussian, sign flip, rescale. */
+static float tamper_value(uint32_t s, uint32_t c, uint32_t e, uint64_t seed, uint32_t cfg_id,
+                          uint32_t tamper, int tamper_base, float tscale, double flip_p,
+                          float scale_f, float base, float v)
+{
+    if (tamper_base == ORC_BASE_CLEAN)
+        v = base;
+    if (tamper & ORC_T_ADD) {
+        float zt = normal1(seed, ST_TADD, cfg_id, s, c, e);
+        v = r32((double)v + (double)r32((double)tscale * (double)zt));
+    }
+    if (tamper & ORC_T_FLIP) {
+        uint32_t u = word1(seed, ST_TFLIP, cfg_id, s, c, e);
+        if (flip_selected(flip_p, u))
+            v = -v;
+    }
+    if (tamper & ORC_T_SCALE)
+        v = r32((double)scale_f * (double)v);
+    return v;
 }
 
 int orc_sim_range_ex(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t seed,
@@ -397,26 +420,51 @@ int orc_sim_range_ex(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64
         uint32_t e = (uint32_t)(e0 + k);
         float a = ref[k];
         float v = benign_value(s, c, e, seed, cfg_id, benign_mode, benign_dist, sigma_f, bscale,
-                               redraw, a);
+                               redraw, a, a);
 
-        /* tampering, Eq. 3 */
-        if (malicious) {
-            if (tamper_base == ORC_BASE_CLEAN)
-                v = a;
-            if (tamper & ORC_T_ADD) {
-                float zt = normal1(seed, ST_TADD, cfg_id, s, c, e);
-                v = r32((double)v + (double)r32((double)tscale * (double)zt));
-            }
-            if (tamper & ORC_T_FLIP) {
-                uint32_t u = word1(seed, ST_TFLIP, cfg_id, s, c, e);
-                if (flip_selected(flip_p, u))
-                    v = -v;
-            }
-            if (tamper & ORC_T_SCALE)
-                v = r32((double)scale_f * (double)v);
-        }
+        if (malicious)
+            v = tamper_value(s, c, e, seed, cfg_id, tamper, tamper_base, tscale, flip_p, scale_f,
+                             a, v);
         h[k] = orc_f16_rne(v);
     }
+    return 0;
+}
+
+/* Propagation model (Sections 4.4, 5.3-5.5: depth, position, collusion,
+ * frontier).  Eq. 2 feeds stage i the live h_{i-1}; with a carry gain g the
+ * live error of the previous stage, d = fp32(h_{s-1} - a_{s-1}), enters
+ * stage s as u = fp32(a + fp32(g d)) (u = a for stage 0).  The benign step is
+ * v = fp32(u + fp32(sc zb)) with sc from |a| (or the block scale), the clean
+ * base of a malicious stage is u, and h = fp16(v).  Stages run in order for
+ * each canary and element; g = 0 is the independent live pass. */
+int orc_canary_sim_chain(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
+                         uint32_t cfg_id, int benign_mode, int benign_dist, double sigma_b,
+                         const float* bscale, uint64_t mal_mask, uint32_t tamper,
+                         int tamper_base, const float* tscale, double flip_p, double scale,
+                         int redraw, double carry, const float* ref, uint16_t* h)
+{
+    uint64_t n = (uint64_t)T * H;
+    float sigma_f = r32(sigma_b);
+    float scale_f = r32(scale);
+    float g = r32(carry);
+    for (uint32_t c = 0; c < C; ++c)
+        for (uint64_t k = 0; k < n; ++k) {
+            uint32_t e = (uint32_t)k;
+            float d = 0.0f;
+            for (uint32_t s = 0; s < S; ++s) {
+                uint64_t b = (uint64_t)s * C + c;
+                float a = ref[b * n + k];
+                float u = (s == 0) ? a : r32((double)a + (double)r32((double)g * (double)d));
+                float v = benign_value(s, c, e, seed, cfg_id, benign_mode, benign_dist, sigma_f,
+                                       bscale ? bscale[b] : 0.0f, redraw, a, u);
+                if (s < 64 && ((mal_mask >> s) & 1u))
+                    v = tamper_value(s, c, e, seed, cfg_id, tamper, tamper_base,
+                                     tscale ? tscale[b] : 0.0f, flip_p, scale_f, u, v);
+                uint16_t hb = orc_f16_rne(v);
+                h[b * n + k] = hb;
+                d = r32(orc_f16_value(hb) - (double)a);
+            }
+        }
     return 0;
 }
 
@@ -438,7 +486,7 @@ float orc_tamper_scale_exact_block(uint32_t s, uint32_t c, uint32_t T, uint32_t 
         float v = (tamper_base == ORC_BASE_CLEAN)
                       ? a
                       : benign_value(s, c, e, seed, cfg_id, benign_mode, benign_dist, sigma_f,
-                                     bscale, redraw, a);
+                                     bscale, redraw, a, a);
         float z = normal1(seed, ST_TADD, cfg_id, s, c, e);
         vv += (double)v * (double)v;
         zz += (double)z * (double)z;

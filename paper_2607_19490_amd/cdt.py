@@ -46,6 +46,7 @@ class SimParams(ctypes.Structure):
         ("scale", ctypes.c_double),
         ("bscale", ctypes.c_void_p),
         ("tscale", ctypes.c_void_p),
+        ("carry", ctypes.c_double),
     ]
 
 
@@ -217,11 +218,11 @@ def block_scales(sumsq, sumabs, T, H, eps, sigma_b, tscale=None, bscale=None):
 
 def sim_params(*, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE, benign_dist=DIST_GAUSS,
                sigma_b=1e-3, mal_mask=0, tamper=0, tamper_base=BASE_BENIGN, flip_p=0.0,
-               scale=1.0, bscale=None, tscale=None, redraw=False):
+               scale=1.0, bscale=None, tscale=None, redraw=False, carry=0.0):
     return SimParams(seed, cfg_id, benign_mode, benign_dist, tamper, tamper_base, int(redraw),
                      mal_mask, sigma_b, flip_p, scale,
                      None if bscale is None else bscale.data_ptr(),
-                     None if tscale is None else tscale.data_ptr())
+                     None if tscale is None else tscale.data_ptr(), carry)
 
 
 def canary_sim(ref, out=None, *, bscale=None, tscale=None, **kw):

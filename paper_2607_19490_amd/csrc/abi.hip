@@ -58,7 +58,7 @@ bool empty(uint32_t S, uint32_t C, uint32_t T, uint32_t H) {
 
 extern "C" {
 
-int cdt_version(void) { return 2; }
+int cdt_version(void) { return 3; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -151,6 +151,8 @@ int check_sim(const char* fn, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
     if (!(p->flip_p >= 0.0 && p->flip_p <= 1.0))
         return fail(CDT_EINVAL, "%s: flip_p must lie in [0, 1]", fn);
     if (!isfinite(p->scale)) return fail(CDT_EINVAL, "%s: scale must be finite", fn);
+    if (!(p->carry >= 0.0 && p->carry <= 1.0))
+        return fail(CDT_EINVAL, "%s: carry must lie in [0, 1]", fn);
     const uint64_t mal = p->mal_mask & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
     if (!empty(S, C, T, H)) {
         if (p->benign_mode == CDT_NOISE_BLOCK && !p->bscale)
@@ -176,6 +178,7 @@ int check_sim(const char* fn, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
     L->flip_all = p->flip_p >= 1.0;
     L->flip_thr = L->flip_all ? 0u : static_cast<uint32_t>(floor(p->flip_p * 4294967296.0));
     L->scale = static_cast<float>(p->scale);
+    L->carry = static_cast<float>(p->carry);
     L->bscale = p->bscale;
     L->tscale = p->tscale;
     return CDT_OK;
@@ -202,6 +205,9 @@ int cdt_sim_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_
     cdt::SimLaunch L;
     int rc = check_sim("cdt_sim_score", S, C, T, H, p, &L);
     if (rc) return rc;
+    if (L.carry != 0.0f)
+        return fail(CDT_EINVAL, "cdt_sim_score: the propagation model (carry > 0) needs "
+                                "cdt_canary_sim then cdt_drift_score");
     if (static_cast<uint64_t>(S) * C == 0) return ok();
     if (!score) return fail(CDT_EINVAL, "cdt_sim_score: score is NULL");
     if (static_cast<uint64_t>(T) * H > 0) {
@@ -226,6 +232,8 @@ int cdt_tamper_scale_exact(uint32_t S, uint32_t C, uint32_t T, uint32_t H,
     if (!p) return fail(CDT_EINVAL, "%s: params is NULL", fn);
     if (!(eps >= 0.0) || !isfinite(eps)) return fail(CDT_EINVAL, "%s: eps must be finite and >= 0", fn);
     // The tamper settings do not enter the norms (tscale is this call's output).
+    if (p->carry != 0.0)
+        return fail(CDT_EINVAL, "%s: not defined for the propagation model (carry > 0)", fn);
     cdt_sim_params q = *p;
     q.tamper = 0;
     q.tscale = nullptr;

@@ -40,6 +40,7 @@ struct SimLaunch {
     uint32_t flip_thr;   // floor(p 2^32) (p < 1)
     uint32_t flip_all;   // p >= 1
     float scale;         // fp32(scale)
+    float carry;         // fp32(carry): propagation gain (0: independent stages)
     const float* bscale;
     const float* tscale;
 };

@@ -87,10 +87,12 @@ __device__ __forceinline__ SimBlock sim_block(const SimArgs& A, uint64_t block) 
     return B;
 }
 
-// Eq. 2: the benign output v = a + sc * zb of elements e0..e0+7.
+// Eq. 2: the benign output v = base + sc * zb of elements e0..e0+7, with the
+// noise scale taken from the reference a (elementwise mode) and base = a for
+// independent stages (base = a + carried error in the propagation model).
 template <bool kT3, bool kBlock>
 __device__ __forceinline__ void benign8(const SimArgs& A, const SimBlock& B, uint32_t e0,
-                                        const float a[8], float v[8]) {
+                                        const float a[8], const float base[8], float v[8]) {
     float zb[8];
     normals8(A.key, e0, B.c, B.s, A.tag_benign, zb);
     if (kT3) {
@@ -108,17 +110,17 @@ __device__ __forceinline__ void benign8(const SimArgs& A, const SimBlock& B, uin
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
         const float sc = kBlock ? B.bsc : A.sigma_b * fabsf(a[k]);
-        v[k] = a[k] + sc * zb[k];
+        v[k] = base[k] + sc * zb[k];
     }
 }
 
 // Eq. 3: the tampering of a malicious shard, in place on v (which holds the
-// benign output; the clean base replaces it by a first).
+// benign output; the clean base replaces it by the noise-free base first).
 __device__ __forceinline__ void tamper8(const SimArgs& A, const SimBlock& B, uint32_t e0,
-                                        const float a[8], float v[8]) {
+                                        const float base[8], float v[8]) {
     if (A.clean) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) v[k] = a[k];
+        for (int k = 0; k < 8; ++k) v[k] = base[k];
     }
     if (A.tamper & 1u) {
         float zt[8];
@@ -140,19 +142,47 @@ __device__ __forceinline__ void tamper8(const SimArgs& A, const SimBlock& B, uin
     }
 }
 
+__device__ __forceinline__ u32x4 pack_half8(const float v[8]) {
+    u32x4 o;
+    o.x = to_half_bits(v[0]) | (static_cast<uint32_t>(to_half_bits(v[1])) << 16);
+    o.y = to_half_bits(v[2]) | (static_cast<uint32_t>(to_half_bits(v[3])) << 16);
+    o.z = to_half_bits(v[4]) | (static_cast<uint32_t>(to_half_bits(v[5])) << 16);
+    o.w = to_half_bits(v[6]) | (static_cast<uint32_t>(to_half_bits(v[7])) << 16);
+    return o;
+}
+
 // Live fp16 activations of elements e0..e0+7 from their references.
 template <bool kT3, bool kBlock>
 __device__ __forceinline__ u32x4 sim_group8(const SimArgs& A, const SimBlock& B, uint32_t e0,
                                             const f32x4& a_lo, const f32x4& a_hi) {
     const float a[8] = {a_lo.x, a_lo.y, a_lo.z, a_lo.w, a_hi.x, a_hi.y, a_hi.z, a_hi.w};
     float v[8];
-    benign8<kT3, kBlock>(A, B, e0, a, v);
+    benign8<kT3, kBlock>(A, B, e0, a, a, v);
     if (B.mal) tamper8(A, B, e0, a, v);
-    u32x4 o;
-    o.x = to_half_bits(v[0]) | (static_cast<uint32_t>(to_half_bits(v[1])) << 16);
-    o.y = to_half_bits(v[2]) | (static_cast<uint32_t>(to_half_bits(v[3])) << 16);
-    o.z = to_half_bits(v[4]) | (static_cast<uint32_t>(to_half_bits(v[5])) << 16);
-    o.w = to_half_bits(v[6]) | (static_cast<uint32_t>(to_half_bits(v[7])) << 16);
+    return pack_half8(v);
+}
+
+// The propagation model: stage s of canary c sees the previous stage's live
+// error d = fp32(h_{s-1} - a_{s-1}) through a carry gain g: its noise-free
+// output is u = a + fp32(g * d) (u = a for the first stage); the benign
+// noise and the tamper act on u.  Updates d to this stage's error.
+template <bool kT3, bool kBlock>
+__device__ __forceinline__ u32x4 chain_group8(const SimArgs& A, const SimBlock& B, uint32_t e0,
+                                              bool first, float gain, const f32x4& a_lo,
+                                              const f32x4& a_hi, float d[8]) {
+    const float a[8] = {a_lo.x, a_lo.y, a_lo.z, a_lo.w, a_hi.x, a_hi.y, a_hi.z, a_hi.w};
+    float u[8], v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) u[k] = first ? a[k] : a[k] + gain * d[k];
+    benign8<kT3, kBlock>(A, B, e0, a, u, v);
+    if (B.mal) tamper8(A, B, e0, u, v);
+    const u32x4 o = pack_half8(v);
+    const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        d[2 * k] = half_bits_to_float(w[k] & 0xFFFFu) - a[2 * k];
+        d[2 * k + 1] = half_bits_to_float(w[k] >> 16) - a[2 * k + 1];
+    }
     return o;
 }
 

@@ -152,6 +152,42 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
     }
 }
 
+// Propagation model: a thread walks one group of 8 elements of one canary
+// through all S stages in order, carrying the live error in registers; a
+// workgroup chunk covers kGenChunkGroups groups of one canary, so the
+// per-stage block state is workgroup-uniform.  Same bytes as the live pass
+// (4 B read, 2 B written per element); nothing is re-read.
+template <bool kT3, bool kBlock>
+__global__ __launch_bounds__(kGenThreads) void canary_chain_kernel(SimArgs A, uint32_t S,
+                                                                   float gain,
+                                                                   const float* __restrict__ ref,
+                                                                   uint16_t* __restrict__ h) {
+    const uint64_t n = static_cast<uint64_t>(A.n8) * 8;
+    for (uint64_t it = blockIdx.x; it < A.total_chunks; it += gridDim.x) {
+        const uint64_t chunk = xcd_contiguous(it, A.total_chunks);
+        const uint32_t c = static_cast<uint32_t>(chunk / A.chunks_per_block);
+        const uint32_t g0 =
+            static_cast<uint32_t>(chunk - static_cast<uint64_t>(c) * A.chunks_per_block) *
+            kGenChunkGroups;
+#pragma unroll 1
+        for (int item = 0; item < kGenItems; ++item) {
+            const uint32_t g = g0 + item * kGenThreads + threadIdx.x;
+            if (g >= A.n8) break;
+            float d[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+            for (uint32_t s = 0; s < S; ++s) {
+                const uint64_t block = static_cast<uint64_t>(s) * A.C + c;
+                const SimBlock B = sim_block<kBlock>(A, block);
+                const f32x4* in = reinterpret_cast<const f32x4*>(ref + block * n);
+                u32x4* out = reinterpret_cast<u32x4*>(h + block * n);
+                const f32x4 a_lo = load_stream(in + 2 * g), a_hi = load_stream(in + 2 * g + 1);
+                store_stream(out + g,
+                             chain_group8<kT3, kBlock>(A, B, g * 8, s == 0, gain, a_lo, a_hi, d));
+            }
+        }
+    }
+}
+
 // Grid for a chunked elementwise walk: 64 workgroups per CU; larger jobs
 // loop with a stride (16384) that is a multiple of the XCD count, as
 // xcd_contiguous needs.
@@ -198,10 +234,32 @@ hipError_t launch_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const d
     return hipGetLastError();
 }
 
+hipError_t launch_canary_chain(const SimLaunch& p, const float* ref, uint16_t* h,
+                               hipStream_t st) {
+    const uint64_t n8 = static_cast<uint64_t>(p.T) * p.H / 8;
+    const uint64_t cpc = (n8 + kGenChunkGroups - 1) / kGenChunkGroups;  // chunks per canary
+    const SimArgs A = make_sim_args(p, cpc, cpc * p.C);
+    const dim3 grid(gen_grid(A.total_chunks)), block(kGenThreads);
+    if (A.t3 && A.block_mode)
+        hipLaunchKernelGGL((canary_chain_kernel<true, true>), grid, block, 0, st, A, p.S, p.carry,
+                           ref, h);
+    else if (A.t3)
+        hipLaunchKernelGGL((canary_chain_kernel<true, false>), grid, block, 0, st, A, p.S,
+                           p.carry, ref, h);
+    else if (A.block_mode)
+        hipLaunchKernelGGL((canary_chain_kernel<false, true>), grid, block, 0, st, A, p.S,
+                           p.carry, ref, h);
+    else
+        hipLaunchKernelGGL((canary_chain_kernel<false, false>), grid, block, 0, st, A, p.S,
+                           p.carry, ref, h);
+    return hipGetLastError();
+}
+
 hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, hipStream_t st) {
     const uint64_t n = static_cast<uint64_t>(p.T) * p.H;
     const uint64_t nblocks = static_cast<uint64_t>(p.S) * p.C;
     if (n == 0 || nblocks == 0) return hipSuccess;
+    if (p.carry != 0.0f) return launch_canary_chain(p, ref, h, st);
     const uint64_t n8 = n / 8;
     const uint64_t cpb = (n8 + kGenChunkGroups - 1) / kGenChunkGroups;
     const SimArgs A = make_sim_args(p, cpb, cpb * nblocks);

@@ -221,7 +221,7 @@ __global__ __launch_bounds__(kReduceThreads) void tamper_norms_partial_kernel(
 #pragma unroll
                 for (int k = 0; k < 8; ++k) v[k] = a[k];
             } else {
-                benign8<kT3, kBlock>(A, B, g * 8, a, v);
+                benign8<kT3, kBlock>(A, B, g * 8, a, a, v);
             }
             normals8(A.key, g * 8, B.c, B.s, A.tag_add, z);
 #pragma unroll

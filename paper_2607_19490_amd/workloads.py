@@ -17,6 +17,8 @@ Workloads
               [1e-4, 1e-1], Gaussian and Student-t noise, tamper 0.02
   paper       12 x 100 x 48 x 768 (the paper's GPT-2 / Pythia-160M shape),
               block-scaled benign noise sigma_hw = 0.002, the six attacks
+  substudies  the depth, position, collusion and frontier substudies on the
+              paper's shape with the live error carried between stages
 """
 from dataclasses import dataclass, field
 from typing import List, Tuple
@@ -49,6 +51,7 @@ class Run:
     scale: float = 1.0      # rescale factor 1 + alpha
     tamper_base: int = BASE_BENIGN
     exact_norm: bool = False  # Gaussian tamper scaled to exactly eps ||v|| (Section 3.2)
+    carry: float = 0.0        # propagation gain of the live error between stages
     label: str = ""
 
 
@@ -182,8 +185,51 @@ def paper() -> Workload:
                                      tuple(runs)),))
 
 
+SUBSTUDY_CARRY = 0.7
+SUBSTUDY_DEPTHS = (2, 4, 6, 8, 10, 12)
+SUBSTUDY_POSITIONS = (0, 2, 5, 8, 11)          # first ... last of 12 stages
+SUBSTUDY_COLLUDERS = (1, 2, 3, 4)
+SUBSTUDY_EPS = (0.10, 0.05, 0.02, 0.01, 0.005, 0.002, 0.001)
+
+
+def colluder_positions(k: int, c: int) -> Tuple[int, ...]:
+    """c colluders spaced uniformly over k stages (0-indexed): the j-th at
+    floor(k (j + 1) / (c + 1)) - 1, so c = 1 is the middle stage floor(k/2)."""
+    return tuple(k * (j + 1) // (c + 1) - 1 for j in range(c))
+
+
+def substudies() -> Workload:
+    """Sections 4.4 and 5.3-5.5 on the paper's shape (100 canaries x 48 tokens
+    x d = 768, block noise sigma_hw = 0.002), with the live error of each
+    stage carried into the next (gain SUBSTUDY_CARRY):
+      depth      k in {2, ..., 12}, attacker at the middle, Gaussian 0.05
+      position   k = 12, attacker at 5 positions from first to last
+      collusion  k = 12, 1..4 colluders spaced uniformly
+      frontier   k = 12, Gaussian eps from 0.10 down to 0.001
+    Each configuration is one reference set with one run; configurations of
+    one shape share their references (same ref_set_id)."""
+    C, T, H = 100, 48, 768
+    n_out = n_outliers(H)
+    sets = []
+
+    def add(name, S, mal, eps):
+        run = Run(len(sets), benign_mode=NOISE_BLOCK, sigma_b=0.002, tamper=T_ADD, eps=eps,
+                  carry=SUBSTUDY_CARRY, label=name)
+        sets.append(RefSet(S, S, C, T, H, n_out, tuple(mal), (run,)))
+
+    for k in SUBSTUDY_DEPTHS:
+        add(f"depth:k{k}", k, (k // 2 - 1,), 0.05)
+    for pos in SUBSTUDY_POSITIONS:
+        add(f"position:{pos}", 12, (pos,), 0.05)
+    for c in SUBSTUDY_COLLUDERS:
+        add(f"collusion:c{c}", 12, colluder_positions(12, c), 0.05)
+    for eps in SUBSTUDY_EPS:
+        add(f"frontier:eps{eps:g}", 12, (5,), eps)
+    return Workload("substudies", tuple(sets))
+
+
 WORKLOADS = {"tiny": tiny, "llama7b": llama7b, "llama70b": llama70b, "sweep": sweep,
-             "snr": snr, "paper": paper}
+             "snr": snr, "paper": paper, "substudies": substudies}
 
 
 def get(name: str) -> Workload:

@@ -38,7 +38,7 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 2
+    assert L.cdt_version() == 3
     assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
@@ -126,6 +126,14 @@ def test_sim_param_validation(cdt):
                            None) == cdt.EALIGN
     assert L.cdt_sim_score(4, 2, 2, 16, ctypes.byref(p), 16, None, 16, None, 16, 1,
                            None) == cdt.EINVAL
+    assert call(carry=1.5) == cdt.EINVAL
+    assert call(carry=-0.1) == cdt.EINVAL
+    p = cdt.sim_params(seed=0, cfg_id=0, carry=0.5)
+    assert L.cdt_sim_score(4, 2, 2, 16, ctypes.byref(p), 16, None, 16, None, 16, 1 << 20,
+                           None) == cdt.EINVAL
+    assert "carry" in _err(cdt)
+    assert L.cdt_tamper_scale_exact(4, 2, 2, 16, ctypes.byref(p), 16, 0.1, 16, None, 16,
+                                    1 << 20, None) == cdt.EINVAL
     p = cdt.sim_params(seed=0, cfg_id=0)
     p.redraw = 2
     assert L.cdt_canary_sim(4, 2, 2, 16, ctypes.byref(p), 16, 16, None) == cdt.EINVAL

@@ -323,3 +323,62 @@ def test_exact_norm_tamper_on_benign_output(orc):
     h = orc.sim_block(0, 0, a, seed=2, cfg_id=1, sigma_b=sigma, malicious=True, tamper=T_ADD,
                       tscale=ts)
     assert abs(_rel(h, a) / math.sqrt(eps**2 + sigma**2) - 1.0) < 0.01
+
+
+# ----------------------------------------------------------------------------
+# propagation model (Eq. 2 with the live input h_{i-1}; Sections 5.3-5.5)
+# ----------------------------------------------------------------------------
+def _chain(orc, ref, carry, **kw):
+    import ctypes
+    ref = np.ascontiguousarray(ref, np.float32)
+    S, C, T, H = ref.shape
+    h = np.empty(ref.shape, np.uint16)
+    args = dict(seed=4, cfg_id=2, benign_mode=0, benign_dist=0, sigma_b=0.0, mal_mask=0,
+                tamper=0, tamper_base=0, flip_p=0.0, scale=1.0, redraw=0)
+    args.update(kw)
+    ts = args.pop("tscale", None)
+    ts = None if ts is None else np.ascontiguousarray(ts, np.float32)
+    orc.lib().orc_canary_sim_chain(
+        S, C, T, H, args["seed"], args["cfg_id"], args["benign_mode"], args["benign_dist"],
+        args["sigma_b"], None, args["mal_mask"], args["tamper"], args["tamper_base"],
+        None if ts is None else ts.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+        args["flip_p"], args["scale"], args["redraw"], carry,
+        ref.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+        h.ctypes.data_as(ctypes.POINTER(ctypes.c_uint16)))
+    return h
+
+
+def test_chain_without_carry_is_the_independent_pass(orc):
+    ref = orc.ref_synth(5, 3, 8, 64, 4, 0, np.ones(64, np.float32))
+    ts = np.full((5, 3), 0.05, np.float32)
+    kw = dict(sigma_b=1e-2, mal_mask=1 << 2, tamper=1 | 2, tscale=ts, flip_p=0.1)
+    want = orc.canary_sim(ref, seed=4, cfg_id=2, **kw)
+    np.testing.assert_array_equal(_chain(orc, ref, 0.0, **kw), want)
+
+
+def test_chain_benign_error_law(orc):
+    """e_s = delta_s + g e_{s-1} with independent deltas: m_s^2 = sigma^2
+    (1 + g^2 + ... + g^(2s))."""
+    S, g, sigma = 6, 0.8, 1e-2
+    ref = orc.ref_synth(S, 1, 128, 512, 5, 0, np.ones(512, np.float32))
+    h = _chain(orc, ref, g, sigma_b=sigma)
+    for s in range(S):
+        m = _rel(h[s, 0], ref[s, 0])
+        want = sigma * math.sqrt(sum(g ** (2 * j) for j in range(s + 1)))
+        assert abs(m / want - 1.0) < 0.02, (s, m, want)
+
+
+def test_chain_carries_the_tamper_downstream(orc):
+    """A Gaussian tamper eps at stage 2 reaches stage 2 + k scaled by g^k; with
+    g = 1 and no noise it propagates undiminished (relative to equal-scale
+    references)."""
+    S, eps = 6, 0.05
+    ref = orc.ref_synth(S, 1, 128, 512, 6, 0, np.ones(512, np.float32))
+    q, _ = orc.ref_stats(ref)
+    ts, _ = orc.block_scales(128, 512, q, q, eps, 0.0)
+    for g in (0.5, 1.0):
+        h = _chain(orc, ref, g, mal_mask=1 << 2, tamper=1, tscale=ts, tamper_base=1)
+        for s in range(S):
+            m = _rel(h[s, 0], ref[s, 0])
+            want = 0.0 if s < 2 else eps * g ** (s - 2)
+            assert abs(m - want) < 0.02 * eps + 3e-4, (g, s, m, want)
