@@ -444,6 +444,18 @@ def run_sweep(torch, cdt, W, reps):
     ms = times[len(times) // 2]
     fused_ms = time_ms(torch, lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs,
                                                auroc_ws, counts, pooled, fused=True), reps)
+    # scoring alone (live activations already resident): every config's
+    # drift_score over its reference set plus the one batched auroc
+    def score_only():
+        k = 0
+        for prep in preps:
+            for _ in prep.rs.runs:
+                cdt.drift_score(prep.h, prep.ref, out=views[k], ws=prep.ws)
+                k += 1
+        cdt.auroc(cfgs, scores, seed=wl.seed, flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED,
+                  counts=counts, pooled=pooled, ws=auroc_ws)
+    score_ms = time_ms(torch, score_only, reps)
+    gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled)
     # auroc alone
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
@@ -463,6 +475,8 @@ def run_sweep(torch, cdt, W, reps):
         "configs_per_s": round(len(cfgs) / (ms * 1e-3), 1),
         "fused_ms": round(fused_ms, 3),
         "fused_configs_per_s": round(len(cfgs) / (fused_ms * 1e-3), 1),
+        "sim_excluded_ms": round(score_ms, 3),
+        "sim_excluded_configs_per_s": round(len(cfgs) / (score_ms * 1e-3), 1),
         "auroc_only_ms": round(auroc_ms, 4),
         "auroc_only_configs_per_s": round(len(cfgs) / (auroc_ms * 1e-3), 1),
         "auroc_min": round(min(strict), 4),
@@ -473,6 +487,67 @@ def run_sweep(torch, cdt, W, reps):
     del preps, h_buf, scores
     torch.cuda.empty_cache()
     return out
+
+
+def attainable(torch):
+    """What torch's own kernels reach on the same box for the detector's two
+    byte streams: a read-only reduction (drift_score's stream), a plain copy,
+    and an fp32 -> fp16 conversion (canary_sim's 4 B read + 2 B write).
+    Context for the roofline fraction, not part of the step."""
+    n = 1 << 30
+    x = torch.ones((n,), dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    y16 = torch.empty((n,), dtype=torch.float16, device="cuda")
+    out = {}
+    for name, fn, nbytes in (("sum_fp32_read", lambda: torch.sum(x), 4 * n),
+                             ("copy_fp32", lambda: y.copy_(x), 8 * n),
+                             ("convert_fp32_to_fp16", lambda: y16.copy_(x), 6 * n)):
+        ms = time_ms(torch, fn, 7)
+        out[name] = {"ms": round(ms, 4), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+    del x, y, y16
+    torch.cuda.empty_cache()
+    out["note"] = "torch kernels over 2^30 elements (4 GiB fp32), median of 7"
+    return out
+
+
+def small_latency(torch, cdt, W):
+    """The 4 x 8 x 16 x 256 workload (0.8 MB of scored bytes, resident in the
+    last-level cache): per-launch and per-step latency, not bandwidth."""
+    wl = W.tiny()
+    preps = [Prepared(torch, cdt, W, wl, rs) for rs in wl.ref_sets]
+    scores, views, cfgs, counts, pooled, auroc_ws = setup_batch(torch, cdt, wl, preps)
+    prep = preps[0]
+    rs, run = prep.rs, prep.rs.runs[0]
+    ts, bs = prep.scales[0]
+    kw = sim_kwargs(wl, rs, run, ts, bs)
+    flags = cdt.AUROC_CONTROL | cdt.AUROC_POOLED
+    cases = (
+        ("canary_sim", lambda: cdt.canary_sim(prep.ref, out=prep.h, **kw)),
+        ("drift_score", lambda: cdt.drift_score(prep.h, prep.ref, out=views[0], ws=prep.ws)),
+        ("auroc", lambda: cdt.auroc(cfgs, scores, seed=wl.seed, flags=flags, counts=counts,
+                                    pooled=pooled, ws=auroc_ws)),
+        ("step", lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws,
+                                  counts, pooled)),
+        ("fused_step", lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws,
+                                        counts, pooled, fused=True)),
+    )
+    out = {name: round(time_ms(torch, fn, 21) * 1e3, 1) for name, fn in cases}
+    del preps, scores, views
+    return {"workload": "tiny 4x8x16x256", "unit": "us (median of 21, HIP events)",
+            "latency": out}
+
+
+def host_cpu():
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, os.cpu_count()
 
 
 def cpu_baseline(W, args):
@@ -515,6 +590,8 @@ def cpu_baseline(W, args):
         "sample": f"{rs.S} shards x {Cs} canary(ies) x {rs.T} x {rs.H}, {len(rs.runs)} runs "
                   f"(canary_sim + drift + auroc), {dt:.1f} s",
         "seconds": round(dt, 2),
+        "host_cpu": host_cpu()[0],
+        "host_threads": host_cpu()[1],
     }
 
 
@@ -542,6 +619,9 @@ def main():
         del x, y
         log("copy calibration: 4 GiB read + 4 GiB written")
     res, _ = run_main(torch, cdt, W, args)
+    if not args.no_ablations:
+        res["attainable"] = attainable(torch)
+        res["small"] = small_latency(torch, cdt, W)
     if not args.no_sweep:
         res["sweep"] = run_sweep(torch, cdt, W, args.sweep_reps)
     if not args.no_ablations:
