@@ -35,7 +35,7 @@ SIM_BYTES_PER_ELEM = 6        # fp32 a read + fp16 h written
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "drift_score_llama70b_hbm_traffic.md")
-DRIFT_SOURCES = ("reduce.hip", "cdt_device.hpp", "cdt_launch.hpp")
+DRIFT_SOURCES = ("drift.hip", "cdt_reduce.hpp", "cdt_device.hpp")
 
 
 def log(msg):

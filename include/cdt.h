@@ -28,6 +28,13 @@
  *     pointers; S <= 64 wherever a shard bit mask is involved.
  *   - Empty shapes (S, C, T or H zero) are valid and do no work, except
  *     that drift scores of empty blocks are written as 0.
+ *   - Canary sharding: every generated value and every per-canary random
+ *     draw is keyed by the canary's global index canary_base + c.  A caller
+ *     holding canaries [c0, c0 + C) of a larger run passes canary_base = c0
+ *     and gets bit for bit those canaries' references, live activations,
+ *     scores and per-canary counts of the whole run; the integer counts of
+ *     cdt_auroc add up exactly over such slices (not the pooled ranking,
+ *     which compares canaries with each other).  canary_base + C <= 2^32.
  */
 #ifndef CDT_H
 #define CDT_H
@@ -85,9 +92,11 @@ int cdt_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed, uint3
  * and 2-3 for odd e, made into z by the Irwin-Hall rule
  *   n = sum of the four 16-bit halves of the two words - 131070,
  *   z = fp32(n) * fp32(sqrt(3 / (2^32 - 1))).
+ * c in the counter is the global canary index canary_base + c.
  * gain: [H] fp32 (device). */
 int cdt_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
-                  uint32_t ref_set_id, const float* gain, float* ref, void* stream);
+                  uint32_t ref_set_id, uint32_t canary_base, const float* gain, float* ref,
+                  void* stream);
 
 /* Workspace (device bytes) needed by cdt_ref_stats and the four block
  * reductions (cdt_drift_score, cdt_drift_score_f16ref, cdt_cosine_score,
@@ -141,6 +150,8 @@ typedef struct cdt_sim_params {
     const float* tscale;    /* device [S][C], needed with CDT_T_ADD                */
     double carry;           /* propagation gain g in [0, 1] (used as fp32(g)); 0:  */
                             /* independent stages                                  */
+    uint32_t canary_base;   /* global index of canary 0 (0 for a whole run)        */
+    uint32_t reserved;      /* must be 0                                           */
 } cdt_sim_params;
 
 /* h = fp16_rne(v) for every element, with (one fp32 operation per step, in
@@ -156,7 +167,8 @@ typedef struct cdt_sim_params {
  *         TAMPER_FLIP call q = e/4
  *   SCALE v = fp32(scale) * v
  * One-normal streams use call q = e/2 like cdt_ref_synth; every counter is
- * (q, c, s, stream<<24 | cfg_id).  p: host struct, read during the call.
+ * (q, canary_base + c, s, stream<<24 | cfg_id).  p: host struct, read
+ * during the call.
  * Needs S <= 64.
  *
  * Propagation model (carry g > 0; the depth, position, collusion and
@@ -250,7 +262,7 @@ typedef struct cdt_auroc_cfg {
     uint64_t score_off;  /* element offset of its [C][S] table in `scores`       */
     uint64_t pos_mask;   /* malicious shards (the positives of the ranking)      */
     uint32_t cfg_id;     /* counter id of the SCRAMBLE stream (< 2^24)            */
-    uint32_t reserved;   /* must be 0                                             */
+    uint32_t canary_base; /* global index of canary 0 (0 for a whole run)          */
 } cdt_auroc_cfg;
 
 /* Bytes of device workspace cdt_auroc needs for n_cfg configurations. */
@@ -263,17 +275,17 @@ size_t cdt_auroc_workspace_bytes(uint32_t n_cfg);
  *       printed is G / pairs, the Mann-Whitney value (G + E/2) / pairs);
  *   counts[g][3..5] = the same for the scrambled-label control (if
  *       CDT_AUROC_CONTROL, else 0): per canary t a benign shard j*, the
- *       (u mod B)-th benign shard in increasing order, u = Philox word 0 of
- *       counter (t, 0, 0, SCRAMBLE<<24 | cfg_id), B the number of benign
- *       shards, ranked against the benign shards other than j* (all other
- *       shards with CDT_CTRL_INCLUDE_TRUE);
+ *       (u mod B)-th benign shard in increasing order, u = Philox word 0
+ *       of counter (canary_base + t, 0, 0, SCRAMBLE<<24 | cfg_id), B the
+ *       number of benign shards, ranked against the benign shards other
+ *       than j* (all other shards with CDT_CTRL_INCLUDE_TRUE);
  *   pooled[g][0..2] = G, E, pairs over every positive score against every
  *       negative score of the configuration (if CDT_AUROC_POOLED; needs
  *       C*S <= 16384; pooled may be NULL otherwise);
  *   baseline[g][0..2] = G, E, pairs of Eq. 5 with every score replaced by
  *       the random-baseline score of Section 4.5, u(t, s) = (w >> 8) 2^-24,
- *       w = Philox word 0 of counter (t, s, 0, RANDOM<<24 | cfg_id) (if
- *       CDT_AUROC_RANDOM; baseline may be NULL otherwise).
+ *       w = Philox word 0 of counter (canary_base + t, s, 0, RANDOM<<24 |
+ *       cfg_id) (if CDT_AUROC_RANDOM; baseline may be NULL otherwise).
  * Score order: NaN below every number, NaN ties NaN, -0 ties +0.
  * counts: device [n_cfg][6] uint64; scores: device fp32; n_scores bounds
  * every configuration's table. */

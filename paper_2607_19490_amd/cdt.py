@@ -47,6 +47,8 @@ class SimParams(ctypes.Structure):
         ("bscale", ctypes.c_void_p),
         ("tscale", ctypes.c_void_p),
         ("carry", ctypes.c_double),
+        ("canary_base", ctypes.c_uint32),
+        ("reserved", ctypes.c_uint32),
     ]
 
 
@@ -57,7 +59,7 @@ class AurocCfg(ctypes.Structure):
         ("score_off", ctypes.c_uint64),
         ("pos_mask", ctypes.c_uint64),
         ("cfg_id", ctypes.c_uint32),
-        ("reserved", ctypes.c_uint32),
+        ("canary_base", ctypes.c_uint32),
     ]
 
 
@@ -67,7 +69,7 @@ _SIGS = {
     "cdt_version": ([], ctypes.c_int),
     "cdt_last_error": ([], ctypes.c_char_p),
     "cdt_outlier_gain": ([_u32, _u32, _f, _u64, _u32, _vp, _vp], ctypes.c_int),
-    "cdt_ref_synth": ([_u32, _u32, _u32, _u32, _u64, _u32, _vp, _vp, _vp], ctypes.c_int),
+    "cdt_ref_synth": ([_u32, _u32, _u32, _u32, _u64, _u32, _u32, _vp, _vp, _vp], ctypes.c_int),
     "cdt_reduce_workspace_bytes": ([_u32, _u32, _u32, _u32], _sz),
     "cdt_ref_stats": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
     "cdt_block_scales": ([_u64, _u32, _u32, _vp, _vp, _d, _d, _vp, _vp, _vp], ctypes.c_int),
@@ -166,12 +168,14 @@ def outlier_gain(H, n_out, big, seed, ref_set_id, out=None):
     return out
 
 
-def ref_synth(S, C, T, H, seed, ref_set_id, gain, out=None):
+def ref_synth(S, C, T, H, seed, ref_set_id, gain, out=None, canary_base=0):
+    """References [S][C][T][H] fp32 of canaries canary_base .. canary_base + C - 1."""
     torch = _torch()
     _need(gain, "gain", torch.float32, (H,))
     out = _empty((S, C, T, H), torch.float32, gain) if out is None else out
     _need(out, "ref", torch.float32, (S, C, T, H))
-    _check(lib().cdt_ref_synth(S, C, T, H, seed, ref_set_id, _ptr(gain), _ptr(out), _stream()))
+    _check(lib().cdt_ref_synth(S, C, T, H, seed, ref_set_id, canary_base, _ptr(gain), _ptr(out),
+                               _stream()))
     return out
 
 
@@ -218,11 +222,11 @@ def block_scales(sumsq, sumabs, T, H, eps, sigma_b, tscale=None, bscale=None):
 
 def sim_params(*, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE, benign_dist=DIST_GAUSS,
                sigma_b=1e-3, mal_mask=0, tamper=0, tamper_base=BASE_BENIGN, flip_p=0.0,
-               scale=1.0, bscale=None, tscale=None, redraw=False, carry=0.0):
+               scale=1.0, bscale=None, tscale=None, redraw=False, carry=0.0, canary_base=0):
     return SimParams(seed, cfg_id, benign_mode, benign_dist, tamper, tamper_base, int(redraw),
                      mal_mask, sigma_b, flip_p, scale,
                      None if bscale is None else bscale.data_ptr(),
-                     None if tscale is None else tscale.data_ptr(), carry)
+                     None if tscale is None else tscale.data_ptr(), carry, canary_base, 0)
 
 
 def canary_sim(ref, out=None, *, bscale=None, tscale=None, **kw):
@@ -318,18 +322,20 @@ def cosine_score_f16ref(h, r, out=None, sums=None, ws=None):
 
 
 def auroc_cfg_array(cfgs):
-    """cfgs: iterable of (S, C, score_off, pos_mask, cfg_id) -> ctypes array."""
+    """cfgs: iterable of (S, C, score_off, pos_mask, cfg_id[, canary_base])
+    -> ctypes array."""
     cfgs = list(cfgs)
     arr = (AurocCfg * max(1, len(cfgs)))()
-    for i, (S, C, off, mask, cid) in enumerate(cfgs):
-        arr[i] = AurocCfg(S, C, off, mask, cid, 0)
+    for i, cfg in enumerate(cfgs):
+        S, C, off, mask, cid = cfg[:5]
+        arr[i] = AurocCfg(S, C, off, mask, cid, cfg[5] if len(cfg) > 5 else 0)
     return arr, len(cfgs)
 
 
 def auroc(cfgs, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_POOLED, counts=None, pooled=None,
           baseline=None, ws=None):
     """Batched AUROC counts.  cfgs: iterable of (S, C, score_off, pos_mask,
-    cfg_id); scores: flat (or any contiguous) fp32 device tensor.
+    cfg_id[, canary_base]); scores: flat (or any contiguous) fp32 device tensor.
     Returns (counts [n][6], pooled [n][3] or None, baseline [n][3] or None),
     uint64 counts held in int64 tensors."""
     torch = _torch()

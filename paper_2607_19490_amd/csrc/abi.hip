@@ -54,11 +54,17 @@ bool empty(uint32_t S, uint32_t C, uint32_t T, uint32_t H) {
     return static_cast<uint64_t>(S) * C * T * H == 0;
 }
 
+// Global canary indices canary_base .. canary_base + C - 1 fit the 32-bit
+// counter word.
+bool canaries_fit(uint32_t canary_base, uint64_t C) {
+    return static_cast<uint64_t>(canary_base) + C <= (1ull << 32);
+}
+
 }  // namespace
 
 extern "C" {
 
-int cdt_version(void) { return 3; }
+int cdt_version(void) { return 4; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -76,16 +82,19 @@ int cdt_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed, uint3
 }
 
 int cdt_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
-                  uint32_t ref_set_id, const float* gain, float* ref, void* stream) {
+                  uint32_t ref_set_id, uint32_t canary_base, const float* gain, float* ref,
+                  void* stream) {
     int rc = check_shape("cdt_ref_synth", S, C, T, H);
     if (rc) return rc;
     if (ref_set_id >= kMaxId) return fail(CDT_ELIMIT, "cdt_ref_synth: ref_set_id >= 2^24");
+    if (!canaries_fit(canary_base, C))
+        return fail(CDT_ELIMIT, "cdt_ref_synth: canary_base + C above 2^32");
     if (empty(S, C, T, H)) return ok();
     if (!gain || !ref) return fail(CDT_EINVAL, "cdt_ref_synth: NULL array");
     if (!aligned16(gain) || !aligned16(ref))
         return fail(CDT_EALIGN, "cdt_ref_synth: arrays must be 16-byte aligned");
-    return device_status(cdt::launch_ref_synth(S, C, T, H, seed, ref_set_id, gain, ref,
-                                               static_cast<hipStream_t>(stream)),
+    return device_status(cdt::launch_ref_synth(S, C, T, H, seed, ref_set_id, canary_base, gain,
+                                               ref, static_cast<hipStream_t>(stream)),
                          "cdt_ref_synth");
 }
 
@@ -153,6 +162,9 @@ int check_sim(const char* fn, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
     if (!isfinite(p->scale)) return fail(CDT_EINVAL, "%s: scale must be finite", fn);
     if (!(p->carry >= 0.0 && p->carry <= 1.0))
         return fail(CDT_EINVAL, "%s: carry must lie in [0, 1]", fn);
+    if (p->reserved != 0) return fail(CDT_EINVAL, "%s: reserved must be 0", fn);
+    if (!canaries_fit(p->canary_base, C))
+        return fail(CDT_ELIMIT, "%s: canary_base + C above 2^32", fn);
     const uint64_t mal = p->mal_mask & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
     if (!empty(S, C, T, H)) {
         if (p->benign_mode == CDT_NOISE_BLOCK && !p->bscale)
@@ -179,6 +191,7 @@ int check_sim(const char* fn, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
     L->flip_thr = L->flip_all ? 0u : static_cast<uint32_t>(floor(p->flip_p * 4294967296.0));
     L->scale = static_cast<float>(p->scale);
     L->carry = static_cast<float>(p->carry);
+    L->canary_base = p->canary_base;
     L->bscale = p->bscale;
     L->tscale = p->tscale;
     return CDT_OK;
@@ -330,7 +343,8 @@ int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, ui
         const cdt_auroc_cfg& c = cfgs[g];
         if (c.S > 64) return fail(CDT_ELIMIT, "cdt_auroc: cfg %u has S=%u above 64", g, c.S);
         if (c.cfg_id >= kMaxId) return fail(CDT_ELIMIT, "cdt_auroc: cfg %u cfg_id >= 2^24", g);
-        if (c.reserved != 0) return fail(CDT_EINVAL, "cdt_auroc: cfg %u reserved must be 0", g);
+        if (!canaries_fit(c.canary_base, c.C))
+            return fail(CDT_ELIMIT, "cdt_auroc: cfg %u canary_base + C above 2^32", g);
         const uint64_t len = static_cast<uint64_t>(c.S) * c.C;
         if ((flags & CDT_AUROC_POOLED) && len > kMaxPooled)
             return fail(CDT_ELIMIT, "cdt_auroc: cfg %u has C*S=%llu above %u for pooled ranking",

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "cdt_reduce.hpp"
+
 namespace cdt {
 
 // Elementwise kernels: a thread owns groups of 8 consecutive elements (one
@@ -16,19 +18,6 @@ namespace cdt {
 constexpr int kGenThreads = 1024;
 constexpr int kGenItems = 2;
 constexpr uint32_t kGenChunkGroups = kGenThreads * kGenItems;
-
-// Block reductions: a workgroup reduces kReduceChunkElems elements of one
-// block to a pair of fp64 partial sums; a second kernel adds the partials of
-// a block in chunk order.  1024 threads with two 8-element groups in flight
-// each measured fastest on the 16 x 256 x 256 x 8192 stream (85% of the HBM
-// peak against 84% for 256 x 4 and 80% for 1024 x 4).
-constexpr int kReduceThreads = 1024;
-constexpr int kReduceUnroll = 2;
-constexpr uint64_t kReduceChunkElems = 32768;
-
-inline uint64_t reduce_chunks_per_block(uint64_t n) {
-    return (n + kReduceChunkElems - 1) / kReduceChunkElems;
-}
 
 struct SimLaunch {
     uint32_t S, C, T, H;
@@ -41,6 +30,7 @@ struct SimLaunch {
     uint32_t flip_all;   // p >= 1
     float scale;         // fp32(scale)
     float carry;         // fp32(carry): propagation gain (0: independent stages)
+    uint32_t canary_base;  // global index of canary 0 (RNG counters)
     const float* bscale;
     const float* tscale;
 };
@@ -50,14 +40,15 @@ struct AurocCfgDev {
     uint64_t score_off;
     uint64_t pos_mask;
     uint32_t cfg_id;
-    uint32_t reserved;
+    uint32_t canary_base;
 };
 static_assert(sizeof(AurocCfgDev) == 32, "cfg layout must match cdt_auroc_cfg");
 
 hipError_t launch_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t seed,
                                uint32_t ref_set_id, float* gain, hipStream_t st);
 hipError_t launch_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
-                            uint32_t ref_set_id, const float* gain, float* ref, hipStream_t st);
+                            uint32_t ref_set_id, uint32_t canary_base, const float* gain,
+                            float* ref, hipStream_t st);
 hipError_t launch_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const double* sumsq,
                                const double* sumabs, double eps, double sigma_b, float* tscale,
                                float* bscale, hipStream_t st);
@@ -65,17 +56,16 @@ hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, 
 
 hipError_t launch_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,
                             double* sumsq, double* sumabs, void* ws, hipStream_t st);
-// Reduction variants of Eq. 4: the relative-L2 mismatch (the detector) and
-// the cosine mismatch (the metric ablation), each against an fp32 reference
-// or an fp16 reference (a second live pass).
-enum class DriftMetric { kL2, kL2HalfRef, kCosine, kCosineHalfRef };
-
-// Partial sums per chunk: (D, R) for the L2 metrics, (D, A, P) for cosine.
-constexpr int kReduceMaxSums = 3;
-
+// Eq. 4 (or its cosine variant) per block: partial sums per chunk into ws,
+// then the combine.
 hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
                         const uint16_t* h, const void* ref, float* score, double* sums, void* ws,
                         hipStream_t st);
+
+// The combine step alone, over partial sums laid out as drift_score's.
+hipError_t launch_drift_combine(DriftMetric metric, const double* partial, uint64_t cpb,
+                                uint64_t nblocks, uint32_t S, uint32_t C, float* score,
+                                double* sums, hipStream_t st);
 
 // Live pass and Eq. 4 in one kernel (h may be NULL: not stored).
 hipError_t launch_sim_score(const SimLaunch& p, const float* ref, uint16_t* h, float* score,

@@ -28,6 +28,7 @@ __device__ __forceinline__ void normals8(Key key, uint32_t e0, uint32_t c, uint3
 // Launch-uniform parameters of the live pass.
 struct SimArgs {
     uint32_t C, n8;
+    uint32_t canary_base;  // global index of canary 0 (RNG counters)
     uint64_t chunks_per_block, total_chunks;
     Key key;
     uint32_t tag_benign, tag_t12, tag_t3, tag_add, tag_flip;
@@ -44,6 +45,7 @@ inline SimArgs make_sim_args(const SimLaunch& p, uint64_t chunks_per_block,
                              uint64_t total_chunks) {
     SimArgs A;
     A.C = p.C;
+    A.canary_base = p.canary_base;
     A.n8 = static_cast<uint32_t>(static_cast<uint64_t>(p.T) * p.H / 8);
     A.chunks_per_block = chunks_per_block;
     A.total_chunks = total_chunks;
@@ -68,7 +70,8 @@ inline SimArgs make_sim_args(const SimLaunch& p, uint64_t chunks_per_block,
     return A;
 }
 
-// Block-uniform state: which (shard, canary) and its scales.
+// Block-uniform state: which (shard, canary) and its scales; c is the
+// global canary index that keys the noise.
 struct SimBlock {
     uint32_t s, c;
     bool mal;
@@ -80,7 +83,7 @@ template <bool kBlock>
 __device__ __forceinline__ SimBlock sim_block(const SimArgs& A, uint64_t block) {
     SimBlock B;
     B.s = static_cast<uint32_t>(block / A.C);
-    B.c = static_cast<uint32_t>(block - static_cast<uint64_t>(B.s) * A.C);
+    B.c = A.canary_base + static_cast<uint32_t>(block - static_cast<uint64_t>(B.s) * A.C);
     B.mal = (A.mal_mask >> B.s) & 1u;
     B.bsc = kBlock ? A.bscale[block] : 0.0f;
     B.tsc = (B.mal && (A.tamper & 1u)) ? A.tscale[block] : 0.0f;

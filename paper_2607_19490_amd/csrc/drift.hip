@@ -1,0 +1,195 @@
+// Eq. 4, the relative-L2 mismatch m = sqrt(sum (h - a)^2 / sum a^2) of
+// every (shard, canary) block, and its ablations (an fp16 reference; the
+// cosine mismatch of Section 4.4).
+//
+// drift_score is bound by HBM bandwidth: 2 B of fp16 h plus 4 B of fp32 a
+// per element, each read exactly once.  Layout of the work:
+//   * a block of n = T*H elements is cut into chunks of kReduceChunkElems;
+//     one kReduceThreads-thread workgroup reduces one chunk;
+//   * each thread streams groups of 8 elements (one 16-byte h load, two
+//     16-byte a loads), kReduceUnroll groups in flight before any use; the
+//     loads are nontemporal (read once, no reuse);
+//   * chunks are handed out so that each XCD streams one contiguous range;
+//   * the squares are accumulated in fp64 from the exactly widened operands
+//     (h - a is exact in fp64), so the partial sums carry no cancellation;
+//   * wave butterfly sums, then an LDS pass over the waves, give one
+//     (D, R) pair per chunk in a fixed order (no atomics);
+//   * a combine kernel adds a block's chunk partials in chunk order and
+//     forms m = sqrt(D / R).
+#include <math.h>
+
+#include "cdt_device.hpp"
+#include "cdt_launch.hpp"
+#include "cdt_reduce.hpp"
+
+#pragma clang fp contract(off)
+
+namespace cdt {
+namespace {
+
+template <DriftMetric kM>
+__global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
+    const uint16_t* __restrict__ h, const void* __restrict__ ref, uint32_t n8,
+    uint64_t chunks_per_block, uint64_t total_chunks, double* __restrict__ partial) {
+    using Tr = DriftTraits<kM>;
+    const uint64_t n = static_cast<uint64_t>(n8) * 8;
+    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
+        const uint64_t chunk = xcd_contiguous(it, total_chunks);
+        const uint64_t b = chunk / chunks_per_block;
+        const uint32_t g0 = static_cast<uint32_t>(chunk - b * chunks_per_block) * kChunkGroups;
+        const uint32_t g_end = min(g0 + kChunkGroups, n8);
+        const u32x4* hb = reinterpret_cast<const u32x4*>(h + b * n);
+        const f32x4* ab = nullptr;  // fp32 reference block
+        const u32x4* rb = nullptr;  // fp16 reference block
+        if constexpr (Tr::kHalfRef)
+            rb = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(ref) + b * n);
+        else
+            ab = reinterpret_cast<const f32x4*>(static_cast<const float*>(ref) + b * n);
+        double acc[Tr::kSums];
+#pragma unroll
+        for (int k = 0; k < Tr::kSums; ++k) acc[k] = 0.0;
+        for (uint32_t base = g0; base < g_end; base += kReduceThreads * kReduceUnroll) {
+            u32x4 hv[kReduceUnroll], rv[kReduceUnroll];
+            f32x4 a0[kReduceUnroll], a1[kReduceUnroll];
+#pragma unroll
+            for (int u = 0; u < kReduceUnroll; ++u) {
+                const uint32_t g = base + u * kReduceThreads + threadIdx.x;
+                hv[u] = u32x4{0u, 0u, 0u, 0u};
+                rv[u] = hv[u];
+                a0[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+                a1[u] = a0[u];
+                if (g < g_end) {
+                    hv[u] = __builtin_nontemporal_load(hb + g);
+                    if constexpr (Tr::kHalfRef) {
+                        rv[u] = __builtin_nontemporal_load(rb + g);
+                    } else {
+                        a0[u] = __builtin_nontemporal_load(ab + 2 * g);
+                        a1[u] = __builtin_nontemporal_load(ab + 2 * g + 1);
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kReduceUnroll; ++u) accumulate8<kM>(hv[u], rv[u], a0[u], a1[u], acc);
+        }
+        block_sum<Tr::kSums>(acc);
+        if (threadIdx.x == 0) {
+#pragma unroll
+            for (int k = 0; k < Tr::kSums; ++k) partial[chunk * Tr::kSums + k] = acc[k];
+        }
+    }
+}
+
+// Eq. 4 from the block sums: m = sqrt(D / R); R = 0 gives 0 (D = 0) or +inf.
+__device__ __forceinline__ double relative_l2(double D, double R) {
+    if (R == 0.0) return (D == 0.0) ? 0.0 : static_cast<double>(INFINITY);
+    return sqrt(D / R);
+}
+
+// 1 - cos(h, a) from D = |h-a|^2, A = |a|^2, P = a.(h-a): with |h|^2 = A + 2P + D
+// and h.a = A + P, 1 - cos = (A D - P^2) / (sqrt(A |h|^2) (sqrt(A |h|^2) + A + P)),
+// which keeps full relative accuracy as the angle goes to 0.
+__device__ __forceinline__ double cosine_mismatch(double D, double A, double P) {
+    const double hn = A + 2.0 * P + D;
+    if (A == 0.0 || hn <= 0.0) return (A == 0.0 && hn <= 0.0) ? 0.0 : 1.0;
+    const double g = sqrt(A * hn);
+    const double dot = A + P;
+    if (dot > 0.0) return (A * D - P * P) / (g * (g + dot));
+    return 1.0 - dot / g;
+}
+
+template <DriftMetric kM>
+__global__ void drift_combine_kernel(const double* __restrict__ partial, uint64_t chunks_per_block,
+                                     uint64_t nblocks, uint32_t S, uint32_t C,
+                                     float* __restrict__ score, double* __restrict__ sums) {
+    using Tr = DriftTraits<kM>;
+    const uint64_t b = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (b >= nblocks) return;
+    double acc[Tr::kSums];
+#pragma unroll
+    for (int k = 0; k < Tr::kSums; ++k) acc[k] = 0.0;
+    for (uint64_t i = 0; i < chunks_per_block; ++i) {
+#pragma unroll
+        for (int k = 0; k < Tr::kSums; ++k) acc[k] += partial[(b * chunks_per_block + i) * Tr::kSums + k];
+    }
+    double m;
+    if constexpr (Tr::kCos)
+        m = cosine_mismatch(acc[0], acc[1], acc[2]);
+    else
+        m = relative_l2(acc[0], acc[1]);
+    const uint64_t s = b / C, c = b - s * C;
+    const uint64_t o = c * S + s;
+    score[o] = static_cast<float>(m);
+    if (sums) {
+#pragma unroll
+        for (int k = 0; k < Tr::kSums; ++k) sums[Tr::kSums * o + k] = acc[k];
+    }
+}
+
+}  // namespace
+
+template <DriftMetric kM>
+hipError_t launch_combine_t(const double* partial, uint64_t cpb, uint64_t nblocks, uint32_t S,
+                            uint32_t C, float* score, double* sums, hipStream_t st) {
+    const uint64_t grid = (nblocks + 255) / 256;
+    hipLaunchKernelGGL(drift_combine_kernel<kM>, dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
+                       st, partial, cpb, nblocks, S, C, score, sums);
+    return hipGetLastError();
+}
+
+template <DriftMetric kM>
+hipError_t launch_drift_t(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                          const void* ref, float* score, double* sums, void* ws, hipStream_t st) {
+    const uint64_t n = static_cast<uint64_t>(T) * H;
+    const uint64_t nblocks = static_cast<uint64_t>(S) * C;
+    if (nblocks == 0) return hipSuccess;
+    const uint64_t cpb = reduce_chunks_per_block(n);
+    const uint64_t total = cpb * nblocks;
+    double* partial = static_cast<double*>(ws);
+    if (total > 0) {
+        hipLaunchKernelGGL(drift_partial_kernel<kM>, dim3(reduce_grid(total)),
+                           dim3(kReduceThreads), 0, st, h, ref, static_cast<uint32_t>(n / 8), cpb,
+                           total, partial);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return launch_combine_t<kM>(partial, cpb, nblocks, S, C, score, sums, st);
+}
+
+hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                        const uint16_t* h, const void* ref, float* score, double* sums, void* ws,
+                        hipStream_t st) {
+    switch (metric) {
+        case DriftMetric::kL2:
+            return launch_drift_t<DriftMetric::kL2>(S, C, T, H, h, ref, score, sums, ws, st);
+        case DriftMetric::kL2HalfRef:
+            return launch_drift_t<DriftMetric::kL2HalfRef>(S, C, T, H, h, ref, score, sums, ws,
+                                                           st);
+        case DriftMetric::kCosine:
+            return launch_drift_t<DriftMetric::kCosine>(S, C, T, H, h, ref, score, sums, ws, st);
+        case DriftMetric::kCosineHalfRef:
+            return launch_drift_t<DriftMetric::kCosineHalfRef>(S, C, T, H, h, ref, score, sums,
+                                                               ws, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_drift_combine(DriftMetric metric, const double* partial, uint64_t cpb,
+                                uint64_t nblocks, uint32_t S, uint32_t C, float* score,
+                                double* sums, hipStream_t st) {
+    switch (metric) {
+        case DriftMetric::kL2:
+            return launch_combine_t<DriftMetric::kL2>(partial, cpb, nblocks, S, C, score, sums, st);
+        case DriftMetric::kL2HalfRef:
+            return launch_combine_t<DriftMetric::kL2HalfRef>(partial, cpb, nblocks, S, C, score,
+                                                             sums, st);
+        case DriftMetric::kCosine:
+            return launch_combine_t<DriftMetric::kCosine>(partial, cpb, nblocks, S, C, score, sums,
+                                                          st);
+        case DriftMetric::kCosineHalfRef:
+            return launch_combine_t<DriftMetric::kCosineHalfRef>(partial, cpb, nblocks, S, C,
+                                                                 score, sums, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace cdt

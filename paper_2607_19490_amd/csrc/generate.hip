@@ -74,8 +74,9 @@ __device__ __forceinline__ ChunkPos chunk_pos(uint64_t chunk, uint64_t chunks_pe
 // Synthetic references: ref = fp32(z_REF * gain[j]).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kGenThreads) void ref_synth_kernel(
-    uint32_t C, uint32_t H, uint32_t n8, uint64_t chunks_per_block, uint64_t total_chunks,
-    Key key, uint32_t tag, const float* __restrict__ gain, float* __restrict__ ref) {
+    uint32_t C, uint32_t canary_base, uint32_t H, uint32_t n8, uint64_t chunks_per_block,
+    uint64_t total_chunks, Key key, uint32_t tag, const float* __restrict__ gain,
+    float* __restrict__ ref) {
     const uint64_t n = static_cast<uint64_t>(n8) * 8;
     for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
         const ChunkPos p = chunk_pos(xcd_contiguous(it, total_chunks), chunks_per_block, C);
@@ -89,7 +90,7 @@ __global__ __launch_bounds__(kGenThreads) void ref_synth_kernel(
             const float4 g_lo = *reinterpret_cast<const float4*>(gain + j0);
             const float4 g_hi = *reinterpret_cast<const float4*>(gain + j0 + 4);
             float z[8];
-            normals8(key, e0, p.c, p.s, tag, z);
+            normals8(key, e0, canary_base + p.c, p.s, tag, z);
             out[2 * g] = make_float4(z[0] * g_lo.x, z[1] * g_lo.y, z[2] * g_lo.z, z[3] * g_lo.w);
             out[2 * g + 1] =
                 make_float4(z[4] * g_hi.x, z[5] * g_hi.y, z[6] * g_hi.z, z[7] * g_hi.w);
@@ -209,15 +210,16 @@ hipError_t launch_outlier_gain(uint32_t H, uint32_t n_out, float big, uint64_t s
 }
 
 hipError_t launch_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
-                            uint32_t ref_set_id, const float* gain, float* ref, hipStream_t st) {
+                            uint32_t ref_set_id, uint32_t canary_base, const float* gain,
+                            float* ref, hipStream_t st) {
     const uint64_t n = static_cast<uint64_t>(T) * H;
     const uint64_t nblocks = static_cast<uint64_t>(S) * C;
     if (n == 0 || nblocks == 0) return hipSuccess;
     const uint32_t n8 = static_cast<uint32_t>(n / 8);
     const uint64_t cpb = (n8 + kGenChunkGroups - 1) / kGenChunkGroups;
     const uint64_t total = cpb * nblocks;
-    hipLaunchKernelGGL(ref_synth_kernel, dim3(gen_grid(total)), dim3(kGenThreads), 0, st, C, H,
-                       n8, cpb, total,
+    hipLaunchKernelGGL(ref_synth_kernel, dim3(gen_grid(total)), dim3(kGenThreads), 0, st, C,
+                       canary_base, H, n8, cpb, total,
                        Key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)},
                        stream_tag(kStreamRef, ref_set_id), gain, ref);
     return hipGetLastError();

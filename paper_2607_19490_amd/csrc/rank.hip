@@ -68,7 +68,8 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
             }
         }
         if (random) {
-            const uint32_t kr = lane_in ? order_key(random_score(key, t, lane, tag_random)) : 0u;
+            const uint32_t kr =
+                lane_in ? order_key(random_score(key, cfg.canary_base + t, lane, tag_random)) : 0u;
             for (uint32_t j = 0; j < cfg.S; ++j) {
                 const uint32_t kj = __shfl(kr, j, kWave);
                 if (lane_pos && ((neg >> j) & 1u)) {
@@ -78,7 +79,7 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
             }
         }
         if (control && n_benign > 0) {
-            const uint32_t u = draw(key, t, 0, 0, tag).x;
+            const uint32_t u = draw(key, cfg.canary_base + t, 0, 0, tag).x;
             const uint32_t js = nth_set_bit(neg, u % n_benign);
             const uint32_t kjs = __shfl(k, js, kWave);
             const bool counted =

@@ -1,149 +1,19 @@
-// Block reductions: the relative-L2 mismatch of Eq. 4 and the reference
-// block statistics (sum a^2, sum |a|; mu_i of Eq. 2).
-//
-// drift_score is bound by HBM bandwidth: 2 B of fp16 h plus 4 B of fp32 a
-// per element, each read exactly once.  Layout of the work:
-//   * a block (shard, canary) of n = T*H elements is cut into chunks of
-//     kReduceChunkElems; one 256-thread workgroup reduces one chunk;
-//   * each thread streams groups of 8 elements (one 16-byte h load, two
-//     16-byte a loads), kReduceUnroll groups in flight before any use; the
-//     loads are nontemporal (read once, no reuse);
-//   * chunks are handed out so that each XCD streams one contiguous range;
-//   * the squares are accumulated in fp64 from the exactly widened operands
-//     (h - a is exact in fp64), so the partial sums carry no cancellation;
-//   * wave butterfly sums, then an LDS pass over the waves, give one
-//     (D, R) pair per chunk in a fixed order (no atomics);
-//   * a combine kernel adds a block's chunk partials in chunk order and
-//     forms m = sqrt(D / R).
+// Block reductions over generated data and the reference statistics: the
+// live pass fused with Eq. 4 (activations scored in registers), the norms of
+// the exact-norm Gaussian tamper of Section 3.2, and the per-block sums
+// sum a^2 and sum |a| (mu_i of Eq. 2).  Chunking, workgroup sums and the
+// per-element accumulation are those of drift_score.
 #include <math.h>
 
 #include "cdt_device.hpp"
 #include "cdt_launch.hpp"
+#include "cdt_reduce.hpp"
 #include "cdt_sim.hpp"
 
 #pragma clang fp contract(off)
 
 namespace cdt {
 namespace {
-
-constexpr uint32_t kChunkGroups = static_cast<uint32_t>(kReduceChunkElems / 8);
-constexpr int kWavesPerGroup = kReduceThreads / kWave;
-
-// Sum kN per-thread values over the workgroup; thread 0 gets the result.
-template <int kN>
-__device__ __forceinline__ void block_sum(double (&v)[kN]) {
-    __shared__ double lds[kN][kWavesPerGroup];
-#pragma unroll
-    for (int k = 0; k < kN; ++k) v[k] = wave_sum(v[k]);
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    if (lane == 0) {
-#pragma unroll
-        for (int k = 0; k < kN; ++k) lds[k][wave] = v[k];
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-#pragma unroll
-        for (int k = 0; k < kN; ++k) {
-            double t = 0.0;
-            for (int w = 0; w < kWavesPerGroup; ++w) t += lds[k][w];
-            v[k] = t;
-        }
-    }
-    __syncthreads();
-}
-
-// Per-metric element step.  h and the reference are widened exactly to
-// fp64, so d = h - a is exact and the sums carry no cancellation.
-template <DriftMetric kM>
-struct DriftTraits {
-    static constexpr bool kHalfRef =
-        kM == DriftMetric::kL2HalfRef || kM == DriftMetric::kCosineHalfRef;
-    static constexpr bool kCos = kM == DriftMetric::kCosine || kM == DriftMetric::kCosineHalfRef;
-    static constexpr int kSums = kCos ? 3 : 2;
-
-    __device__ static __forceinline__ void add(double hv, double av, double (&acc)[kSums]) {
-        const double d = hv - av;
-        acc[0] = fma(d, d, acc[0]);      // D = sum d^2
-        acc[1] = fma(av, av, acc[1]);    // R = A = sum a^2
-        if constexpr (kSums == 3) acc[2] = fma(av, d, acc[2]);  // P = sum a d
-    }
-};
-
-template <DriftMetric kM>
-__device__ __forceinline__ void accumulate8(const u32x4& hv, const u32x4& r_half,
-                                            const f32x4& a0, const f32x4& a1,
-                                            double (&acc)[DriftTraits<kM>::kSums]) {
-    const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
-    const uint32_t rw[4] = {r_half.x, r_half.y, r_half.z, r_half.w};
-    const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const double h_lo = static_cast<double>(half_bits_to_float(hw[k] & 0xFFFFu));
-        const double h_hi = static_cast<double>(half_bits_to_float(hw[k] >> 16));
-        double a_lo, a_hi;
-        if constexpr (DriftTraits<kM>::kHalfRef) {
-            a_lo = static_cast<double>(half_bits_to_float(rw[k] & 0xFFFFu));
-            a_hi = static_cast<double>(half_bits_to_float(rw[k] >> 16));
-        } else {
-            a_lo = static_cast<double>(av[2 * k]);
-            a_hi = static_cast<double>(av[2 * k + 1]);
-        }
-        DriftTraits<kM>::add(h_lo, a_lo, acc);
-        DriftTraits<kM>::add(h_hi, a_hi, acc);
-    }
-}
-
-template <DriftMetric kM>
-__global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
-    const uint16_t* __restrict__ h, const void* __restrict__ ref, uint32_t n8,
-    uint64_t chunks_per_block, uint64_t total_chunks, double* __restrict__ partial) {
-    using Tr = DriftTraits<kM>;
-    const uint64_t n = static_cast<uint64_t>(n8) * 8;
-    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
-        const uint64_t chunk = xcd_contiguous(it, total_chunks);
-        const uint64_t b = chunk / chunks_per_block;
-        const uint32_t g0 = static_cast<uint32_t>(chunk - b * chunks_per_block) * kChunkGroups;
-        const uint32_t g_end = min(g0 + kChunkGroups, n8);
-        const u32x4* hb = reinterpret_cast<const u32x4*>(h + b * n);
-        const f32x4* ab = nullptr;  // fp32 reference block
-        const u32x4* rb = nullptr;  // fp16 reference block
-        if constexpr (Tr::kHalfRef)
-            rb = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(ref) + b * n);
-        else
-            ab = reinterpret_cast<const f32x4*>(static_cast<const float*>(ref) + b * n);
-        double acc[Tr::kSums];
-#pragma unroll
-        for (int k = 0; k < Tr::kSums; ++k) acc[k] = 0.0;
-        for (uint32_t base = g0; base < g_end; base += kReduceThreads * kReduceUnroll) {
-            u32x4 hv[kReduceUnroll], rv[kReduceUnroll];
-            f32x4 a0[kReduceUnroll], a1[kReduceUnroll];
-#pragma unroll
-            for (int u = 0; u < kReduceUnroll; ++u) {
-                const uint32_t g = base + u * kReduceThreads + threadIdx.x;
-                hv[u] = u32x4{0u, 0u, 0u, 0u};
-                rv[u] = hv[u];
-                a0[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-                a1[u] = a0[u];
-                if (g < g_end) {
-                    hv[u] = __builtin_nontemporal_load(hb + g);
-                    if constexpr (Tr::kHalfRef) {
-                        rv[u] = __builtin_nontemporal_load(rb + g);
-                    } else {
-                        a0[u] = __builtin_nontemporal_load(ab + 2 * g);
-                        a1[u] = __builtin_nontemporal_load(ab + 2 * g + 1);
-                    }
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kReduceUnroll; ++u) accumulate8<kM>(hv[u], rv[u], a0[u], a1[u], acc);
-        }
-        block_sum<Tr::kSums>(acc);
-        if (threadIdx.x == 0) {
-#pragma unroll
-            for (int k = 0; k < Tr::kSums; ++k) partial[chunk * Tr::kSums + k] = acc[k];
-        }
-    }
-}
 
 // Fused live pass and Eq. 4: each group of 8 references is read once, turned
 // into fp16 live activations in registers (exactly as canary_sim does), and
@@ -257,52 +127,6 @@ __global__ void tamper_scale_combine_kernel(const double* __restrict__ partial,
     }
 }
 
-// Eq. 4 from the block sums: m = sqrt(D / R); R = 0 gives 0 (D = 0) or +inf.
-__device__ __forceinline__ double relative_l2(double D, double R) {
-    if (R == 0.0) return (D == 0.0) ? 0.0 : static_cast<double>(INFINITY);
-    return sqrt(D / R);
-}
-
-// 1 - cos(h, a) from D = |h-a|^2, A = |a|^2, P = a.(h-a): with |h|^2 = A + 2P + D
-// and h.a = A + P, 1 - cos = (A D - P^2) / (sqrt(A |h|^2) (sqrt(A |h|^2) + A + P)),
-// which keeps full relative accuracy as the angle goes to 0.
-__device__ __forceinline__ double cosine_mismatch(double D, double A, double P) {
-    const double hn = A + 2.0 * P + D;
-    if (A == 0.0 || hn <= 0.0) return (A == 0.0 && hn <= 0.0) ? 0.0 : 1.0;
-    const double g = sqrt(A * hn);
-    const double dot = A + P;
-    if (dot > 0.0) return (A * D - P * P) / (g * (g + dot));
-    return 1.0 - dot / g;
-}
-
-template <DriftMetric kM>
-__global__ void drift_combine_kernel(const double* __restrict__ partial, uint64_t chunks_per_block,
-                                     uint64_t nblocks, uint32_t S, uint32_t C,
-                                     float* __restrict__ score, double* __restrict__ sums) {
-    using Tr = DriftTraits<kM>;
-    const uint64_t b = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (b >= nblocks) return;
-    double acc[Tr::kSums];
-#pragma unroll
-    for (int k = 0; k < Tr::kSums; ++k) acc[k] = 0.0;
-    for (uint64_t i = 0; i < chunks_per_block; ++i) {
-#pragma unroll
-        for (int k = 0; k < Tr::kSums; ++k) acc[k] += partial[(b * chunks_per_block + i) * Tr::kSums + k];
-    }
-    double m;
-    if constexpr (Tr::kCos)
-        m = cosine_mismatch(acc[0], acc[1], acc[2]);
-    else
-        m = relative_l2(acc[0], acc[1]);
-    const uint64_t s = b / C, c = b - s * C;
-    const uint64_t o = c * S + s;
-    score[o] = static_cast<float>(m);
-    if (sums) {
-#pragma unroll
-        for (int k = 0; k < Tr::kSums; ++k) sums[Tr::kSums * o + k] = acc[k];
-    }
-}
-
 __global__ __launch_bounds__(kReduceThreads) void ref_stats_partial_kernel(
     const float* __restrict__ ref, uint32_t n8, uint64_t chunks_per_block, uint64_t total_chunks,
     double2* __restrict__ partial) {
@@ -345,54 +169,7 @@ __global__ void ref_stats_combine_kernel(const double2* __restrict__ partial,
     sumabs[b] = M;
 }
 
-// One workgroup per chunk up to 2^20 chunks, then a grid-stride walk whose
-// stride (2^20) is a multiple of the XCD count, as xcd_contiguous needs.
-inline uint32_t reduce_grid(uint64_t total_chunks) {
-    const uint64_t cap = 1ull << 20;
-    return static_cast<uint32_t>(total_chunks < cap ? total_chunks : cap);
-}
-
 }  // namespace
-
-template <DriftMetric kM>
-hipError_t launch_drift_t(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
-                          const void* ref, float* score, double* sums, void* ws, hipStream_t st) {
-    const uint64_t n = static_cast<uint64_t>(T) * H;
-    const uint64_t nblocks = static_cast<uint64_t>(S) * C;
-    if (nblocks == 0) return hipSuccess;
-    const uint64_t cpb = reduce_chunks_per_block(n);
-    const uint64_t total = cpb * nblocks;
-    double* partial = static_cast<double*>(ws);
-    if (total > 0) {
-        hipLaunchKernelGGL(drift_partial_kernel<kM>, dim3(reduce_grid(total)),
-                           dim3(kReduceThreads), 0, st, h, ref, static_cast<uint32_t>(n / 8), cpb,
-                           total, partial);
-        const hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    const uint64_t grid = (nblocks + 255) / 256;
-    hipLaunchKernelGGL(drift_combine_kernel<kM>, dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
-                       st, partial, cpb, nblocks, S, C, score, sums);
-    return hipGetLastError();
-}
-
-hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
-                        const uint16_t* h, const void* ref, float* score, double* sums, void* ws,
-                        hipStream_t st) {
-    switch (metric) {
-        case DriftMetric::kL2:
-            return launch_drift_t<DriftMetric::kL2>(S, C, T, H, h, ref, score, sums, ws, st);
-        case DriftMetric::kL2HalfRef:
-            return launch_drift_t<DriftMetric::kL2HalfRef>(S, C, T, H, h, ref, score, sums, ws,
-                                                           st);
-        case DriftMetric::kCosine:
-            return launch_drift_t<DriftMetric::kCosine>(S, C, T, H, h, ref, score, sums, ws, st);
-        case DriftMetric::kCosineHalfRef:
-            return launch_drift_t<DriftMetric::kCosineHalfRef>(S, C, T, H, h, ref, score, sums,
-                                                               ws, st);
-    }
-    return hipErrorInvalidValue;
-}
 
 template <bool kT3, bool kBlock>
 void launch_sim_score_t(const SimArgs& A, dim3 grid, const float* ref, uint16_t* h,
@@ -427,10 +204,8 @@ hipError_t launch_sim_score(const SimLaunch& p, const float* ref, uint16_t* h, f
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const uint64_t grid = (nblocks + 255) / 256;
-    hipLaunchKernelGGL(drift_combine_kernel<DriftMetric::kL2>, dim3(static_cast<uint32_t>(grid)),
-                       dim3(256), 0, st, partial, cpb, nblocks, p.S, p.C, score, num_den);
-    return hipGetLastError();
+    return launch_drift_combine(DriftMetric::kL2, partial, cpb, nblocks, p.S, p.C, score,
+                                num_den, st);
 }
 
 hipError_t launch_tamper_scale_exact(const SimLaunch& p, const float* ref, double eps,

@@ -38,7 +38,7 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 3
+    assert L.cdt_version() == 4
     assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
@@ -88,8 +88,14 @@ def test_shape_and_pointer_validation(cdt):
         assert fn(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
     # empty shapes are accepted without touching the device
     assert L.cdt_drift_score(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
-    assert L.cdt_ref_synth(2, 0, 3, 16, 0, 0, None, None, None) == cdt.OK
-    assert L.cdt_ref_synth(2, 2, 3, 16, 0, 1 << 24, 16, 16, None) == cdt.ELIMIT
+    assert L.cdt_ref_synth(2, 0, 3, 16, 0, 0, 0, None, None, None) == cdt.OK
+    assert L.cdt_ref_synth(2, 2, 3, 16, 0, 1 << 24, 0, 16, 16, None) == cdt.ELIMIT
+    # global canary indices must fit the 32-bit counter word
+    # (2 canaries from 2^32 - 2 pass that check and stop at the NULL arrays)
+    assert L.cdt_ref_synth(2, 2, 3, 16, 0, 0, (1 << 32) - 2, None, None, None) == cdt.EINVAL
+    assert "NULL" in _err(cdt)
+    assert L.cdt_ref_synth(2, 3, 3, 16, 0, 0, (1 << 32) - 2, 16, 16, None) == cdt.ELIMIT
+    assert "canary_base" in _err(cdt)
 
 
 def test_sim_param_validation(cdt):
@@ -126,6 +132,11 @@ def test_sim_param_validation(cdt):
                            None) == cdt.EALIGN
     assert L.cdt_sim_score(4, 2, 2, 16, ctypes.byref(p), 16, None, 16, None, 16, 1,
                            None) == cdt.EINVAL
+    assert call(canary_base=(1 << 32) - 1) == cdt.ELIMIT  # C = 2 canaries from 2^32 - 1
+    assert "canary_base" in _err(cdt)
+    p = cdt.sim_params(seed=0, cfg_id=0)
+    p.reserved = 1
+    assert L.cdt_canary_sim(4, 2, 2, 16, ctypes.byref(p), 16, 16, None) == cdt.EINVAL
     assert call(carry=1.5) == cdt.EINVAL
     assert call(carry=-0.1) == cdt.EINVAL
     p = cdt.sim_params(seed=0, cfg_id=0, carry=0.5)
@@ -158,6 +169,9 @@ def test_auroc_validation(cdt):
     assert L.cdt_auroc(n, arr, 16, 32, 0, 8, 16, None, None, 16, 64, None) == cdt.EINVAL
     assert "baseline" in _err(cdt)
     assert L.cdt_auroc(n, arr, 16, 32, 0, 16, 16, None, None, 16, 64, None) == cdt.EINVAL
+    arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0, (1 << 32) - 3)])
+    assert L.cdt_auroc(n, arr, 16, 32, 0, 0, 16, None, None, 16, 64, None) == cdt.ELIMIT
+    assert "canary_base" in _err(cdt)
 
 
 def test_scale_and_outlier_validation(cdt):

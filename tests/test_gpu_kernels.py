@@ -51,6 +51,43 @@ def test_ref_synth(gpu, shape):
     np.testing.assert_array_equal(ref.cpu().numpy(), oracle.ref_synth(S, C, T, H, 11, 2, gain))
 
 
+def test_fp16_conversion_exhaustive(gpu):
+    """Every fp32 bit pattern, fed through the live pass with zero noise
+    (block mode, scale 0: v = a + 0 z), must come out as its IEEE
+    round-to-nearest-even fp16.  All 2^32 inputs are checked against torch's
+    device conversion (a library routine), and a sample of each slab against
+    numpy's.  Zeros are compared by magnitude, since a + (+-0) can flip a
+    zero's sign; NaN is compared by class."""
+    torch, cdt = gpu
+    n, H = 1 << 28, 8192
+    T = n // H
+    bs = torch.zeros((1, 1), dtype=torch.float32, device="cuda")
+    h = torch.empty((1, 1, T, H), dtype=torch.float16, device="cuda")
+    rng = np.random.default_rng(0)
+    for start in range(0, 1 << 32, n):
+        announce(f"fp16 conversion inputs [{start:#x}, {start + n:#x})")
+        idx = torch.arange(start, start + n, dtype=torch.int64, device="cuda")
+        x = torch.where(idx >= 1 << 31, idx - (1 << 32), idx).to(torch.int32)
+        del idx
+        x = x.view(torch.float32).view(1, 1, T, H)
+        cdt.canary_sim(x, out=h, seed=1, cfg_id=0, benign_mode=1, sigma_b=0.0, bscale=bs)
+        got = h.view(torch.int16).reshape(-1)
+        want = x.to(torch.float16).view(torch.int16).reshape(-1)
+        same = got == want
+        zeros = ((got & 0x7FFF) == 0) & ((want & 0x7FFF) == 0)
+        nans = torch.isnan(x.reshape(-1)) & torch.isnan(h.reshape(-1))
+        bad = int((~(same | zeros | nans)).sum())
+        assert bad == 0, f"{bad} inputs in [{start:#x}, {start + n:#x}) differ"
+        pick = np.sort(rng.integers(0, n, 1 << 14))
+        xs = x.reshape(-1)[torch.from_numpy(pick).cuda()].cpu().numpy()
+        gs = got[torch.from_numpy(pick).cuda()].cpu().numpy().view(np.uint16)
+        ws = xs.astype(np.float16).view(np.uint16)
+        ok = (gs == ws) | (((gs & 0x7FFF) == 0) & ((ws & 0x7FFF) == 0)) | np.isnan(xs)
+        assert ok.all()
+        del x, got, want, same, zeros, nans
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("shape", SHAPES)
 def test_ref_stats_and_block_scales(gpu, shape):
     torch, cdt = gpu
