@@ -489,6 +489,41 @@ def run_sweep(torch, cdt, W, reps):
     return out
 
 
+def config_runs(torch, cdt, W, name):
+    """One of the remaining workloads run by itself: per run, the live pass
+    and Eq. 4 timed per launch (median of 3 passes, HIP events) and the
+    detection AUROC; drift_score's rate against the HBM peak."""
+    wl = W.get(name)
+    rs = wl.ref_sets[0]
+    prep = Prepared(torch, cdt, W, wl, rs)
+    score = torch.empty((rs.C, rs.S), dtype=torch.float32, device="cuda")
+    nbytes = rs.elems * DRIFT_BYTES_PER_ELEM + rs.S * rs.C * DRIFT_BYTES_PER_BLOCK
+    flags = cdt.AUROC_CONTROL | cdt.AUROC_RANDOM
+    rows, drift_all, sim_all = {}, [], []
+    for k, run in enumerate(rs.runs):
+        ts, bs = prep.scales[k]
+        kw = sim_kwargs(wl, rs, run, ts, bs)
+        sim_ms = time_ms(torch, lambda: cdt.canary_sim(prep.ref, out=prep.h, **kw), 3)
+        drift_ms = time_ms(torch, lambda: cdt.drift_score(prep.h, prep.ref, out=score, ws=prep.ws),
+                           3)
+        row = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
+        row.update(sim_ms=round(sim_ms, 4), drift_ms=round(drift_ms, 4))
+        rows[run.label] = row
+        drift_all.append(drift_ms)
+        sim_all.append(sim_ms)
+    drift_ms = sorted(drift_all)[len(drift_all) // 2]
+    sim_ms = sorted(sim_all)[len(sim_all) // 2]
+    out = {"shape_SxCxTxH": [rs.S, rs.C, rs.T, rs.H],
+           "drift_ms": round(drift_ms, 4),
+           "drift_GBps": round(nbytes / (drift_ms * 1e-3) / 1e9, 1),
+           "drift_frac_of_hbm_peak": round(nbytes / (drift_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+           "canary_sim_ms": round(sim_ms, 4),
+           "runs": rows}
+    del prep, score
+    torch.cuda.empty_cache()
+    return out
+
+
 def attainable(torch):
     """What torch's own kernels reach on the same box for the detector's two
     byte streams: a read-only reduction (drift_score's stream), a plain copy,
@@ -582,6 +617,31 @@ def cpu_baseline(W, args):
         elems += h.size
     dt = time.perf_counter() - t0
     nbytes = elems * DRIFT_BYTES_PER_ELEM + len(rs.runs) * rs.S * Cs * DRIFT_BYTES_PER_BLOCK
+    # Eq. 4 alone on the last run's activations
+    t1 = time.perf_counter()
+    oracle.drift_score(h, refs)
+    dt_drift = time.perf_counter() - t1
+    # one configuration of the 216-run sweep (the smallest shape) end to end,
+    # scaled to the sweep by its total element count
+    sw = W.sweep()
+    srs = min(sw.ref_sets, key=lambda r: r.elems)
+    srun = srs.runs[0]
+    t2 = time.perf_counter()
+    sgain = oracle.outlier_gain(srs.H, srs.n_out, W.OUTLIER_GAIN, sw.seed, srs.ref_set_id)
+    sref = oracle.ref_synth(srs.S, srs.C, srs.T, srs.H, sw.seed, srs.ref_set_id, sgain)
+    t3 = time.perf_counter()
+    q, m = oracle.ref_stats(sref)
+    ts, bs = oracle.block_scales(srs.T, srs.H, q, m, srun.eps, srun.sigma_b)
+    hs = oracle.canary_sim(sref, seed=sw.seed, cfg_id=srun.cfg_id, sigma_b=srun.sigma_b,
+                           mal_mask=srs.mal_mask, tamper=srun.tamper, tscale=ts,
+                           flip_p=srun.flip_p, scale=srun.scale)
+    _, s32, _ = oracle.drift_score(hs, sref)
+    oracle.auroc_config(s32, srs.mal_mask, seed=sw.seed, cfg_id=srun.cfg_id)
+    dt_cfg = time.perf_counter() - t3
+    sweep_elems = sum(len(r.runs) * r.elems for r in sw.ref_sets)
+    sweep_s = dt_cfg * sweep_elems / srs.elems
+    del sref, hs, sgain
+    dt_all = dt + dt_drift + (time.perf_counter() - t2)
     return {
         "value": round(nbytes / dt / 1e9, 4),
         "unit": "GB/s",
@@ -589,7 +649,11 @@ def cpu_baseline(W, args):
         "kind": "oracle",
         "sample": f"{rs.S} shards x {Cs} canary(ies) x {rs.T} x {rs.H}, {len(rs.runs)} runs "
                   f"(canary_sim + drift + auroc), {dt:.1f} s",
-        "seconds": round(dt, 2),
+        "seconds": round(dt_all, 2),
+        "drift_only_GBps": round(h.size * DRIFT_BYTES_PER_ELEM / dt_drift / 1e9, 4),
+        "sweep_configs_per_s": round(len([r for x in sw.ref_sets for r in x.runs]) / sweep_s, 4),
+        "sweep_sample": f"one {srs.S}x{srs.C}x{srs.T}x{srs.H} configuration (sim + drift + "
+                        f"auroc) in {dt_cfg:.1f} s, scaled by the sweep's element count",
         "host_cpu": host_cpu()[0],
         "host_threads": host_cpu()[1],
     }
@@ -622,6 +686,9 @@ def main():
     if not args.no_ablations:
         res["attainable"] = attainable(torch)
         res["small"] = small_latency(torch, cdt, W)
+        log("llama7b and snr workloads")
+        res["configs"] = {"llama7b": config_runs(torch, cdt, W, "llama7b"),
+                          "snr": config_runs(torch, cdt, W, "snr")}
     if not args.no_sweep:
         res["sweep"] = run_sweep(torch, cdt, W, args.sweep_reps)
     if not args.no_ablations:
