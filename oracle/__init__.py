@@ -90,12 +90,15 @@ _SIGS = {
 
 
 def lib():
-    """Load liboracle.so, compiling it first if it has not been built."""
+    """Load liboracle.so, compiling it first if it has not been built.
+    CDT_ORACLE_LIB names another build of oracle.c to load instead: the test
+    that plants mistakes in copies of the oracle runs the pins against them."""
     global _LIB
     if _LIB is None:
-        if not os.path.exists(_build.LIB):
+        path = os.environ.get("CDT_ORACLE_LIB", _build.LIB)
+        if path == _build.LIB and not os.path.exists(path):
             _build.build()
-        L = ctypes.CDLL(_build.LIB)
+        L = ctypes.CDLL(path)
         for name, (args, res) in _SIGS.items():
             fn = getattr(L, name)
             fn.argtypes = args

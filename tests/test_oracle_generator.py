@@ -46,11 +46,13 @@ def _rel(h_bits, a):
 # ----------------------------------------------------------------------------
 # references and outlier channels
 # ----------------------------------------------------------------------------
-def test_outlier_channels_are_the_smallest_words(orc):
+def test_outlier_channels_are_the_smallest_words(orc, philox_pin):
     H, n_out = 4096, 41
     g = orc.outlier_gain(H, n_out, 20.0, 5, 2)
-    words = np.array([orc.philox([j, 0, 0, (8 << 24) | 2], [5, 0])[0] for j in range(H)],
-                     np.uint64)
+    ctr = np.zeros((H, 4), np.uint32)
+    ctr[:, 0] = np.arange(H)
+    ctr[:, 3] = (8 << 24) | 2
+    words = philox_pin(ctr, np.tile(np.array([5, 0], np.uint32), (H, 1)))[:, 0].astype(np.uint64)
     order = np.lexsort((np.arange(H), words))  # by word, then channel
     want = np.ones(H, np.float32)
     want[order[:n_out]] = 20.0
@@ -91,6 +93,97 @@ def test_reference_blocks_are_distinct_and_deterministic(orc):
     full = orc.ref_synth(2, 2, 8, 64, 3, 0, np.ones(64, np.float32))
     np.testing.assert_array_equal(full[0, 1], a01)
     np.testing.assert_array_equal(full[1, 0], a10)
+
+
+# ----------------------------------------------------------------------------
+# counter layout of every stream, against rocRAND's Philox4x32-10
+# ----------------------------------------------------------------------------
+K16 = np.float32(math.sqrt(3.0 / (2.0**32 - 1.0)))
+
+
+def _ih(w0, w1):
+    """Irwin-Hall normal from two words (its moments are pinned above)."""
+    w0 = w0.astype(np.int64)
+    w1 = w1.astype(np.int64)
+    n = (w0 & 0xFFFF) + (w0 >> 16) + (w1 & 0xFFFF) + (w1 >> 16) - 131070
+    return n.astype(np.float32) * K16
+
+
+def _words(philox_pin, q, c, s, stream, cid, seed):
+    q = np.asarray(q, np.uint64)
+    ctr = np.zeros((q.size, 4), np.uint32)
+    ctr[:, 0] = q
+    ctr[:, 1] = c
+    ctr[:, 2] = s
+    ctr[:, 3] = (stream << 24) | cid
+    key = np.tile(np.array([seed & 0xFFFFFFFF, seed >> 32], np.uint32), (q.size, 1))
+    return philox_pin(ctr, key)
+
+
+def _one_normal(philox_pin, e, c, s, stream, cid, seed):
+    """Element e draws call q = e / 2: words 0-1 for even e, 2-3 for odd e."""
+    w = _words(philox_pin, e // 2, c, s, stream, cid, seed)
+    odd = (e % 2) == 1
+    return np.where(odd, _ih(w[:, 2], w[:, 3]), _ih(w[:, 0], w[:, 1]))
+
+
+@pytest.mark.parametrize("s,c", [(0, 0), (3, 1), (1, 6)])
+def test_stream_counters_against_rocrand(orc, philox_pin, s, c):
+    """Each stream's draw for element e of block (s, c) is the Philox call
+    with counter (q, c, s, stream << 24 | id) under key (lo32 seed, hi32
+    seed), with q and the words used as the generator's spec states.
+    rocRAND's Philox (an independent library routine) supplies the words;
+    each stream is made visible through a case where it alone sets the
+    output."""
+    T, H, seed, cid = 4, 64, (7 << 32) | 11, 5
+    e = np.arange(T * H)
+    zero = np.zeros((T, H), np.float32)
+    # REF: with unit gains the reference is the normal itself
+    a = orc.ref_block(s, c, T, H, seed, cid, np.ones(H, np.float32))
+    np.testing.assert_array_equal(a.ravel(), _one_normal(philox_pin, e, c, s, 0, cid, seed))
+    # BENIGN: a = 0 and block scale 1 give h = fp16(z_BENIGN)
+    h = orc.sim_block(s, c, zero, seed=seed, cfg_id=cid, benign_mode=NOISE_BLOCK, bscale=1.0)
+    np.testing.assert_array_equal(h.ravel(), _f16(_one_normal(philox_pin, e, c, s, 1, cid, seed)))
+    # ALT (independent recompute): the same with stream 9
+    h = orc.sim_block(s, c, zero, seed=seed, cfg_id=cid, benign_mode=NOISE_BLOCK, bscale=1.0,
+                      redraw=True)
+    np.testing.assert_array_equal(h.ravel(), _f16(_one_normal(philox_pin, e, c, s, 9, cid, seed)))
+    # TAMPER_ADD: clean base a = 0 and scale 1 give h = fp16(z_TADD)
+    h = orc.sim_block(s, c, zero, seed=seed, cfg_id=cid, sigma_b=0.0, malicious=True,
+                      tamper=T_ADD, tscale=1.0, tamper_base=BASE_CLEAN)
+    np.testing.assert_array_equal(h.ravel(), _f16(_one_normal(philox_pin, e, c, s, 4, cid, seed)))
+    # TAMPER_FLIP: element e uses word e % 4 of call e / 4; p = 1/2 flips u < 2^31
+    one = np.ones((T, H), np.float32)
+    h = orc.sim_block(s, c, one, seed=seed, cfg_id=cid, sigma_b=0.0, malicious=True,
+                      tamper=T_FLIP, flip_p=0.5)
+    w = _words(philox_pin, e // 4, c, s, 5, cid, seed)
+    u = w[np.arange(e.size), e % 4]
+    np.testing.assert_array_equal(h.ravel(), _f16(np.where(u < 2**31, -1.0, 1.0)))
+    # Student-t: T12 call q = e (words 0-1, 2-3), T3 one normal per element
+    h = orc.sim_block(s, c, zero, seed=seed, cfg_id=cid, benign_mode=NOISE_BLOCK, bscale=1.0,
+                      benign_dist=DIST_T3)
+    z0 = _one_normal(philox_pin, e, c, s, 1, cid, seed)
+    w12 = _words(philox_pin, e, c, s, 2, cid, seed)
+    z1, z2 = _ih(w12[:, 0], w12[:, 1]), _ih(w12[:, 2], w12[:, 3])
+    z3 = _one_normal(philox_pin, e, c, s, 3, cid, seed)
+    q = (z1 * z1 + z2 * z2) + z3 * z3
+    with np.errstate(divide="ignore", invalid="ignore"):
+        t = np.where(q == 0, np.float32(0), z0 / np.sqrt(q))
+    np.testing.assert_array_equal(h.ravel(), _f16(t))
+
+
+def test_control_and_random_counters_against_rocrand(orc, philox_pin):
+    """Scrambled stage j* of canary t: word 0 of (t, 0, 0, SCRAMBLE<<24|id)
+    modulo the number of benign stages; random-baseline score of (t, s):
+    (word 0 of (t, s, 0, RANDOM<<24|id) >> 8) 2^-24."""
+    seed, cid, S, pos = 9, 3, 7, (1 << 2) | (1 << 5)
+    benign = [j for j in range(S) if not (pos >> j) & 1]
+    for t in range(50):
+        w = _words(philox_pin, [t], 0, 0, 6, cid, seed)[0]
+        assert orc.scramble_jstar(S, pos, seed, cid, t) == benign[int(w[0]) % len(benign)]
+        for s in range(S):
+            w = _words(philox_pin, [t], s, 0, 7, cid, seed)[0]
+            assert orc.random_score(seed, cid, t, s) == np.float32((int(w[0]) >> 8) * 2.0**-24)
 
 
 # ----------------------------------------------------------------------------
@@ -319,6 +412,14 @@ def test_exact_norm_tamper_on_benign_output(orc):
     ts, vv, zz = orc.tamper_scale_exact_block(0, 0, a, eps, seed=2, cfg_id=1, sigma_b=sigma)
     q, _ = orc.ref_stats_block(a)
     assert abs(vv / q - 1.0) < 5 * sigma**2
+    # sum v^2 is the norm of the benign output itself: at a large noise level
+    # it differs from sum a^2 by ~sigma^2 and matches the stored fp16 output
+    # to within fp16 rounding
+    big = 0.3
+    _, vv_big, _ = orc.tamper_scale_exact_block(0, 0, a, eps, seed=2, cfg_id=1, sigma_b=big)
+    v16 = _h(orc.sim_block(0, 0, a, seed=2, cfg_id=1, sigma_b=big))
+    assert abs(vv_big / (v16 * v16).sum() - 1.0) < 2.0**-10
+    assert abs(vv_big / q - (1.0 + big**2)) < 0.02
     assert abs(zz / a.size - 1.0) < 0.05  # unit-variance normals
     h = orc.sim_block(0, 0, a, seed=2, cfg_id=1, sigma_b=sigma, malicious=True, tamper=T_ADD,
                       tscale=ts)
@@ -338,9 +439,12 @@ def _chain(orc, ref, carry, **kw):
     args.update(kw)
     ts = args.pop("tscale", None)
     ts = None if ts is None else np.ascontiguousarray(ts, np.float32)
+    bs = args.pop("bscale", None)
+    bs = None if bs is None else np.ascontiguousarray(bs, np.float32)
     orc.lib().orc_canary_sim_chain(
         S, C, T, H, args["seed"], args["cfg_id"], args["benign_mode"], args["benign_dist"],
-        args["sigma_b"], None, args["mal_mask"], args["tamper"], args["tamper_base"],
+        args["sigma_b"], None if bs is None else bs.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+        args["mal_mask"], args["tamper"], args["tamper_base"],
         None if ts is None else ts.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
         args["flip_p"], args["scale"], args["redraw"], carry,
         ref.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
@@ -366,6 +470,21 @@ def test_chain_benign_error_law(orc):
         m = _rel(h[s, 0], ref[s, 0])
         want = sigma * math.sqrt(sum(g ** (2 * j) for j in range(s + 1)))
         assert abs(m / want - 1.0) < 0.02, (s, m, want)
+
+
+def test_chain_carry_has_the_sign_of_the_previous_error(orc):
+    """With noise at stage 0 only, stage 1's live error is g times stage 0's
+    (e_1 = delta_1 + g e_0 with delta_1 = 0), up to fp16 rounding: a
+    regression of e_1 on e_0 has slope g, not -g."""
+    S, g = 3, 0.6
+    ref = orc.ref_synth(S, 1, 64, 512, 8, 0, np.ones(512, np.float32))
+    bscale = np.zeros((S, 1), np.float32)
+    bscale[0, 0] = 0.05
+    h = _chain(orc, ref, g, benign_mode=1, bscale=bscale)
+    e0 = _h(h[0, 0]) - ref[0, 0].astype(np.float64)
+    e1 = _h(h[1, 0]) - ref[1, 0].astype(np.float64)
+    slope = (e0 * e1).sum() / (e0 * e0).sum()
+    assert abs(slope / g - 1.0) < 0.01, slope
 
 
 def test_chain_carries_the_tamper_downstream(orc):
