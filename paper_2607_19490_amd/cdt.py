@@ -93,6 +93,11 @@ _SIGS = {
 _LIB = None
 
 
+# Interface version of include/cdt.h that the structures and signatures
+# below mirror (cdt_version()).
+ABI_VERSION = 4
+
+
 def lib():
     """Load libcdt.so (built by paper_2607_19490_amd.build); raises if absent."""
     global _LIB
@@ -104,6 +109,9 @@ def lib():
             fn = getattr(L, name)
             fn.argtypes = args
             fn.restype = res
+        if L.cdt_version() != ABI_VERSION:
+            raise RuntimeError(f"libcdt.so has interface version {L.cdt_version()}, this binding "
+                               f"expects {ABI_VERSION}; rebuild with __graft_entry__.build()")
         _LIB = L
     return _LIB
 
