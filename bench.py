@@ -336,6 +336,14 @@ def ablation_kernels(torch, cdt, wl, prep):
         out[name] = row
     out["redraw_canary_sim"] = {"ms": round(sim_ms, 4),
                                 "GBps": round(elems * SIM_BYTES_PER_ELEM / (sim_ms * 1e-3) / 1e9, 1)}
+    # the exact-norm Gaussian tamper's per-block scale (Section 3.2): one read
+    # of the references, the benign output and the tamper normals in registers
+    kw_x = dict(kw, mal_mask=0, tamper=0, tscale=None)
+    kw_x.pop("bscale")
+    ex_ms = time_ms(torch, lambda: cdt.tamper_scale_exact(prep.ref, 0.05, ws=prep.ws, bscale=bs,
+                                                          **kw_x))
+    out["tamper_scale_exact"] = {"ms": round(ex_ms, 4),
+                                 "reference_read_GBps": round(elems * 4 / (ex_ms * 1e-3) / 1e9, 1)}
     # the propagation model: stages in order per canary, live error carried
     kw_c = dict(kw, carry=0.7)
     chain_ms = time_ms(torch, lambda: cdt.canary_sim(prep.ref, out=r, **kw_c))
