@@ -575,7 +575,28 @@ def small_latency(torch, cdt, W):
                                         counts, pooled, fused=True)),
     )
     out = {name: round(time_ms(torch, fn, 21) * 1e3, 1) for name, fn in cases}
-    del preps, scores, views
+    # the same step captured once into a HIP graph (AUROC table uploaded
+    # beforehand, so the step is kernel launches only) and replayed
+    table, n_cfg = cdt.auroc_upload(cfgs, scores.numel(), flags=flags)
+
+    def step_launches():
+        cdt.canary_sim(prep.ref, out=prep.h, **kw)
+        cdt.drift_score(prep.h, prep.ref, out=views[0], ws=prep.ws)
+        cdt.auroc_launch(table, n_cfg, scores, seed=wl.seed, flags=flags, counts=counts,
+                         pooled=pooled)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step_launches()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step_launches()
+    torch.cuda.synchronize()
+    out["graph_step"] = round(time_ms(torch, graph.replay, 21) * 1e3, 1)
+    del graph, preps, scores, views
     return {"workload": "tiny 4x8x16x256", "unit": "us (median of 21, HIP events)",
             "latency": out}
 

@@ -293,6 +293,28 @@ int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, ui
               uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
               uint64_t* baseline, void* ws, size_t ws_bytes, void* stream);
 
+/* cdt_auroc in two parts, for a fixed set of configurations scored again and
+ * again (a serving loop, or a stream capture replayed as a HIP graph).
+ *
+ * cdt_auroc_upload validates the HOST table cfgs exactly as cdt_auroc does,
+ * against n_scores scores and the flags the launches will use, and copies
+ * it into the device buffer `table` (cdt_auroc_workspace_bytes(n_cfg)
+ * bytes, 16-byte aligned) on `stream`.  cfgs may be reused as soon as the
+ * call returns.
+ *
+ * cdt_auroc_launch scores `scores` against an uploaded table: it only
+ * launches kernels (no copies, no host reads of device memory), so a stream
+ * capture can record it.  Results are those of cdt_auroc with the same
+ * arguments.  The kernels check every configuration again against the
+ * n_scores given here (S <= 64, its table inside the scores, C*S <= 16384
+ * for the pooled ranking); a configuration that fails writes 2^64 - 1 to
+ * all its counts instead of being read. */
+int cdt_auroc_upload(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, uint64_t n_scores,
+                     uint32_t flags, void* table, size_t table_bytes, void* stream);
+int cdt_auroc_launch(uint32_t n_cfg, const void* table, const float* scores, uint64_t n_scores,
+                     uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
+                     uint64_t* baseline, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -88,6 +88,8 @@ _SIGS = {
     "cdt_auroc_workspace_bytes": ([_u32], _sz),
     "cdt_auroc": ([_u32, ctypes.POINTER(AurocCfg), _vp, _u64, _u64, _u32, _vp, _vp, _vp, _vp, _sz,
                    _vp], ctypes.c_int),
+    "cdt_auroc_upload": ([_u32, ctypes.POINTER(AurocCfg), _u64, _u32, _vp, _sz, _vp], ctypes.c_int),
+    "cdt_auroc_launch": ([_u32, _vp, _vp, _u64, _u64, _u32, _vp, _vp, _vp, _vp], ctypes.c_int),
 }
 
 _LIB = None
@@ -95,7 +97,7 @@ _LIB = None
 
 # Interface version of include/cdt.h that the structures and signatures
 # below mirror (cdt_version()).
-ABI_VERSION = 4
+ABI_VERSION = 5
 
 
 def lib():
@@ -361,6 +363,39 @@ def auroc(cfgs, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_POOLED, counts=No
         ws = _empty((max(16, lib().cdt_auroc_workspace_bytes(n)),), torch.uint8, scores)
     _check(lib().cdt_auroc(n, arr, _ptr(scores), scores.numel(), seed, flags, _ptr(counts),
                            _ptr(pooled), _ptr(baseline), _ptr(ws), ws.numel(), _stream()))
+    return (counts, pooled if flags & AUROC_POOLED else None,
+            baseline if flags & AUROC_RANDOM else None)
+
+
+def auroc_upload(cfgs, n_scores, *, flags=AUROC_CONTROL | AUROC_POOLED, table=None, like=None):
+    """Validate a configuration table (as auroc does) against n_scores scores
+    and copy it to the device.  Returns (table, n_cfg) for auroc_launch."""
+    torch = _torch()
+    arr, n = auroc_cfg_array(cfgs)
+    nbytes = max(16, lib().cdt_auroc_workspace_bytes(n))
+    table = _empty((nbytes,), torch.uint8, like) if table is None else table
+    _need(table, "table", torch.uint8)
+    _check(lib().cdt_auroc_upload(n, arr, n_scores, flags, _ptr(table), table.numel(), _stream()))
+    return table, n
+
+
+def auroc_launch(table, n_cfg, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_POOLED,
+                 counts=None, pooled=None, baseline=None):
+    """Score `scores` against an uploaded table: kernel launches only, so it
+    can be recorded by a stream capture.  Returns what auroc returns."""
+    torch = _torch()
+    _need(scores, "scores", torch.float32)
+    _need(table, "table", torch.uint8)
+    counts = _empty((n_cfg, 6), torch.int64, scores) if counts is None else counts
+    _need(counts, "counts", torch.int64, (n_cfg, 6))
+    if flags & AUROC_POOLED:
+        pooled = _empty((n_cfg, 3), torch.int64, scores) if pooled is None else pooled
+        _need(pooled, "pooled", torch.int64, (n_cfg, 3))
+    if flags & AUROC_RANDOM:
+        baseline = _empty((n_cfg, 3), torch.int64, scores) if baseline is None else baseline
+        _need(baseline, "baseline", torch.int64, (n_cfg, 3))
+    _check(lib().cdt_auroc_launch(n_cfg, _ptr(table), _ptr(scores), scores.numel(), seed, flags,
+                                  _ptr(counts), _ptr(pooled), _ptr(baseline), _stream()))
     return (counts, pooled if flags & AUROC_POOLED else None,
             baseline if flags & AUROC_RANDOM else None)
 

@@ -64,7 +64,7 @@ bool canaries_fit(uint32_t canary_base, uint64_t C) {
 
 extern "C" {
 
-int cdt_version(void) { return 4; }
+int cdt_version(void) { return 5; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -327,47 +327,111 @@ size_t cdt_auroc_workspace_bytes(uint32_t n_cfg) {
     return static_cast<size_t>(n_cfg) * sizeof(cdt_auroc_cfg);
 }
 
+namespace {
+
+// Host checks of a configuration table against n_scores scores and flags.
+int check_auroc_table(const char* fn, uint32_t n_cfg, const cdt_auroc_cfg* cfgs,
+                      uint64_t n_scores, uint32_t flags) {
+    if (flags & ~15u) return fail(CDT_EINVAL, "%s: bad flags", fn);
+    if (!cfgs) return fail(CDT_EINVAL, "%s: NULL cfgs", fn);
+    if (n_cfg > (1u << 24)) return fail(CDT_ELIMIT, "%s: n_cfg above 2^24", fn);
+    for (uint32_t g = 0; g < n_cfg; ++g) {
+        const cdt_auroc_cfg& c = cfgs[g];
+        if (c.S > 64) return fail(CDT_ELIMIT, "%s: cfg %u has S=%u above 64", fn, g, c.S);
+        if (c.cfg_id >= kMaxId) return fail(CDT_ELIMIT, "%s: cfg %u cfg_id >= 2^24", fn, g);
+        if (!canaries_fit(c.canary_base, c.C))
+            return fail(CDT_ELIMIT, "%s: cfg %u canary_base + C above 2^32", fn, g);
+        const uint64_t len = static_cast<uint64_t>(c.S) * c.C;
+        if ((flags & CDT_AUROC_POOLED) && len > kMaxPooled)
+            return fail(CDT_ELIMIT, "%s: cfg %u has C*S=%llu above %u for pooled ranking", fn,
+                        g, static_cast<unsigned long long>(len), kMaxPooled);
+        if (c.C > (1u << 30)) return fail(CDT_ELIMIT, "%s: cfg %u C above 2^30", fn, g);
+        if (c.score_off > n_scores || len > n_scores - c.score_off)
+            return fail(CDT_EINVAL, "%s: cfg %u table [%llu, +%llu) outside %llu scores", fn, g,
+                        static_cast<unsigned long long>(c.score_off),
+                        static_cast<unsigned long long>(len),
+                        static_cast<unsigned long long>(n_scores));
+    }
+    return CDT_OK;
+}
+
+// Host checks of the output arrays of one scoring launch.
+int check_auroc_outputs(const char* fn, uint32_t flags, uint64_t* counts, uint64_t* pooled,
+                        uint64_t* baseline) {
+    if (flags & ~15u) return fail(CDT_EINVAL, "%s: bad flags", fn);
+    if (!counts) return fail(CDT_EINVAL, "%s: NULL counts", fn);
+    if ((flags & CDT_AUROC_POOLED) && !pooled)
+        return fail(CDT_EINVAL, "%s: pooled counts requested but pooled is NULL", fn);
+    if ((flags & CDT_AUROC_RANDOM) && !baseline)
+        return fail(CDT_EINVAL, "%s: baseline counts requested but baseline is NULL", fn);
+    return CDT_OK;
+}
+
+// Copy a validated table into the device buffer `table` on `st`.
+int upload_table(const char* fn, uint32_t n_cfg, const cdt_auroc_cfg* cfgs, void* table,
+                 size_t table_bytes, hipStream_t st) {
+    const size_t need = cdt_auroc_workspace_bytes(n_cfg);
+    if (!table || table_bytes < need)
+        return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                    table ? table_bytes : 0);
+    if (!aligned16(table)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
+    const hipError_t e = hipMemcpyAsync(table, cfgs, need, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return device_status(e, fn);
+    return CDT_OK;
+}
+
+}  // namespace
+
 int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, uint64_t n_scores,
               uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
               uint64_t* baseline, void* ws, size_t ws_bytes, void* stream) {
     static_assert(sizeof(cdt_auroc_cfg) == sizeof(cdt::AurocCfgDev), "cfg layout");
     if (flags & ~15u) return fail(CDT_EINVAL, "cdt_auroc: bad flags");
     if (n_cfg == 0) return ok();
-    if (!cfgs || !counts) return fail(CDT_EINVAL, "cdt_auroc: NULL cfgs or counts");
-    if ((flags & CDT_AUROC_POOLED) && !pooled)
-        return fail(CDT_EINVAL, "cdt_auroc: pooled counts requested but pooled is NULL");
-    if ((flags & CDT_AUROC_RANDOM) && !baseline)
-        return fail(CDT_EINVAL, "cdt_auroc: baseline counts requested but baseline is NULL");
-    if (n_cfg > (1u << 24)) return fail(CDT_ELIMIT, "cdt_auroc: n_cfg above 2^24");
-    for (uint32_t g = 0; g < n_cfg; ++g) {
-        const cdt_auroc_cfg& c = cfgs[g];
-        if (c.S > 64) return fail(CDT_ELIMIT, "cdt_auroc: cfg %u has S=%u above 64", g, c.S);
-        if (c.cfg_id >= kMaxId) return fail(CDT_ELIMIT, "cdt_auroc: cfg %u cfg_id >= 2^24", g);
-        if (!canaries_fit(c.canary_base, c.C))
-            return fail(CDT_ELIMIT, "cdt_auroc: cfg %u canary_base + C above 2^32", g);
-        const uint64_t len = static_cast<uint64_t>(c.S) * c.C;
-        if ((flags & CDT_AUROC_POOLED) && len > kMaxPooled)
-            return fail(CDT_ELIMIT, "cdt_auroc: cfg %u has C*S=%llu above %u for pooled ranking",
-                        g, static_cast<unsigned long long>(len), kMaxPooled);
-        if (c.C > (1u << 30)) return fail(CDT_ELIMIT, "cdt_auroc: cfg %u C above 2^30", g);
-        if (c.score_off > n_scores || len > n_scores - c.score_off)
-            return fail(CDT_EINVAL, "cdt_auroc: cfg %u table [%llu, +%llu) outside %llu scores", g,
-                        static_cast<unsigned long long>(c.score_off),
-                        static_cast<unsigned long long>(len),
-                        static_cast<unsigned long long>(n_scores));
-        if (len > 0 && !scores) return fail(CDT_EINVAL, "cdt_auroc: scores is NULL");
+    int rc = check_auroc_outputs("cdt_auroc", flags, counts, pooled, baseline);
+    if (rc) return rc;
+    rc = check_auroc_table("cdt_auroc", n_cfg, cfgs, n_scores, flags);
+    if (rc) return rc;
+    if (!scores) {
+        for (uint32_t g = 0; g < n_cfg; ++g)
+            if (static_cast<uint64_t>(cfgs[g].S) * cfgs[g].C > 0)
+                return fail(CDT_EINVAL, "cdt_auroc: scores is NULL");
     }
-    const size_t need = cdt_auroc_workspace_bytes(n_cfg);
-    if (!ws || ws_bytes < need)
-        return fail(CDT_EINVAL, "cdt_auroc: workspace of %zu bytes needed, %zu given", need,
-                    ws ? ws_bytes : 0);
-    if (!aligned16(ws)) return fail(CDT_EALIGN, "cdt_auroc: ws must be 16-byte aligned");
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e = hipMemcpyAsync(ws, cfgs, need, hipMemcpyHostToDevice, st);
-    if (e != hipSuccess) return device_status(e, "cdt_auroc: config upload");
+    rc = upload_table("cdt_auroc", n_cfg, cfgs, ws, ws_bytes, st);
+    if (rc) return rc;
     return device_status(cdt::launch_auroc(n_cfg, static_cast<const cdt::AurocCfgDev*>(ws),
-                                           scores, seed, flags, counts, pooled, baseline, st),
+                                           scores, n_scores, seed, flags, counts, pooled,
+                                           baseline, st),
                          "cdt_auroc");
+}
+
+int cdt_auroc_upload(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, uint64_t n_scores,
+                     uint32_t flags, void* table, size_t table_bytes, void* stream) {
+    if (flags & ~15u) return fail(CDT_EINVAL, "cdt_auroc_upload: bad flags");
+    if (n_cfg == 0) return ok();
+    int rc = check_auroc_table("cdt_auroc_upload", n_cfg, cfgs, n_scores, flags);
+    if (rc) return rc;
+    rc = upload_table("cdt_auroc_upload", n_cfg, cfgs, table, table_bytes,
+                      static_cast<hipStream_t>(stream));
+    if (rc) return rc;
+    return ok();
+}
+
+int cdt_auroc_launch(uint32_t n_cfg, const void* table, const float* scores, uint64_t n_scores,
+                     uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
+                     uint64_t* baseline, void* stream) {
+    if (flags & ~15u) return fail(CDT_EINVAL, "cdt_auroc_launch: bad flags");
+    if (n_cfg == 0) return ok();
+    if (n_cfg > (1u << 24)) return fail(CDT_ELIMIT, "cdt_auroc_launch: n_cfg above 2^24");
+    int rc = check_auroc_outputs("cdt_auroc_launch", flags, counts, pooled, baseline);
+    if (rc) return rc;
+    if (!table || !scores) return fail(CDT_EINVAL, "cdt_auroc_launch: NULL table or scores");
+    if (!aligned16(table)) return fail(CDT_EALIGN, "cdt_auroc_launch: table must be 16-byte aligned");
+    return device_status(cdt::launch_auroc(n_cfg, static_cast<const cdt::AurocCfgDev*>(table),
+                                           scores, n_scores, seed, flags, counts, pooled,
+                                           baseline, static_cast<hipStream_t>(stream)),
+                         "cdt_auroc_launch");
 }
 
 }  // extern "C"

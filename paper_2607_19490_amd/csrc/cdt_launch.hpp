@@ -75,8 +75,11 @@ hipError_t launch_sim_score(const SimLaunch& p, const float* ref, uint16_t* h, f
 hipError_t launch_tamper_scale_exact(const SimLaunch& p, const float* ref, double eps,
                                      float* tscale, double* norms, void* ws, hipStream_t st);
 
+// Eqs. 5-6 over a device table of configurations; a configuration whose
+// table lies outside [0, n_scores) (or, pooled, exceeds the LDS sort) gets
+// counts of all ones instead of being read.
 hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float* scores,
-                        uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
-                        uint64_t* baseline, hipStream_t st);
+                        uint64_t n_scores, uint64_t seed, uint32_t flags, uint64_t* counts,
+                        uint64_t* pooled, uint64_t* baseline, hipStream_t st);
 
 }  // namespace cdt

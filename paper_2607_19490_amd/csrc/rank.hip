@@ -38,11 +38,30 @@ __device__ __forceinline__ float random_score(Key key, uint32_t t, uint32_t s, u
     return static_cast<float>(draw(key, t, s, 0, tag).x >> 8) * 0x1p-24f;
 }
 
+// A configuration the kernels can score without reading outside the score
+// array or the pooled sort's LDS.  The host validates every table before it
+// reaches the device; this check keeps a table reused against a different
+// score array from reading out of bounds.
+__device__ __forceinline__ bool cfg_in_bounds(const AurocCfgDev& cfg, uint64_t n_scores) {
+    const uint64_t len = static_cast<uint64_t>(cfg.S) * cfg.C;
+    return cfg.S <= 64 && cfg.score_off <= n_scores && len <= n_scores - cfg.score_off;
+}
+
+constexpr unsigned long long kBadCfg = ~0ull;  // counts of a configuration out of bounds
+
 __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
-    const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, Key key,
-    uint32_t flags, unsigned long long* __restrict__ counts,
+    const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, uint64_t n_scores,
+    Key key, uint32_t flags, unsigned long long* __restrict__ counts,
     unsigned long long* __restrict__ baseline) {
     const AurocCfgDev cfg = cfgs[blockIdx.x];
+    if (!cfg_in_bounds(cfg, n_scores)) {  // uniform over the workgroup
+        if (threadIdx.x == 0) {
+            for (int q = 0; q < 6; ++q) counts[6ull * blockIdx.x + q] = kBadCfg;
+            if (flags & 8u)
+                for (int q = 0; q < 3; ++q) baseline[3ull * blockIdx.x + q] = kBadCfg;
+        }
+        return;
+    }
     const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const uint64_t all = shard_mask(cfg.S);
     const uint64_t pos = cfg.pos_mask & all;
@@ -126,12 +145,18 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
 // Element layout in the pooled sort: key << 32 | label (label 1 = positive);
 // after the negative scan: key << 32 | negatives_before << 1 | label.
 __global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
-    const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores,
+    const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, uint64_t n_scores,
     unsigned long long* __restrict__ pooled) {
     __shared__ uint64_t v[kPoolMax];
     __shared__ uint32_t scan[kPoolThreads];
     __shared__ unsigned long long red[2][kPoolThreads / kWave];
     const AurocCfgDev cfg = cfgs[blockIdx.x];
+    if (!cfg_in_bounds(cfg, n_scores) ||
+        static_cast<uint64_t>(cfg.S) * cfg.C > kPoolMax) {  // uniform over the workgroup
+        if (threadIdx.x == 0)
+            for (int q = 0; q < 3; ++q) pooled[3ull * blockIdx.x + q] = kBadCfg;
+        return;
+    }
     const uint32_t n = cfg.S * cfg.C;
     uint32_t P2 = 1;
     while (P2 < n) P2 <<= 1;
@@ -238,17 +263,17 @@ __global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
 }  // namespace
 
 hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float* scores,
-                        uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
-                        uint64_t* baseline, hipStream_t st) {
+                        uint64_t n_scores, uint64_t seed, uint32_t flags, uint64_t* counts,
+                        uint64_t* pooled, uint64_t* baseline, hipStream_t st) {
     if (n_cfg == 0) return hipSuccess;
     const Key key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)};
     hipLaunchKernelGGL(auroc_counts_kernel, dim3(n_cfg), dim3(kCountThreads), 0, st, cfgs_dev,
-                       scores, key, flags, reinterpret_cast<unsigned long long*>(counts),
+                       scores, n_scores, key, flags, reinterpret_cast<unsigned long long*>(counts),
                        reinterpret_cast<unsigned long long*>(baseline));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !(flags & 2u)) return e;
     hipLaunchKernelGGL(auroc_pooled_kernel, dim3(n_cfg), dim3(kPoolThreads), 0, st, cfgs_dev,
-                       scores, reinterpret_cast<unsigned long long*>(pooled));
+                       scores, n_scores, reinterpret_cast<unsigned long long*>(pooled));
     return hipGetLastError();
 }
 

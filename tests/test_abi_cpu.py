@@ -38,7 +38,7 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 4 == cdt.ABI_VERSION
+    assert L.cdt_version() == 5 == cdt.ABI_VERSION
     assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
@@ -172,6 +172,34 @@ def test_auroc_validation(cdt):
     arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0, (1 << 32) - 3)])
     assert L.cdt_auroc(n, arr, 16, 32, 0, 0, 16, None, None, 16, 64, None) == cdt.ELIMIT
     assert "canary_base" in _err(cdt)
+
+
+def test_auroc_upload_and_launch_validation(cdt):
+    """The upload checks the table as cdt_auroc does; the launch checks its
+    own arguments (the table itself is re-checked by the kernels)."""
+    L = cdt.lib()
+    up, run = L.cdt_auroc_upload, L.cdt_auroc_launch
+    arr, n = cdt.auroc_cfg_array([(65, 4, 0, 1, 0)])
+    assert up(n, arr, 1000, 0, 16, 64, None) == cdt.ELIMIT
+    arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0), (8, 4, 30, 1, 1)])
+    assert up(n, arr, 60, 0, 16, 64, None) == cdt.EINVAL and "outside" in _err(cdt)
+    arr, n = cdt.auroc_cfg_array([(64, 300, 0, 1, 0)])
+    assert up(n, arr, 64 * 300, cdt.AUROC_POOLED, 16, 64, None) == cdt.ELIMIT
+    arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0)])
+    assert up(n, arr, 32, 0, 16, 31, None) == cdt.EINVAL  # table too small
+    assert up(n, arr, 32, 0, 8, 64, None) == cdt.EALIGN
+    assert up(n, None, 32, 0, 16, 64, None) == cdt.EINVAL
+    assert up(n, arr, 32, 16, 16, 64, None) == cdt.EINVAL  # bad flags
+    assert up(0, None, 0, 0, None, 0, None) == cdt.OK
+    assert run(1, 16, 16, 32, 0, 16, 16, None, None, None) == cdt.EINVAL  # bad flags
+    assert run(1, 16, 16, 32, 0, 0, None, None, None, None) == cdt.EINVAL  # no counts
+    assert run(1, 16, 16, 32, 0, cdt.AUROC_POOLED, 16, None, None, None) == cdt.EINVAL
+    assert run(1, 16, 16, 32, 0, cdt.AUROC_RANDOM, 16, None, None, None) == cdt.EINVAL
+    assert run(1, None, 16, 32, 0, 0, 16, None, None, None) == cdt.EINVAL
+    assert run(1, 16, None, 32, 0, 0, 16, None, None, None) == cdt.EINVAL
+    assert run(1, 8, 16, 32, 0, 0, 16, None, None, None) == cdt.EALIGN
+    assert run((1 << 24) + 1, 16, 16, 32, 0, 0, 16, None, None, None) == cdt.ELIMIT
+    assert run(0, None, None, 0, 0, 0, None, None, None, None) == cdt.OK
 
 
 def test_scale_and_outlier_validation(cdt):
