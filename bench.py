@@ -670,6 +670,33 @@ def cpu_baseline(W, args):
     sweep_elems = sum(len(r.runs) * r.elems for r in sw.ref_sets)
     sweep_s = dt_cfg * sweep_elems / srs.elems
     del sref, hs, sgain
+    # the other rows of the path on one canary of the same sample
+    one_ref = np.ascontiguousarray(refs[:, :1])
+    one_h = np.ascontiguousarray(h[:, :1])
+    run = rs.runs[0]
+    ts1, bs1 = oracle.block_scales(rs.T, rs.H, sumsq[:, :1], sumabs[:, :1], run.eps, run.sigma_b)
+    rows = {}
+    t4 = time.perf_counter()
+    oracle.cosine_score(one_h, one_ref)
+    rows["cosine_score_GBps"] = one_h.size * DRIFT_BYTES_PER_ELEM / (time.perf_counter() - t4) / 1e9
+    t4 = time.perf_counter()
+    oracle.canary_sim(one_ref, seed=wl.seed, cfg_id=run.cfg_id, sigma_b=run.sigma_b,
+                      mal_mask=rs.mal_mask, tamper=run.tamper, tscale=ts1, carry=0.7)
+    rows["chain_canary_sim_GBps"] = (one_h.size * SIM_BYTES_PER_ELEM /
+                                     (time.perf_counter() - t4) / 1e9)
+    t4 = time.perf_counter()
+    oracle.tamper_scale_exact(one_ref, 0.05, seed=wl.seed, cfg_id=run.cfg_id, sigma_b=run.sigma_b)
+    rows["tamper_scale_exact_reference_read_GBps"] = (one_h.size * 4 /
+                                                      (time.perf_counter() - t4) / 1e9)
+    # Eqs. 5-6 with control and pooled ranking on 216 sweep-shaped tables
+    rng = np.random.default_rng(0)
+    tabs = [(rng.standard_normal((32, S)).astype(np.float32), 1 << (S // 2))
+            for S in (8, 16, 32) for _ in range(72)]
+    t4 = time.perf_counter()
+    for tab, mask in tabs:
+        oracle.auroc_config(tab, mask, seed=wl.seed, cfg_id=1)
+    rows["auroc_configs_per_s"] = len(tabs) / (time.perf_counter() - t4)
+    rows = {k: round(v, 4) for k, v in rows.items()}
     dt_all = dt + dt_drift + (time.perf_counter() - t2)
     return {
         "value": round(nbytes / dt / 1e9, 4),
@@ -683,6 +710,9 @@ def cpu_baseline(W, args):
         "sweep_configs_per_s": round(len([r for x in sw.ref_sets for r in x.runs]) / sweep_s, 4),
         "sweep_sample": f"one {srs.S}x{srs.C}x{srs.T}x{srs.H} configuration (sim + drift + "
                         f"auroc) in {dt_cfg:.1f} s, scaled by the sweep's element count",
+        "other_rows": rows,
+        "other_rows_sample": f"{rs.S} shards x 1 canary x {rs.T} x {rs.H} (cosine, chain, "
+                             f"exact-norm scale); 216 random 32-canary tables (auroc)",
         "host_cpu": host_cpu()[0],
         "host_threads": host_cpu()[1],
     }
