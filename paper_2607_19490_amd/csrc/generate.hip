@@ -155,11 +155,21 @@ __global__ __launch_bounds__(kGenThreads) void canary_sim_kernel(SimArgs A,
 
 // Propagation model: a thread walks one group of 8 elements of one canary
 // through all S stages in order, carrying the live error in registers; a
-// workgroup chunk covers kGenChunkGroups groups of one canary, so the
+// workgroup chunk covers kChainChunkGroups groups of one canary, so the
 // per-stage block state is workgroup-uniform.  Same bytes as the live pass
-// (4 B read, 2 B written per element); nothing is re-read.
+// (4 B read, 2 B written per element); nothing is re-read.  With Student-t
+// noise the carried error and the extra draws need more than the 128
+// registers a 1024-thread workgroup allows, so that variant runs 256-thread
+// workgroups (no spills: 26.5 ms against 27.9 ms on the 16 x 256 x 256 x 8192
+// shape); the Gaussian variant keeps 1024 threads (10.5 ms against 11.5 ms).
+template <bool kT3>
+constexpr int chain_threads() { return kT3 ? 256 : kGenThreads; }
+
+template <bool kT3>
+constexpr uint32_t chain_chunk_groups() { return chain_threads<kT3>() * kGenItems; }
+
 template <bool kT3, bool kBlock>
-__global__ __launch_bounds__(kGenThreads) void canary_chain_kernel(SimArgs A, uint32_t S,
+__global__ __launch_bounds__(chain_threads<kT3>()) void canary_chain_kernel(SimArgs A, uint32_t S,
                                                                    float gain,
                                                                    const float* __restrict__ ref,
                                                                    uint16_t* __restrict__ h) {
@@ -169,10 +179,10 @@ __global__ __launch_bounds__(kGenThreads) void canary_chain_kernel(SimArgs A, ui
         const uint32_t c = static_cast<uint32_t>(chunk / A.chunks_per_block);
         const uint32_t g0 =
             static_cast<uint32_t>(chunk - static_cast<uint64_t>(c) * A.chunks_per_block) *
-            kGenChunkGroups;
+            chain_chunk_groups<kT3>();
 #pragma unroll 1
         for (int item = 0; item < kGenItems; ++item) {
-            const uint32_t g = g0 + item * kGenThreads + threadIdx.x;
+            const uint32_t g = g0 + item * chain_threads<kT3>() + threadIdx.x;
             if (g >= A.n8) break;
             float d[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll 1
@@ -236,25 +246,23 @@ hipError_t launch_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const d
     return hipGetLastError();
 }
 
+template <bool kT3, bool kBlock>
+hipError_t launch_chain_t(const SimLaunch& p, const float* ref, uint16_t* h, hipStream_t st) {
+    const uint64_t n8 = static_cast<uint64_t>(p.T) * p.H / 8;
+    const uint64_t cpc = (n8 + chain_chunk_groups<kT3>() - 1) / chain_chunk_groups<kT3>();
+    const SimArgs A = make_sim_args(p, cpc, cpc * p.C);  // cpc chunks per canary
+    hipLaunchKernelGGL((canary_chain_kernel<kT3, kBlock>), dim3(gen_grid(A.total_chunks)),
+                       dim3(chain_threads<kT3>()), 0, st, A, p.S, p.carry, ref, h);
+    return hipGetLastError();
+}
+
 hipError_t launch_canary_chain(const SimLaunch& p, const float* ref, uint16_t* h,
                                hipStream_t st) {
-    const uint64_t n8 = static_cast<uint64_t>(p.T) * p.H / 8;
-    const uint64_t cpc = (n8 + kGenChunkGroups - 1) / kGenChunkGroups;  // chunks per canary
-    const SimArgs A = make_sim_args(p, cpc, cpc * p.C);
-    const dim3 grid(gen_grid(A.total_chunks)), block(kGenThreads);
-    if (A.t3 && A.block_mode)
-        hipLaunchKernelGGL((canary_chain_kernel<true, true>), grid, block, 0, st, A, p.S, p.carry,
-                           ref, h);
-    else if (A.t3)
-        hipLaunchKernelGGL((canary_chain_kernel<true, false>), grid, block, 0, st, A, p.S,
-                           p.carry, ref, h);
-    else if (A.block_mode)
-        hipLaunchKernelGGL((canary_chain_kernel<false, true>), grid, block, 0, st, A, p.S,
-                           p.carry, ref, h);
-    else
-        hipLaunchKernelGGL((canary_chain_kernel<false, false>), grid, block, 0, st, A, p.S,
-                           p.carry, ref, h);
-    return hipGetLastError();
+    const bool t3 = p.benign_dist == 1, block_mode = p.benign_mode == 1;
+    if (t3 && block_mode) return launch_chain_t<true, true>(p, ref, h, st);
+    if (t3) return launch_chain_t<true, false>(p, ref, h, st);
+    if (block_mode) return launch_chain_t<false, true>(p, ref, h, st);
+    return launch_chain_t<false, false>(p, ref, h, st);
 }
 
 hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, hipStream_t st) {
