@@ -11,11 +11,24 @@ Default workload: Llama-70B-shaped, 16 shards x 256 canaries x 256 tokens x
 hidden 8192 (48 GiB of activations), three runs: additive Gaussian eps 0.05,
 sign flip of 0.1% of elements, uniform rescale by 1.05.
 
-Prints one JSON line.  `value` is drift-scored activation bytes (2 B fp16 +
-4 B fp32 per element, each read once) per second of the whole step; the
-`roofline` object reports the drift kernel alone against the 8 TB/s HBM peak;
-`sweep` reports the 216-run factorial in configurations per second;
-`cpu_baseline` times the CPU oracle on a bounded sample of the same step.
+Prints one JSON line:
+  value          drift-scored activation bytes (2 B fp16 + 4 B fp32 per
+                 element, each read once) per second of the whole step;
+  roofline       the drift kernel alone against the 8 TB/s HBM peak, with
+                 the HBM traffic of the committed counter pass;
+  canary_sim, fused_step
+                 the live pass's own rate; the step with the live pass and
+                 Eq. 4 fused into one launch per run;
+  ablation_kernels, table1, substudies
+                 the reference conditions and ablations of Sections 4.4-4.5,
+                 Table 1's structure on the paper's shape, the propagation
+                 substudies of Sections 5.3-5.5;
+  sweep          the 216-run factorial in configurations per second;
+  attainable, small, configs
+                 torch's own kernels on the same byte streams, latencies of
+                 the cache-resident tiny workload (eager, fused, HIP graph),
+                 the 7B-shaped and SNR workloads run by themselves;
+  cpu_baseline   the CPU oracle on a bounded sample of the same step.
 """
 import argparse
 import json
