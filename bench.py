@@ -398,6 +398,21 @@ def table1(torch, cdt, W):
         rows["full_detector"][run.label] = dict(full, ceiling=ceil["auroc"])
         rows["noisy_reference"][run.label] = dict(ceil, ceiling=ceil["auroc"])
         rows["cosine_metric"][run.label] = dict(cos, ceiling=cos_ceil["auroc"])
+    # the same attacks with the live error carried between stages (the
+    # propagation model of the substudies; Gaussian attacks at eps rms, the
+    # exact norm being defined for independent stages only): a pure rescale
+    # then leaves its stage with less angular error than the stages after it,
+    # which inherit its error, so the cosine metric ranks it below chance
+    prop = {}
+    for k, run in enumerate(rs.runs):
+        ts, bs = cdt.block_scales(prep.sumsq, prep.sumabs, rs.T, rs.H, run.eps, run.sigma_b)
+        kw = dict(sim_kwargs(wl, rs, run, ts, bs), carry=W.SUBSTUDY_CARRY)
+        cdt.canary_sim(prep.ref, out=prep.h, **kw)
+        cdt.drift_score(prep.h, prep.ref, out=score, ws=prep.ws)
+        l2 = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
+        cdt.cosine_score(prep.h, prep.ref, out=score, ws=prep.ws)
+        cos = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
+        prop[run.label] = {"auroc_l2": l2["auroc"], "auroc_cosine": cos["auroc"]}
     summary = {}
     for name, per in rows.items():
         vals = list(per.values())
@@ -407,7 +422,8 @@ def table1(torch, cdt, W):
     del prep, r
     torch.cuda.empty_cache()
     return {"workload": "paper 12x100x48x768, block noise sigma_hw 0.002",
-            "mean_over_six_attacks": summary, "per_attack": rows}
+            "mean_over_six_attacks": summary, "per_attack": rows,
+            "with_propagation": {"carry": W.SUBSTUDY_CARRY, "per_attack": prop}}
 
 
 def substudies(torch, cdt, W):

@@ -356,3 +356,11 @@ def test_table1_structure(gpu, gold):
     for name, summ in t["mean_over_six_attacks"].items():
         assert lo <= summ["random_baseline"] <= hi, (name, summ)
         assert lo <= summ["control"] <= hi, (name, summ)
+    # with the live error carried between stages, the cosine metric ranks the
+    # pure rescale below chance (Table 1 reports 0.194); Eq. 4 is unaffected
+    for label, row in t["with_propagation"]["per_attack"].items():
+        assert row["auroc_l2"] == 1.0, (label, row)
+        if label.startswith("rescale"):
+            assert row["auroc_cosine"] < 0.45, row
+        else:
+            assert row["auroc_cosine"] == 1.0, (label, row)

@@ -68,3 +68,31 @@ def test_detection_fades_when_noise_swamps_the_tamper(orc):
         aucs.append(orc.auroc_mw(counts))
     assert aucs[0] == 1.0
     assert aucs[2] < 0.75
+
+
+def test_cosine_ranks_a_rescale_below_chance_under_propagation(orc):
+    """Table 1 reports the cosine metric at 0.194 on the alpha = 0.10
+    rescale: below chance, not merely at it.  With the live error carried
+    between stages (gain 0.7), the rescaled stage keeps the angle of its
+    input while the stages after it inherit its error, so its cosine
+    mismatch ranks below theirs; Eq. 4 still ranks it first."""
+    S, C, T, H = 12, 20, 48, 768
+    gain = orc.outlier_gain(H, W.n_outliers(H), W.OUTLIER_GAIN, 0, 0)
+    ref = orc.ref_synth(S, C, T, H, 0, 0, gain)
+    q, m = orc.ref_stats(ref)
+    _, bs = orc.block_scales(T, H, q, m, 0.0, 0.002)
+    mal = 1 << 5
+    h = orc.canary_sim(ref, seed=0, cfg_id=5, benign_mode=1, sigma_b=0.002, bscale=bs,
+                       mal_mask=mal, tamper=4, scale=1.10, carry=W.SUBSTUDY_CARRY)
+    cos, _ = orc.cosine_score(h, ref)
+    _, l2, _ = orc.drift_score(h, ref)
+    c_cos, _ = orc.auroc_config(cos.astype(np.float32), mal, seed=0, cfg_id=5, flags=0)
+    c_l2, _ = orc.auroc_config(l2, mal, seed=0, cfg_id=5, flags=0)
+    assert orc.auroc_strict(c_l2) == 1.0
+    assert orc.auroc_strict(c_cos) < 0.45
+    # without propagation the same rescale sits at chance
+    h0 = orc.canary_sim(ref, seed=0, cfg_id=5, benign_mode=1, sigma_b=0.002, bscale=bs,
+                        mal_mask=mal, tamper=4, scale=1.10)
+    cos0, _ = orc.cosine_score(h0, ref)
+    c0, _ = orc.auroc_config(cos0.astype(np.float32), mal, seed=0, cfg_id=5, flags=0)
+    assert 0.4 < orc.auroc_strict(c0) < 0.6
