@@ -460,6 +460,34 @@ def substudies(torch, cdt, W):
             "studies": out}
 
 
+def benign_fpr(torch, cdt, W, n_cfg=24):
+    """The pre-registered false-positive criterion of Section 4.6 on the
+    paper's shape: pipelines with no malicious stage, each scored with the
+    scrambled-label control (a random benign stage per canary ranked as if
+    it were the attacker).  A configuration is a false positive when that
+    AUROC reaches the 0.90 success threshold; the rate must stay at or below
+    5%."""
+    wl = W.paper()
+    rs = wl.ref_sets[0]
+    prep = Prepared(torch, cdt, W, wl, rs)
+    scores = torch.empty((n_cfg, rs.C, rs.S), dtype=torch.float32, device="cuda")
+    _, bs = prep.scales[0]
+    for g in range(n_cfg):
+        cdt.canary_sim(prep.ref, out=prep.h, seed=wl.seed, cfg_id=100 + g,
+                       benign_mode=W.NOISE_BLOCK, sigma_b=0.002, bscale=bs)
+        cdt.drift_score(prep.h, prep.ref, out=scores[g], ws=prep.ws)
+    cfgs = [(rs.S, rs.C, g * rs.C * rs.S, 0, 100 + g) for g in range(n_cfg)]
+    counts, _, _ = cdt.auroc(cfgs, scores.view(-1), seed=wl.seed, flags=cdt.AUROC_CONTROL)
+    c = cdt.u64(counts)
+    ctrl = [int(x[3]) / int(x[5]) for x in c]
+    del prep, scores
+    torch.cuda.empty_cache()
+    return {"configs": n_cfg, "false_positive_rate": sum(a >= 0.90 for a in ctrl) / n_cfg,
+            "control_auroc_mean": round(sum(ctrl) / n_cfg, 4),
+            "control_auroc_max": round(max(ctrl), 4),
+            "criterion": "false-positive rate <= 0.05 (success threshold 0.90)"}
+
+
 def run_sweep(torch, cdt, W, reps):
     wl = W.sweep()
     log("sweep: preparing 9 reference sets")
@@ -784,6 +812,7 @@ def main():
         res["table1"] = table1(torch, cdt, W)
         log("substudies (depth, position, collusion, frontier)")
         res["substudies"] = substudies(torch, cdt, W)
+        res["benign_fpr"] = benign_fpr(torch, cdt, W)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(W, args)
