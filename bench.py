@@ -427,8 +427,8 @@ def table1(torch, cdt, W):
 
 
 def substudies(torch, cdt, W):
-    """Depth, position, collusion and frontier substudies (Sections 4.4 and
-    5.3-5.5) on the paper's shape with the live error carried between
+    """Depth, position, collusion, frontier and SNR substudies (Sections 4.4
+    and 5.3-5.5) on the paper's shape with the live error carried between
     stages: detection AUROC per configuration."""
     wl = W.substudies()
     out = {}
@@ -456,7 +456,8 @@ def substudies(torch, cdt, W):
         out.setdefault(study, {})[name] = row
     cache.clear()
     torch.cuda.empty_cache()
-    return {"carry": W.SUBSTUDY_CARRY, "shape": "k x 100 x 48 x 768, block noise 0.002",
+    return {"carry": W.SUBSTUDY_CARRY,
+            "shape": "k x 100 x 48 x 768, block noise 0.002 (raised in the snr study)",
             "studies": out}
 
 

@@ -17,8 +17,8 @@ Workloads
               [1e-4, 1e-1], Gaussian and Student-t noise, tamper 0.02
   paper       12 x 100 x 48 x 768 (the paper's GPT-2 / Pythia-160M shape),
               block-scaled benign noise sigma_hw = 0.002, the six attacks
-  substudies  the depth, position, collusion and frontier substudies on the
-              paper's shape with the live error carried between stages
+  substudies  the depth, position, collusion, frontier and SNR substudies
+              on the paper's shape with the live error carried between stages
 """
 from dataclasses import dataclass, field
 from typing import List, Tuple
@@ -190,6 +190,7 @@ SUBSTUDY_DEPTHS = (2, 4, 6, 8, 10, 12)
 SUBSTUDY_POSITIONS = (0, 2, 5, 8, 11)          # first ... last of 12 stages
 SUBSTUDY_COLLUDERS = (1, 2, 3, 4)
 SUBSTUDY_EPS = (0.10, 0.05, 0.02, 0.01, 0.005, 0.002, 0.001)
+SUBSTUDY_SIGMA_HW = (0.002, 0.01, 0.02, 0.05, 0.1, 0.2)
 
 
 def colluder_positions(k: int, c: int) -> Tuple[int, ...]:
@@ -206,14 +207,16 @@ def substudies() -> Workload:
       position   k = 12, attacker at 5 positions from first to last
       collusion  k = 12, 1..4 colluders spaced uniformly
       frontier   k = 12, Gaussian eps from 0.10 down to 0.001
+      snr        k = 12, Gaussian 0.05, sigma_hw raised from 0.002 to 0.2
+                 (Section 5.4)
     Each configuration is one reference set with one run; configurations of
     one shape share their references (same ref_set_id)."""
     C, T, H = 100, 48, 768
     n_out = n_outliers(H)
     sets = []
 
-    def add(name, S, mal, eps):
-        run = Run(len(sets), benign_mode=NOISE_BLOCK, sigma_b=0.002, tamper=T_ADD, eps=eps,
+    def add(name, S, mal, eps, sigma_hw=0.002):
+        run = Run(len(sets), benign_mode=NOISE_BLOCK, sigma_b=sigma_hw, tamper=T_ADD, eps=eps,
                   carry=SUBSTUDY_CARRY, label=name)
         sets.append(RefSet(S, S, C, T, H, n_out, tuple(mal), (run,)))
 
@@ -225,6 +228,8 @@ def substudies() -> Workload:
         add(f"collusion:c{c}", 12, colluder_positions(12, c), 0.05)
     for eps in SUBSTUDY_EPS:
         add(f"frontier:eps{eps:g}", 12, (5,), eps)
+    for sigma in SUBSTUDY_SIGMA_HW:
+        add(f"snr:sigma{sigma:g}", 12, (5,), 0.05, sigma)
     return Workload("substudies", tuple(sets))
 
 

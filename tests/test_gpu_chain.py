@@ -49,8 +49,8 @@ def test_chain_bit_exact(gpu, shape, case, carry):
 
 def test_substudies(gpu):
     """Depth, position and collusion leave the detector at 1.0 (Section
-    5.3); along the frontier (Section 5.5) the attacker's lead over the
-    benign floor shrinks toward 1 as eps falls to the floor.  One
+    5.3); along the frontier (Section 5.5) and as the noise floor rises
+    (Section 5.4) the attacker's lead over the benign floor shrinks.  One
     configuration is compared whole with the oracle's chain."""
     torch, cdt = gpu
     import bench
@@ -71,6 +71,17 @@ def test_substudies(gpu):
     assert all(b <= a + 0.01 for a, b in zip(lead, lead[1:])), lead
     assert lead[0] > 1.2 and lead[-1] < 1.1, lead
     assert all(fr[f"eps{e}"]["auroc"] >= 0.5 for e in eps)
+    # SNR (Section 5.4): raising sigma_hw from 0.002 to 0.2 at eps = 0.05
+    # shrinks the lead and, once the benign floor reaches the tamper, the
+    # detector starts to miss (the paper reports 0.46-0.86 at 0.2 on real
+    # models)
+    snr = res["snr"]
+    sig = ("0.002", "0.01", "0.02", "0.05", "0.1", "0.2")
+    lead = [snr[f"sigma{x}"]["median_m_malicious"] / snr[f"sigma{x}"]["max_m_benign"]
+            for x in sig]
+    assert all(b <= a + 0.01 for a, b in zip(lead, lead[1:])), lead
+    assert all(snr[f"sigma{x}"]["auroc"] == 1.0 for x in sig[:4])
+    assert snr["sigma0.2"]["auroc"] < 1.0 and lead[-1] < 1.0, (snr["sigma0.2"], lead)
     # whole-configuration parity: depth k = 4
     wl = W.substudies()
     rs = [r for r in wl.ref_sets if r.runs[0].label == "depth:k4"][0]
