@@ -1,5 +1,4 @@
 """Helpers shared by the GPU parity tests (no arithmetic of the method)."""
-import math
 
 import numpy as np
 import pytest

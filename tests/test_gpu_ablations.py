@@ -3,7 +3,6 @@ against the CPU oracle, through the C ABI: the independent benign redraw
 (bit-exact), Eq. 4 against an fp16 reference (1e-5), the cosine mismatch
 (1e-5 plus the fp64 rounding bound of its sums), and the random-baseline
 counts (bit-exact)."""
-import math
 
 import numpy as np
 import pytest

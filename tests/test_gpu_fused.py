@@ -1,7 +1,6 @@
 """The fused live-pass-and-score launch (cdt_sim_score) against the two-launch
 path it replaces (cdt_canary_sim, then cdt_drift_score) and the oracle: the
 scores, the fp64 sums and the stored activations are bitwise identical."""
-import numpy as np
 import pytest
 
 import oracle

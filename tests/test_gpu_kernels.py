@@ -5,7 +5,6 @@ activations), outlier channels and AUROC counts; 1e-5 relative for drift
 scores (Eq. 4); the fp64 sums within the bound of two n-term fp64 sums.  Shapes span several
 chunks, ragged tails, single-element blocks and empty inputs.
 """
-import math
 
 import numpy as np
 import pytest

@@ -18,7 +18,7 @@ import pytest
 
 import oracle
 from paper_2607_19490_amd import workloads as W
-from tests.gpu_util import announce, h_bits, rel_err, require_gpu, ulp_diff_f32
+from tests.gpu_util import announce, rel_err, require_gpu, ulp_diff_f32
 
 pytestmark = pytest.mark.gpu
 

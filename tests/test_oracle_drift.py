@@ -9,7 +9,6 @@ import math
 from fractions import Fraction
 
 import numpy as np
-import pytest
 
 from paper_2607_19490_amd import inputs
 

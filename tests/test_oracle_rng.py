@@ -6,7 +6,6 @@ symmetry and distribution; fp32 -> fp16 rounding against numpy's float16
 conversion (a library routine) on every rounding boundary.
 """
 import math
-import os
 import warnings
 
 import numpy as np
