@@ -82,6 +82,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--workload", default="llama70b")
     p.add_argument("--no-sweep", action="store_true")
+    p.add_argument("--sweep-only", action="store_true",
+                   help="run only the 216-run factorial (for a kernel trace of it); prints "
+                        "the sweep object alone")
     p.add_argument("--sweep-reps", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-ablations", action="store_true",
@@ -798,6 +801,9 @@ def main():
         torch.cuda.synchronize()
         del x, y
         log("copy calibration: 4 GiB read + 4 GiB written")
+    if args.sweep_only:
+        print(json.dumps({"sweep": run_sweep(torch, cdt, W, args.sweep_reps)}), flush=True)
+        return
     res, _ = run_main(torch, cdt, W, args)
     if not args.no_ablations:
         res["attainable"] = attainable(torch)
@@ -810,7 +816,7 @@ def main():
     if not args.no_ablations:
         log("table 1 structure on the paper's shape")
         res["table1"] = table1(torch, cdt, W)
-        log("substudies (depth, position, collusion, frontier)")
+        log("substudies (depth, position, collusion, frontier, snr)")
         res["substudies"] = substudies(torch, cdt, W)
         res["benign_fpr"] = benign_fpr(torch, cdt, W)
     if not args.no_cpu_baseline:
