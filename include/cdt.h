@@ -98,10 +98,12 @@ int cdt_ref_synth(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
                   uint32_t ref_set_id, uint32_t canary_base, const float* gain, float* ref,
                   void* stream);
 
-/* Workspace (device bytes) needed by cdt_ref_stats and the four block
+/* Workspace (device bytes) needed by cdt_ref_stats, the four block
  * reductions (cdt_drift_score, cdt_drift_score_f16ref, cdt_cosine_score,
- * cdt_cosine_score_f16ref) for this shape: per-block partial sums (up to
- * three fp64 per chunk) of a fixed chunking. */
+ * cdt_cosine_score_f16ref), cdt_sim_score and cdt_tamper_scale_exact for
+ * this shape: per-block partial sums (up to three fp64 per chunk of 32768
+ * elements).  Calls on one stream may share one workspace; calls that can
+ * overlap (different streams) need their own. */
 size_t cdt_reduce_workspace_bytes(uint32_t S, uint32_t C, uint32_t T, uint32_t H);
 
 /* Per-block reference statistics in fp64: sumsq[s][c] = sum a^2 and
