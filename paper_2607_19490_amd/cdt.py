@@ -202,6 +202,7 @@ def workspace(S, C, T, H, like=None):
 def _ws_arg(ws, S, C, T, H, like):
     if ws is None:
         ws = workspace(S, C, T, H, like)
+    _need(ws, "ws", ws.dtype)
     return ws, ctypes.c_size_t(ws.numel() * ws.element_size())
 
 
@@ -361,6 +362,7 @@ def auroc(cfgs, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_POOLED, counts=No
         _need(baseline, "baseline", torch.int64, (n, 3))
     if ws is None:
         ws = _empty((max(16, lib().cdt_auroc_workspace_bytes(n)),), torch.uint8, scores)
+    _need(ws, "ws", torch.uint8)
     _check(lib().cdt_auroc(n, arr, _ptr(scores), scores.numel(), seed, flags, _ptr(counts),
                            _ptr(pooled), _ptr(baseline), _ptr(ws), ws.numel(), _stream()))
     return (counts, pooled if flags & AUROC_POOLED else None,
