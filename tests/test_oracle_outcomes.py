@@ -47,8 +47,9 @@ def test_paper_shape_six_attacks(orc):
             assert abs(mal.mean() - gold["sign_flip_mismatch"]["value"]) < 0.01
         if run.label == "rescale0.10":
             assert abs(mal.mean() - gold["rescale_mismatch"]["value"]) < 0.005
-    # the smallest Gaussian tamper clears the benign floor by an order of magnitude
-    assert margins["gauss0.02"] > 10.0
+    # the smallest Gaussian tamper clears the benign floor by an order of
+    # magnitude, as the paper's 22x does
+    assert margins["gauss0.02"] > 0.5 * gold["margin_smallest_eps"]["value"]
     assert margins["signflip"] > 1000.0
 
 
@@ -89,6 +90,10 @@ def test_cosine_ranks_a_rescale_below_chance_under_propagation(orc):
     c_cos, _ = orc.auroc_config(cos.astype(np.float32), mal, seed=0, cfg_id=5, flags=0)
     c_l2, _ = orc.auroc_config(l2, mal, seed=0, cfg_id=5, flags=0)
     assert orc.auroc_strict(c_l2) == 1.0
+    with open(os.path.join(GOLDEN, "paper_outcomes.json")) as f:
+        gold = json.load(f)
+    # the same side of chance as Table 1's value
+    assert gold["cosine_rescale_auroc"]["value"] < 0.5
     assert orc.auroc_strict(c_cos) < 0.45
     # without propagation the same rescale sits at chance
     h0 = orc.canary_sim(ref, seed=0, cfg_id=5, benign_mode=1, sigma_b=0.002, bscale=bs,
