@@ -24,8 +24,9 @@
  *     launched and an error code is returned.  cdt_last_error() gives a
  *     per-thread description of the last failure.
  *   - Results are deterministic: fixed reduction orders, no atomics.
- *   - activations need H % 8 == 0, T*H < 2^32, and 16-byte aligned
- *     pointers; S <= 64 wherever a shard bit mask is involved.
+ *   - activations need H % 8 == 0, T*H < 2^32, S*C <= 2^32,
+ *     S*C*T*H <= 2^40 and 16-byte aligned pointers; S <= 64 wherever a
+ *     shard bit mask is involved (CDT_ELIMIT otherwise).
  *   - Empty shapes (S, C, T or H zero) are valid and do no work, except
  *     that drift scores of empty blocks are written as 0.
  *   - Canary sharding: every generated value and every per-canary random

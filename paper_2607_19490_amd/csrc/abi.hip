@@ -34,19 +34,28 @@ int device_status(hipError_t e, const char* what) {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 constexpr uint64_t kMaxBlockElems = 1ull << 32;  // element index e must fit 32 bits
+constexpr uint64_t kMaxBlocks = 1ull << 32;      // (shard, canary) blocks per call
+constexpr uint64_t kMaxElems = 1ull << 40;       // elements per call
 constexpr uint32_t kMaxId = 1u << 24;            // counter id field
 constexpr uint32_t kMaxOutlierH = 32768;
 constexpr uint32_t kMaxPooled = 16384;
 
-// Shape checks common to every activation call.
+// Shape checks common to every activation call.  Beyond the per-block limit,
+// the block count must fit 32 bits and the whole array 2^40 elements (4 TiB
+// of fp32, far beyond one device), so that every size derived from the
+// shape (workspace bytes, grids, offsets) is exact in 64 bits.
 int check_shape(const char* fn, uint32_t S, uint32_t C, uint32_t T, uint32_t H) {
-    (void)S;
-    (void)C;
     if (H % 8 != 0) return fail(CDT_EINVAL, "%s: H=%u must be a multiple of 8", fn, H);
     const uint64_t n = static_cast<uint64_t>(T) * H;
     if (n >= kMaxBlockElems)
         return fail(CDT_ELIMIT, "%s: T*H=%llu must be below 2^32", fn,
                     static_cast<unsigned long long>(n));
+    const uint64_t nblocks = static_cast<uint64_t>(S) * C;
+    if (nblocks > kMaxBlocks)
+        return fail(CDT_ELIMIT, "%s: S*C=%llu above 2^32", fn,
+                    static_cast<unsigned long long>(nblocks));
+    if (n > 0 && nblocks > kMaxElems / n)
+        return fail(CDT_ELIMIT, "%s: S*C*T*H above 2^40", fn);
     return CDT_OK;
 }
 

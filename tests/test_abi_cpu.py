@@ -88,6 +88,13 @@ def test_shape_and_pointer_validation(cdt):
         assert fn(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
     # empty shapes are accepted without touching the device
     assert L.cdt_drift_score(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
+    # block count and total size limits (sizes derived from the shape stay exact)
+    assert L.cdt_drift_score(1 << 20, 1 << 13, 1, 8, 16, 16, 16, None, 16, 1 << 20,
+                             None) == cdt.ELIMIT
+    assert "S*C=" in _err(cdt)
+    assert L.cdt_drift_score(1 << 16, 1 << 16, 1 << 10, 8, 16, 16, 16, None, 16, 1 << 20,
+                             None) == cdt.ELIMIT
+    assert "2^40" in _err(cdt)
     assert L.cdt_ref_synth(2, 0, 3, 16, 0, 0, 0, None, None, None) == cdt.OK
     assert L.cdt_ref_synth(2, 2, 3, 16, 0, 1 << 24, 0, 16, 16, None) == cdt.ELIMIT
     # global canary indices must fit the 32-bit counter word
