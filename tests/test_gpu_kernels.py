@@ -202,6 +202,40 @@ def test_drift_degenerate_and_empty(gpu):
     assert sc.shape == (2, 0)
 
 
+def test_drift_special_values(gpu):
+    """Non-finite and extreme operands, against the oracle: fp16 infinities
+    and NaNs in h, an infinite reference element, fp16 subnormals (tiny
+    activations, widened exactly), and values at the fp16 limit.  Scores
+    agree bit for bit in class (inf, NaN) and within the drift tolerance
+    otherwise."""
+    torch, cdt = gpu
+    S, C, T, H = 6, 2, 5, 40
+    announce("drift special values")
+    a = inputs.ref_normal((S, C, T, H), seed=21)
+    a[3] *= np.float32(1e-6)                 # tiny: h in the fp16 subnormal range
+    a[4] *= np.float32(6e4 / np.abs(a[4]).max())  # near the fp16 limit
+    h = inputs.live_near(a, seed=22, rel=1e-2)
+    h[0, 0, 1, 3] = 0x7C00                   # +inf
+    h[0, 1, 2, 5] = 0xFC00                   # -inf
+    h[1, 0, 0, 0] = 0x7E00                   # NaN
+    h[2, 1, 4, 39] = 0x7C00
+    a[2, 1, 4, 39] = np.inf                  # inf - inf = NaN
+    a[5, 0, 0, 0] = np.inf                   # infinite reference element
+    sc = cdt.drift_score(to_dev(torch, h).view(torch.float16), to_dev(torch, a))
+    torch.cuda.synchronize()
+    got = sc.cpu().numpy().astype(np.float64)
+    want, _, _ = oracle.drift_score(h, a)
+    np.testing.assert_array_equal(np.isnan(got), np.isnan(want))
+    np.testing.assert_array_equal(np.isposinf(got), np.isposinf(want))
+    fin = np.isfinite(want)
+    assert np.all(np.abs(got[fin] - want[fin]) <= DRIFT_RTOL * np.abs(want[fin]))
+    # the planted cases ([C][S]): +inf and -inf in h give +inf; NaN in h,
+    # inf - inf, and an infinite reference (D and R both infinite) give NaN
+    assert np.isposinf(want[0, 0]) and np.isposinf(want[1, 0])
+    assert np.isnan(want[0, 1]) and np.isnan(want[1, 2]) and np.isnan(want[0, 5])
+    assert np.all(np.isfinite(want[:, 3:5]))  # subnormal and near-limit blocks
+
+
 def test_drift_deterministic(gpu):
     """No atomics: two runs give bitwise-equal scores and sums."""
     torch, cdt = gpu
