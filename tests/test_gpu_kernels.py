@@ -236,6 +236,40 @@ def test_drift_special_values(gpu):
     assert np.all(np.isfinite(want[:, 3:5]))  # subnormal and near-limit blocks
 
 
+@pytest.mark.parametrize("kw", [dict(sigma_b=1e-2), dict(benign_mode=1, sigma_b=1e-2),
+                                dict(sigma_b=1e-2, tamper=7, eps=0.05, flip_p=0.5, scale=1.5)],
+                         ids=["elementwise", "block", "mixed_tamper"])
+def test_canary_sim_special_references(gpu, kw):
+    """References holding infinities, NaNs, values beyond the fp16 range and
+    fp32 subnormals go through the live pass as the oracle takes them: every
+    output that is a number or an infinity matches bit for bit, NaNs match
+    as NaNs."""
+    torch, cdt = gpu
+    S, C, T, H = 4, 2, 3, 64
+    announce(f"canary_sim special references {kw}")
+    kw = dict(kw)
+    eps = kw.pop("eps", 0.0)
+    ref = inputs.ref_normal((S, C, T, H), seed=31)
+    flat = ref.reshape(-1)
+    specials = [np.inf, -np.inf, np.nan, 1e30, -7e4, 65519.0, 1e-40, -1e-45, 0.0, -0.0]
+    flat[:: 97][: len(specials)] = np.array(specials, np.float32)
+    ref[S // 2, 1, 2, :8] = np.float32(1e6)     # a whole row beyond fp16 on the tampered shard
+    q, m = oracle.ref_stats(ref)
+    ts, bs = oracle.block_scales(T, H, q, m, eps, kw.get("sigma_b", 0.0))
+    mal = 1 << (S // 2)
+    h = cdt.canary_sim(to_dev(torch, ref), seed=4, cfg_id=2, mal_mask=mal,
+                       bscale=to_dev(torch, bs), tscale=to_dev(torch, ts), **kw)
+    torch.cuda.synchronize()
+    got = h_bits(h)
+    want = oracle.canary_sim(ref, seed=4, cfg_id=2, mal_mask=mal, bscale=bs, tscale=ts, **kw)
+    nan_g = (got & 0x7C00) == 0x7C00
+    nan_g &= (got & 0x3FF) != 0
+    nan_w = ((want & 0x7C00) == 0x7C00) & ((want & 0x3FF) != 0)
+    np.testing.assert_array_equal(nan_g, nan_w)
+    np.testing.assert_array_equal(got[~nan_w], want[~nan_w])
+    assert nan_w.any() and np.any(want == 0x7C00)  # the specials reached the output
+
+
 def test_drift_deterministic(gpu):
     """No atomics: two runs give bitwise-equal scores and sums."""
     torch, cdt = gpu
