@@ -132,4 +132,41 @@ __device__ __forceinline__ unsigned long long wave_sum(unsigned long long v) {
     return v;
 }
 
+// Reading the fp32 reference of one wave's 64 groups of 8 elements (512
+// elements, 2 KB).  One 16-byte load per group and thread (lane L: quads
+// 2L and 2L + 1 of the wave's 128 four-element quads) makes each load
+// instruction touch every other 16 bytes of the 2 KB span, and such a
+// stream runs a few percent below contiguous runs.  So lane L loads quads
+// L and 64 + L instead (two contiguous 1 KB runs), and quads_to_groups
+// moves them to their owners in two steps:
+//   1. neighbours 2m and 2m + 1 swap one quad (DPP quad_perm [1, 0, 3, 2]):
+//      lane 2m then holds quads 2m, 2m + 1 and lane 2m + 1 holds 64 + 2m,
+//      65 + 2m;
+//   2. lane L pulls both quads from lane 2L (L < 32) or 2L - 63 (L >= 32)
+//      (ds_bpermute).
+// The values each thread ends with are exactly those of the direct loads.
+// Every lane of the wave must execute it: callers branch on a
+// workgroup-uniform condition.
+__device__ __forceinline__ float swap_adjacent_lanes(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float pull_from_lane(int src_lane, float x) {
+    return __int_as_float(__builtin_amdgcn_ds_bpermute(src_lane * 4, __float_as_int(x)));
+}
+
+// r0, r1: quads L and 64 + L (as loaded); lo, hi: quads 2L and 2L + 1.
+__device__ __forceinline__ void quads_to_groups(const f32x4& r0, const f32x4& r1, f32x4& lo,
+                                                f32x4& hi) {
+    const int lane = static_cast<int>(threadIdx.x % kWave);
+    const bool even = (lane & 1) == 0;
+    const int src = ((lane << 1) & (kWave - 1)) | (lane >> 5);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const float got = swap_adjacent_lanes(even ? r1[k] : r0[k]);
+        lo[k] = pull_from_lane(src, even ? r0[k] : got);
+        hi[k] = pull_from_lane(src, even ? got : r1[k]);
+    }
+}
+
 }  // namespace cdt

@@ -15,10 +15,11 @@
 
 namespace cdt {
 
-// On the 16 x 256 x 256 x 8192 stream, 512 threads with four 8-element
-// groups in flight each (85.7% of the HBM peak) tie 1024 x 2 (85.5%) and
-// beat 256 x 4 (84%) and 1024 x 4 (80%); the fused live-pass-and-score
-// kernel, which shares this thread-to-group mapping, runs 6% faster at 512.
+// On the 16 x 256 x 256 x 8192 stream with one 16-byte load per group and
+// thread, 512 threads with four 8-element groups in flight each (85.7% of
+// the HBM peak) tie 1024 x 2 (85.5%) and beat 256 x 4 (84%) and 1024 x 4
+// (80%); the fused live-pass-and-score kernel, which shares this
+// thread-to-group mapping, runs 6% faster at 512.
 constexpr int kReduceThreads = 512;
 constexpr int kReduceUnroll = 4;
 constexpr uint64_t kReduceChunkElems = 32768;

@@ -9,6 +9,9 @@
 //   * each thread streams groups of 8 elements (one 16-byte h load, two
 //     16-byte a loads), kReduceUnroll groups in flight before any use; the
 //     loads are nontemporal (read once, no reuse);
+//   * an fp32 reference is read so that each load instruction covers one
+//     contiguous 1 KB run per wave, then moved across lanes to the thread
+//     that owns the elements (quads_to_groups);
 //   * chunks are handed out so that each XCD streams one contiguous range;
 //   * the squares are accumulated in fp64 from the exactly widened operands
 //     (h - a is exact in fp64), so the partial sums carry no cancellation;
@@ -51,6 +54,23 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
         for (uint32_t base = g0; base < g_end; base += kReduceThreads * kReduceUnroll) {
             u32x4 hv[kReduceUnroll], rv[kReduceUnroll];
             f32x4 a0[kReduceUnroll], a1[kReduceUnroll];
+            if (!Tr::kHalfRef && base + kReduceThreads * kReduceUnroll <= g_end) {
+                // every group of the step is in range (workgroup-uniform)
+                const uint32_t lane = threadIdx.x % kWave, wave0 = threadIdx.x - lane;
+#pragma unroll
+                for (int u = 0; u < kReduceUnroll; ++u) {
+                    const uint32_t g = base + u * kReduceThreads + threadIdx.x;
+                    const f32x4* aw = ab + 2 * (base + u * kReduceThreads + wave0);
+                    hv[u] = __builtin_nontemporal_load(hb + g);
+                    rv[u] = u32x4{0u, 0u, 0u, 0u};
+                    quads_to_groups(__builtin_nontemporal_load(aw + lane),
+                                    __builtin_nontemporal_load(aw + kWave + lane), a0[u], a1[u]);
+                }
+#pragma unroll
+                for (int u = 0; u < kReduceUnroll; ++u)
+                    accumulate8<kM>(hv[u], rv[u], a0[u], a1[u], acc);
+                continue;
+            }
 #pragma unroll
             for (int u = 0; u < kReduceUnroll; ++u) {
                 const uint32_t g = base + u * kReduceThreads + threadIdx.x;
