@@ -15,13 +15,15 @@
 
 namespace cdt {
 
-// On the 16 x 256 x 256 x 8192 stream with one 16-byte load per group and
-// thread, 512 threads with four 8-element groups in flight each (85.7% of
-// the HBM peak) tie 1024 x 2 (85.5%) and beat 256 x 4 (84%) and 1024 x 4
-// (80%); the fused live-pass-and-score kernel, which shares this
-// thread-to-group mapping, runs 6% faster at 512.
-constexpr int kReduceThreads = 512;
-constexpr int kReduceUnroll = 4;
+// Threads per workgroup and 8-element groups in flight per thread.  On the
+// 16 x 256 x 256 x 8192 stream, with the fp32 reference read in contiguous
+// runs, 256 x 8 reaches 89.4-89.6% of the HBM peak against 87.3-88.1% for
+// 512 x 4, 89.1-89.3% for 256 x 4 and 89.8-90.2% for 256 x 16 and 128 x 16;
+// over the 216-configuration sweep's smaller blocks 256 x 8 is the fastest
+// of these, and the fused live-pass-and-score kernel, which shares this
+// thread-to-group mapping, runs 3-4% faster than at 512 x 4.
+constexpr int kReduceThreads = 256;
+constexpr int kReduceUnroll = 8;
 constexpr uint64_t kReduceChunkElems = 32768;
 
 inline uint64_t reduce_chunks_per_block(uint64_t n) {
