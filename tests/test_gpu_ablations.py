@@ -13,7 +13,8 @@ from tests.gpu_util import announce, h_bits, rel_err, require_gpu, to_dev
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(4, 8, 16, 256), (3, 5, 7, 264), (2, 3, 41, 1000), (5, 2, 1, 8), (1, 1, 130, 8192)]
+SHAPES = [(4, 8, 16, 256), (3, 5, 7, 264), (2, 3, 41, 1000), (5, 2, 1, 8), (1, 1, 130, 8192),
+          (2, 3, 5, 4800)]
 DRIFT_RTOL = 1e-5
 
 

@@ -8,7 +8,8 @@ from tests.gpu_util import announce, h_bits, rel_err, require_gpu, to_dev
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(4, 8, 16, 256), (3, 5, 7, 264), (2, 3, 41, 1000), (5, 2, 1, 8), (1, 1, 130, 8192)]
+SHAPES = [(4, 8, 16, 256), (3, 5, 7, 264), (2, 3, 41, 1000), (5, 2, 1, 8), (1, 1, 130, 8192),
+          (2, 3, 5, 4800), (1, 2, 9, 8000)]
 CASES = {
     "gauss_add": dict(sigma_b=1e-3, tamper=1, eps=0.05),
     "t3_flip": dict(benign_dist=1, sigma_b=2e-2, tamper=2, flip_p=0.3),

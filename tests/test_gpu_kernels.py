@@ -146,7 +146,15 @@ def test_canary_sim(gpu, case, shape):
 # ----------------------------------------------------------------------------
 # Eq. 4
 # ----------------------------------------------------------------------------
-@pytest.mark.parametrize("shape", SHAPES + [(16, 4, 4, 32768)])
+# Blocks of 3000 and 9000 eight-element groups: a workgroup step of 2048
+# groups that is whole, then one that is partial, inside one chunk; and two
+# whole chunks followed by a chunk shorter than one step.  The whole steps
+# read the fp32 reference in contiguous runs and exchange quads across lanes;
+# the partial ones read it directly.
+EXCHANGE_TAIL_SHAPES = [(2, 3, 5, 4800), (1, 2, 9, 8000)]
+
+
+@pytest.mark.parametrize("shape", SHAPES + [(16, 4, 4, 32768)] + EXCHANGE_TAIL_SHAPES)
 def test_drift_score(gpu, shape):
     torch, cdt = gpu
     S, C, T, H = shape
