@@ -13,10 +13,13 @@ namespace cdt {
 // Elementwise kernels: a thread owns groups of 8 consecutive elements (one
 // 16-byte fp16 vector, two 16-byte fp32 vectors); a 1024-thread workgroup
 // covers kGenItems groups per thread of one block per chunk.  On the
-// 16 x 256 x 256 x 8192 live pass 1024 x 2 with the XCD-contiguous chunk
-// order measured ~3% faster than 256 x 4 (10.0 ms against 10.3 ms).
+// 16 x 256 x 256 x 8192 live pass, with the XCD-contiguous chunk order,
+// 1024 x 8 runs 9.8 ms against 10.1 ms for 1024 x 2, 9.9 ms for 1024 x 16,
+// 10.1 ms for 1024 x 32 and 10.2-10.3 ms for 256 x 2..8 (the next group's
+// reference is always loaded before the current one is generated, so only
+// the first load of a chunk is exposed).
 constexpr int kGenThreads = 1024;
-constexpr int kGenItems = 2;
+constexpr int kGenItems = 8;
 constexpr uint32_t kGenChunkGroups = kGenThreads * kGenItems;
 
 struct SimLaunch {
