@@ -781,7 +781,7 @@ def cpu_baseline(W, args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus above 1 is not supported"}))
+        print(json.dumps({"error": "the detector runs on one GPU per process; --gpus above 1 is not supported (the split by canary across GPUs is designed, not implemented)"}))
         sys.exit(2)
     import torch
 
