@@ -17,8 +17,11 @@ Prints one JSON line:
   roofline       the drift kernel alone against the 8 TB/s HBM peak, with
                  the HBM traffic of the committed counter pass;
   canary_sim, fused_step
-                 the live pass's own rate; the step with the live pass and
-                 Eq. 4 fused into one launch per run;
+                 the live pass's own rate, its share of the step and its
+                 vector-ALU load from the committed counter pass (it takes
+                 more of the step than drift_score, but stands in for the
+                 activations that the pipeline's stages deliver); the step
+                 with the live pass and Eq. 4 fused into one launch per run;
   ablation_kernels, table1, substudies
                  the reference conditions and ablations of Sections 4.4-4.5,
                  Table 1's structure on the paper's shape, the propagation
@@ -48,31 +51,50 @@ SIM_BYTES_PER_ELEM = 6        # fp32 a read + fp16 h written
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "drift_score_llama70b_hbm_traffic.md")
 DRIFT_SOURCES = ("drift.hip", "cdt_reduce.hpp", "cdt_device.hpp")
+VALU_FILE = os.path.join(ROOT, "profiles", "llama70b_valu_busy.md")
+SIM_SOURCES = ("generate.hip", "cdt_sim.hpp", "cdt_launch.hpp", "cdt_device.hpp")
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def _profile_fields(path, prefix, sources, workload):
+    """The machine-readable `prefix*: value` lines of a committed rocprofv3
+    summary, or None if it covers another workload or other kernel sources
+    (its `<prefix>source_sha256` must match the sources as they are now)."""
+    import hashlib
+    if workload != "llama70b" or not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.startswith(prefix):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for f in sources:
+        with open(os.path.join(ROOT, "paper_2607_19490_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    if fields.get(prefix + "source_sha256") != h.hexdigest():
+        return None
+    return fields
+
+
 def measured_traffic(workload):
     """HBM bytes per drift_score launch from the committed rocprofv3 FETCH_SIZE
     and WRITE_SIZE passes (scaled by a plain copy of known size), or None if
     they were taken on another workload or on different kernel sources."""
-    import hashlib
-    if workload != "llama70b" or not os.path.exists(TRAFFIC_FILE):
-        return None
-    fields = {}
-    for line in open(TRAFFIC_FILE):
-        if ":" in line and line.startswith("drift_score_"):
-            k, v = line.split(":", 1)
-            fields[k.strip()] = v.strip()
-    h = hashlib.sha256()
-    for f in DRIFT_SOURCES:
-        with open(os.path.join(ROOT, "paper_2607_19490_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    if fields.get("drift_score_source_sha256") != h.hexdigest():
-        return None
-    return int(fields["drift_score_traffic_bytes_per_launch"])
+    f = _profile_fields(TRAFFIC_FILE, "drift_score_", DRIFT_SOURCES, workload)
+    return None if f is None else int(f["drift_score_traffic_bytes_per_launch"])
+
+
+def measured_valu(workload):
+    """canary_sim's VALUBusy share and VALU instructions per element from the
+    committed rocprofv3 counter pass, or (None, None) as above."""
+    f = _profile_fields(VALU_FILE, "canary_sim_", SIM_SOURCES, workload)
+    if f is None:
+        return None, None
+    return float(f["canary_sim_valu_busy"]), float(f["canary_sim_valu_per_element"])
 
 
 def parse():
@@ -226,6 +248,7 @@ def run_main(torch, cdt, W, args):
     sim_avg = sum(big_sim) / len(big_sim)
     achieved = per_launch / (drift_avg * 1e-3) / 1e9
     sim_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (sim_avg * 1e-3) / 1e9
+    valu_busy, valu_per_el = measured_valu(wl.name)
 
     res = {
         "metric": "drift-scored activation GB/s",
@@ -262,6 +285,11 @@ def run_main(torch, cdt, W, args):
             "avg_launch_ms": round(sim_avg, 4),
             "GBps": round(sim_gbps, 1),
             "frac_of_hbm_peak": round(sim_gbps / HBM_PEAK_GBPS, 4),
+            "share_of_step": round(sim_avg * len(big.rs.runs) / ms_step, 4)
+            if len(preps) == 1 else None,
+            "bound": "valu+hbm",
+            "valu_busy": valu_busy,
+            "valu_instr_per_element": valu_per_el,
         },
     }
     c = cdt.u64(counts)
