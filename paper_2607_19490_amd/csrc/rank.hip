@@ -3,9 +3,10 @@
 //
 // Per-canary counts: one workgroup per configuration; each wave takes one
 // canary at a time with lane s holding shard s's score as an order key
-// (S <= 64 = one wave).  Every positive lane compares itself with every
-// negative shard through wave shuffles; integer counts are summed over waves
-// in a fixed order.
+// (S <= 64 = one wave), and loads its next canary's scores before ranking
+// the current one.  Every positive lane compares itself with every negative
+// shard through wave shuffles; integer counts are summed over waves in a
+// fixed order.
 //
 // Pooled Mann-Whitney: one 1024-thread workgroup per configuration sorts the
 // C*S (key, label) pairs with an LDS bitonic network, scans the negatives in
@@ -17,7 +18,9 @@
 namespace cdt {
 namespace {
 
-constexpr int kCountThreads = 256;
+// 16 waves per configuration: on 256 canaries (one 70B-shaped run) each wave
+// walks 16 of them instead of 64 at 256 threads.
+constexpr int kCountThreads = 1024;
 constexpr int kCountWaves = kCountThreads / kWave;
 constexpr int kPoolThreads = 1024;
 constexpr uint32_t kPoolMax = 16384;
@@ -76,9 +79,13 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
     const uint32_t tag_random = stream_tag(kStreamRandom, cfg.cfg_id);
 
     unsigned long long g = 0, e = 0, gc = 0, ec = 0, gr = 0, er = 0;
+    const float* base = scores + cfg.score_off;
+    float next = (wave < cfg.C && lane_in) ? base[static_cast<uint64_t>(wave) * cfg.S + lane] : 0.f;
     for (uint32_t t = wave; t < cfg.C; t += kCountWaves) {
-        const float* row = scores + cfg.score_off + static_cast<uint64_t>(t) * cfg.S;
-        const uint32_t k = lane_in ? order_key(row[lane]) : 0u;
+        const float cur = next;
+        const uint32_t tn = t + kCountWaves;
+        if (tn < cfg.C && lane_in) next = base[static_cast<uint64_t>(tn) * cfg.S + lane];
+        const uint32_t k = lane_in ? order_key(cur) : 0u;
         for (uint32_t j = 0; j < cfg.S; ++j) {
             const uint32_t kj = __shfl(k, j, kWave);
             if (lane_pos && ((neg >> j) & 1u)) {
