@@ -15,7 +15,9 @@ Prints one JSON line:
   value          drift-scored activation bytes (2 B fp16 + 4 B fp32 per
                  element, each read once) per second of the whole step;
   roofline       the drift kernel alone against the 8 TB/s HBM peak, with
-                 the HBM traffic of the committed counter pass;
+                 the HBM traffic of the committed counter pass, and against
+                 a compute-free read of the same bytes in the same access
+                 pattern (cdt_drift_read_stream, timed after the steps);
   canary_sim, fused_step
                  the live pass's own rate, its share of the step and its
                  vector-ALU load from the committed counter pass (it takes
@@ -249,6 +251,10 @@ def run_main(torch, cdt, W, args):
     achieved = per_launch / (drift_avg * 1e-3) / 1e9
     sim_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (sim_avg * 1e-3) / 1e9
     valu_busy, valu_per_el = measured_valu(wl.name)
+    # The same reads with no arithmetic (after the timed region): what the
+    # memory system gives the drift kernel's access pattern.
+    read_ms = time_ms(torch, lambda: cdt.drift_read_stream(big.h, big.ref, ws=big.ws), 7)
+    read_gbps = big.rs.elems * DRIFT_BYTES_PER_ELEM / (read_ms * 1e-3) / 1e9
 
     res = {
         "metric": "drift-scored activation GB/s",
@@ -280,6 +286,8 @@ def run_main(torch, cdt, W, args):
             "traffic": measured_traffic(wl.name),
             "bytes_per_launch": per_launch,
             "avg_launch_ms": round(drift_avg, 4),
+            "read_stream_GBps": round(read_gbps, 1),
+            "frac_of_read_stream": round(achieved / read_gbps, 4),
         },
         "canary_sim": {
             "avg_launch_ms": round(sim_avg, 4),

@@ -223,6 +223,15 @@ int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16
                     const float* ref, float* score, double* num_den, void* ws, size_t ws_bytes,
                     void* stream);
 
+/* Measurement aid for Eq. 4's memory bound: reads h and ref exactly as
+ * cdt_drift_score does (the same chunks, loads, lane exchange and order)
+ * and computes nothing from them, so its rate is what the memory system
+ * delivers for the drift kernel's access pattern.  Produces no result: ws
+ * (cdt_reduce_workspace_bytes bytes, 16-byte aligned) may be overwritten.
+ * Errors as cdt_drift_score. */
+int cdt_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                          const float* ref, void* ws, size_t ws_bytes, void* stream);
+
 /* Relative-L2 mismatch against an fp16 reference r (Eq. 4 with the stored
  * fp32 reference replaced by a second live pass, Section 4.5: the
  * noisy-reference ablation and the redundant-recompute ceiling):

@@ -80,6 +80,7 @@ _SIGS = {
     "cdt_sim_score": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp, _vp, _vp,
                        _sz, _vp], ctypes.c_int),
     "cdt_drift_score": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "cdt_drift_read_stream": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
     "cdt_drift_score_f16ref": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
                                ctypes.c_int),
     "cdt_cosine_score": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
@@ -315,6 +316,18 @@ def _drift(fn, h, ref, ref_dtype, out, sums, nsums, ws):
 def drift_score(h, ref, out=None, num_den=None, ws=None):
     """Eq. 4 per block -> scores [C][S] fp32 (and optional [C][S][2] fp64)."""
     return _drift(lib().cdt_drift_score, h, ref, _torch().float32, out, num_den, 2, ws)
+
+
+def drift_read_stream(h, ref, ws=None):
+    """drift_score's reads of h and ref with no arithmetic (a measurement of
+    the memory bound of Eq. 4's access pattern); returns nothing."""
+    torch = _torch()
+    _need(h, "h", torch.float16)
+    S, C, T, H = h.shape
+    _need(ref, "ref", torch.float32, (S, C, T, H))
+    ws, nbytes = _ws_arg(ws, S, C, T, H, h)
+    _check(lib().cdt_drift_read_stream(S, C, T, H, _ptr(h), _ptr(ref), _ptr(ws), nbytes,
+                                       _stream()))
 
 
 def drift_score_f16ref(h, r, out=None, num_den=None, ws=None):

@@ -311,6 +311,25 @@ int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16
                         num_den, ws, ws_bytes, stream);
 }
 
+int cdt_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                          const float* ref, void* ws, size_t ws_bytes, void* stream) {
+    const char* fn = "cdt_drift_read_stream";
+    int rc = check_shape(fn, S, C, T, H);
+    if (rc) return rc;
+    if (static_cast<uint64_t>(S) * C * T * H == 0) return ok();
+    if (!h || !ref) return fail(CDT_EINVAL, "%s: NULL array", fn);
+    if (!aligned16(h) || !aligned16(ref))
+        return fail(CDT_EALIGN, "%s: arrays must be 16-byte aligned", fn);
+    const size_t need = cdt_reduce_workspace_bytes(S, C, T, H);
+    if (!ws || ws_bytes < need)
+        return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                    ws ? ws_bytes : 0);
+    if (!aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
+    return device_status(cdt::launch_drift_read_stream(S, C, T, H, h, ref, ws,
+                                                       static_cast<hipStream_t>(stream)),
+                         fn);
+}
+
 int cdt_drift_score_f16ref(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
                            const uint16_t* r, float* score, double* num_den, void* ws,
                            size_t ws_bytes, void* stream) {

@@ -65,6 +65,11 @@ hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, 
                         const uint16_t* h, const void* ref, float* score, double* sums, void* ws,
                         hipStream_t st);
 
+// drift_score's reads (same chunks, loads and order) with no arithmetic; ws
+// is drift_score's workspace and may be overwritten.
+hipError_t launch_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                                   const uint16_t* h, const float* ref, void* ws, hipStream_t st);
+
 // The combine step alone, over partial sums laid out as drift_score's.
 hipError_t launch_drift_combine(DriftMetric metric, const double* partial, uint64_t cpb,
                                 uint64_t nblocks, uint32_t S, uint32_t C, float* score,

@@ -30,7 +30,22 @@
 namespace cdt {
 namespace {
 
-template <DriftMetric kM>
+// XOR of every word a thread loaded; a value no load pattern is meant to
+// produce selects the (practically never taken) store that keeps the loads.
+constexpr uint32_t kFoldSentinel = 0x7F3A5C91u;
+
+__device__ __forceinline__ uint32_t fold_group(const u32x4& hv, const u32x4& rv, const f32x4& a0,
+                                               const f32x4& a1) {
+    uint32_t x = hv.x ^ hv.y ^ hv.z ^ hv.w ^ rv.x ^ rv.y ^ rv.z ^ rv.w;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) x ^= __float_as_uint(a0[k]) ^ __float_as_uint(a1[k]);
+    return x;
+}
+
+// kReadOnly: the same chunks, loads and lane exchange with Eq. 4's
+// arithmetic replaced by an XOR fold of the loaded words: the rate the memory
+// system gives this access pattern, against which the drift kernel is judged.
+template <DriftMetric kM, bool kReadOnly = false>
 __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
     const uint16_t* __restrict__ h, const void* __restrict__ ref, uint32_t n8,
     uint64_t chunks_per_block, uint64_t total_chunks, double* __restrict__ partial) {
@@ -51,6 +66,7 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
         double acc[Tr::kSums];
 #pragma unroll
         for (int k = 0; k < Tr::kSums; ++k) acc[k] = 0.0;
+        uint32_t fold = 0;
         for (uint32_t base = g0; base < g_end; base += kReduceThreads * kReduceUnroll) {
             u32x4 hv[kReduceUnroll], rv[kReduceUnroll];
             f32x4 a0[kReduceUnroll], a1[kReduceUnroll];
@@ -67,8 +83,12 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
                                     __builtin_nontemporal_load(aw + kWave + lane), a0[u], a1[u]);
                 }
 #pragma unroll
-                for (int u = 0; u < kReduceUnroll; ++u)
-                    accumulate8<kM>(hv[u], rv[u], a0[u], a1[u], acc);
+                for (int u = 0; u < kReduceUnroll; ++u) {
+                    if constexpr (kReadOnly)
+                        fold ^= fold_group(hv[u], rv[u], a0[u], a1[u]);
+                    else
+                        accumulate8<kM>(hv[u], rv[u], a0[u], a1[u], acc);
+                }
                 continue;
             }
 #pragma unroll
@@ -89,12 +109,21 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
                 }
             }
 #pragma unroll
-            for (int u = 0; u < kReduceUnroll; ++u) accumulate8<kM>(hv[u], rv[u], a0[u], a1[u], acc);
+            for (int u = 0; u < kReduceUnroll; ++u) {
+                if constexpr (kReadOnly)
+                    fold ^= fold_group(hv[u], rv[u], a0[u], a1[u]);
+                else
+                    accumulate8<kM>(hv[u], rv[u], a0[u], a1[u], acc);
+            }
         }
-        block_sum<Tr::kSums>(acc);
-        if (threadIdx.x == 0) {
+        if constexpr (kReadOnly) {
+            if (fold == kFoldSentinel) partial[chunk * Tr::kSums] = static_cast<double>(fold);
+        } else {
+            block_sum<Tr::kSums>(acc);
+            if (threadIdx.x == 0) {
 #pragma unroll
-            for (int k = 0; k < Tr::kSums; ++k) partial[chunk * Tr::kSums + k] = acc[k];
+                for (int k = 0; k < Tr::kSums; ++k) partial[chunk * Tr::kSums + k] = acc[k];
+            }
         }
     }
 }
@@ -173,6 +202,17 @@ hipError_t launch_drift_t(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const 
         if (e != hipSuccess) return e;
     }
     return launch_combine_t<kM>(partial, cpb, nblocks, S, C, score, sums, st);
+}
+
+hipError_t launch_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                                   const uint16_t* h, const float* ref, void* ws, hipStream_t st) {
+    const uint64_t n = static_cast<uint64_t>(T) * H;
+    const uint64_t total = reduce_chunks_per_block(n) * S * C;
+    if (total == 0) return hipSuccess;
+    hipLaunchKernelGGL((drift_partial_kernel<DriftMetric::kL2, true>), dim3(reduce_grid(total)),
+                       dim3(kReduceThreads), 0, st, h, ref, static_cast<uint32_t>(n / 8),
+                       reduce_chunks_per_block(n), total, static_cast<double*>(ws));
+    return hipGetLastError();
 }
 
 hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, uint32_t H,

@@ -86,6 +86,16 @@ def test_shape_and_pointer_validation(cdt):
         assert fn(2, 2, 3, 16, 8, 16, 16, None, 16, 1 << 20, None) == cdt.EALIGN
         assert fn(2, 2, 3, 16, 16, 16, 16, None, 16, 15, None) == cdt.EINVAL
         assert fn(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
+    # the compute-free read of Eq. 4's stream checks its arguments the same way
+    rs = L.cdt_drift_read_stream
+    assert rs(2, 2, 3, 12, None, None, None, 0, None) == cdt.EINVAL
+    assert rs(2, 2, 3, 16, None, 16, 16, 1 << 20, None) == cdt.EINVAL
+    assert rs(2, 2, 3, 16, 8, 16, 16, 1 << 20, None) == cdt.EALIGN
+    assert rs(2, 2, 3, 16, 16, 16, 16, 15, None) == cdt.EINVAL
+    assert "workspace" in _err(cdt)
+    assert rs(2, 2, 3, 16, 16, 16, 24, 1 << 20, None) == cdt.EALIGN
+    assert rs(2, 2, 0, 16, None, None, None, 0, None) == cdt.OK
+    assert rs(1 << 16, 1 << 16, 1 << 10, 8, 16, 16, 16, 1 << 20, None) == cdt.ELIMIT
     # empty shapes are accepted without touching the device
     assert L.cdt_drift_score(0, 2, 3, 16, None, None, None, None, None, 0, None) == cdt.OK
     # block count and total size limits (sizes derived from the shape stay exact)

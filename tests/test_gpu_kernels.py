@@ -172,6 +172,27 @@ def test_drift_score(gpu, shape):
     assert ulp_diff_f32(sc.cpu().numpy(), s32).max() <= 1
 
 
+@pytest.mark.parametrize("shape", [(4, 8, 16, 256)] + EXCHANGE_TAIL_SHAPES)
+def test_drift_read_stream(gpu, shape):
+    """The compute-free read of Eq. 4's stream runs on ragged shapes, leaves
+    its inputs untouched, and a drift_score after it (same workspace) still
+    matches the oracle."""
+    torch, cdt = gpu
+    S, C, T, H = shape
+    announce(f"drift_read_stream {shape}")
+    a = inputs.ref_normal(shape, seed=11, outlier_frac=0.01)
+    h = inputs.live_near(a, seed=12, rel=1e-3, flip_frac=0.001)
+    h_d, a_d = to_dev(torch, h).view(torch.float16), to_dev(torch, a)
+    ws = cdt.workspace(S, C, T, H, a_d)
+    cdt.drift_read_stream(h_d, a_d, ws=ws)
+    sc = cdt.drift_score(h_d, a_d, ws=ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(h_d.view(torch.int16).cpu().numpy().view(np.uint16), h)
+    assert np.array_equal(a_d.cpu().numpy(), a)
+    s64, _, _ = oracle.drift_score(h, a)
+    assert rel_err(sc.cpu().numpy(), s64) < DRIFT_RTOL
+
+
 def test_drift_exact_special_cases(gpu):
     """h = a gives 0, h = -a gives 2, h = 2a gives 1, h = 0 gives 1, exactly."""
     torch, cdt = gpu
