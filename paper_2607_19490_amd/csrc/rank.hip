@@ -9,9 +9,13 @@
 // fixed order.
 //
 // Pooled Mann-Whitney: one 1024-thread workgroup per configuration sorts the
-// C*S (key, label) pairs with an LDS bitonic network, scans the negatives in
+// C*S (key, label) pairs with a bitonic network, scans the negatives in
 // sorted order, and for each positive binary-searches its tie group: it beats
-// the negatives before the group and ties those inside it.
+// the negatives before the group and ties those inside it.  Each thread holds
+// E = max(1, P2 / 1024) consecutive elements of the padded length P2 in
+// registers: compare-exchange stages between elements of one thread run in
+// registers, stages between threads of one wave through lane shuffles, and
+// only the stages that span waves go through LDS, with one barrier each.
 #include "cdt_device.hpp"
 #include "cdt_launch.hpp"
 
@@ -149,6 +153,89 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
     }
 }
 
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int m) {
+    const int lo = __shfl_xor(static_cast<int>(static_cast<uint32_t>(x)), m, kWave);
+    const int hi = __shfl_xor(static_cast<int>(static_cast<uint32_t>(x >> 32)), m, kWave);
+    return (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo);
+}
+
+// Ascending bitonic sort of P2 (a power of two, <= kE * kPoolThreads)
+// elements, thread t holding elements t*kE .. t*kE + kE - 1 in x; v is LDS
+// scratch of P2 elements.  Every thread of the workgroup must call it.
+template <int kE>
+__device__ __forceinline__ void bitonic_sort_regs(uint64_t (&x)[kE], uint32_t P2, uint64_t* v) {
+    const uint32_t t = threadIdx.x, base = t * kE;
+    for (uint32_t k = 2; k <= P2; k <<= 1) {
+        uint32_t j = k >> 1;
+        if (j >= kWave * kE) {  // partners in other waves: in place in LDS
+#pragma unroll
+            for (int r = 0; r < kE; ++r)
+                if (base + r < P2) v[base + r] = x[r];
+            __syncthreads();
+            for (; j >= kWave * kE; j >>= 1) {
+                for (uint32_t p = t; p < P2 / 2; p += kPoolThreads) {
+                    const uint32_t i = 2 * p - (p & (j - 1));
+                    const uint32_t l = i + j;
+                    const uint64_t a = v[i], b = v[l];
+                    if ((a > b) == ((i & k) == 0)) {
+                        v[i] = b;
+                        v[l] = a;
+                    }
+                }
+                __syncthreads();
+            }
+#pragma unroll
+            for (int r = 0; r < kE; ++r)
+                if (base + r < P2) x[r] = v[base + r];
+        }
+        for (; j >= static_cast<uint32_t>(kE); j >>= 1) {  // partner lane t ^ (j / kE)
+            const int m = static_cast<int>(j / kE);
+            const bool keep_min = ((t & m) == 0) == ((base & k) == 0);
+#pragma unroll
+            for (int r = 0; r < kE; ++r) {
+                const uint64_t y = shfl_xor_u64(x[r], m);
+                x[r] = keep_min ? (x[r] < y ? x[r] : y) : (x[r] < y ? y : x[r]);
+            }
+        }
+#pragma unroll
+        for (int jj = kE / 2; jj >= 1; jj >>= 1) {  // partner in this thread
+            if (static_cast<uint32_t>(jj) < k) {
+#pragma unroll
+                for (int r = 0; r < kE; ++r) {
+                    const int rp = r ^ jj;
+                    if (rp > r) {
+                        const uint64_t a = x[r], b = x[rp];
+                        if ((a > b) == (((base + r) & k) == 0)) {
+                            x[r] = b;
+                            x[rp] = a;
+                        }
+                    }
+                }
+            }
+        }
+    }
+}
+
+// Loads the configuration's n (key, label) pairs padded to P2, sorts them,
+// and leaves the sorted array in v[0 .. P2).
+template <int kE>
+__device__ void pooled_sort(const float* tab, uint32_t n, uint32_t P2, uint32_t S, uint64_t pos,
+                            uint64_t* v) {
+    uint64_t x[kE];
+    const uint32_t base = threadIdx.x * kE;
+#pragma unroll
+    for (int r = 0; r < kE; ++r) {
+        const uint32_t i = base + r;
+        x[r] = i < n ? (static_cast<uint64_t>(order_key(tab[i])) << 32) | ((pos >> (i % S)) & 1u)
+                     : ~0ull;  // padding sorts last
+    }
+    bitonic_sort_regs<kE>(x, P2, v);
+#pragma unroll
+    for (int r = 0; r < kE; ++r)
+        if (base + r < P2) v[base + r] = x[r];
+    __syncthreads();
+}
+
 // Element layout in the pooled sort: key << 32 | label (label 1 = positive);
 // after the negative scan: key << 32 | negatives_before << 1 | label.
 __global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
@@ -170,31 +257,13 @@ __global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
     const uint64_t pos = cfg.pos_mask & shard_mask(cfg.S);
     const float* tab = scores + cfg.score_off;
 
-    for (uint32_t i = threadIdx.x; i < P2; i += kPoolThreads) {
-        if (i < n) {
-            const uint32_t s = i % cfg.S;
-            v[i] = (static_cast<uint64_t>(order_key(tab[i])) << 32) | ((pos >> s) & 1u);
-        } else {
-            v[i] = ~0ull;  // padding sorts last
-        }
-    }
-    __syncthreads();
-
-    // Bitonic sort, ascending.
-    for (uint32_t k = 2; k <= P2; k <<= 1) {
-        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-            for (uint32_t p = threadIdx.x; p < P2 / 2; p += kPoolThreads) {
-                const uint32_t i = 2 * p - (p & (j - 1));
-                const uint32_t l = i + j;
-                const uint64_t x = v[i], y = v[l];
-                const bool up = (i & k) == 0;
-                if ((x > y) == up) {
-                    v[i] = y;
-                    v[l] = x;
-                }
-            }
-            __syncthreads();
-        }
+    static_assert(kPoolMax == 16 * kPoolThreads, "at most 16 elements per thread");
+    switch (P2 <= kPoolThreads ? 1u : P2 / kPoolThreads) {  // uniform over the workgroup
+        case 1: pooled_sort<1>(tab, n, P2, cfg.S, pos, v); break;
+        case 2: pooled_sort<2>(tab, n, P2, cfg.S, pos, v); break;
+        case 4: pooled_sort<4>(tab, n, P2, cfg.S, pos, v); break;
+        case 8: pooled_sort<8>(tab, n, P2, cfg.S, pos, v); break;
+        default: pooled_sort<16>(tab, n, P2, cfg.S, pos, v); break;
     }
 
     // Exclusive scan of negatives over the sorted order: each thread owns a
