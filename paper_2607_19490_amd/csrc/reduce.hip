@@ -189,22 +189,50 @@ __global__ void tamper_scale_combine_kernel(const double* __restrict__ partial,
 __global__ __launch_bounds__(kReduceThreads) void ref_stats_partial_kernel(
     const float* __restrict__ ref, uint32_t n8, uint64_t chunks_per_block, uint64_t total_chunks,
     double2* __restrict__ partial) {
+    // Same chunking, XCD order and reads as drift_score: kReduceUnroll groups
+    // in flight per thread, the reference in contiguous runs moved to the
+    // owning lanes (quads_to_groups); each thread adds its groups in
+    // ascending order (groups past the block end contribute exact zeros).
     const uint64_t n = static_cast<uint64_t>(n8) * 8;
-    for (uint64_t chunk = blockIdx.x; chunk < total_chunks; chunk += gridDim.x) {
+    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
+        const uint64_t chunk = xcd_contiguous(it, total_chunks);
         const uint64_t b = chunk / chunks_per_block;
         const uint32_t g0 = static_cast<uint32_t>(chunk - b * chunks_per_block) * kChunkGroups;
         const uint32_t g_end = min(g0 + kChunkGroups, n8);
-        const float4* ab = reinterpret_cast<const float4*>(ref + b * n);
+        const f32x4* ab = reinterpret_cast<const f32x4*>(ref + b * n);
         double Q = 0.0, M = 0.0;
-        for (uint32_t g = g0 + threadIdx.x; g < g_end; g += kReduceThreads) {
-            const float4 a0 = ab[2 * g];
-            const float4 a1 = ab[2 * g + 1];
-            const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        for (uint32_t base = g0; base < g_end; base += kReduceThreads * kReduceUnroll) {
+            f32x4 a0[kReduceUnroll], a1[kReduceUnroll];
+            if (base + kReduceThreads * kReduceUnroll <= g_end) {  // workgroup-uniform
+                const uint32_t lane = threadIdx.x % kWave, wave0 = threadIdx.x - lane;
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const double x = static_cast<double>(av[k]);
-                Q = fma(x, x, Q);
-                M += fabs(x);
+                for (int u = 0; u < kReduceUnroll; ++u) {
+                    const f32x4* aw = ab + 2 * (base + u * kReduceThreads + wave0);
+                    quads_to_groups(__builtin_nontemporal_load(aw + lane),
+                                    __builtin_nontemporal_load(aw + kWave + lane), a0[u], a1[u]);
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < kReduceUnroll; ++u) {
+                    const uint32_t g = base + u * kReduceThreads + threadIdx.x;
+                    a0[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    a1[u] = a0[u];
+                    if (g < g_end) {
+                        a0[u] = __builtin_nontemporal_load(ab + 2 * g);
+                        a1[u] = __builtin_nontemporal_load(ab + 2 * g + 1);
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kReduceUnroll; ++u) {
+                const float av[8] = {a0[u].x, a0[u].y, a0[u].z, a0[u].w,
+                                     a1[u].x, a1[u].y, a1[u].z, a1[u].w};
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const double x = static_cast<double>(av[k]);
+                    Q = fma(x, x, Q);
+                    M += fabs(x);
+                }
             }
         }
         double acc[2] = {Q, M};
