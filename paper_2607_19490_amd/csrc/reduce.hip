@@ -73,7 +73,8 @@ struct ReduceWalk {
 // generated and scored (also across chunks), and the register budget is
 // held to 64 (a few spills) so that eight waves share each SIMD.  Per
 // 16 x 256 x 256 x 8192 run: 13.1 ms without the prefetch, 12.4 ms with it,
-// 12.0 ms with the cap (1024-thread groups), 11.4 ms with 512-thread groups.
+// 12.0 ms with the cap (1024-thread groups), 11.4 ms with 512-thread groups,
+// 10.6-11.2 ms with the current 256-thread groups.
 template <bool kT3, bool kBlock, bool kStoreH>
 __global__ __launch_bounds__(kReduceThreads) __attribute__((amdgpu_waves_per_eu(8, 8)))
 void sim_score_partial_kernel(
