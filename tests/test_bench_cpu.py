@@ -40,3 +40,15 @@ def test_valu_figures_are_plausible():
     if busy is not None:
         assert 0.0 < busy <= 1.05
         assert 10.0 < per < 100.0
+
+
+def test_cpu_baseline_fields_on_tiny():
+    """The oracle leg on the tiny workload (CPU only): the fields the
+    benchmark contract names."""
+    import types
+
+    from paper_2607_19490_amd import workloads as W
+    args = types.SimpleNamespace(workload="tiny", cpu_canaries=2)
+    cb = bench.cpu_baseline(W, args)
+    assert cb["kind"] == "oracle" and cb["unit"] == "GB/s" and cb["cores"] >= 1
+    assert cb["value"] > 0 and isinstance(cb["sample"], str) and cb["sample"]
