@@ -68,7 +68,8 @@ extern "C" {
 #define CDT_STREAM_ALT_T12 10
 #define CDT_STREAM_ALT_T3 11
 
-/* Interface version; changes whenever a layout or generator rule changes. */
+/* Interface version; changes whenever a layout, a generator rule or the set
+ * of entry points changes (6: cdt_drift_read_stream added). */
 int cdt_version(void);
 
 /* Description of the last error on the calling thread ("" if none). */

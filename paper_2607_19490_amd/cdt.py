@@ -98,7 +98,7 @@ _LIB = None
 
 # Interface version of include/cdt.h that the structures and signatures
 # below mirror (cdt_version()).
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 
 def lib():
@@ -108,13 +108,14 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"libcdt.so is not built ({LIB_PATH}); run __graft_entry__.build()")
         L = ctypes.CDLL(LIB_PATH)
+        L.cdt_version.argtypes, L.cdt_version.restype = [], ctypes.c_int
+        if L.cdt_version() != ABI_VERSION:  # before binding entry points it may lack
+            raise RuntimeError(f"libcdt.so has interface version {L.cdt_version()}, this binding "
+                               f"expects {ABI_VERSION}; rebuild with __graft_entry__.build()")
         for name, (args, res) in _SIGS.items():
             fn = getattr(L, name)
             fn.argtypes = args
             fn.restype = res
-        if L.cdt_version() != ABI_VERSION:
-            raise RuntimeError(f"libcdt.so has interface version {L.cdt_version()}, this binding "
-                               f"expects {ABI_VERSION}; rebuild with __graft_entry__.build()")
         _LIB = L
     return _LIB
 

@@ -73,7 +73,7 @@ bool canaries_fit(uint32_t canary_base, uint64_t C) {
 
 extern "C" {
 
-int cdt_version(void) { return 5; }
+int cdt_version(void) { return 6; }
 
 const char* cdt_last_error(void) { return g_error; }
 

@@ -22,7 +22,7 @@ int main() {
     void* q = reinterpret_cast<void*>(8);    // misaligned
     float* fp = static_cast<float*>(p);
     uint16_t* hp = static_cast<uint16_t*>(p);
-    expect(cdt_version(), 5, "version");
+    expect(cdt_version(), 6, "version");
     expect(cdt_outlier_gain(40000, 1, 20.f, 0, 0, fp, nullptr), CDT_ELIMIT, "gain H");
     expect(cdt_outlier_gain(16, 17, 20.f, 0, 0, fp, nullptr), CDT_EINVAL, "gain n_out");
     expect(cdt_ref_synth(2, 2, 3, 12, 0, 0, 0, fp, fp, nullptr), CDT_EINVAL, "synth H%8");
@@ -61,6 +61,11 @@ int main() {
                                   1 << 20, nullptr), CDT_EALIGN, "f16ref align");
     expect(cdt_cosine_score(0, 2, 3, 16, nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr),
            CDT_OK, "cosine empty");
+    expect(cdt_drift_read_stream(2, 2, 3, 16, hp, fp, p, 15, nullptr), CDT_EINVAL, "read ws");
+    expect(cdt_drift_read_stream(2, 2, 3, 16, static_cast<uint16_t*>(q), fp, p, 1 << 20, nullptr),
+           CDT_EALIGN, "read align");
+    expect(cdt_drift_read_stream(2, 2, 0, 16, nullptr, nullptr, nullptr, 0, nullptr), CDT_OK,
+           "read empty");
     cdt_auroc_cfg cfgs[2];
     memset(cfgs, 0, sizeof(cfgs));
     cfgs[0].S = 8; cfgs[0].C = 4; cfgs[0].pos_mask = 1;
