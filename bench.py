@@ -617,10 +617,15 @@ def config_runs(torch, cdt, W, name):
         sim_all.append(sim_ms)
     drift_ms = sorted(drift_all)[len(drift_all) // 2]
     sim_ms = sorted(sim_all)[len(sim_all) // 2]
+    # the compute-free read of the same arrays: what a launch of this size gets
+    read_ms = time_ms(torch, lambda: cdt.drift_read_stream(prep.h, prep.ref, ws=prep.ws), 5)
+    read_gbps = rs.elems * DRIFT_BYTES_PER_ELEM / (read_ms * 1e-3) / 1e9
     out = {"shape_SxCxTxH": [rs.S, rs.C, rs.T, rs.H],
            "drift_ms": round(drift_ms, 4),
            "drift_GBps": round(nbytes / (drift_ms * 1e-3) / 1e9, 1),
            "drift_frac_of_hbm_peak": round(nbytes / (drift_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+           "read_stream_GBps": round(read_gbps, 1),
+           "drift_frac_of_read_stream": round(nbytes / (drift_ms * 1e-3) / 1e9 / read_gbps, 4),
            "canary_sim_ms": round(sim_ms, 4),
            "runs": rows}
     del prep, score
