@@ -107,6 +107,15 @@ __device__ __forceinline__ uint16_t to_half_bits(float v) {
     return __builtin_bit_cast(uint16_t, h);
 }
 
+// Two fp32 values -> packed fp16 bits (lo in bits 0-15), the same IEEE
+// round to nearest even as to_half_bits; gfx950 converts the pair with one
+// v_cvt_pk_f16_f32.
+__device__ __forceinline__ uint32_t to_half2_bits(float lo, float hi) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, f16x2));
+}
+
 __device__ __forceinline__ float half_bits_to_float(uint32_t bits16) {
     return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
 }

@@ -147,10 +147,10 @@ __device__ __forceinline__ void tamper8(const SimArgs& A, const SimBlock& B, uin
 
 __device__ __forceinline__ u32x4 pack_half8(const float v[8]) {
     u32x4 o;
-    o.x = to_half_bits(v[0]) | (static_cast<uint32_t>(to_half_bits(v[1])) << 16);
-    o.y = to_half_bits(v[2]) | (static_cast<uint32_t>(to_half_bits(v[3])) << 16);
-    o.z = to_half_bits(v[4]) | (static_cast<uint32_t>(to_half_bits(v[5])) << 16);
-    o.w = to_half_bits(v[6]) | (static_cast<uint32_t>(to_half_bits(v[7])) << 16);
+    o.x = to_half2_bits(v[0], v[1]);
+    o.y = to_half2_bits(v[2], v[3]);
+    o.z = to_half2_bits(v[4], v[5]);
+    o.w = to_half2_bits(v[6], v[7]);
     return o;
 }
 
