@@ -359,6 +359,33 @@ def test_auroc_counts(gpu, flags):
             np.testing.assert_array_equal(got_p[g], want_p, err_msg=f"pooled cfg {g}")
 
 
+# Pooled sizes C*S padded to P2 = 64 .. 16384: every width of the pooled
+# sort (1, 2, 4, 8 and 16 elements per thread), lengths just off a power of
+# two, many positives, ties and NaNs.
+POOLED_CASES = [(7, 9, (3,), dict(tie_levels=4)), (3, 43, (1,), dict(nan_frac=0.05)),
+                (33, 31, (0, 16, 32), dict(gap=0.1)), (5, 205, (2,), dict(tie_levels=7)),
+                (16, 150, (8,), dict(gap=0.02, nan_frac=0.01)),
+                (48, 120, tuple(range(0, 48, 5)), dict(tie_levels=40)),
+                (64, 200, tuple(range(1, 64, 3)), dict(gap=-0.05, tie_levels=100, nan_frac=0.01))]
+
+
+@pytest.mark.parametrize("case", range(len(POOLED_CASES)))
+def test_auroc_pooled_widths(gpu, case):
+    torch, cdt = gpu
+    S, C, pos, kw = POOLED_CASES[case]
+    announce(f"auroc pooled {S}x{C}")
+    t = inputs.scores(C, S, seed=500 + case, mal=pos, **kw)
+    mask = 0
+    for s_ in pos:
+        mask |= 1 << s_
+    counts, pooled, _ = cdt.auroc([(S, C, 0, mask, 7 + case)], to_dev(torch, t.ravel()),
+                                  seed=5, flags=3)
+    torch.cuda.synchronize()
+    want, want_p = oracle.auroc_config(t, mask, seed=5, cfg_id=7 + case, flags=3)
+    np.testing.assert_array_equal(cdt.u64(counts)[0], want)
+    np.testing.assert_array_equal(cdt.u64(pooled)[0], want_p)
+
+
 def test_auroc_pooled_at_capacity(gpu):
     torch, cdt = gpu
     announce("auroc pooled 64x256")
