@@ -21,6 +21,13 @@ DRIFT_RTOL = 1e-5  # tolerance stated for drift scores
 # with a partial last chunk, and single-group blocks
 SHAPES = [(4, 8, 16, 256), (3, 5, 7, 264), (2, 3, 41, 1000), (5, 2, 1, 8), (1, 1, 130, 8192)]
 
+# Blocks of 3000 and 9000 eight-element groups: a workgroup step of 2048
+# groups that is whole, then one that is partial, inside one chunk; and two
+# whole chunks followed by a chunk shorter than one step.  The whole steps
+# read the fp32 reference in contiguous runs and exchange quads across lanes;
+# the partial ones read it directly.
+EXCHANGE_TAIL_SHAPES = [(2, 3, 5, 4800), (1, 2, 9, 8000)]
+
 
 @pytest.fixture(scope="module")
 def gpu():
@@ -87,7 +94,7 @@ def test_fp16_conversion_exhaustive(gpu):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("shape", SHAPES + EXCHANGE_TAIL_SHAPES)
 def test_ref_stats_and_block_scales(gpu, shape):
     torch, cdt = gpu
     S, C, T, H = shape
@@ -146,14 +153,6 @@ def test_canary_sim(gpu, case, shape):
 # ----------------------------------------------------------------------------
 # Eq. 4
 # ----------------------------------------------------------------------------
-# Blocks of 3000 and 9000 eight-element groups: a workgroup step of 2048
-# groups that is whole, then one that is partial, inside one chunk; and two
-# whole chunks followed by a chunk shorter than one step.  The whole steps
-# read the fp32 reference in contiguous runs and exchange quads across lanes;
-# the partial ones read it directly.
-EXCHANGE_TAIL_SHAPES = [(2, 3, 5, 4800), (1, 2, 9, 8000)]
-
-
 @pytest.mark.parametrize("shape", SHAPES + [(16, 4, 4, 32768)] + EXCHANGE_TAIL_SHAPES)
 def test_drift_score(gpu, shape):
     torch, cdt = gpu
