@@ -128,7 +128,7 @@ SIM_CASES = {
 
 
 @pytest.mark.parametrize("case", sorted(SIM_CASES))
-@pytest.mark.parametrize("shape", SHAPES[:3] + [(64, 2, 3, 16)])
+@pytest.mark.parametrize("shape", SHAPES[:3] + [(64, 2, 3, 16), (1, 2, 9, 8000), (1, 1, 130, 8192)])
 def test_canary_sim(gpu, case, shape):
     torch, cdt = gpu
     S, C, T, H = shape
