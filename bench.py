@@ -181,12 +181,13 @@ def gpu_step(torch, cdt, wl, preps, scores, score_views, cfgs, auroc_ws, counts,
             if drift_ev is not None:
                 drift_ev[k][1].record()
             k += 1
-    cdt.auroc(cfgs, scores, seed=wl.seed, flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED,
-              counts=counts, pooled=pooled, ws=auroc_ws)
+    cdt.auroc_launch(auroc_ws, len(cfgs), scores, seed=wl.seed,
+                     flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED, counts=counts, pooled=pooled)
 
 
 def setup_batch(torch, cdt, wl, preps):
-    """Scores slab for every run of the workload plus the batched AUROC table."""
+    """Scores slab for every run of the workload plus the batched AUROC table,
+    validated and uploaded once into auroc_ws (the step only launches)."""
     views, cfgs, off = [], [], 0
     total = sum(p.rs.C * p.rs.S * len(p.rs.runs) for p in preps)
     scores = torch.empty((total,), dtype=torch.float32, device="cuda")
@@ -202,6 +203,7 @@ def setup_batch(torch, cdt, wl, preps):
     pooled = torch.empty((ncfg, 3), dtype=torch.int64, device="cuda")
     auroc_ws = torch.empty((max(16, cdt.lib().cdt_auroc_workspace_bytes(ncfg)),),
                            dtype=torch.uint8, device="cuda")
+    cdt.auroc_upload(cfgs, total, flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED, table=auroc_ws)
     return scores, views, cfgs, counts, pooled, auroc_ws
 
 
@@ -671,6 +673,8 @@ def small_latency(torch, cdt, W):
         ("drift_score", lambda: cdt.drift_score(prep.h, prep.ref, out=views[0], ws=prep.ws)),
         ("auroc", lambda: cdt.auroc(cfgs, scores, seed=wl.seed, flags=flags, counts=counts,
                                     pooled=pooled, ws=auroc_ws)),
+        ("auroc_launch", lambda: cdt.auroc_launch(auroc_ws, len(cfgs), scores, seed=wl.seed,
+                                                  flags=flags, counts=counts, pooled=pooled)),
         ("step", lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws,
                                   counts, pooled)),
         ("fused_step", lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws,
