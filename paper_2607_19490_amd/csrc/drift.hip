@@ -30,6 +30,45 @@
 namespace cdt {
 namespace {
 
+// Eq. 4 from the block sums: m = sqrt(D / R); R = 0 gives 0 (D = 0) or +inf.
+__device__ __forceinline__ double relative_l2(double D, double R) {
+    if (R == 0.0) return (D == 0.0) ? 0.0 : static_cast<double>(INFINITY);
+    return sqrt(D / R);
+}
+
+// 1 - cos(h, a) from D = |h-a|^2, A = |a|^2, P = a.(h-a): with |h|^2 = A + 2P + D
+// and h.a = A + P, 1 - cos = (A D - P^2) / (sqrt(A |h|^2) (sqrt(A |h|^2) + A + P)),
+// which keeps full relative accuracy as the angle goes to 0.
+__device__ __forceinline__ double cosine_mismatch(double D, double A, double P) {
+    const double hn = A + 2.0 * P + D;
+    if (A == 0.0 || hn <= 0.0) return (A == 0.0 && hn <= 0.0) ? 0.0 : 1.0;
+    const double g = sqrt(A * hn);
+    const double dot = A + P;
+    if (dot > 0.0) return (A * D - P * P) / (g * (g + dot));
+    return 1.0 - dot / g;
+}
+
+// Score and optional sums of block b = s * C + c from its total sums,
+// written at [c][s] (scores) and [c][s][k] (sums).
+template <DriftMetric kM>
+__device__ __forceinline__ void finish_block(const double (&acc)[DriftTraits<kM>::kSums],
+                                             uint64_t b, uint32_t S, uint32_t C,
+                                             float* __restrict__ score, double* __restrict__ sums) {
+    using Tr = DriftTraits<kM>;
+    double m;
+    if constexpr (Tr::kCos)
+        m = cosine_mismatch(acc[0], acc[1], acc[2]);
+    else
+        m = relative_l2(acc[0], acc[1]);
+    const uint64_t s = b / C, c = b - s * C;
+    const uint64_t o = c * S + s;
+    score[o] = static_cast<float>(m);
+    if (sums) {
+#pragma unroll
+        for (int k = 0; k < Tr::kSums; ++k) sums[Tr::kSums * o + k] = acc[k];
+    }
+}
+
 // XOR of every word a thread loaded; a value no load pattern is meant to
 // produce selects the (practically never taken) store that keeps the loads.
 constexpr uint32_t kFoldSentinel = 0x7F3A5C91u;
@@ -45,10 +84,14 @@ __device__ __forceinline__ uint32_t fold_group(const u32x4& hv, const u32x4& rv,
 // kReadOnly: the same chunks, loads and lane exchange with Eq. 4's
 // arithmetic replaced by an XOR fold of the loaded words: the rate the memory
 // system gives this access pattern, against which the drift kernel is judged.
+// direct (a block is one chunk): the chunk's sums are the block's, and the
+// score is written here; the combine launch is skipped (it would add the one
+// partial to zero, which changes nothing).
 template <DriftMetric kM, bool kReadOnly = false>
 __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
     const uint16_t* __restrict__ h, const void* __restrict__ ref, uint32_t n8,
-    uint64_t chunks_per_block, uint64_t total_chunks, double* __restrict__ partial) {
+    uint64_t chunks_per_block, uint64_t total_chunks, double* __restrict__ partial, bool direct,
+    uint32_t S, uint32_t C, float* __restrict__ score, double* __restrict__ sums) {
     using Tr = DriftTraits<kM>;
     const uint64_t n = static_cast<uint64_t>(n8) * 8;
     for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
@@ -121,29 +164,15 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
         } else {
             block_sum<Tr::kSums>(acc);
             if (threadIdx.x == 0) {
+                if (direct) {
+                    finish_block<kM>(acc, chunk, S, C, score, sums);
+                } else {
 #pragma unroll
-                for (int k = 0; k < Tr::kSums; ++k) partial[chunk * Tr::kSums + k] = acc[k];
+                    for (int k = 0; k < Tr::kSums; ++k) partial[chunk * Tr::kSums + k] = acc[k];
+                }
             }
         }
     }
-}
-
-// Eq. 4 from the block sums: m = sqrt(D / R); R = 0 gives 0 (D = 0) or +inf.
-__device__ __forceinline__ double relative_l2(double D, double R) {
-    if (R == 0.0) return (D == 0.0) ? 0.0 : static_cast<double>(INFINITY);
-    return sqrt(D / R);
-}
-
-// 1 - cos(h, a) from D = |h-a|^2, A = |a|^2, P = a.(h-a): with |h|^2 = A + 2P + D
-// and h.a = A + P, 1 - cos = (A D - P^2) / (sqrt(A |h|^2) (sqrt(A |h|^2) + A + P)),
-// which keeps full relative accuracy as the angle goes to 0.
-__device__ __forceinline__ double cosine_mismatch(double D, double A, double P) {
-    const double hn = A + 2.0 * P + D;
-    if (A == 0.0 || hn <= 0.0) return (A == 0.0 && hn <= 0.0) ? 0.0 : 1.0;
-    const double g = sqrt(A * hn);
-    const double dot = A + P;
-    if (dot > 0.0) return (A * D - P * P) / (g * (g + dot));
-    return 1.0 - dot / g;
 }
 
 template <DriftMetric kM>
@@ -160,18 +189,7 @@ __global__ void drift_combine_kernel(const double* __restrict__ partial, uint64_
 #pragma unroll
         for (int k = 0; k < Tr::kSums; ++k) acc[k] += partial[(b * chunks_per_block + i) * Tr::kSums + k];
     }
-    double m;
-    if constexpr (Tr::kCos)
-        m = cosine_mismatch(acc[0], acc[1], acc[2]);
-    else
-        m = relative_l2(acc[0], acc[1]);
-    const uint64_t s = b / C, c = b - s * C;
-    const uint64_t o = c * S + s;
-    score[o] = static_cast<float>(m);
-    if (sums) {
-#pragma unroll
-        for (int k = 0; k < Tr::kSums; ++k) sums[Tr::kSums * o + k] = acc[k];
-    }
+    finish_block<kM>(acc, b, S, C, score, sums);
 }
 
 }  // namespace
@@ -194,13 +212,15 @@ hipError_t launch_drift_t(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const 
     const uint64_t cpb = reduce_chunks_per_block(n);
     const uint64_t total = cpb * nblocks;
     double* partial = static_cast<double*>(ws);
+    const bool direct = cpb == 1;
     if (total > 0) {
         hipLaunchKernelGGL(drift_partial_kernel<kM>, dim3(reduce_grid(total)),
                            dim3(kReduceThreads), 0, st, h, ref, static_cast<uint32_t>(n / 8), cpb,
-                           total, partial);
+                           total, partial, direct, S, C, score, sums);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
+    if (direct) return hipSuccess;
     return launch_combine_t<kM>(partial, cpb, nblocks, S, C, score, sums, st);
 }
 
@@ -211,7 +231,8 @@ hipError_t launch_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t
     if (total == 0) return hipSuccess;
     hipLaunchKernelGGL((drift_partial_kernel<DriftMetric::kL2, true>), dim3(reduce_grid(total)),
                        dim3(kReduceThreads), 0, st, h, ref, static_cast<uint32_t>(n / 8),
-                       reduce_chunks_per_block(n), total, static_cast<double*>(ws));
+                       reduce_chunks_per_block(n), total, static_cast<double*>(ws), false, S, C,
+                       nullptr, nullptr);
     return hipGetLastError();
 }
 
