@@ -112,3 +112,32 @@ def test_canary_base_changes_the_draws(gpu):
     np.testing.assert_array_equal(no_base, ref[:, :2])
     np.testing.assert_array_equal(based, ref[:, 2:])
     assert not np.array_equal(no_base, based)
+
+
+def test_last_canary_indices(gpu):
+    """A slice at the top of the 32-bit canary word (canary_base = 2^32 - 3,
+    three canaries, the last one 2^32 - 1): references and live activations
+    equal the oracle's blocks generated at those global indices directly."""
+    torch, cdt = gpu
+    announce("sharding last canary indices")
+    S, C, T, H = 4, 3, 6, 128
+    c0 = (1 << 32) - C
+    gain = oracle.outlier_gain(H, 2, 20.0, SEED, REF_ID)
+    ref_d = cdt.ref_synth(S, C, T, H, SEED, REF_ID, to_dev(torch, gain), canary_base=c0)
+    mal = 1 << 2
+    ts = np.full((S, C), 0.03, np.float32)
+    kw = dict(seed=SEED, cfg_id=CFG, sigma_b=1e-2, mal_mask=mal, tamper=3, flip_p=0.2)
+    h_d = cdt.canary_sim(ref_d, tscale=to_dev(torch, ts), canary_base=c0, **kw)
+    torch.cuda.synchronize()
+    ref, h = ref_d.cpu().numpy(), h_bits(h_d)
+    for s in range(S):
+        for c in range(C):
+            a = oracle.ref_block(s, c0 + c, T, H, SEED, REF_ID, gain)
+            np.testing.assert_array_equal(ref[s, c], a, err_msg=f"ref block ({s}, {c0 + c})")
+            want = oracle.sim_block(s, c0 + c, a, seed=SEED, cfg_id=CFG, sigma_b=1e-2,
+                                    malicious=bool((mal >> s) & 1), tamper=3, tscale=0.03,
+                                    flip_p=0.2)
+            assert int((h[s, c] != want).sum()) == 0, f"live block ({s}, {c0 + c})"
+    # one canary further would leave the counter word
+    with pytest.raises(RuntimeError):
+        cdt.ref_synth(S, C + 1, T, H, SEED, REF_ID, to_dev(torch, gain), canary_base=c0)
