@@ -141,3 +141,31 @@ def test_last_canary_indices(gpu):
     # one canary further would leave the counter word
     with pytest.raises(RuntimeError):
         cdt.ref_synth(S, C + 1, T, H, SEED, REF_ID, to_dev(torch, gain), canary_base=c0)
+
+
+def test_largest_seed_and_configuration_id(gpu):
+    """Counter and key words at their maxima: seed 2^64 - 1 (both key words
+    all ones) and cfg_id 2^24 - 1 (the 24-bit id field of the stream word),
+    for the live pass, the control and the random baseline."""
+    torch, cdt = gpu
+    announce("largest seed and cfg_id")
+    S, C, T, H = 5, 6, 4, 64
+    seed, cid = (1 << 64) - 1, (1 << 24) - 1
+    gain = oracle.outlier_gain(H, 1, 20.0, seed, REF_ID)
+    ref = oracle.ref_synth(S, C, T, H, seed, REF_ID, gain)
+    ts = np.full((S, C), 0.05, np.float32)
+    kw = dict(seed=seed, cfg_id=cid, sigma_b=2e-2, mal_mask=1 << 2, tamper=3, flip_p=0.3)
+    h_d = cdt.canary_sim(to_dev(torch, ref), tscale=to_dev(torch, ts), **kw)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(
+        cdt.ref_synth(S, C, T, H, seed, REF_ID, to_dev(torch, gain)).cpu().numpy(), ref)
+    want = oracle.canary_sim(ref, tscale=ts, **kw)
+    assert int((h_bits(h_d) != want).sum()) == 0
+    score = cdt.drift_score(h_d, to_dev(torch, ref))
+    counts, _, base = cdt.auroc([(S, C, 0, 1 << 2, cid)], score.view(-1), seed=seed,
+                                flags=cdt.AUROC_CONTROL | cdt.AUROC_RANDOM)
+    torch.cuda.synchronize()
+    c_o, _ = oracle.auroc_config(score.cpu().numpy(), 1 << 2, seed=seed, cfg_id=cid, flags=1)
+    np.testing.assert_array_equal(cdt.u64(counts)[0], c_o)
+    np.testing.assert_array_equal(cdt.u64(base)[0],
+                                  oracle.random_baseline(C, S, 1 << 2, seed=seed, cfg_id=cid))
