@@ -1,7 +1,8 @@
 """Pins of the oracle's random and rounding primitives (CPU only).
 
-Philox4x32-10 (Salmon et al., SC'11) is checked against rocRAND's independent
-header implementation; the Irwin-Hall normal against its closed-form moments,
+Philox4x32-10 (Salmon et al., SC'11) is checked against the authors'
+published known-answer vectors and rocRAND's independent header
+implementation; the Irwin-Hall normal against its closed-form moments,
 symmetry and distribution; fp32 -> fp16 rounding against numpy's float16
 conversion (a library routine) on every rounding boundary.
 """
@@ -10,6 +11,19 @@ import warnings
 
 import numpy as np
 import pytest
+
+
+def test_philox_known_answers(orc):
+    """The generator authors' published known-answer vectors
+    (tests/golden/philox4x32_10_kat.json)."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "philox4x32_10_kat.json")
+    for v in json.load(open(path))["vectors"]:
+        ctr = np.array([int(x, 16) for x in v["counter"]], np.uint64).astype(np.uint32)
+        key = np.array([int(x, 16) for x in v["key"]], np.uint64).astype(np.uint32)
+        want = np.array([int(x, 16) for x in v["output"]], np.uint64).astype(np.uint32)
+        np.testing.assert_array_equal(orc.philox(ctr, key), want)
 
 
 def test_philox_matches_rocrand(orc, philox_pin):
