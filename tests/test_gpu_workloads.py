@@ -4,11 +4,10 @@ configuration the benchmark times, checked against the CPU oracle.
 The 7B-shaped workload is regenerated whole by the oracle, block by block
 on host threads.  At sizes the oracle cannot regenerate whole in a test,
 sampled (shard, canary) blocks are regenerated one by one and compared bit
-for bit (references, block
-scales, live fp16 activations) and within 1e-5 (drift scores); AUROC counts
-are checked by properties that hold at any size (pair counts, the detector
-at 1.0 where the tamper dwarfs the noise floor, the scrambled-label control
-inside the pre-registered window).  Small configurations of the sweep and
+for bit (references, block scales, live fp16 activations) and within 1e-5
+(drift scores); AUROC counts are checked by properties that hold at any
+size (pair counts, the detector at 1.0 where the tamper dwarfs the noise
+floor, the scrambled-label control inside the pre-registered window).  Small configurations of the sweep and
 the paper's own shape are compared whole, counts included.
 """
 import json
