@@ -172,56 +172,83 @@ def _single_set_workload(gpu, name, nsample=4):
     return wl, rs, c, cdt.u64(pooled)
 
 
+def host_threads():
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def check_blocks_threaded(gs, run, score, ts, bs, blocks, gain_o):
+    """check_blocks for many blocks: the blocks are copied to the host here,
+    then regenerated by the oracle on up to 16 host threads (ctypes releases
+    the interpreter lock inside the oracle's C routines, which keep no shared
+    state).  Per-element tamper scales only."""
+    from concurrent.futures import ThreadPoolExecutor
+    rs, wl = gs.rs, gs.wl
+    assert not run.exact_norm
+    sc, ts_d, bs_d = score.cpu().numpy(), ts.cpu().numpy(), bs.cpu().numpy()
+    refs = {b: gs.ref[b].cpu().numpy() for b in blocks}
+    hs = {b: gs.h[b].cpu().numpy().view(np.uint16) for b in blocks}
+
+    def one(b):
+        s, c = b
+        ref_o = oracle.ref_block(s, c, rs.T, rs.H, wl.seed, rs.ref_set_id, gain_o)
+        if not np.array_equal(refs[b], ref_o):
+            return f"reference {b}"
+        q, m = oracle.ref_stats_block(ref_o)
+        ts_o, bs_o = oracle.block_scales(rs.T, rs.H, np.array([q]), np.array([m]), run.eps,
+                                         run.sigma_b)
+        if ts_d[s, c] != ts_o[0] or bs_d[s, c] != bs_o[0]:
+            return f"scales {b}"
+        h_o = oracle.sim_block(s, c, ref_o, seed=wl.seed, cfg_id=run.cfg_id,
+                               benign_mode=run.benign_mode, benign_dist=run.benign_dist,
+                               sigma_b=run.sigma_b, bscale=bs_o[0], malicious=s in rs.mal_shards,
+                               tamper=run.tamper, tamper_base=run.tamper_base, tscale=ts_o[0],
+                               flip_p=run.flip_p, scale=run.scale)
+        if not np.array_equal(hs[b], h_o):
+            return f"live activations {b}"
+        m_o, _, _ = oracle.drift_block(h_o, ref_o)
+        if not rel_err(sc[c, s], m_o) < DRIFT_RTOL:
+            return f"score {b}"
+        return None
+
+    with ThreadPoolExecutor(max_workers=host_threads()) as ex:
+        bad = [r for r in ex.map(one, blocks) if r is not None]
+    assert not bad, f"{run.label}: {len(bad)} of {len(blocks)} blocks differ, first: {bad[:5]}"
+
+
 def test_llama7b_every_block(gpu):
     """The whole 7B-shaped workload against the oracle, every (shard, canary)
     block of both runs: references, block scales and live fp16 activations
-    bit for bit, drift scores within 1e-5.  The blocks are regenerated on up
-    to 16 host threads (ctypes releases the interpreter lock inside the
-    oracle's C routines, which keep no shared state)."""
-    from concurrent.futures import ThreadPoolExecutor
+    bit for bit, drift scores within 1e-5."""
     torch, cdt = gpu
     wl = W.get("llama7b")
     rs = wl.ref_sets[0]
-    announce(f"llama7b every block: {rs.S}x{rs.C}x{rs.T}x{rs.H}")
     gs = GpuSet(torch, cdt, wl, rs)
     gain_o = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
-    ref = gs.ref.cpu().numpy()
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
     for run in rs.runs:
-        assert not run.exact_norm
+        announce(f"llama7b every block: run {run.label}, {host_threads()} threads")
         score, ts, bs = gs.run(run)
         torch.cuda.synchronize()
-        h = gs.h.cpu().numpy().view(np.uint16)
-        sc, ts_d, bs_d = score.cpu().numpy(), ts.cpu().numpy(), bs.cpu().numpy()
-        announce(f"llama7b every block: run {run.label}, {threads} threads")
+        check_blocks_threaded(gs, run, score, ts, bs,
+                              [(s, c) for s in range(rs.S) for c in range(rs.C)], gain_o)
+    del gs
+    torch.cuda.empty_cache()
 
-        def block(sc_pair):
-            s, c = sc_pair
-            ref_o = oracle.ref_block(s, c, rs.T, rs.H, wl.seed, rs.ref_set_id, gain_o)
-            if not np.array_equal(ref[s, c], ref_o):
-                return f"reference ({s}, {c})"
-            q, m = oracle.ref_stats_block(ref_o)
-            ts_o, bs_o = oracle.block_scales(rs.T, rs.H, np.array([q]), np.array([m]), run.eps,
-                                             run.sigma_b)
-            if ts_d[s, c] != ts_o[0] or bs_d[s, c] != bs_o[0]:
-                return f"scales ({s}, {c})"
-            h_o = oracle.sim_block(s, c, ref_o, seed=wl.seed, cfg_id=run.cfg_id,
-                                   benign_mode=run.benign_mode, benign_dist=run.benign_dist,
-                                   sigma_b=run.sigma_b, bscale=bs_o[0],
-                                   malicious=s in rs.mal_shards, tamper=run.tamper,
-                                   tamper_base=run.tamper_base, tscale=ts_o[0],
-                                   flip_p=run.flip_p, scale=run.scale)
-            if not np.array_equal(h[s, c], h_o):
-                return f"live activations ({s}, {c})"
-            m_o, _, _ = oracle.drift_block(h_o, ref_o)
-            if not rel_err(sc[c, s], m_o) < DRIFT_RTOL:
-                return f"score ({s}, {c})"
-            return None
 
-        with ThreadPoolExecutor(max_workers=threads) as ex:
-            bad = [r for r in ex.map(block, [(s, c) for s in range(rs.S) for c in range(rs.C)])
-                   if r is not None]
-        assert not bad, f"{len(bad)} blocks differ, first: {bad[:5]}"
+def test_llama70b_every_shard(gpu):
+    """The 70B-shaped workload against the oracle on every shard of eight
+    canaries (the first, the last and six spread between), all three runs."""
+    torch, cdt = gpu
+    wl = W.get("llama70b")
+    rs = wl.ref_sets[0]
+    gs = GpuSet(torch, cdt, wl, rs)
+    gain_o = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
+    canaries = sorted({int(x) for x in np.linspace(0, rs.C - 1, 8)})
+    blocks = [(s, c) for s in range(rs.S) for c in canaries]
+    for run in rs.runs:
+        announce(f"llama70b {len(blocks)} blocks: run {run.label}, {host_threads()} threads")
+        score, ts, bs = gs.run(run)
+        torch.cuda.synchronize()
+        check_blocks_threaded(gs, run, score, ts, bs, blocks, gain_o)
     del gs
     torch.cuda.empty_cache()
 
