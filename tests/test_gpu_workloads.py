@@ -285,8 +285,9 @@ def test_snr_curve(gpu):
 
 def test_sweep(gpu, gold):
     """All 216 runs as the benchmark launches them; three small runs compared
-    whole with the oracle (scores and counts), a large one by sampled blocks;
-    the pre-registered criteria on the batch."""
+    whole with the oracle (scores and counts), one run of every shape block by
+    block on host threads, a large one by sampled blocks; the pre-registered
+    criteria on the batch."""
     torch, cdt = gpu
     wl = W.sweep()
     max_elems = max(rs.elems for rs in wl.ref_sets)
@@ -317,6 +318,13 @@ def test_sweep(gpu, gold):
                 whole_scores[run.cfg_id] = s64
             if rs.ref_set_id == len(wl.ref_sets) - 1 and run.cfg_id % 24 in (3, 14):
                 check_blocks(gs, run, score, ts, bs, sample_blocks(rs, 2, run.cfg_id), gain_o)
+            if run.cfg_id % 24 == (5 * rs.ref_set_id + 2) % 24:
+                # one configuration of every shape, every block, a different
+                # tamper setting per shape
+                announce(f"sweep cfg {run.cfg_id} every block, {host_threads()} threads")
+                check_blocks_threaded(gs, run, score, ts, bs,
+                                      [(s_, c_) for s_ in range(rs.S) for c_ in range(rs.C)],
+                                      gain_o)
             scores.append(score.clone())
             cfgs.append((rs.S, rs.C, off, rs.mal_mask, run.cfg_id))
             off += rs.S * rs.C
