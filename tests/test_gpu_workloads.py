@@ -147,7 +147,7 @@ def detector_properties(cdt, counts, cfgs):
 
 
 # ----------------------------------------------------------------------------
-def _single_set_workload(gpu, name, nsample=4):
+def _single_set_workload(gpu, name, nsample=4, every_shard_runs=()):
     torch, cdt = gpu
     wl = W.get(name)
     rs = wl.ref_sets[0]
@@ -161,6 +161,11 @@ def _single_set_workload(gpu, name, nsample=4):
         torch.cuda.synchronize()
         if k < 6 or k % 10 == 0 or k == len(rs.runs) - 1:
             check_blocks(gs, run, score, ts, bs, sample_blocks(rs, nsample, k), gain_o)
+        if k in every_shard_runs:  # every shard of four canaries, on host threads
+            canaries = sorted({int(x) for x in np.linspace(0, rs.C - 1, 4)})
+            announce(f"{name} run {run.label}: every shard of {len(canaries)} canaries")
+            check_blocks_threaded(gs, run, score, ts, bs,
+                                  [(s_, c_) for s_ in range(rs.S) for c_ in canaries], gain_o)
         scores.append(score)
         cfgs.append((rs.S, rs.C, k * rs.C * rs.S, rs.mal_mask, run.cfg_id))
     flat = torch.cat([s.reshape(-1) for s in scores])
@@ -274,7 +279,9 @@ def test_llama70b(gpu):
 
 
 def test_snr_curve(gpu):
-    wl, rs, c, _ = _single_set_workload(gpu, "snr", nsample=2)
+    # every shard checked on a Gaussian and a Student-t run at sigma_b near
+    # 0.01, and on the noisiest Student-t run
+    wl, rs, c, _ = _single_set_workload(gpu, "snr", nsample=2, every_shard_runs=(22, 23, 39))
     auc = [(int(x[0]) + 0.5 * int(x[1])) / int(x[2]) for x in c]
     gauss = auc[0::2]
     t3 = auc[1::2]
