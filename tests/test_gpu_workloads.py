@@ -213,17 +213,20 @@ def check_blocks_threaded(gs, run, score, ts, bs, blocks, gain_o):
         m_o, _, _ = oracle.drift_block(h_o, ref_o)
         if not rel_err(sc[c, s], m_o) < DRIFT_RTOL:
             return f"score {b}"
-        return None
+        return m_o
 
     with ThreadPoolExecutor(max_workers=host_threads()) as ex:
-        bad = [r for r in ex.map(one, blocks) if r is not None]
+        out = list(ex.map(one, blocks))
+    bad = [r for r in out if isinstance(r, str)]
     assert not bad, f"{run.label}: {len(bad)} of {len(blocks)} blocks differ, first: {bad[:5]}"
+    return dict(zip(blocks, out))
 
 
 def test_llama7b_every_block(gpu):
     """The whole 7B-shaped workload against the oracle, every (shard, canary)
     block of both runs: references, block scales and live fp16 activations
-    bit for bit, drift scores within 1e-5."""
+    bit for bit, drift scores within 1e-5, and the AUROC counts of the
+    device's scores against the oracle's end to end."""
     torch, cdt = gpu
     wl = W.get("llama7b")
     rs = wl.ref_sets[0]
@@ -233,8 +236,16 @@ def test_llama7b_every_block(gpu):
         announce(f"llama7b every block: run {run.label}, {host_threads()} threads")
         score, ts, bs = gs.run(run)
         torch.cuda.synchronize()
-        check_blocks_threaded(gs, run, score, ts, bs,
-                              [(s, c) for s in range(rs.S) for c in range(rs.C)], gain_o)
+        m_o = check_blocks_threaded(gs, run, score, ts, bs,
+                                    [(s, c) for s in range(rs.S) for c in range(rs.C)], gain_o)
+        # and end to end: the counts of the device scores against the oracle's
+        s64 = np.empty((rs.C, rs.S), np.float64)
+        for (s, c), v in m_o.items():
+            s64[c, s] = v
+        counts, _, _ = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, run.cfg_id)], score.view(-1),
+                                 seed=wl.seed, flags=cdt.AUROC_CONTROL)
+        torch.cuda.synchronize()
+        assert counts_match(cdt.u64(counts)[0], s64, rs.mal_mask, wl.seed, run.cfg_id)
     del gs
     torch.cuda.empty_cache()
 
