@@ -260,11 +260,32 @@ def test_llama70b_every_shard(gpu):
     gain_o = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
     canaries = sorted({int(x) for x in np.linspace(0, rs.C - 1, 8)})
     blocks = [(s, c) for s in range(rs.S) for c in canaries]
-    for run in rs.runs:
+    for k, run in enumerate(rs.runs):
         announce(f"llama70b {len(blocks)} blocks: run {run.label}, {host_threads()} threads")
         score, ts, bs = gs.run(run)
         torch.cuda.synchronize()
         check_blocks_threaded(gs, run, score, ts, bs, blocks, gain_o)
+        if k:
+            continue
+        # at this size too: the fused launch equals the two launches bit for
+        # bit, and the cosine ablation matches the oracle on the last canary
+        fused = cdt.sim_score(gs.ref, ws=gs.ws, seed=wl.seed, cfg_id=run.cfg_id,
+                              benign_mode=run.benign_mode, benign_dist=run.benign_dist,
+                              sigma_b=run.sigma_b, mal_mask=rs.mal_mask, tamper=run.tamper,
+                              tamper_base=run.tamper_base, flip_p=run.flip_p, scale=run.scale,
+                              bscale=bs, tscale=ts)
+        cos = cdt.cosine_score(gs.h, gs.ref, ws=gs.ws)
+        torch.cuda.synchronize()
+        assert torch.equal(fused, score)
+        got = cos.cpu().numpy().astype(np.float64)
+        sc = score.cpu().numpy().astype(np.float64)
+        c = rs.C - 1
+        for s in range(rs.S):
+            h_b = gs.h[s, c].cpu().numpy().view(np.uint16)
+            want = oracle.cosine_block(h_b, gs.ref[s, c].cpu().numpy())
+            # fp64 sums of n terms on both sides (see the cosine ablation tests)
+            tol = (DRIFT_RTOL + 2.0**-24) * abs(want) + 8.0 * rs.T * rs.H * 2.0**-53 * sc[c, s]**2
+            assert abs(got[c, s] - want) <= tol, (s, got[c, s], want)
     del gs
     torch.cuda.empty_cache()
 
