@@ -64,6 +64,8 @@ _SIGS = {
                           _d, _d, _i, _f32p, _u16p], _i),
     "orc_canary_sim_chain": ([_u32, _u32, _u32, _u32, _u64, _u32, _i, _i, _d, _f32p, _u64, _u32,
                               _i, _f32p, _d, _d, _i, _d, _f32p, _u16p], _i),
+    "orc_canary_sim_chain_at": ([_u32, _u32, _u32, _u32, _u32, _u64, _u32, _i, _i, _d, _f32p,
+                                 _u64, _u32, _i, _f32p, _d, _d, _i, _d, _f32p, _u16p], _i),
     "orc_tamper_scale_exact_block": ([_u32, _u32, _u32, _u32, _u64, _u32, _i, _i, _d, _f, _i, _i,
                                       _d, _f32p, _f64p, _f64p], _f),
     "orc_drift_block_f16ref": ([_u64, _u16p, _u16p, _f64p, _f64p], _d),
@@ -282,20 +284,24 @@ def tamper_scale_exact(ref, eps, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE,
 
 def canary_sim(ref, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE, benign_dist=DIST_GAUSS,
                sigma_b=1e-3, bscale=None, mal_mask=0, tamper=0, tamper_base=BASE_BENIGN,
-               tscale=None, flip_p=0.0, scale=1.0, redraw=False, carry=0.0):
+               tscale=None, flip_p=0.0, scale=1.0, redraw=False, carry=0.0, canary_base=0):
     """ref [S][C][T][H] fp32 -> h [S][C][T][H] fp16 bit patterns (uint16).
-    carry > 0 runs the propagation model (stages in order per canary)."""
+    carry > 0 runs the propagation model (stages in order per canary);
+    canary_base: the run's index of the arrays' first canary (propagation
+    model only)."""
     ref = _c(ref, np.float32)
     S, C, T, H = ref.shape
     bs = None if bscale is None else _c(bscale, np.float32)
     ts = None if tscale is None else _c(tscale, np.float32)
     h = np.empty((S, C, T, H), np.uint16)
     if carry != 0.0:
-        lib().orc_canary_sim_chain(S, C, T, H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
-                                   _p(bs, ctypes.c_float), mal_mask, tamper, tamper_base,
-                                   _p(ts, ctypes.c_float), flip_p, scale, int(bool(redraw)),
-                                   carry, _p(ref, ctypes.c_float), _p(h, ctypes.c_uint16))
+        lib().orc_canary_sim_chain_at(canary_base, S, C, T, H, seed, cfg_id, benign_mode,
+                                      benign_dist, sigma_b, _p(bs, ctypes.c_float), mal_mask,
+                                      tamper, tamper_base, _p(ts, ctypes.c_float), flip_p, scale,
+                                      int(bool(redraw)), carry, _p(ref, ctypes.c_float),
+                                      _p(h, ctypes.c_uint16))
         return h
+    assert canary_base == 0, "canary_base is for the propagation model; use sim_block"
     lib().orc_canary_sim(S, C, T, H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
                          _p(bs, ctypes.c_float), mal_mask, tamper, tamper_base,
                          _p(ts, ctypes.c_float), flip_p, scale, int(bool(redraw)),

@@ -437,11 +437,13 @@ int orc_sim_range_ex(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64
  * v = fp32(u + fp32(sc zb)) with sc from |a| (or the block scale), the clean
  * base of a malicious stage is u, and h = fp16(v).  Stages run in order for
  * each canary and element; g = 0 is the independent live pass. */
-int orc_canary_sim_chain(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
-                         uint32_t cfg_id, int benign_mode, int benign_dist, double sigma_b,
-                         const float* bscale, uint64_t mal_mask, uint32_t tamper,
-                         int tamper_base, const float* tscale, double flip_p, double scale,
-                         int redraw, double carry, const float* ref, uint16_t* h)
+/* Canary c of the arrays is the run's canary c0 + c: that global index keys
+ * its noise (c0 = 0 for a whole run). */
+int orc_canary_sim_chain_at(uint32_t c0, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                            uint64_t seed, uint32_t cfg_id, int benign_mode, int benign_dist,
+                            double sigma_b, const float* bscale, uint64_t mal_mask,
+                            uint32_t tamper, int tamper_base, const float* tscale, double flip_p,
+                            double scale, int redraw, double carry, const float* ref, uint16_t* h)
 {
     uint64_t n = (uint64_t)T * H;
     float sigma_f = r32(sigma_b);
@@ -455,10 +457,10 @@ int orc_canary_sim_chain(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_
                 uint64_t b = (uint64_t)s * C + c;
                 float a = ref[b * n + k];
                 float u = (s == 0) ? a : r32((double)a + (double)r32((double)g * (double)d));
-                float v = benign_value(s, c, e, seed, cfg_id, benign_mode, benign_dist, sigma_f,
-                                       bscale ? bscale[b] : 0.0f, redraw, a, u);
+                float v = benign_value(s, c0 + c, e, seed, cfg_id, benign_mode, benign_dist,
+                                       sigma_f, bscale ? bscale[b] : 0.0f, redraw, a, u);
                 if (s < 64 && ((mal_mask >> s) & 1u))
-                    v = tamper_value(s, c, e, seed, cfg_id, tamper, tamper_base,
+                    v = tamper_value(s, c0 + c, e, seed, cfg_id, tamper, tamper_base,
                                      tscale ? tscale[b] : 0.0f, flip_p, scale_f, u, v);
                 uint16_t hb = orc_f16_rne(v);
                 h[b * n + k] = hb;
@@ -466,6 +468,17 @@ int orc_canary_sim_chain(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_
             }
         }
     return 0;
+}
+
+int orc_canary_sim_chain(uint32_t S, uint32_t C, uint32_t T, uint32_t H, uint64_t seed,
+                         uint32_t cfg_id, int benign_mode, int benign_dist, double sigma_b,
+                         const float* bscale, uint64_t mal_mask, uint32_t tamper,
+                         int tamper_base, const float* tscale, double flip_p, double scale,
+                         int redraw, double carry, const float* ref, uint16_t* h)
+{
+    return orc_canary_sim_chain_at(0, S, C, T, H, seed, cfg_id, benign_mode, benign_dist, sigma_b,
+                                   bscale, mal_mask, tamper, tamper_base, tscale, flip_p, scale,
+                                   redraw, carry, ref, h);
 }
 
 /* Exact-norm Gaussian tamper of Section 3.2, tau(v) = v + eps ||v|| N / ||N||,

@@ -252,7 +252,9 @@ def test_llama7b_every_block(gpu):
 
 def test_llama70b_every_shard(gpu):
     """The 70B-shaped workload against the oracle on every shard of eight
-    canaries (the first, the last and six spread between), all three runs."""
+    canaries (the first, the last and six spread between), all three runs;
+    at the same size, the fused launch, the cosine ablation and the
+    propagation model on two canaries."""
     torch, cdt = gpu
     wl = W.get("llama70b")
     rs = wl.ref_sets[0]
@@ -286,6 +288,29 @@ def test_llama70b_every_shard(gpu):
             # fp64 sums of n terms on both sides (see the cosine ablation tests)
             tol = (DRIFT_RTOL + 2.0**-24) * abs(want) + 8.0 * rs.T * rs.H * 2.0**-53 * sc[c, s]**2
             assert abs(got[c, s] - want) <= tol, (s, got[c, s], want)
+        # the propagation model (carry 0.7) at this size: the first and the
+        # last canary through all 16 stages, against the oracle at those
+        # global canary indices
+        from concurrent.futures import ThreadPoolExecutor
+        kw = dict(seed=wl.seed, cfg_id=run.cfg_id, benign_mode=run.benign_mode,
+                  benign_dist=run.benign_dist, sigma_b=run.sigma_b, mal_mask=rs.mal_mask,
+                  tamper=run.tamper, tamper_base=run.tamper_base, flip_p=run.flip_p,
+                  scale=run.scale, carry=0.7)
+        cdt.canary_sim(gs.ref, out=gs.h, bscale=bs, tscale=ts, **kw)
+        torch.cuda.synchronize()
+        ts_h, bs_h = ts.cpu().numpy(), bs.cpu().numpy()
+        picks = [0, rs.C - 1]
+        refs = {c: np.ascontiguousarray(gs.ref[:, c:c + 1].cpu().numpy()) for c in picks}
+        hs = {c: gs.h[:, c:c + 1].cpu().numpy().view(np.uint16) for c in picks}
+
+        def chain(c):
+            want = oracle.canary_sim(refs[c], bscale=np.ascontiguousarray(bs_h[:, c:c + 1]),
+                                     tscale=np.ascontiguousarray(ts_h[:, c:c + 1]),
+                                     canary_base=c, **kw)
+            return int((hs[c] != want).sum())
+
+        with ThreadPoolExecutor(max_workers=2) as ex:
+            assert list(ex.map(chain, picks)) == [0, 0]
     del gs
     torch.cuda.empty_cache()
 

@@ -501,3 +501,21 @@ def test_chain_carries_the_tamper_downstream(orc):
             m = _rel(h[s, 0], ref[s, 0])
             want = 0.0 if s < 2 else eps * g ** (s - 2)
             assert abs(m - want) < 0.02 * eps + 3e-4, (g, s, m, want)
+
+
+def test_chain_canary_base_picks_the_run_canaries(orc):
+    """The propagation model on a slice of canaries with canary_base c0
+    reproduces those canaries of the whole run; without the offset it repeats
+    canary 0's noise instead."""
+    S, C, T, H = 4, 5, 3, 16
+    ref = orc.ref_synth(S, C, T, H, 11, 0, np.ones(H, np.float32))
+    ts = np.full((S, C), 0.04, np.float32)
+    kw = dict(seed=11, cfg_id=4, sigma_b=2e-2, mal_mask=1 << 2, tamper=3, flip_p=0.2,
+              carry=0.7)
+    whole = orc.canary_sim(ref, tscale=ts, **kw)
+    part = orc.canary_sim(np.ascontiguousarray(ref[:, 2:4]), tscale=np.ascontiguousarray(ts[:, 2:4]),
+                          canary_base=2, **kw)
+    np.testing.assert_array_equal(part, whole[:, 2:4])
+    unshifted = orc.canary_sim(np.ascontiguousarray(ref[:, 2:4]),
+                               tscale=np.ascontiguousarray(ts[:, 2:4]), **kw)
+    assert not np.array_equal(unshifted, whole[:, 2:4])
