@@ -253,8 +253,8 @@ def test_llama7b_every_block(gpu):
 def test_llama70b_every_shard(gpu):
     """The 70B-shaped workload against the oracle on every shard of eight
     canaries (the first, the last and six spread between), all three runs;
-    at the same size, the fused launch, the cosine ablation and the
-    propagation model on two canaries."""
+    at the same size, the fused launch, the cosine ablation, the propagation
+    model on two canaries and the exact-norm tamper scales on one."""
     torch, cdt = gpu
     wl = W.get("llama70b")
     rs = wl.ref_sets[0]
@@ -311,6 +311,32 @@ def test_llama70b_every_shard(gpu):
 
         with ThreadPoolExecutor(max_workers=2) as ex:
             assert list(ex.map(chain, picks)) == [0, 0]
+        # the exact-norm Gaussian tamper's block scales (eps 0.05) on every
+        # shard of the last canary: fp64 norms within the rounding of two
+        # n-term sums, the fp32 scale within one ulp
+        norms = torch.empty((rs.S, rs.C, 2), dtype=torch.float64, device="cuda")
+        ex_ts = cdt.tamper_scale_exact(gs.ref, 0.05, norms=norms, ws=gs.ws, bscale=bs,
+                                       seed=wl.seed, cfg_id=run.cfg_id,
+                                       benign_mode=run.benign_mode, benign_dist=run.benign_dist,
+                                       sigma_b=run.sigma_b, tamper_base=run.tamper_base)
+        torch.cuda.synchronize()
+        ex_ts, norms = ex_ts.cpu().numpy(), norms.cpu().numpy()
+        c = rs.C - 1
+        n = rs.T * rs.H
+
+        def exact(s):
+            t_o, vv, zz = oracle.tamper_scale_exact_block(
+                s, c, gs_refs[s], 0.05, seed=wl.seed, cfg_id=run.cfg_id,
+                benign_mode=run.benign_mode, benign_dist=run.benign_dist, sigma_b=run.sigma_b,
+                bscale=bs_h[s, c], tamper_base=run.tamper_base)
+            ok = ulp_diff_f32(ex_ts[s, c], t_o) <= 1
+            ok &= rel_err(norms[s, c, 0], vv) < max(1e-14, 2 * n * 2.0**-53)
+            ok &= rel_err(norms[s, c, 1], zz) < max(1e-14, 2 * n * 2.0**-53)
+            return ok
+
+        gs_refs = {s: gs.ref[s, c].cpu().numpy() for s in range(rs.S)}
+        with ThreadPoolExecutor(max_workers=host_threads()) as ex:
+            assert all(ex.map(exact, range(rs.S)))
     del gs
     torch.cuda.empty_cache()
 
