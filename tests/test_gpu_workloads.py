@@ -254,7 +254,8 @@ def test_llama70b_every_shard(gpu):
     """The 70B-shaped workload against the oracle on every shard of eight
     canaries (the first, the last and six spread between), all three runs;
     at the same size, the fused launch, the cosine ablation, the propagation
-    model on two canaries and the exact-norm tamper scales on one."""
+    model on two canaries, the exact-norm tamper scales and the
+    noisy-reference ablation on one."""
     torch, cdt = gpu
     wl = W.get("llama70b")
     rs = wl.ref_sets[0]
@@ -337,6 +338,30 @@ def test_llama70b_every_shard(gpu):
         gs_refs = {s: gs.ref[s, c].cpu().numpy() for s in range(rs.S)}
         with ThreadPoolExecutor(max_workers=host_threads()) as ex:
             assert all(ex.map(exact, range(rs.S)))
+        # the noisy-reference ablation: an independent benign redraw r, and
+        # Eq. 4 of the live pass against it, on every shard of the last canary
+        kw_sim = dict(seed=wl.seed, cfg_id=run.cfg_id, benign_mode=run.benign_mode,
+                      benign_dist=run.benign_dist, sigma_b=run.sigma_b, mal_mask=rs.mal_mask,
+                      tamper=run.tamper, tamper_base=run.tamper_base, flip_p=run.flip_p,
+                      scale=run.scale, bscale=bs, tscale=ts)
+        cdt.canary_sim(gs.ref, out=gs.h, **kw_sim)
+        r = torch.empty_like(gs.h)
+        cdt.canary_sim(gs.ref, out=r, **dict(kw_sim, mal_mask=0, redraw=True))
+        f16 = cdt.drift_score_f16ref(gs.h, r, ws=gs.ws).cpu().numpy()
+        hs_c = {s: gs.h[s, c].cpu().numpy().view(np.uint16) for s in range(rs.S)}
+        rs_c = {s: r[s, c].cpu().numpy().view(np.uint16) for s in range(rs.S)}
+
+        def redraw(s):
+            r_o = oracle.sim_block(s, c, gs_refs[s], seed=wl.seed, cfg_id=run.cfg_id,
+                                   benign_mode=run.benign_mode, benign_dist=run.benign_dist,
+                                   sigma_b=run.sigma_b, bscale=bs_h[s, c], redraw=True)
+            if not np.array_equal(rs_c[s], r_o):
+                return False
+            m_o, _, _ = oracle.drift_block_f16ref(hs_c[s], r_o)
+            return rel_err(f16[c, s], m_o) < DRIFT_RTOL
+
+        with ThreadPoolExecutor(max_workers=host_threads()) as ex:
+            assert all(ex.map(redraw, range(rs.S)))
     del gs
     torch.cuda.empty_cache()
 
