@@ -242,10 +242,13 @@ def test_llama7b_every_block(gpu):
         s64 = np.empty((rs.C, rs.S), np.float64)
         for (s, c), v in m_o.items():
             s64[c, s] = v
-        counts, _, _ = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, run.cfg_id)], score.view(-1),
-                                 seed=wl.seed, flags=cdt.AUROC_CONTROL)
+        counts, _, base = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, run.cfg_id)], score.view(-1),
+                                    seed=wl.seed, flags=cdt.AUROC_CONTROL | cdt.AUROC_RANDOM)
         torch.cuda.synchronize()
         assert counts_match(cdt.u64(counts)[0], s64, rs.mal_mask, wl.seed, run.cfg_id)
+        np.testing.assert_array_equal(
+            cdt.u64(base)[0],
+            oracle.random_baseline(rs.C, rs.S, rs.mal_mask, seed=wl.seed, cfg_id=run.cfg_id))
     del gs
     torch.cuda.empty_cache()
 
