@@ -549,6 +549,17 @@ def run_sweep(torch, cdt, W, reps):
         times.append(a.elapsed_time(b))
     times.sort()
     ms = times[len(times) // 2]
+    # one more pass with events around every launch: the two kernels' rates
+    # over the sweep's 216 launches each (0.2-3.2 GB per launch)
+    E = torch.cuda.Event
+    drift_ev = [(E(enable_timing=True), E(enable_timing=True)) for _ in cfgs]
+    sim_ev = [(E(enable_timing=True), E(enable_timing=True)) for _ in cfgs]
+    gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled, drift_ev,
+             sim_ev)
+    torch.cuda.synchronize()
+    drift_total = sum(a.elapsed_time(b) for a, b in drift_ev)
+    sim_total = sum(a.elapsed_time(b) for a, b in sim_ev)
+    sweep_elems = sum(len(p.rs.runs) * p.rs.elems for p in preps)
     fused_ms = time_ms(torch, lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs,
                                                auroc_ws, counts, pooled, fused=True), reps)
     # scoring alone (live activations already resident): every config's
@@ -590,6 +601,9 @@ def run_sweep(torch, cdt, W, reps):
         "configs_at_auroc_1": sum(1 for x in strict if x == 1.0),
         "control_pooled_mean": round(ctrl_mean, 4),
         "control_pooled_pairs": round(ctrl, 4),
+        "drift_score_GBps": round(sweep_elems * DRIFT_BYTES_PER_ELEM / (drift_total * 1e-3) / 1e9,
+                                  1),
+        "canary_sim_GBps": round(sweep_elems * SIM_BYTES_PER_ELEM / (sim_total * 1e-3) / 1e9, 1),
     }
     del preps, h_buf, scores
     torch.cuda.empty_cache()
