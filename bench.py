@@ -303,22 +303,20 @@ def run_main(torch, cdt, W, args):
             "valu_instr_per_element": valu_per_el,
         },
     }
-    c = cdt.u64(counts)
-    res["detection"] = {r.label: round(cdt.strict_auroc(c[i]), 4)
-                        for i, r in enumerate([r for p in preps for r in p.rs.runs])}
-    res["control"] = {r.label: round(int(c[i][3]) / max(1, int(c[i][5])), 4)
-                      for i, r in enumerate([r for p in preps for r in p.rs.runs])}
+    vals = cdt.auroc_values(counts, pooled).cpu().numpy()  # Eq. 6 on the device
+    labels = [r.label for p in preps for r in p.rs.runs]
+    res["detection"] = {lab: round(float(vals[i][0]), 4) for i, lab in enumerate(labels)}
+    res["control"] = {lab: round(float(vals[i][2]), 4) for i, lab in enumerate(labels)}
     # the fused live-pass-and-score path on the same workload
     fused_ms = time_ms(torch, lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs,
                                                auroc_ws, counts, pooled, fused=True))
-    ck = cdt.u64(counts)
+    vals = cdt.auroc_values(counts, pooled).cpu().numpy()
     res["fused_step"] = {
         "ms_per_step": round(fused_ms, 4),
         "value": round(scored_bytes / (fused_ms * 1e-3) / 1e9, 2),
         "unit": "GB/s of drift-scored activations (one cdt_sim_score launch per run)",
         "reference_read_GBps": round(elems_per_step * 4 / (fused_ms * 1e-3) / 1e9, 1),
-        "detection": {r.label: round(cdt.strict_auroc(ck[i]), 4)
-                      for i, r in enumerate([r for p in preps for r in p.rs.runs])},
+        "detection": {lab: round(float(vals[i][0]), 4) for i, lab in enumerate(labels)},
     }
     if not args.no_ablations:
         res["ablation_kernels"] = ablation_kernels(torch, cdt, wl, big)
@@ -346,12 +344,11 @@ def time_ms(torch, fn, reps=5):
 def auroc_row(cdt, torch, score, rs, cfg_id, seed, flags):
     counts, _, base = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, cfg_id)], score.reshape(-1),
                                 seed=seed, flags=flags)
-    torch.cuda.synchronize()
-    c = cdt.u64(counts)[0]
-    out = {"auroc": round(cdt.strict_auroc(c), 4), "auroc_mw": round(cdt.mw_auroc(c), 4),
-           "control": round(int(c[3]) / int(c[5]), 4) if int(c[5]) else None}
+    v = cdt.auroc_values(counts, None, base).cpu().numpy()[0]  # Eq. 6 on the device
+    out = {"auroc": round(float(v[0]), 4), "auroc_mw": round(float(v[1]), 4),
+           "control": round(float(v[2]), 4) if flags & cdt.AUROC_CONTROL else None}
     if base is not None:
-        out["random_baseline"] = round(cdt.strict_auroc(cdt.u64(base)[0]), 4)
+        out["random_baseline"] = round(float(v[6]), 4)
     return out
 
 
@@ -502,34 +499,6 @@ def substudies(torch, cdt, W):
             "studies": out}
 
 
-def benign_fpr(torch, cdt, W, n_cfg=24):
-    """The pre-registered false-positive criterion of Section 4.6 on the
-    paper's shape: pipelines with no malicious stage, each scored with the
-    scrambled-label control (a random benign stage per canary ranked as if
-    it were the attacker).  A configuration is a false positive when that
-    AUROC reaches the 0.90 success threshold; the rate must stay at or below
-    5%."""
-    wl = W.paper()
-    rs = wl.ref_sets[0]
-    prep = Prepared(torch, cdt, W, wl, rs)
-    scores = torch.empty((n_cfg, rs.C, rs.S), dtype=torch.float32, device="cuda")
-    _, bs = prep.scales[0]
-    for g in range(n_cfg):
-        cdt.canary_sim(prep.ref, out=prep.h, seed=wl.seed, cfg_id=100 + g,
-                       benign_mode=W.NOISE_BLOCK, sigma_b=0.002, bscale=bs)
-        cdt.drift_score(prep.h, prep.ref, out=scores[g], ws=prep.ws)
-    cfgs = [(rs.S, rs.C, g * rs.C * rs.S, 0, 100 + g) for g in range(n_cfg)]
-    counts, _, _ = cdt.auroc(cfgs, scores.view(-1), seed=wl.seed, flags=cdt.AUROC_CONTROL)
-    c = cdt.u64(counts)
-    ctrl = [int(x[3]) / int(x[5]) for x in c]
-    del prep, scores
-    torch.cuda.empty_cache()
-    return {"configs": n_cfg, "false_positive_rate": sum(a >= 0.90 for a in ctrl) / n_cfg,
-            "control_auroc_mean": round(sum(ctrl) / n_cfg, 4),
-            "control_auroc_max": round(max(ctrl), 4),
-            "criterion": "false-positive rate <= 0.05 (success threshold 0.90)"}
-
-
 def run_sweep(torch, cdt, W, reps):
     wl = W.sweep()
     log("sweep: preparing 9 reference sets")
@@ -583,9 +552,10 @@ def run_sweep(torch, cdt, W, reps):
     torch.cuda.synchronize()
     auroc_ms = a.elapsed_time(b)
     c = cdt.u64(counts)
-    strict = [int(x[0]) / int(x[2]) for x in c]
-    ctrl = sum(int(x[3]) for x in c) / sum(int(x[5]) for x in c)
-    ctrl_mean = sum(int(x[3]) / int(x[5]) for x in c) / len(c)
+    vals = cdt.auroc_values(counts, pooled).cpu().numpy()  # Eq. 6 on the device
+    strict = [float(x[0]) for x in vals]
+    ctrl = sum(int(x[3]) for x in c) / sum(int(x[5]) for x in c)  # pooled over configurations
+    ctrl_mean = float(vals[:, 2].mean())
     log(f"sweep: {ms:.2f} ms for {len(cfgs)} configs")
     out = {
         "configs": len(cfgs),
@@ -924,7 +894,6 @@ def main():
         res["table1"] = table1(torch, cdt, W)
         log("substudies (depth, position, collusion, frontier, snr)")
         res["substudies"] = substudies(torch, cdt, W)
-        res["benign_fpr"] = benign_fpr(torch, cdt, W)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(W, args)

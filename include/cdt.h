@@ -69,7 +69,8 @@ extern "C" {
 #define CDT_STREAM_ALT_T3 11
 
 /* Interface version; changes whenever a layout, a generator rule or the set
- * of entry points changes (6: cdt_drift_read_stream added). */
+ * of entry points changes (7: cdt_auroc_values added, NaN scores rank
+ * above every number). */
 int cdt_version(void);
 
 /* Description of the last error on the calling thread ("" if none). */
@@ -299,7 +300,9 @@ size_t cdt_auroc_workspace_bytes(uint32_t n_cfg);
  *       the random-baseline score of Section 4.5, u(t, s) = (w >> 8) 2^-24,
  *       w = Philox word 0 of counter (canary_base + t, s, 0, RANDOM<<24 |
  *       cfg_id) (if CDT_AUROC_RANDOM; baseline may be NULL otherwise).
- * Score order: NaN below every number, NaN ties NaN, -0 ties +0.
+ * Score order: the numeric order with -0 tying +0, and NaN above every
+ * number (+inf included), NaN tying NaN: a block whose Eq. 4 mismatch is
+ * not a number ranks as the most suspicious stage.
  * counts: device [n_cfg][6] uint64; scores: device fp32; n_scores bounds
  * every configuration's table. */
 int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, uint64_t n_scores,
@@ -327,6 +330,20 @@ int cdt_auroc_upload(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, uint64_t n_score
 int cdt_auroc_launch(uint32_t n_cfg, const void* table, const float* scores, uint64_t n_scores,
                      uint64_t seed, uint32_t flags, uint64_t* counts, uint64_t* pooled,
                      uint64_t* baseline, void* stream);
+
+/* Eq. 6 from the counts above, on the device, in fp64: for configuration g
+ *   values[g][0] = G / pairs           (Eq. 6 as printed: a tie counts 0)
+ *   values[g][1] = (G + E/2) / pairs   (the Mann-Whitney reading stated after
+ *                                       Eq. 6: a tie counts one half)
+ *   values[g][2..3] the same for the scrambled-label control (counts[g][3..5]),
+ *   values[g][4..5] the same for the pooled ranking (pooled[g][0..2]),
+ *   values[g][6..7] the same for the random baseline (baseline[g][0..2]).
+ * A ratio over zero pairs, or over counts holding the out-of-bounds marker
+ * 2^64 - 1, is NaN; so are the pooled or baseline entries when that array is
+ * NULL.  counts: device [n_cfg][6]; pooled, baseline: device [n_cfg][3] or
+ * NULL; values: device [n_cfg][8] fp64 (written, caller-owned). */
+int cdt_auroc_values(uint32_t n_cfg, const uint64_t* counts, const uint64_t* pooled,
+                     const uint64_t* baseline, double* values, void* stream);
 
 #ifdef __cplusplus
 }

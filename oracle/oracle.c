@@ -692,14 +692,18 @@ void orc_cosine_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint
 
 /* ------------------------------------------------------------------------ */
 /* Detection AUROC.                                                          */
-/* Score order: NaN below every number, NaN ties NaN, -0 ties +0, otherwise  */
-/* the numeric order.                                                         */
+/* Score order: the numeric order, -0 ties +0, and NaN above every number    */
+/* (+inf included), NaN tying NaN.  Eq. 5 ranks the stage with the larger    */
+/* mismatch as the more suspicious one; a block whose mismatch is not a      */
+/* number (a NaN in the activations it returned) has no finite agreement     */
+/* with the reference at all, so it ranks as the most suspicious, and a      */
+/* single corrupted element cannot hide a stage below the benign ones.       */
 /* ------------------------------------------------------------------------ */
 static int score_cmp(float x, float y)
 {
     int nx = isnan(x), ny = isnan(y);
     if (nx || ny)
-        return nx && ny ? 0 : (nx ? -1 : 1);
+        return nx && ny ? 0 : (nx ? 1 : -1);
     if (x > y)
         return 1;
     if (x < y)

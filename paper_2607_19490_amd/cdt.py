@@ -3,7 +3,8 @@
 Argument marshalling only: every function checks the torch tensors it is
 given (device, dtype, contiguity, shape), passes their device pointers and
 the current HIP stream to the C ABI, and raises CdtError on a non-zero
-return.  All arithmetic runs in the HIP kernels.  If libcdt.so has not been
+return.  Every step of the method, Eq. 6's ratios included
+(auroc_values), runs in the HIP kernels.  If libcdt.so has not been
 built, loading fails loudly; there is no fallback path.
 
 fp16 activations travel as torch.float16 tensors (their bits are the
@@ -91,6 +92,7 @@ _SIGS = {
                    _vp], ctypes.c_int),
     "cdt_auroc_upload": ([_u32, ctypes.POINTER(AurocCfg), _u64, _u32, _vp, _sz, _vp], ctypes.c_int),
     "cdt_auroc_launch": ([_u32, _vp, _vp, _u64, _u64, _u32, _vp, _vp, _vp, _vp], ctypes.c_int),
+    "cdt_auroc_values": ([_u32, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
 }
 
 _LIB = None
@@ -98,7 +100,7 @@ _LIB = None
 
 # Interface version of include/cdt.h that the structures and signatures
 # below mirror (cdt_version()).
-ABI_VERSION = 6
+ABI_VERSION = 7
 
 
 def lib():
@@ -416,16 +418,27 @@ def auroc_launch(table, n_cfg, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_PO
             baseline if flags & AUROC_RANDOM else None)
 
 
-def strict_auroc(counts_row):
-    """Eq. 6 as printed (ties count 0) from one counts row (G, E, pairs)."""
-    G, E, N = (int(x) for x in counts_row[:3])
-    return G / N if N else float("nan")
+VALUE_NAMES = ("auroc", "auroc_mw", "control", "control_mw", "pooled", "pooled_mw", "random",
+               "random_mw")
 
 
-def mw_auroc(counts_row):
-    """Mann-Whitney normalisation (ties count one half)."""
-    G, E, N = (int(x) for x in counts_row[:3])
-    return (G + 0.5 * E) / N if N else float("nan")
+def auroc_values(counts, pooled=None, baseline=None, out=None):
+    """Eq. 6 from the counts of auroc(), computed on the device
+    (cdt_auroc_values): [n][8] fp64, columns VALUE_NAMES (strict and
+    Mann-Whitney for the detector, the control, the pooled ranking and the
+    random baseline; NaN where there are no pairs or no such counts)."""
+    torch = _torch()
+    _need(counts, "counts", torch.int64)
+    n = counts.shape[0]
+    _need(counts, "counts", torch.int64, (n, 6))
+    for name, t in (("pooled", pooled), ("baseline", baseline)):
+        if t is not None:
+            _need(t, name, torch.int64, (n, 3))
+    out = _empty((n, 8), torch.float64, counts) if out is None else out
+    _need(out, "values", torch.float64, (n, 8))
+    _check(lib().cdt_auroc_values(n, _ptr(counts), _ptr(pooled), _ptr(baseline), _ptr(out),
+                                  _stream()))
+    return out
 
 
 def u64(counts):

@@ -73,7 +73,7 @@ bool canaries_fit(uint32_t canary_base, uint64_t C) {
 
 extern "C" {
 
-int cdt_version(void) { return 6; }
+int cdt_version(void) { return 7; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -460,6 +460,16 @@ int cdt_auroc_launch(uint32_t n_cfg, const void* table, const float* scores, uin
                                            scores, n_scores, seed, flags, counts, pooled,
                                            baseline, static_cast<hipStream_t>(stream)),
                          "cdt_auroc_launch");
+}
+
+int cdt_auroc_values(uint32_t n_cfg, const uint64_t* counts, const uint64_t* pooled,
+                     const uint64_t* baseline, double* values, void* stream) {
+    if (n_cfg == 0) return ok();
+    if (n_cfg > (1u << 24)) return fail(CDT_ELIMIT, "cdt_auroc_values: n_cfg above 2^24");
+    if (!counts || !values) return fail(CDT_EINVAL, "cdt_auroc_values: NULL counts or values");
+    return device_status(cdt::launch_auroc_values(n_cfg, counts, pooled, baseline, values,
+                                                  static_cast<hipStream_t>(stream)),
+                         "cdt_auroc_values");
 }
 
 }  // extern "C"

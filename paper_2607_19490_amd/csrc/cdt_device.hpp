@@ -120,9 +120,12 @@ __device__ __forceinline__ float half_bits_to_float(uint32_t bits16) {
     return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
 }
 
-// Order-preserving key of a score: NaN lowest, -0 == +0, numeric otherwise.
+// Order-preserving key of a score: numeric order with -0 == +0, and NaN
+// above every number (+inf included): a block whose mismatch is not a number
+// ranks as the most suspicious stage (Eq. 5 ranks larger mismatches higher).
+// Every number maps below 0xFFFFFFFF (+inf maps to 0xFF800000).
 __device__ __forceinline__ uint32_t order_key(float x) {
-    if (x != x) return 0u;
+    if (x != x) return 0xFFFFFFFFu;
     uint32_t u = __float_as_uint(x);
     if (x == 0.0f) u = 0u;
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);

@@ -90,4 +90,8 @@ hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float
                         uint64_t n_scores, uint64_t seed, uint32_t flags, uint64_t* counts,
                         uint64_t* pooled, uint64_t* baseline, hipStream_t st);
 
+// Eq. 6 (strict and Mann-Whitney) from the counts of launch_auroc.
+hipError_t launch_auroc_values(uint32_t n_cfg, const uint64_t* counts, const uint64_t* pooled,
+                               const uint64_t* baseline, double* values, hipStream_t st);
+
 }  // namespace cdt

@@ -336,7 +336,53 @@ __global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
     }
 }
 
+// Eq. 6 from integer counts: G / pairs (ties count 0, the equation as
+// printed) and (G + E / 2) / pairs (ties count one half, the Mann-Whitney
+// form), in fp64.  A triple with no pairs, or one holding the out-of-bounds
+// marker, gives NaN.
+__device__ __forceinline__ void ratios(const unsigned long long* c, double* out) {
+    const unsigned long long G = c[0], E = c[1], N = c[2];
+    if (N == 0 || G == kBadCfg || E == kBadCfg || N == kBadCfg) {
+        out[0] = out[1] = __builtin_nan("");
+        return;
+    }
+    const double n = static_cast<double>(N);
+    out[0] = static_cast<double>(G) / n;
+    out[1] = (static_cast<double>(G) + 0.5 * static_cast<double>(E)) / n;
+}
+
+__global__ void auroc_values_kernel(uint32_t n_cfg, const unsigned long long* __restrict__ counts,
+                                    const unsigned long long* __restrict__ pooled,
+                                    const unsigned long long* __restrict__ baseline,
+                                    double* __restrict__ values) {
+    const uint32_t g = blockIdx.x * blockDim.x + threadIdx.x;
+    if (g >= n_cfg) return;
+    double* v = values + 8ull * g;
+    ratios(counts + 6ull * g, v);
+    ratios(counts + 6ull * g + 3, v + 2);
+    if (pooled) {
+        ratios(pooled + 3ull * g, v + 4);
+    } else {
+        v[4] = v[5] = __builtin_nan("");
+    }
+    if (baseline) {
+        ratios(baseline + 3ull * g, v + 6);
+    } else {
+        v[6] = v[7] = __builtin_nan("");
+    }
+}
+
 }  // namespace
+
+hipError_t launch_auroc_values(uint32_t n_cfg, const uint64_t* counts, const uint64_t* pooled,
+                               const uint64_t* baseline, double* values, hipStream_t st) {
+    if (n_cfg == 0) return hipSuccess;
+    hipLaunchKernelGGL(auroc_values_kernel, dim3((n_cfg + 255) / 256), dim3(256), 0, st, n_cfg,
+                       reinterpret_cast<const unsigned long long*>(counts),
+                       reinterpret_cast<const unsigned long long*>(pooled),
+                       reinterpret_cast<const unsigned long long*>(baseline), values);
+    return hipGetLastError();
+}
 
 hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float* scores,
                         uint64_t n_scores, uint64_t seed, uint32_t flags, uint64_t* counts,

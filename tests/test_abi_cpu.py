@@ -38,7 +38,7 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 6 == cdt.ABI_VERSION
+    assert L.cdt_version() == 7 == cdt.ABI_VERSION
     assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0

@@ -264,6 +264,37 @@ def test_drift_special_values(gpu):
     assert np.all(np.isfinite(want[:, 3:5]))  # subnormal and near-limit blocks
 
 
+def test_nan_element_ranks_most_suspicious(gpu):
+    """A malicious stage that returns benign-looking activations except for a
+    single NaN element per block: its mismatch is NaN, which ranks above
+    every number, so Eq. 5 counts it above every benign stage (AUROC 1.0;
+    ranking NaN lowest would give 0.0 and let the stage escape).  Scores,
+    detector, control and pooled counts against the oracle on the same h."""
+    torch, cdt = gpu
+    S, C, T, H = 8, 16, 16, 256
+    mal = 5
+    announce("NaN element in the malicious stage")
+    ref = inputs.ref_normal((S, C, T, H), seed=41)
+    h = inputs.live_near(ref, seed=42, rel=1e-3)  # every stage benign-looking
+    for c in range(C):
+        h[mal, c, c % T, (7 * c) % H] = 0x7E00  # one NaN element per canary
+    sc = cdt.drift_score(to_dev(torch, h).view(torch.float16), to_dev(torch, ref))
+    counts, pooled, _ = cdt.auroc([(S, C, 0, 1 << mal, 9)], sc.view(-1), seed=2, flags=3)
+    torch.cuda.synchronize()
+    want64, want32, _ = oracle.drift_score(h, ref)
+    got = sc.cpu().numpy()
+    assert np.isnan(got[:, mal]).all() and np.isnan(want64[:, mal]).all()
+    ben = [s for s in range(S) if s != mal]
+    assert rel_err(got[:, ben], want64[:, ben]) < DRIFT_RTOL
+    want_c, want_p = oracle.auroc_config(want32, 1 << mal, seed=2, cfg_id=9, flags=3)
+    np.testing.assert_array_equal(cdt.u64(counts)[0], want_c)
+    np.testing.assert_array_equal(cdt.u64(pooled)[0], want_p)
+    c = cdt.u64(counts)[0]
+    assert int(c[0]) == int(c[2]) == C * (S - 1) and int(c[1]) == 0
+    p = cdt.u64(pooled)[0]
+    assert int(p[0]) == int(p[2])
+
+
 @pytest.mark.parametrize("kw", [dict(sigma_b=1e-2), dict(benign_mode=1, sigma_b=1e-2),
                                 dict(sigma_b=1e-2, tamper=7, eps=0.05, flip_p=0.5, scale=1.5)],
                          ids=["elementwise", "block", "mixed_tamper"])

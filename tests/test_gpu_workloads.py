@@ -572,16 +572,3 @@ def test_table1_structure(gpu, gold):
             assert row["auroc_cosine"] < 0.45, row
         else:
             assert row["auroc_cosine"] == 1.0, (label, row)
-
-
-def test_benign_false_positive_rate(gpu, gold):
-    """Section 4.6: on pipelines with no malicious stage the scrambled-label
-    control reaches the 0.90 success threshold in at most 5% of the
-    configurations, and its mean sits in the control window."""
-    torch, cdt = gpu
-    import bench
-    announce("benign false-positive rate")
-    r = bench.benign_fpr(torch, cdt, W)
-    lo, hi = gold["control_window"]["value"]
-    assert r["false_positive_rate"] <= 0.05, r
-    assert lo <= r["control_auroc_mean"] <= hi, r

@@ -31,8 +31,8 @@ def _mask(shards):
 
 
 def _key(x):
-    # NaN lowest, NaN == NaN, otherwise numeric order (-0 == +0)
-    return (0, 0.0) if math.isnan(x) else (1, float(x))
+    # numeric order (-0 == +0), NaN above every number, NaN == NaN
+    return (1, 0.0) if math.isnan(x) else (0, float(x))
 
 
 def _brute(scores, pos):
@@ -108,7 +108,8 @@ def test_exhaustive_label_sets_with_ties(orc):
 
 
 def test_nan_and_signed_zero_order(orc):
-    assert orc.score_cmp(float("nan"), -math.inf) == -1
+    assert orc.score_cmp(float("nan"), math.inf) == 1
+    assert orc.score_cmp(-math.inf, float("nan")) == -1
     assert orc.score_cmp(float("nan"), float("nan")) == 0
     assert orc.score_cmp(-0.0, 0.0) == 0
     assert orc.score_cmp(math.inf, 1e30) == 1

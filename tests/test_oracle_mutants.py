@@ -82,8 +82,8 @@ MUTANTS = [
      "return (double)(1.0L + ha / sqrtl(hh * aa));"),
     # Eqs. 5-6, control and random baseline
     ("ties counted as wins", "counts[0] += (r > 0);", "counts[0] += (r >= 0);"),
-    ("NaN ranked highest", "return nx && ny ? 0 : (nx ? -1 : 1);",
-     "return nx && ny ? 0 : (nx ? 1 : -1);"),
+    ("NaN ranked lowest", "return nx && ny ? 0 : (nx ? 1 : -1);",
+     "return nx && ny ? 0 : (nx ? -1 : 1);"),
     ("control keeps true positives",
      "if (!(flags & ORC_CTRL_INCLUDE_TRUE) && ((pos_mask >> j) & 1u))",
      "if ((flags & ORC_CTRL_INCLUDE_TRUE) && ((pos_mask >> j) & 1u))"),

@@ -101,25 +101,3 @@ def test_cosine_ranks_a_rescale_below_chance_under_propagation(orc):
     cos0, _ = orc.cosine_score(h0, ref)
     c0, _ = orc.auroc_config(cos0.astype(np.float32), mal, seed=0, cfg_id=5, flags=0)
     assert 0.4 < orc.auroc_strict(c0) < 0.6
-
-
-def test_benign_only_pipelines_give_no_false_positives(orc):
-    """Section 4.6's false-positive criterion, read per configuration: with
-    no malicious stage, the scrambled-label control (a random benign stage
-    per canary ranked as the attacker) must reach the 0.90 success threshold
-    in at most 5% of configurations.  Its per-configuration AUROC is a mean
-    over canaries of exchangeable ranks, centred on 0.5."""
-    S, C, T, H = 12, 20, 48, 768
-    gain = orc.outlier_gain(H, W.n_outliers(H), W.OUTLIER_GAIN, 0, 0)
-    ref = orc.ref_synth(S, C, T, H, 0, 0, gain)
-    q, m = orc.ref_stats(ref)
-    _, bs = orc.block_scales(T, H, q, m, 0.0, 0.002)
-    ctrl = []
-    for g in range(6):
-        h = orc.canary_sim(ref, seed=0, cfg_id=100 + g, benign_mode=1, sigma_b=0.002, bscale=bs)
-        _, s32, _ = orc.drift_score(h, ref)
-        c, _ = orc.auroc_config(s32, 0, seed=0, cfg_id=100 + g, flags=1)
-        assert int(c[2]) == 0  # no positives, no detector pairs
-        ctrl.append(int(c[3]) / int(c[5]))
-    assert sum(a >= 0.90 for a in ctrl) / len(ctrl) <= 0.05, ctrl
-    assert 0.35 < sum(ctrl) / len(ctrl) < 0.65, ctrl
