@@ -70,7 +70,9 @@ extern "C" {
 
 /* Interface version; changes whenever a layout, a generator rule or the set
  * of entry points changes (7: cdt_auroc_values added, NaN scores rank
- * above every number). */
+ * above every number).  cdt_version() returns the library's, which a caller
+ * compares with the CDT_INTERFACE_VERSION of the header it was built with. */
+#define CDT_INTERFACE_VERSION 7
 int cdt_version(void);
 
 /* Description of the last error on the calling thread ("" if none). */

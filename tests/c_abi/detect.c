@@ -40,8 +40,9 @@ int main(int argc, char** argv) {
     const uint32_t T = (uint32_t)atoi(argv[3]), H = (uint32_t)atoi(argv[4]);
     const uint64_t seed = strtoull(argv[5], NULL, 10);
     const double eps = atof(argv[6]), sigma_b = atof(argv[7]);
-    if (cdt_version() != 6) {
-        fprintf(stderr, "libcdt interface version %d, expected 6\n", cdt_version());
+    if (cdt_version() != CDT_INTERFACE_VERSION) {
+        fprintf(stderr, "libcdt interface version %d, this header declares %d\n", cdt_version(),
+                CDT_INTERFACE_VERSION);
         return 1;
     }
     const size_t n = (size_t)S * C * T * H, nb = (size_t)S * C;
