@@ -69,10 +69,11 @@ extern "C" {
 #define CDT_STREAM_ALT_T3 11
 
 /* Interface version; changes whenever a layout, a generator rule or the set
- * of entry points changes (7: cdt_auroc_values added, NaN scores rank
- * above every number).  cdt_version() returns the library's, which a caller
- * compares with the CDT_INTERFACE_VERSION of the header it was built with. */
-#define CDT_INTERFACE_VERSION 7
+ * of entry points changes (8: cdt_drift_score_noalloc added; 7:
+ * cdt_auroc_values added, NaN scores rank above every number).
+ * cdt_version() returns the library's, which a caller compares with the
+ * CDT_INTERFACE_VERSION of the header it was built with. */
+#define CDT_INTERFACE_VERSION 8
 int cdt_version(void);
 
 /* Description of the last error on the calling thread ("" if none). */
@@ -226,6 +227,25 @@ int cdt_sim_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_
 int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
                     const float* ref, float* score, double* num_den, void* ws, size_t ws_bytes,
                     void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): exactly
+ * cdt_drift_score (same kernels, same results bit for bit) with no workspace
+ * argument.  The per-chunk partial sums go to a fixed scratch array of
+ * CDT_NOALLOC_SCRATCH_BYTES in the library's own device memory, which each
+ * GPU the library runs on holds until the process ends.  A shape needs
+ * 16 bytes per chunk of 32768 elements when its blocks span more than one
+ * chunk (S*C*ceil(T*H/32768) chunks; the 16 x 256 x 256 x 8192 shape needs
+ * 4 MiB) and none otherwise; a shape beyond the limit returns CDT_ELIMIT and
+ * launches nothing.  No memory is allocated or freed, and every partial sum
+ * is written before it is read, so nothing needs clearing between calls.
+ * All calls on one GPU share its array: calls that can overlap there (on
+ * different streams, or from several threads without ordering) race and
+ * must be serialised by the caller.  The first call on a device looks up
+ * the array's device address (with that device current). */
+#define CDT_NOALLOC_SCRATCH_BYTES 8388608u
+int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                            const float* ref, float* score, double* num_den, void* stream);
 
 /* Measurement aid for Eq. 4's memory bound: reads h and ref exactly as
  * cdt_drift_score does (the same chunks, loads, lane exchange and order)

@@ -81,6 +81,7 @@ _SIGS = {
     "cdt_sim_score": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp, _vp, _vp,
                        _sz, _vp], ctypes.c_int),
     "cdt_drift_score": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "cdt_drift_score_noalloc": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
     "cdt_drift_read_stream": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
     "cdt_drift_score_f16ref": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
                                ctypes.c_int),
@@ -100,7 +101,7 @@ _LIB = None
 
 # Interface version of include/cdt.h that the structures and signatures
 # below mirror (cdt_version()).
-ABI_VERSION = 7
+ABI_VERSION = 8
 
 
 def lib():
@@ -319,6 +320,26 @@ def _drift(fn, h, ref, ref_dtype, out, sums, nsums, ws):
 def drift_score(h, ref, out=None, num_den=None, ws=None):
     """Eq. 4 per block -> scores [C][S] fp32 (and optional [C][S][2] fp64)."""
     return _drift(lib().cdt_drift_score, h, ref, _torch().float32, out, num_den, 2, ws)
+
+
+NOALLOC_SCRATCH_BYTES = 8388608  # CDT_NOALLOC_SCRATCH_BYTES
+
+
+def drift_score_noalloc(h, ref, out=None, num_den=None):
+    """Eq. 4 through cdt_drift_score_noalloc: no workspace; the library's
+    own fixed scratch holds the partial sums (shapes up to its limit).  The
+    outputs must be passed in (out [C][S] fp32, optional num_den [C][S][2]
+    fp64) so that the call allocates nothing."""
+    torch = _torch()
+    _need(h, "h", torch.float16)
+    S, C, T, H = h.shape
+    _need(ref, "ref", torch.float32, (S, C, T, H))
+    _need(out, "score", torch.float32, (C, S))
+    if num_den is not None:
+        _need(num_den, "num_den", torch.float64, (C, S, 2))
+    _check(lib().cdt_drift_score_noalloc(S, C, T, H, _ptr(h), _ptr(ref), _ptr(out), _ptr(num_den),
+                                         _stream()))
+    return out
 
 
 def drift_read_stream(h, ref, ws=None):

@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "cdt.h"
 #include "cdt_launch.hpp"
 
@@ -73,7 +75,7 @@ bool canaries_fit(uint32_t canary_base, uint64_t C) {
 
 extern "C" {
 
-int cdt_version(void) { return 7; }
+int cdt_version(void) { return 8; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -309,6 +311,78 @@ int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16
                     void* stream) {
     return drift_common("cdt_drift_score", cdt::DriftMetric::kL2, S, C, T, H, h, ref, score,
                         num_den, ws, ws_bytes, stream);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// cdt_drift_score_noalloc: Eq. 4 with its per-chunk partial sums in a fixed
+// array of the library's own device memory, for callers that cannot
+// allocate.  Each GPU the library runs on holds its own copy of `scratch`
+// until the process ends.  In host code `scratch` names a host-side stand-in,
+// not device memory: its device address is looked up once per device, with
+// that device current, and only that address is ever passed to a kernel.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) double scratch[CDT_NOALLOC_SCRATCH_BYTES / sizeof(double)];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of the current device's `scratch` (looked up on its first
+// use on that device).
+int scratch_of_current_device(const char* fn, void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return device_status(e, fn);
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(CDT_ELIMIT, "%s: device %d beyond the %d the library serves", fn, dev,
+                    kMaxScratchDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return device_status(e, fn);
+        if (!p) return fail(CDT_EDEVICE, "%s: no device address for the scratch array", fn);
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return CDT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
+                            const float* ref, float* score, double* num_den, void* stream) {
+    const char* fn = "cdt_drift_score_noalloc";
+    int rc = check_shape(fn, S, C, T, H);
+    if (rc) return rc;
+    if (static_cast<uint64_t>(S) * C == 0) return ok();
+    // Scratch in use: one (D, R) fp64 pair per chunk when a block spans
+    // several chunks; a block of one chunk is scored directly.
+    const uint64_t n = static_cast<uint64_t>(T) * H;
+    const uint64_t cpb = cdt::reduce_chunks_per_block(n);
+    const uint64_t need = cpb > 1 ? cpb * S * C * 2 * sizeof(double) : 0;
+    if (need > CDT_NOALLOC_SCRATCH_BYTES)
+        return fail(CDT_ELIMIT, "%s: this shape needs %llu bytes of scratch, above the %u the "
+                                "library holds; use cdt_drift_score with a workspace", fn,
+                    static_cast<unsigned long long>(need), CDT_NOALLOC_SCRATCH_BYTES);
+    if (!score) return fail(CDT_EINVAL, "%s: score is NULL", fn);
+    if (n > 0) {
+        if (!h || !ref) return fail(CDT_EINVAL, "%s: NULL array", fn);
+        if (!aligned16(h) || !aligned16(ref))
+            return fail(CDT_EALIGN, "%s: arrays must be 16-byte aligned", fn);
+    }
+    void* ws = nullptr;
+    rc = scratch_of_current_device(fn, &ws);
+    if (rc) return rc;
+    return device_status(cdt::launch_drift(cdt::DriftMetric::kL2, S, C, T, H, h, ref, score,
+                                           num_den, ws, static_cast<hipStream_t>(stream)),
+                         fn);
 }
 
 int cdt_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,

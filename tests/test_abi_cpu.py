@@ -38,7 +38,7 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 7 == cdt.ABI_VERSION
+    assert L.cdt_version() == 8 == cdt.ABI_VERSION
     assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
@@ -228,3 +228,20 @@ def test_scale_and_outlier_validation(cdt):
     assert L.cdt_outlier_gain(16, 17, 20.0, 0, 0, 16, None) == cdt.EINVAL
     assert L.cdt_outlier_gain(16, 1, 20.0, 0, 0, None, None) == cdt.EINVAL
     assert L.cdt_outlier_gain(0, 0, 20.0, 0, 0, None, None) == cdt.OK
+
+
+def test_noalloc_limit_is_checked_on_the_host(cdt):
+    """cdt_drift_score_noalloc rejects a shape whose partial sums exceed the
+    library's scratch, and a bad shape, before any device call."""
+    L = cdt.lib()
+    # 16 x 1024 blocks of 64 chunks: 16 MiB of partial sums against 8 MiB
+    assert L.cdt_drift_score_noalloc(16, 1024, 256, 8192, None, None, None, None, None) == \
+        cdt.ELIMIT
+    assert "scratch" in _err(cdt) and "8388608" in _err(cdt)
+    assert L.cdt_drift_score_noalloc(2, 2, 3, 12, None, None, None, None, None) == cdt.EINVAL
+    assert "multiple of 8" in _err(cdt)
+    # one-chunk blocks use no scratch: any number of them passes the limit
+    # and fails only on the NULL score pointer
+    assert L.cdt_drift_score_noalloc(64, 1 << 20, 1, 8, None, None, None, None, None) == \
+        cdt.EINVAL
+    assert "score is NULL" in _err(cdt)
