@@ -37,6 +37,7 @@ Prints one JSON line:
                  over up to 16 host threads (and on one thread).
 """
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -137,16 +138,7 @@ class Prepared:
             self.h = torch.empty((S, C, T, H), dtype=torch.float16, device="cuda")
         else:
             self.h = h_buf[:n].view(S, C, T, H)
-        self.scales = []
-        for run in rs.runs:
-            ts, bs = cdt.block_scales(self.sumsq, self.sumabs, T, H, run.eps, run.sigma_b)
-            if run.exact_norm:
-                ts = cdt.tamper_scale_exact(self.ref, run.eps, ws=self.ws, bscale=bs,
-                                            seed=wl.seed, cfg_id=run.cfg_id,
-                                            benign_mode=run.benign_mode,
-                                            benign_dist=run.benign_dist, sigma_b=run.sigma_b,
-                                            tamper_base=run.tamper_base)
-            self.scales.append((ts, bs))
+        self.scales = [run_scales(cdt, wl, rs, run, self) for run in rs.runs]
 
 
 def sim_kwargs(wl, rs, run, ts, bs):
@@ -154,6 +146,19 @@ def sim_kwargs(wl, rs, run, ts, bs):
                 benign_dist=run.benign_dist, sigma_b=run.sigma_b, mal_mask=rs.mal_mask,
                 tamper=run.tamper, tamper_base=run.tamper_base, flip_p=run.flip_p,
                 scale=run.scale, bscale=bs, tscale=ts, carry=run.carry)
+
+
+def run_scales(cdt, wl, rs, run, prep):
+    """Per-block scales of one run: the Gaussian tamper's eps rms and Eq. 2's
+    block scale from the reference statistics, or, for the paper's
+    exact-norm attack, eps ||v|| / ||N|| with v the stage's untampered output
+    (under the propagation model, given everything upstream)."""
+    ts, bs = cdt.block_scales(prep.sumsq, prep.sumabs, rs.T, rs.H, run.eps, run.sigma_b)
+    if run.exact_norm:
+        kw = sim_kwargs(wl, rs, run, None, bs)
+        del kw["tscale"], kw["bscale"]
+        ts = cdt.tamper_scale_exact(prep.ref, run.eps, ws=prep.ws, bscale=bs, **kw)
+    return ts, bs
 
 
 def gpu_step(torch, cdt, wl, preps, scores, score_views, cfgs, auroc_ws, counts, pooled,
@@ -437,14 +442,15 @@ def table1(torch, cdt, W):
         rows["noisy_reference"][run.label] = dict(ceil, ceiling=ceil["auroc"])
         rows["cosine_metric"][run.label] = dict(cos, ceiling=cos_ceil["auroc"])
     # the same attacks with the live error carried between stages (the
-    # propagation model of the substudies; Gaussian attacks at eps rms, the
-    # exact norm being defined for independent stages only): a pure rescale
-    # then leaves its stage with less angular error than the stages after it,
+    # propagation model of the substudies; the Gaussian attacks at exactly
+    # eps ||v||, v the stage's untampered live output): a pure rescale then
+    # leaves its stage with less angular error than the stages after it,
     # which inherit its error, so the cosine metric ranks it below chance
     prop = {}
     for k, run in enumerate(rs.runs):
-        ts, bs = cdt.block_scales(prep.sumsq, prep.sumabs, rs.T, rs.H, run.eps, run.sigma_b)
-        kw = dict(sim_kwargs(wl, rs, run, ts, bs), carry=W.SUBSTUDY_CARRY)
+        run = dataclasses.replace(run, carry=W.SUBSTUDY_CARRY)
+        ts, bs = run_scales(cdt, wl, rs, run, prep)
+        kw = sim_kwargs(wl, rs, run, ts, bs)
         cdt.canary_sim(prep.ref, out=prep.h, **kw)
         cdt.drift_score(prep.h, prep.ref, out=score, ws=prep.ws)
         l2 = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
@@ -479,7 +485,8 @@ def substudies(torch, cdt, W):
             cache[key] = Prepared(torch, cdt, W, wl, rs)
         prep = cache[key]
         run = rs.runs[0]
-        ts, bs = cdt.block_scales(prep.sumsq, prep.sumabs, rs.T, rs.H, run.eps, run.sigma_b)
+        # configurations sharing references differ in attackers and eps
+        ts, bs = run_scales(cdt, wl, rs, run, prep)
         cdt.canary_sim(prep.ref, out=prep.h, **sim_kwargs(wl, rs, run, ts, bs))
         score = cdt.drift_score(prep.h, prep.ref, ws=prep.ws)
         row = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed,

@@ -197,6 +197,18 @@ int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim
  * so that cdt_canary_sim's Gaussian tamper, given this tscale, adds a
  * perturbation of norm eps ||v|| (up to rounding).  p gives the benign
  * settings, seed and cfg_id of the run (its tamper fields are ignored).
+ *
+ * Under the propagation model (p->carry > 0) v is a malicious stage's
+ * untampered output given the live error carried in from the stage before
+ * (the clean base: its noise-free u), so it depends on every stage
+ * upstream.  The scales are found for the malicious stages (p->mal_mask) in
+ * pipeline order: for stage m, every element is walked through stages
+ * 0 .. m as cdt_canary_sim walks it, the earlier malicious stages tampered
+ * with p's tamper settings and the Gaussian scales this call has already
+ * written to tscale, and tscale[m][c] is formed as above from stage m's
+ * sums.  Entries of benign stages are set to 0 (norms too).  Passing the
+ * result as tscale to cdt_canary_sim with the same p then runs the paper's
+ * attack, every colluder at exactly eps ||v||.
  * norms: optional device [S][C][2] fp64 (sum v^2, sum N^2), or NULL.
  * ws: cdt_reduce_workspace_bytes bytes. */
 int cdt_tamper_scale_exact(uint32_t S, uint32_t C, uint32_t T, uint32_t H,

@@ -68,6 +68,9 @@ _SIGS = {
                                  _u64, _u32, _i, _f32p, _d, _d, _i, _d, _f32p, _u16p], _i),
     "orc_tamper_scale_exact_block": ([_u32, _u32, _u32, _u32, _u64, _u32, _i, _i, _d, _f, _i, _i,
                                       _d, _f32p, _f64p, _f64p], _f),
+    "orc_tamper_scale_exact_chain_at": ([_u32, _u32, _u32, _u32, _u32, _u64, _u32, _i, _i, _d,
+                                         _f32p, _u64, _u32, _i, _d, _d, _i, _d, _d, _f32p, _f32p,
+                                         _f64p], _i),
     "orc_drift_block_f16ref": ([_u64, _u16p, _u16p, _f64p, _f64p], _d),
     "orc_drift_score_f16ref": ([_u32, _u32, _u32, _u32, _u16p, _u16p, _f64p, _f32p], None),
     "orc_cosine_block": ([_u64, _u16p, _f32p], _d),
@@ -264,10 +267,27 @@ def tamper_scale_exact_block(s, c, ref_block_arr, eps, *, seed, cfg_id,
 
 def tamper_scale_exact(ref, eps, *, seed, cfg_id, benign_mode=NOISE_ELEMENTWISE,
                        benign_dist=DIST_GAUSS, sigma_b=1e-3, bscale=None,
-                       tamper_base=BASE_BENIGN, redraw=False):
-    """[S][C] exact-norm tamper scales (and the [S][C][2] norms) of a whole array."""
+                       tamper_base=BASE_BENIGN, redraw=False, carry=0.0, mal_mask=0, tamper=0,
+                       flip_p=0.0, scale=1.0, canary_base=0):
+    """[S][C] exact-norm tamper scales (and the [S][C][2] norms) of a whole array.
+    carry > 0: the propagation model, malicious stages only (in pipeline
+    order, each from its untampered output given everything upstream; the
+    tamper settings apply to the earlier malicious stages); benign entries 0."""
     ref = _c(ref, np.float32)
     S, C = ref.shape[:2]
+    if carry != 0.0:
+        T, H = ref.shape[2:]
+        bs = None if bscale is None else _c(bscale, np.float32)
+        ts = np.empty((S, C), np.float32)
+        norms = np.empty((S, C, 2), np.float64)
+        lib().orc_tamper_scale_exact_chain_at(canary_base, S, C, T, H, seed, cfg_id, benign_mode,
+                                              benign_dist, sigma_b, _p(bs, ctypes.c_float),
+                                              mal_mask, tamper, tamper_base, flip_p, scale,
+                                              int(bool(redraw)), carry, eps,
+                                              _p(ref, ctypes.c_float), _p(ts, ctypes.c_float),
+                                              _p(norms, ctypes.c_double))
+        return ts, norms
+    assert canary_base == 0, "canary_base is for the propagation model"
     ts = np.empty((S, C), np.float32)
     norms = np.empty((S, C, 2), np.float64)
     for s in range(S):

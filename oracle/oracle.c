@@ -437,6 +437,13 @@ int orc_sim_range_ex(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64
  * v = fp32(u + fp32(sc zb)) with sc from |a| (or the block scale), the clean
  * base of a malicious stage is u, and h = fp16(v).  Stages run in order for
  * each canary and element; g = 0 is the independent live pass. */
+/* Noise-free output u of stage s under the propagation model: its reference
+ * a plus the carried live error g d of the stage before (a at stage 0). */
+static float carried_input(uint32_t s, float a, float g, float d)
+{
+    return (s == 0) ? a : r32((double)a + (double)r32((double)g * (double)d));
+}
+
 /* Canary c of the arrays is the run's canary c0 + c: that global index keys
  * its noise (c0 = 0 for a whole run). */
 int orc_canary_sim_chain_at(uint32_t c0, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
@@ -456,7 +463,7 @@ int orc_canary_sim_chain_at(uint32_t c0, uint32_t S, uint32_t C, uint32_t T, uin
             for (uint32_t s = 0; s < S; ++s) {
                 uint64_t b = (uint64_t)s * C + c;
                 float a = ref[b * n + k];
-                float u = (s == 0) ? a : r32((double)a + (double)r32((double)g * (double)d));
+                float u = carried_input(s, a, g, d);
                 float v = benign_value(s, c0 + c, e, seed, cfg_id, benign_mode, benign_dist,
                                        sigma_f, bscale ? bscale[b] : 0.0f, redraw, a, u);
                 if (s < 64 && ((mal_mask >> s) & 1u))
@@ -509,6 +516,73 @@ float orc_tamper_scale_exact_block(uint32_t s, uint32_t c, uint32_t T, uint32_t 
     if (zz_out)
         *zz_out = zz;
     return zz > 0.0 ? r32(eps * sqrt(vv / zz)) : 0.0f;
+}
+
+/* The same exact-norm tamper under the propagation model (carry g > 0).
+ * For a malicious stage m the untampered output v is the stage's benign
+ * output given the live error carried in from stage m - 1 (the clean base:
+ * the noise-free u), so it depends on everything upstream, earlier
+ * malicious stages included.  The scales are therefore found stage by stage
+ * in pipeline order: for each malicious stage m, every element of the block
+ * is walked through stages 0 .. m as the propagation model walks it (earlier
+ * malicious stages tampered with the scales already found and the run's
+ * other tamper settings), and vv = sum v^2 at stage m, zz = sum z^2 of its
+ * TAMPER_ADD normals give tscale[m][c] = fp32(eps sqrt(vv / zz)).  Entries
+ * of benign stages are 0 (norms 0 as well).  Canary c of the arrays is the
+ * run's canary c0 + c.  tscale, norms: [S][C] and [S][C][2] outputs. */
+int orc_tamper_scale_exact_chain_at(uint32_t c0, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                                    uint64_t seed, uint32_t cfg_id, int benign_mode,
+                                    int benign_dist, double sigma_b, const float* bscale,
+                                    uint64_t mal_mask, uint32_t tamper, int tamper_base,
+                                    double flip_p, double scale, int redraw, double carry,
+                                    double eps, const float* ref, float* tscale, double* norms)
+{
+    uint64_t n = (uint64_t)T * H;
+    float sigma_f = r32(sigma_b);
+    float scale_f = r32(scale);
+    float g = r32(carry);
+    for (uint64_t b = 0; b < (uint64_t)S * C; ++b) {
+        tscale[b] = 0.0f;
+        if (norms) {
+            norms[2 * b] = 0.0;
+            norms[2 * b + 1] = 0.0;
+        }
+    }
+    for (uint32_t c = 0; c < C; ++c)
+        for (uint32_t m = 0; m < S && m < 64; ++m) {
+            if (!((mal_mask >> m) & 1u))
+                continue;
+            double vv = 0.0, zz = 0.0;
+            for (uint64_t k = 0; k < n; ++k) {
+                uint32_t e = (uint32_t)k;
+                float d = 0.0f;
+                for (uint32_t s = 0; s <= m; ++s) {
+                    uint64_t b = (uint64_t)s * C + c;
+                    float a = ref[b * n + k];
+                    float u = carried_input(s, a, g, d);
+                    float v = benign_value(s, c0 + c, e, seed, cfg_id, benign_mode, benign_dist,
+                                           sigma_f, bscale ? bscale[b] : 0.0f, redraw, a, u);
+                    if (s == m) {
+                        float vt = (tamper_base == ORC_BASE_CLEAN) ? u : v;
+                        float z = normal1(seed, ST_TADD, cfg_id, s, c0 + c, e);
+                        vv += (double)vt * (double)vt;
+                        zz += (double)z * (double)z;
+                        break;
+                    }
+                    if ((mal_mask >> s) & 1u)
+                        v = tamper_value(s, c0 + c, e, seed, cfg_id, tamper, tamper_base,
+                                         tscale[b], flip_p, scale_f, u, v);
+                    d = r32(orc_f16_value(orc_f16_rne(v)) - (double)a);
+                }
+            }
+            uint64_t bm = (uint64_t)m * C + c;
+            tscale[bm] = zz > 0.0 ? r32(eps * sqrt(vv / zz)) : 0.0f;
+            if (norms) {
+                norms[2 * bm] = vv;
+                norms[2 * bm + 1] = zz;
+            }
+        }
+    return 0;
 }
 
 int orc_sim_range(uint32_t s, uint32_t c, uint64_t e0, uint64_t count, uint64_t seed,

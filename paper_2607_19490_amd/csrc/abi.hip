@@ -255,12 +255,17 @@ int cdt_tamper_scale_exact(uint32_t S, uint32_t C, uint32_t T, uint32_t H,
     const char* fn = "cdt_tamper_scale_exact";
     if (!p) return fail(CDT_EINVAL, "%s: params is NULL", fn);
     if (!(eps >= 0.0) || !isfinite(eps)) return fail(CDT_EINVAL, "%s: eps must be finite and >= 0", fn);
-    // The tamper settings do not enter the norms (tscale is this call's output).
-    if (p->carry != 0.0)
-        return fail(CDT_EINVAL, "%s: not defined for the propagation model (carry > 0)", fn);
+    // Independent stages: the tamper settings do not enter the norms.  Under
+    // the propagation model they shape the earlier malicious stages, whose
+    // Gaussian scales are the ones this call writes first (tscale).
+    const bool chain = p->carry != 0.0;
     cdt_sim_params q = *p;
-    q.tamper = 0;
-    q.tscale = nullptr;
+    if (chain) {
+        q.tscale = tscale;
+    } else {
+        q.tamper = 0;
+        q.tscale = nullptr;
+    }
     cdt::SimLaunch L;
     int rc = check_sim(fn, S, C, T, H, &q, &L);
     if (rc) return rc;
@@ -275,6 +280,10 @@ int cdt_tamper_scale_exact(uint32_t S, uint32_t C, uint32_t T, uint32_t H,
         return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
                     ws ? ws_bytes : 0);
     if (ws && !aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
+    if (chain)
+        return device_status(cdt::launch_tamper_scale_exact_chain(
+                                 L, ref, eps, tscale, norms, ws, static_cast<hipStream_t>(stream)),
+                             fn);
     return device_status(cdt::launch_tamper_scale_exact(L, ref, eps, tscale, norms, ws,
                                                         static_cast<hipStream_t>(stream)),
                          fn);

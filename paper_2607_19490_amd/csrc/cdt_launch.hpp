@@ -83,6 +83,12 @@ hipError_t launch_sim_score(const SimLaunch& p, const float* ref, uint16_t* h, f
 hipError_t launch_tamper_scale_exact(const SimLaunch& p, const float* ref, double eps,
                                      float* tscale, double* norms, void* ws, hipStream_t st);
 
+// The same under the propagation model (p.carry > 0): the malicious stages'
+// scales in pipeline order, benign entries cleared to 0.
+hipError_t launch_tamper_scale_exact_chain(const SimLaunch& p, const float* ref, double eps,
+                                           float* tscale, double* norms, void* ws,
+                                           hipStream_t st);
+
 // Eqs. 5-6 over a device table of configurations; a configuration whose
 // table lies outside [0, n_scores) (or, pooled, exceeds the LDS sort) gets
 // counts of all ones instead of being read.

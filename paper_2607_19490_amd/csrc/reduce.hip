@@ -169,6 +169,96 @@ __global__ __launch_bounds__(kReduceThreads) void tamper_norms_partial_kernel(
     }
 }
 
+// The same norms under the propagation model, for one malicious stage m:
+// every element is walked through stages 0 .. m-1 exactly as
+// canary_chain_kernel walks it (earlier malicious stages tampered with the
+// scales already written to A.tscale), and at stage m the untampered output
+// v (or the clean base u) and the TAMPER_ADD normals are summed in fp64.
+// Chunks are reduction chunks of one canary's stage-m block: chunk index =
+// canary * chunks_per_block + chunk within the block.
+template <bool kT3, bool kBlock>
+__global__ __launch_bounds__(kReduceThreads) void chain_norms_partial_kernel(
+    SimArgs A, uint32_t m, float gain, const float* __restrict__ ref,
+    double* __restrict__ partial) {
+    const uint64_t n = static_cast<uint64_t>(A.n8) * 8;
+    for (uint64_t it = blockIdx.x; it < A.total_chunks; it += gridDim.x) {
+        const uint64_t chunk = xcd_contiguous(it, A.total_chunks);
+        const uint32_t c = static_cast<uint32_t>(chunk / A.chunks_per_block);
+        const uint32_t g0 =
+            static_cast<uint32_t>(chunk - static_cast<uint64_t>(c) * A.chunks_per_block) *
+            kChunkGroups;
+        const uint32_t g_end = min(g0 + kChunkGroups, A.n8);
+        double acc[2] = {0.0, 0.0};
+        for (uint32_t g = g0 + threadIdx.x; g < g_end; g += kReduceThreads) {
+            float d[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+            for (uint32_t s = 0; s < m; ++s) {
+                const uint64_t block = static_cast<uint64_t>(s) * A.C + c;
+                const SimBlock B = sim_block<kBlock>(A, block);
+                const f32x4* in = reinterpret_cast<const f32x4*>(ref + block * n);
+                chain_group8<kT3, kBlock>(A, B, g * 8, s == 0, gain, in[2 * g], in[2 * g + 1], d);
+            }
+            const uint64_t block = static_cast<uint64_t>(m) * A.C + c;
+            const SimBlock B = sim_block<kBlock>(A, block);
+            const f32x4* in = reinterpret_cast<const f32x4*>(ref + block * n);
+            const f32x4 lo = in[2 * g], hi = in[2 * g + 1];
+            const float a[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+            float u[8], v[8], z[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) u[k] = m == 0 ? a[k] : a[k] + gain * d[k];
+            benign8<kT3, kBlock>(A, B, g * 8, a, u, v);
+            normals8(A.key, g * 8, B.c, B.s, A.tag_add, z);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const double vd = static_cast<double>(A.clean ? u[k] : v[k]);
+                const double zd = static_cast<double>(z[k]);
+                acc[0] = fma(vd, vd, acc[0]);
+                acc[1] = fma(zd, zd, acc[1]);
+            }
+        }
+        block_sum<2>(acc);
+        if (threadIdx.x == 0) {
+            partial[chunk * 2] = acc[0];
+            partial[chunk * 2 + 1] = acc[1];
+        }
+    }
+}
+
+// Stage m's scales from chain_norms_partial_kernel's partials: one thread per
+// canary adds its chunks in order.
+__global__ void chain_scale_combine_kernel(const double* __restrict__ partial,
+                                           uint64_t chunks_per_block, uint32_t C, uint32_t m,
+                                           double eps, float* __restrict__ tscale,
+                                           double* __restrict__ norms) {
+    const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C) return;
+    double vv = 0.0, zz = 0.0;
+    for (uint64_t i = 0; i < chunks_per_block; ++i) {
+        vv += partial[(c * chunks_per_block + i) * 2];
+        zz += partial[(c * chunks_per_block + i) * 2 + 1];
+    }
+    const uint64_t b = static_cast<uint64_t>(m) * C + c;
+    tscale[b] = zz > 0.0 ? static_cast<float>(eps * sqrt(vv / zz)) : 0.0f;
+    if (norms) {
+        norms[2 * b] = vv;
+        norms[2 * b + 1] = zz;
+    }
+}
+
+// Benign stages get no exact-norm scale under the propagation model: their
+// entries are cleared first (a kernel, not a memset, so that a stream
+// capture records no memset node).
+__global__ void clear_scales_kernel(uint64_t nblocks, float* __restrict__ tscale,
+                                    double* __restrict__ norms) {
+    const uint64_t b = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (b >= nblocks) return;
+    tscale[b] = 0.0f;
+    if (norms) {
+        norms[2 * b] = 0.0;
+        norms[2 * b + 1] = 0.0;
+    }
+}
+
 __global__ void tamper_scale_combine_kernel(const double* __restrict__ partial,
                                             uint64_t chunks_per_block, uint64_t nblocks,
                                             double eps, float* __restrict__ tscale,
@@ -326,6 +416,49 @@ hipError_t launch_tamper_scale_exact(const SimLaunch& p, const float* ref, doubl
     hipLaunchKernelGGL(tamper_scale_combine_kernel, dim3(static_cast<uint32_t>(grid)), dim3(256),
                        0, st, partial, cpb, nblocks, eps, tscale, norms);
     return hipGetLastError();
+}
+
+template <bool kT3, bool kBlock>
+void launch_chain_norms_t(const SimArgs& A, uint32_t m, float gain, const float* ref,
+                          double* partial, hipStream_t st) {
+    hipLaunchKernelGGL((chain_norms_partial_kernel<kT3, kBlock>), dim3(reduce_grid(A.total_chunks)),
+                       dim3(kReduceThreads), 0, st, A, m, gain, ref, partial);
+}
+
+hipError_t launch_tamper_scale_exact_chain(const SimLaunch& p, const float* ref, double eps,
+                                           float* tscale, double* norms, void* ws,
+                                           hipStream_t st) {
+    const uint64_t n = static_cast<uint64_t>(p.T) * p.H;
+    const uint64_t nblocks = static_cast<uint64_t>(p.S) * p.C;
+    if (nblocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(clear_scales_kernel, dim3(static_cast<uint32_t>((nblocks + 255) / 256)),
+                       dim3(256), 0, st, nblocks, tscale, norms);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n == 0) return e;
+    const uint64_t cpb = reduce_chunks_per_block(n);
+    // The scales of earlier malicious stages are read from tscale itself.
+    SimLaunch q = p;
+    q.tscale = tscale;
+    const SimArgs A = make_sim_args(q, cpb, cpb * p.C);  // one stage's blocks
+    double* partial = static_cast<double*>(ws);
+    for (uint32_t m = 0; m < p.S; ++m) {  // malicious stages in pipeline order
+        if (!((p.mal_mask >> m) & 1u)) continue;
+        if (A.t3 && A.block_mode)
+            launch_chain_norms_t<true, true>(A, m, p.carry, ref, partial, st);
+        else if (A.t3)
+            launch_chain_norms_t<true, false>(A, m, p.carry, ref, partial, st);
+        else if (A.block_mode)
+            launch_chain_norms_t<false, true>(A, m, p.carry, ref, partial, st);
+        else
+            launch_chain_norms_t<false, false>(A, m, p.carry, ref, partial, st);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(chain_scale_combine_kernel, dim3((p.C + 255) / 256), dim3(256), 0, st,
+                           partial, cpb, p.C, m, eps, tscale, norms);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,

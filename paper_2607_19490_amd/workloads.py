@@ -209,6 +209,9 @@ def substudies() -> Workload:
       frontier   k = 12, Gaussian eps from 0.10 down to 0.001
       snr        k = 12, Gaussian 0.05, sigma_hw raised from 0.002 to 0.2
                  (Section 5.4)
+    Every Gaussian attack is the paper's exact-norm one, eps ||v|| with v the
+    attacker's untampered live output given the error carried in from
+    upstream (Section 3.2).
     Each configuration is one reference set with one run; configurations of
     one shape share their references (same ref_set_id)."""
     C, T, H = 100, 48, 768
@@ -217,7 +220,7 @@ def substudies() -> Workload:
 
     def add(name, S, mal, eps, sigma_hw=0.002):
         run = Run(len(sets), benign_mode=NOISE_BLOCK, sigma_b=sigma_hw, tamper=T_ADD, eps=eps,
-                  carry=SUBSTUDY_CARRY, label=name)
+                  exact_norm=True, carry=SUBSTUDY_CARRY, label=name)
         sets.append(RefSet(S, S, C, T, H, n_out, tuple(mal), (run,)))
 
     for k in SUBSTUDY_DEPTHS:

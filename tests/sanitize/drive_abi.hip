@@ -22,7 +22,7 @@ int main() {
     void* q = reinterpret_cast<void*>(8);    // misaligned
     float* fp = static_cast<float*>(p);
     uint16_t* hp = static_cast<uint16_t*>(p);
-    expect(cdt_version(), 6, "version");
+    expect(cdt_version(), CDT_INTERFACE_VERSION, "version");
     expect(cdt_outlier_gain(40000, 1, 20.f, 0, 0, fp, nullptr), CDT_ELIMIT, "gain H");
     expect(cdt_outlier_gain(16, 17, 20.f, 0, 0, fp, nullptr), CDT_EINVAL, "gain n_out");
     expect(cdt_ref_synth(2, 2, 3, 12, 0, 0, 0, fp, fp, nullptr), CDT_EINVAL, "synth H%8");
@@ -81,6 +81,20 @@ int main() {
            "launch align");
     expect(cdt_auroc_launch(2, p, fp, 64, 0, 2, up, nullptr, nullptr, nullptr), CDT_EINVAL,
            "launch pooled");
+    expect(cdt_drift_score_noalloc(16, 1024, 256, 8192, hp, fp, fp, nullptr, nullptr), CDT_ELIMIT,
+           "noalloc scratch");
+    expect(cdt_drift_score_noalloc(2, 2, 3, 16, static_cast<uint16_t*>(q), fp, fp, nullptr,
+                                   nullptr), CDT_EALIGN, "noalloc align");
+    expect(cdt_auroc_values(2, nullptr, nullptr, nullptr, static_cast<double*>(p), nullptr),
+           CDT_EINVAL, "values counts");
+    expect(cdt_auroc_values((1u << 24) + 1, up, nullptr, nullptr, static_cast<double*>(p),
+                            nullptr), CDT_ELIMIT, "values n_cfg");
+    sp.carry = 0.5;
+    expect(cdt_tamper_scale_exact(65, 2, 2, 16, &sp, fp, 0.1, fp, nullptr, p, 1 << 20, nullptr),
+           CDT_ELIMIT, "exact chain S");
+    expect(cdt_tamper_scale_exact(4, 2, 2, 16, &sp, fp, 0.1, nullptr, nullptr, p, 1 << 20,
+                                  nullptr), CDT_EINVAL, "exact chain tscale");
+    sp.carry = 0.0;
     if (cdt_last_error()[0] == '\0') bad = 1;
     return bad;
 }

@@ -160,8 +160,16 @@ def test_sim_param_validation(cdt):
     assert L.cdt_sim_score(4, 2, 2, 16, ctypes.byref(p), 16, None, 16, None, 16, 1 << 20,
                            None) == cdt.EINVAL
     assert "carry" in _err(cdt)
-    assert L.cdt_tamper_scale_exact(4, 2, 2, 16, ctypes.byref(p), 16, 0.1, 16, None, 16,
+    # under the propagation model the exact-norm scale is defined (from the
+    # attacker's untampered live output); its argument checks still apply
+    assert L.cdt_tamper_scale_exact(65, 2, 2, 16, ctypes.byref(p), 16, 0.1, 16, None, 16,
+                                    1 << 20, None) == cdt.ELIMIT
+    assert L.cdt_tamper_scale_exact(4, 2, 2, 16, ctypes.byref(p), 16, 0.1, None, None, 16,
                                     1 << 20, None) == cdt.EINVAL
+    assert "tscale is NULL" in _err(cdt)
+    assert L.cdt_tamper_scale_exact(4, 2, 2, 16, ctypes.byref(p), 16, 0.1, 16, None, 16,
+                                    8, None) == cdt.EINVAL
+    assert "workspace" in _err(cdt)
     p = cdt.sim_params(seed=0, cfg_id=0)
     p.redraw = 2
     assert L.cdt_canary_sim(4, 2, 2, 16, ctypes.byref(p), 16, 16, None) == cdt.EINVAL

@@ -519,3 +519,77 @@ def test_chain_canary_base_picks_the_run_canaries(orc):
     unshifted = orc.canary_sim(np.ascontiguousarray(ref[:, 2:4]),
                                tscale=np.ascontiguousarray(ts[:, 2:4]), **kw)
     assert not np.array_equal(unshifted, whole[:, 2:4])
+
+
+# ----------------------------------------------------------------------------
+# exact-norm Gaussian tamper under the propagation model
+# ----------------------------------------------------------------------------
+def _tamper_normals_sumsq(orc, seed, cfg_id, s, c, n):
+    """Sum of squares of the TAMPER_ADD normals of block (s, c), element by
+    element from the Philox words (call e/2, words 0-1 even / 2-3 odd) and
+    the Irwin-Hall rule, in fp64 in index order."""
+    tot = 0.0
+    key = np.array([seed & 0xFFFFFFFF, seed >> 32], np.uint32)
+    for e in range(n):
+        w = orc.philox(np.array([e >> 1, c, s, (4 << 24) | cfg_id], np.uint32), key)
+        z = float(orc.z16(w[0], w[1]) if e % 2 == 0 else orc.z16(w[2], w[3]))
+        tot += z * z
+    return tot
+
+
+def test_exact_norm_chain_first_stage_is_the_independent_form(orc):
+    """An attacker at stage 0 has no upstream: its exact-norm scale under the
+    propagation model equals the independent-stage one bit for bit."""
+    S, C, T, H = 5, 3, 6, 64
+    ref = orc.ref_synth(S, C, T, H, 9, 0, np.ones(H, np.float32))
+    q, m = orc.ref_stats(ref)
+    _, bs = orc.block_scales(T, H, q, m, 0.0, 0.01)
+    kw = dict(seed=9, cfg_id=5, benign_mode=NOISE_BLOCK, sigma_b=0.01, bscale=bs)
+    ts, nm = orc.tamper_scale_exact(ref, 0.05, carry=0.7, mal_mask=1, tamper=T_ADD, **kw)
+    ts_i, nm_i = orc.tamper_scale_exact(ref, 0.05, **kw)
+    np.testing.assert_array_equal(ts[0], ts_i[0])
+    np.testing.assert_array_equal(nm[0], nm_i[0])
+    assert (ts[1:] == 0).all() and (nm[1:] == 0).all()  # benign stages: no scale
+
+
+def test_exact_norm_chain_uses_the_untampered_live_output(orc):
+    """For an attacker at stage 3 of a carried pipeline, sum v^2 is the norm
+    of the stage's own benign output given the live error carried in: the
+    all-benign chain's stage-3 fp16 output reproduces it to fp16 rounding,
+    while the reference block alone does not; sum N^2 is the TAMPER_ADD
+    normals' of that block, recomputed from the Philox words."""
+    S, C, T, H, g, m = 6, 2, 8, 64, 0.7, 3
+    ref = orc.ref_synth(S, C, T, H, 4, 0, np.ones(H, np.float32))
+    kw = dict(seed=4, cfg_id=2, sigma_b=0.05)
+    ts, nm = orc.tamper_scale_exact(ref, 0.05, carry=g, mal_mask=1 << m, tamper=T_ADD, **kw)
+    h = _chain(orc, ref, g, **kw)
+    for c in range(C):
+        v16 = _h(h[m, c])
+        assert abs(nm[m, c, 0] / (v16 * v16).sum() - 1.0) < 2.0**-10
+        a2 = (ref[m, c].astype(np.float64) ** 2).sum()
+        assert abs(nm[m, c, 0] / a2 - 1.0) > 4 * 2.0**-10  # not the reference's norm
+        assert nm[m, c, 1] == _tamper_normals_sumsq(orc, 4, 2, m, c, T * H)
+
+
+def test_exact_norm_chain_colluders_in_pipeline_order(orc):
+    """Two colluders at stages 1 and 3: the second one's v carries the
+    first one's tamper (taken with its own exact scale; g^2 eps = 0.25 of
+    the reference norm reaches stage 3), and each added perturbation has
+    norm eps ||v|| (Section 3.2), measured as the change of the stage's fp16
+    output when it tampers."""
+    S, C, T, H, g, eps = 5, 2, 16, 128, 0.7, 0.5
+    ref = orc.ref_synth(S, C, T, H, 6, 0, np.ones(H, np.float32))
+    mal = (1 << 1) | (1 << 3)
+    kw = dict(seed=6, cfg_id=3, sigma_b=0.01)
+    ts, nm = orc.tamper_scale_exact(ref, eps, carry=g, mal_mask=mal, tamper=T_ADD, **kw)
+    only1 = _chain(orc, ref, g, mal_mask=1 << 1, tamper=T_ADD, tscale=ts, **kw)
+    benign = _chain(orc, ref, g, **kw)
+    both = _chain(orc, ref, g, mal_mask=mal, tamper=T_ADD, tscale=ts, **kw)
+    for c in range(C):
+        v3 = _h(only1[3, c])  # stage 3 untampered, downstream of the tampered stage 1
+        assert abs(nm[3, c, 0] / (v3 * v3).sum() - 1.0) < 2.0**-10
+        w3 = _h(benign[3, c])
+        assert abs(nm[3, c, 0] / (w3 * w3).sum() - 1.0) > 0.02
+        for s, base in ((1, benign), (3, only1)):
+            d = _h(both[s, c]) - _h(base[s, c])
+            assert abs(math.sqrt((d * d).sum()) / (eps * math.sqrt(nm[s, c, 0])) - 1.0) < 2e-3

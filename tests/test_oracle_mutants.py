@@ -62,13 +62,17 @@ MUTANTS = [
      "v = r32((double)v + (double)r32((double)tscale * (double)zt));",
      "v = r32((double)base + (double)r32((double)tscale * (double)zt));"),
     ("flip selects complement", "return (double)u < thr;", "return (double)u > thr;"),
-    ("carry sign", "float u = (s == 0) ? a : r32((double)a + (double)r32((double)g * (double)d));",
-     "float u = (s == 0) ? a : r32((double)a - (double)r32((double)g * (double)d));"),
+    ("carry sign", "return (s == 0) ? a : r32((double)a + (double)r32((double)g * (double)d));",
+     "return (s == 0) ? a : r32((double)a - (double)r32((double)g * (double)d));"),
     ("carry from reference", "d = r32(orc_f16_value(hb) - (double)a);",
      "d = r32(orc_f16_value(hb) - (double)u);"),
     ("exact norm without sqrt", "return zz > 0.0 ? r32(eps * sqrt(vv / zz)) : 0.0f;",
      "return zz > 0.0 ? r32(eps * vv / zz) : 0.0f;"),
     ("exact norm of reference", "vv += (double)v * (double)v;", "vv += (double)a * (double)a;"),
+    ("chain exact norm drops earlier tampers", "tscale[b], flip_p, scale_f, u, v);",
+     "0.0f, flip_p, scale_f, u, v);"),
+    ("chain exact norm of the reference", "float vt = (tamper_base == ORC_BASE_CLEAN) ? u : v;",
+     "float vt = a;"),
     # Eq. 4 and its ablations
     ("drift denominator from h", "        R += av * av;\n", "        R += hv * hv;\n"),
     ("drift without sqrt", "        return D == 0.0 ? 0.0 : INFINITY;\n    return sqrt(D / R);\n}\n\n/* Scores",
