@@ -1,0 +1,203 @@
+"""Full-size parity, every block: the SNR study (40 runs of 16 x 128 x 128 x
+4096), the 216-configuration sweep and the 70B-shaped workload (3 runs of
+16 x 256 x 256 x 8192), run in the launch configuration the benchmark times
+(per run canary_sim then drift_score; for the sweep, per reference set one
+batched live-pass launch and one batched Eq. 4 launch over its 24
+configurations; then one batched AUROC launch), against the
+CPU oracle's stored results for every (shard, canary) block of every run
+(tests/golden/fullsize_*.npz, written by tests/golden/make_fullsize.py from
+oracle/ alone; tests/test_golden_fullsize.py re-derives sampled blocks of
+those files with the oracle):
+  * every fp32 reference block and every fp16 live block by digest (a
+    single differing element changes it): bit for bit;
+  * every Eq. 4 score within 1e-5 relative of the oracle's fp64 score;
+  * Eqs. 5-6 end to end: the detector, scrambled-control and pooled counts
+    of the device's scores against the oracle's counts of its own scores,
+    exactly where both score tables round alike to fp32 (else only pairs
+    within 2e-5 of a tie may differ), and the random baseline's counts bit
+    for bit;
+  * the pre-registered criteria on the sweep (detector at or above the
+    success threshold, control mean inside its window).
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_19490_amd import workloads as W
+from tests.digest import digest_torch
+from tests.gpu_util import announce, rel_err, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+DRIFT_RTOL = 1e-5
+NEAR_TIE = 2e-5
+FLAGS = 1 | 2 | 8  # control, pooled, random baseline
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    return require_gpu()
+
+
+def load_golden(name):
+    z = np.load(os.path.join(GOLDEN, f"fullsize_{name}.npz"))
+    meta = json.loads(str(z["meta"]))
+    return z["score64"], z["hdig"], z["refdig"], meta
+
+
+def block_digests(torch, x):
+    """[S][C][T][H] device array -> [S][C] uint64 digests, one shard at a time."""
+    S, C = x.shape[:2]
+    out = np.empty((S, C), np.uint64)
+    for s in range(S):
+        out[s] = digest_torch(torch, x[s].reshape(C, -1)).cpu().numpy().view(np.uint64)
+    return out
+
+
+def near_tie_pairs(s64, mask, pooled):
+    """Pairs whose oracle scores lie within NEAR_TIE of each other: per canary
+    (any two stages), or for the pooled ranking every positive against every
+    negative score of the configuration."""
+    C, S = s64.shape
+    if not pooled:
+        n = 0
+        for t in range(C):
+            r = s64[t]
+            d = np.abs(r[:, None] - r[None, :]) <= NEAR_TIE * np.maximum(np.abs(r[:, None]),
+                                                                      np.abs(r[None, :]))
+            n += int(np.triu(d, 1).sum())
+        return n
+    pos = np.array([(mask >> s) & 1 for s in range(S)], bool)
+    p, q = s64[:, pos].ravel(), s64[:, ~pos].ravel()
+    d = np.abs(p[:, None] - q[None, :]) <= NEAR_TIE * np.maximum(np.abs(p[:, None]),
+                                                              np.abs(q[None, :]))
+    return int(d.sum())
+
+
+def check_counts(label, got, got_p, got_r, dev32, s64, mask, seed, cfg_id):
+    """Device counts of one configuration against the oracle's counts of its
+    own scores."""
+    want, want_p = oracle.auroc_config(s64.astype(np.float32), mask, seed=seed, cfg_id=cfg_id,
+                                       flags=FLAGS & 3)
+    C, S = s64.shape
+    np.testing.assert_array_equal(
+        got_r, oracle.random_baseline(C, S, mask, seed=seed, cfg_id=cfg_id), err_msg=label)
+    if np.array_equal(dev32, s64.astype(np.float32)):  # same fp32 scores: exact
+        np.testing.assert_array_equal(got, want, err_msg=label)
+        np.testing.assert_array_equal(got_p, want_p, err_msg=label)
+        return 0
+    amb = near_tie_pairs(s64, mask, False)
+    diff = int(np.abs(got.astype(np.int64) - want.astype(np.int64)).sum())
+    assert diff <= 2 * amb, (label, got, want, amb)
+    amb_p = near_tie_pairs(s64, mask, True)
+    diff_p = int(np.abs(got_p.astype(np.int64) - want_p.astype(np.int64)).sum())
+    assert diff_p <= 2 * amb_p, (label, got_p, want_p, amb_p)
+    return 1
+
+
+def run_workload(torch, cdt, name, batched=False):
+    """Every run of the workload as the benchmark launches it (batched: per
+    reference set one live-pass launch and one Eq. 4 launch over all its
+    runs, as the sweep runs); returns the comparison summary.  Per-block
+    digests and scores are compared as each run (or set) completes, the
+    counts after one batched AUROC launch."""
+    wl = W.get(name)
+    score64, hdig, refdig, meta = load_golden(name)
+    assert meta["cfg_ids"] == [r.cfg_id for rs in wl.ref_sets for r in rs.runs]
+    assert meta["shapes"] == [[rs.S, rs.C, rs.T, rs.H] for rs in wl.ref_sets]
+    max_elems = max(rs.elems * (len(rs.runs) if batched else 1) for rs in wl.ref_sets)
+    h_buf = torch.empty((max_elems,), dtype=torch.float16, device="cuda")
+    total = sum(rs.S * rs.C * len(rs.runs) for rs in wl.ref_sets)
+    scores = torch.empty((total,), dtype=torch.float32, device="cuda")
+    cfgs, labels, o_set, o_run = [], [], 0, 0
+    worst = 0.0
+    for rs in wl.ref_sets:
+        S, C, T, H = rs.S, rs.C, rs.T, rs.H
+        nb = S * C
+        announce(f"{name} set {rs.ref_set_id}: {S}x{C}x{T}x{H}, {len(rs.runs)} runs")
+        gain = cdt.outlier_gain(H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
+        ref = cdt.ref_synth(S, C, T, H, wl.seed, rs.ref_set_id, gain)
+        ws = cdt.workspace(S, C, T, H, ref)
+        sumsq, sumabs = cdt.ref_stats(ref, ws=ws)
+        got_rd = block_digests(torch, ref)
+        bad = int((got_rd != refdig[o_set:o_set + nb].reshape(S, C)).sum())
+        assert bad == 0, f"{name} set {rs.ref_set_id}: {bad} reference blocks differ"
+        o_set += nb
+        kws, hs = [], []
+        for r, run in enumerate(rs.runs):
+            ts, bs = cdt.block_scales(sumsq, sumabs, T, H, run.eps, run.sigma_b)
+            kws.append(dict(seed=wl.seed, cfg_id=run.cfg_id, benign_mode=run.benign_mode,
+                            benign_dist=run.benign_dist, sigma_b=run.sigma_b,
+                            mal_mask=rs.mal_mask, tamper=run.tamper,
+                            tamper_base=run.tamper_base, flip_p=run.flip_p, scale=run.scale,
+                            bscale=bs, tscale=ts))
+            k = r if batched else 0
+            hs.append(h_buf[k * rs.elems:(k + 1) * rs.elems].view(S, C, T, H))
+        if batched:
+            cdt.canary_sim_batch([(ref, hs[r], kws[r]) for r in range(len(rs.runs))])
+            cdt.drift_score_batch([(hs[r], ref, scores[o_run + r * nb:o_run + (r + 1) * nb]
+                                    .view(C, S), None) for r in range(len(rs.runs))])
+        for r, run in enumerate(rs.runs):
+            h = hs[r]
+            sc = scores[o_run:o_run + nb].view(C, S)
+            if not batched:
+                cdt.canary_sim(ref, out=h, **kws[r])
+                cdt.drift_score(h, ref, out=sc, ws=ws)
+            got_hd = block_digests(torch, h)
+            bad = int((got_hd != hdig[o_run:o_run + nb].reshape(S, C)).sum())
+            assert bad == 0, f"{name} {run.label}: {bad} of {nb} live blocks differ"
+            err = rel_err(sc.cpu().numpy(), score64[o_run:o_run + nb].reshape(C, S))
+            assert err < DRIFT_RTOL, (run.label, err)
+            worst = max(worst, err)
+            cfgs.append((S, C, o_run, rs.mal_mask, run.cfg_id))
+            labels.append(run.label)
+            o_run += nb
+        del ref, ws, sumsq, sumabs
+    counts, pooled, base = cdt.auroc(cfgs, scores, seed=wl.seed, flags=FLAGS)
+    vals = cdt.auroc_values(counts, pooled, base).cpu().numpy()
+    c, p, r = cdt.u64(counts), cdt.u64(pooled), cdt.u64(base)
+    dev = scores.cpu().numpy()
+    del h_buf, scores
+    torch.cuda.empty_cache()
+    announce(f"{name}: counts of {len(cfgs)} configurations against the oracle")
+    inexact = 0
+    for g, (S, C, off, mask, cid) in enumerate(cfgs):
+        s64 = score64[off:off + S * C].reshape(C, S)
+        inexact += check_counts(f"{name} {labels[g]}", c[g], p[g], r[g],
+                                dev[off:off + S * C].reshape(C, S), s64, mask, wl.seed, cid)
+    return {"configs": len(cfgs), "worst_rel": worst, "inexact_count_configs": inexact,
+            "values": vals, "labels": labels}
+
+
+def test_snr_every_block(gpu):
+    torch, cdt = gpu
+    out = run_workload(torch, cdt, "snr")
+    assert out["configs"] == 40
+    announce(f"snr: worst score error {out['worst_rel']:.2e}, "
+             f"{out['inexact_count_configs']} configurations compared with the near-tie rule")
+
+
+def test_sweep_every_block(gpu):
+    torch, cdt = gpu
+    with open(os.path.join(GOLDEN, "paper_outcomes.json")) as f:
+        gold = json.load(f)
+    out = run_workload(torch, cdt, "sweep", batched=True)
+    assert out["configs"] == 216
+    v = out["values"]
+    assert v[:, 0].min() >= gold["success_auroc"]["value"]
+    lo, hi = gold["control_window"]["value"]
+    assert lo <= float(v[:, 2].mean()) <= hi
+    announce(f"sweep: worst score error {out['worst_rel']:.2e}, "
+             f"{out['inexact_count_configs']} configurations compared with the near-tie rule")
+
+
+def test_llama70b_every_block(gpu):
+    torch, cdt = gpu
+    out = run_workload(torch, cdt, "llama70b")
+    assert out["configs"] == 3
+    assert (out["values"][:, 0] == 1.0).all()  # the detector separates every run fully
+    announce(f"llama70b: worst score error {out['worst_rel']:.2e}")

@@ -2,13 +2,12 @@
 configuration the benchmark times, checked against the CPU oracle.
 
 The 7B-shaped workload is regenerated whole by the oracle, block by block
-on host threads.  At sizes the oracle cannot regenerate whole in a test,
-sampled (shard, canary) blocks are regenerated one by one and compared bit
-for bit (references, block scales, live fp16 activations) and within 1e-5
-(drift scores); AUROC counts are checked by properties that hold at any
-size (pair counts, the detector at 1.0 where the tamper dwarfs the noise
-floor, the scrambled-label control inside the pre-registered window).  Small configurations of the sweep and
-the paper's own shape are compared whole, counts included.
+on host threads, at test time.  On the 70B shape every shard of eight
+canaries is regenerated the same way, and the ablations, the propagation
+model and the exact-norm scales are checked there too.  The paper's own
+shape is compared whole, counts included.  (Every block of the SNR study,
+the sweep and the 70B runs is compared with stored oracle results in
+test_gpu_fullsize.py.)
 """
 import json
 import math
@@ -134,47 +133,6 @@ def counts_match(got, scores64, mask, seed, cfg_id):
                     amb += 1
     diff = int(np.abs(got[:6].astype(np.int64) - want.astype(np.int64)).sum())
     return diff <= 2 * amb
-
-
-def detector_properties(cdt, counts, cfgs):
-    c = cdt.u64(counts)
-    for g, (S, C, off, mask, cid) in enumerate(cfgs):
-        n_pos = bin(mask).count("1")
-        assert int(c[g][2]) == C * n_pos * (S - n_pos)
-        assert int(c[g][5]) == C * (S - n_pos - 1)
-        assert int(c[g][0]) + int(c[g][1]) <= int(c[g][2])
-    return c
-
-
-# ----------------------------------------------------------------------------
-def _single_set_workload(gpu, name, nsample=4, every_shard_runs=()):
-    torch, cdt = gpu
-    wl = W.get(name)
-    rs = wl.ref_sets[0]
-    announce(f"{name}: preparing {rs.S}x{rs.C}x{rs.T}x{rs.H}")
-    gs = GpuSet(torch, cdt, wl, rs)
-    gain_o = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
-    np.testing.assert_array_equal(gs.gain.cpu().numpy(), gain_o)
-    scores, cfgs = [], []
-    for k, run in enumerate(rs.runs):
-        score, ts, bs = gs.run(run)
-        torch.cuda.synchronize()
-        if k < 6 or k % 10 == 0 or k == len(rs.runs) - 1:
-            check_blocks(gs, run, score, ts, bs, sample_blocks(rs, nsample, k), gain_o)
-        if k in every_shard_runs:  # every shard of four canaries, on host threads
-            canaries = sorted({int(x) for x in np.linspace(0, rs.C - 1, 4)})
-            announce(f"{name} run {run.label}: every shard of {len(canaries)} canaries")
-            check_blocks_threaded(gs, run, score, ts, bs,
-                                  [(s_, c_) for s_ in range(rs.S) for c_ in canaries], gain_o)
-        scores.append(score)
-        cfgs.append((rs.S, rs.C, k * rs.C * rs.S, rs.mal_mask, run.cfg_id))
-    flat = torch.cat([s.reshape(-1) for s in scores])
-    counts, pooled, _ = cdt.auroc(cfgs, flat, seed=wl.seed)
-    torch.cuda.synchronize()
-    c = detector_properties(cdt, counts, cfgs)
-    del gs, flat, scores
-    torch.cuda.empty_cache()
-    return wl, rs, c, cdt.u64(pooled)
 
 
 def host_threads():
@@ -366,101 +324,6 @@ def test_llama70b_every_shard(gpu):
         with ThreadPoolExecutor(max_workers=host_threads()) as ex:
             assert all(ex.map(redraw, range(rs.S)))
     del gs
-    torch.cuda.empty_cache()
-
-
-def test_llama7b(gpu):
-    wl, rs, c, _ = _single_set_workload(gpu, "llama7b")
-    for g in range(len(rs.runs)):
-        assert int(c[g][0]) == int(c[g][2]), rs.runs[g].label  # detector at 1.0
-
-
-def test_llama70b(gpu):
-    wl, rs, c, pooled = _single_set_workload(gpu, "llama70b")
-    for g, run in enumerate(rs.runs):
-        assert int(c[g][0]) == int(c[g][2]), run.label
-        a_ctrl = int(c[g][3]) / int(c[g][5])
-        # per canary the scrambled stage's rank among the B benign stages is
-        # uniform, so A_ctrl(t) is uniform on {0, 1/(B-1), ..., 1}: variance
-        # (B^2 - 1) / (12 (B - 1)^2); five standard deviations of the mean
-        B = rs.S - len(rs.mal_shards)
-        sd = math.sqrt((B * B - 1) / 12.0) / (B - 1) / math.sqrt(rs.C)
-        assert abs(a_ctrl - 0.5) < 5 * sd, a_ctrl
-        assert int(pooled[g][0]) == int(pooled[g][2])  # pooled ranking separates fully too
-
-
-def test_snr_curve(gpu):
-    # every shard checked on a Gaussian and a Student-t run at sigma_b near
-    # 0.01, and on the noisiest Student-t run
-    wl, rs, c, _ = _single_set_workload(gpu, "snr", nsample=2, every_shard_runs=(22, 23, 39))
-    auc = [(int(x[0]) + 0.5 * int(x[1])) / int(x[2]) for x in c]
-    gauss = auc[0::2]
-    t3 = auc[1::2]
-    assert gauss[0] == 1.0 and t3[0] == 1.0  # noise floor far below the tamper
-    assert gauss[-1] < gauss[0] and t3[-1] < t3[0]  # the floor crosses the tamper
-    assert min(auc) >= 0.0 and max(auc) <= 1.0
-
-
-def test_sweep(gpu, gold):
-    """All 216 runs as the benchmark launches them; three small runs compared
-    whole with the oracle (scores and counts), one run of every shape block by
-    block on host threads, a large one by sampled blocks; the pre-registered
-    criteria on the batch."""
-    torch, cdt = gpu
-    wl = W.sweep()
-    max_elems = max(rs.elems for rs in wl.ref_sets)
-    h_buf = torch.empty((max_elems,), dtype=torch.float16, device="cuda")
-    scores, cfgs, off = [], [], 0
-    whole = {0, 13, 23}  # add/flip/scale/mixed mix on the smallest set
-    whole_scores = {}
-    for rs in wl.ref_sets:
-        announce(f"sweep set {rs.ref_set_id}: {rs.S}x{rs.C}x{rs.T}x{rs.H}")
-        gs = GpuSet(torch, cdt, wl, rs, h=h_buf[:rs.elems].view(rs.S, rs.C, rs.T, rs.H))
-        gain_o = oracle.outlier_gain(rs.H, rs.n_out, W.OUTLIER_GAIN, wl.seed, rs.ref_set_id)
-        ref_o = oracle.ref_synth(rs.S, rs.C, rs.T, rs.H, wl.seed, rs.ref_set_id, gain_o) \
-            if rs.ref_set_id == 0 else None
-        for run in rs.runs:
-            score, ts, bs = gs.run(run)
-            torch.cuda.synchronize()
-            if run.cfg_id in whole:
-                announce(f"sweep cfg {run.cfg_id} whole")
-                q, m = oracle.ref_stats(ref_o)
-                ts_o, bs_o = oracle.block_scales(rs.T, rs.H, q, m, run.eps, run.sigma_b)
-                h_o = oracle.canary_sim(ref_o, seed=wl.seed, cfg_id=run.cfg_id,
-                                        sigma_b=run.sigma_b, mal_mask=rs.mal_mask,
-                                        tamper=run.tamper, tscale=ts_o, flip_p=run.flip_p,
-                                        scale=run.scale)
-                assert np.array_equal(gs.h.cpu().numpy().view(np.uint16), h_o)
-                s64, _, _ = oracle.drift_score(h_o, ref_o)
-                assert rel_err(score.cpu().numpy(), s64) < DRIFT_RTOL
-                whole_scores[run.cfg_id] = s64
-            if rs.ref_set_id == len(wl.ref_sets) - 1 and run.cfg_id % 24 in (3, 14):
-                check_blocks(gs, run, score, ts, bs, sample_blocks(rs, 2, run.cfg_id), gain_o)
-            if run.cfg_id % 24 == (5 * rs.ref_set_id + 2) % 24:
-                # one configuration of every shape, every block, a different
-                # tamper setting per shape
-                announce(f"sweep cfg {run.cfg_id} every block, {host_threads()} threads")
-                check_blocks_threaded(gs, run, score, ts, bs,
-                                      [(s_, c_) for s_ in range(rs.S) for c_ in range(rs.C)],
-                                      gain_o)
-            scores.append(score.clone())
-            cfgs.append((rs.S, rs.C, off, rs.mal_mask, run.cfg_id))
-            off += rs.S * rs.C
-        del gs
-    flat = torch.cat([s.reshape(-1) for s in scores])
-    counts, _, _ = cdt.auroc(cfgs, flat, seed=wl.seed)
-    torch.cuda.synchronize()
-    c = detector_properties(cdt, counts, cfgs)
-    for cid, s64 in whole_scores.items():
-        g = [k for k, x in enumerate(cfgs) if x[4] == cid][0]
-        assert counts_match(c[g], s64, cfgs[g][3], wl.seed, cid), cid
-    strict = [int(x[0]) / int(x[2]) for x in c]
-    assert min(strict) >= gold["success_auroc"]["value"]
-    assert sum(1 for a in strict if a == 1.0) == len(strict)
-    ctrl = np.mean([int(x[3]) / int(x[5]) for x in c])
-    lo, hi = gold["control_window"]["value"]
-    assert lo <= ctrl <= hi
-    del h_buf, flat, scores
     torch.cuda.empty_cache()
 
 
