@@ -263,6 +263,9 @@ def run_main(torch, cdt, W, args):
     # memory system gives the drift kernel's access pattern.
     read_ms = time_ms(torch, lambda: cdt.drift_read_stream(big.h, big.ref, ws=big.ws), 7)
     read_gbps = big.rs.elems * DRIFT_BYTES_PER_ELEM / (read_ms * 1e-3) / 1e9
+    # and the live pass's reads and writes with no random numbers (h = fp16(a))
+    sim_stream_ms = time_ms(torch, lambda: cdt.canary_sim_stream(big.ref, out=big.h), 7)
+    sim_stream_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (sim_stream_ms * 1e-3) / 1e9
 
     res = {
         "metric": "drift-scored activation GB/s",
@@ -304,6 +307,8 @@ def run_main(torch, cdt, W, args):
             "share_of_step": round(sim_avg * len(big.rs.runs) / ms_step, 4)
             if len(preps) == 1 else None,
             "bound": "valu+hbm",
+            "stream_GBps": round(sim_stream_gbps, 1),
+            "frac_of_stream": round(sim_gbps / sim_stream_gbps, 4),
             "valu_busy": valu_busy,
             "valu_instr_per_element": valu_per_el,
         },
@@ -506,13 +511,67 @@ def substudies(torch, cdt, W):
             "studies": out}
 
 
+class SweepBatches:
+    """The sweep's batched launches: per reference set, one live-pass launch
+    over all its configurations (each into its own activation array) and one
+    Eq. 4 launch over them, tables prepared once."""
+
+    def __init__(self, torch, cdt, wl, preps, views):
+        most = max(len(p.rs.runs) * p.rs.elems for p in preps)
+        self.h = torch.empty((most,), dtype=torch.float16, device="cuda")
+        self.sets, k = [], 0
+        for p in preps:
+            rs = p.rs
+            hs = [self.h[r * rs.elems:(r + 1) * rs.elems].view(rs.S, rs.C, rs.T, rs.H)
+                  for r in range(len(rs.runs))]
+            sim = cdt.sim_batch([(p.ref, hs[r], sim_kwargs(wl, rs, run, *p.scales[r]))
+                                 for r, run in enumerate(rs.runs)])
+            drift = cdt.drift_batch([(hs[r], p.ref, views[k + r], None)
+                                     for r in range(len(rs.runs))])
+            self.sets.append((sim, drift, rs))
+            k += len(rs.runs)
+
+
+def sweep_step_batched(cdt, wl, sb, scores, cfgs, auroc_ws, counts, pooled, ev=None):
+    """One pass of the sweep with the batched launches (per reference set: the
+    live pass of its configurations, then Eq. 4 of them), then the AUROC."""
+    for i, (sim, drift, _) in enumerate(sb.sets):
+        if ev is not None:
+            ev[i][0].record()
+        cdt.canary_sim_batch(sim)
+        if ev is not None:
+            ev[i][1].record()
+            ev[i][2].record()
+        cdt.drift_score_batch(drift)
+        if ev is not None:
+            ev[i][3].record()
+    cdt.auroc_launch(auroc_ws, len(cfgs), scores, seed=wl.seed,
+                     flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED, counts=counts, pooled=pooled)
+
+
 def run_sweep(torch, cdt, W, reps):
+    import numpy as np
     wl = W.sweep()
     log("sweep: preparing 9 reference sets")
     max_elems = max(rs.elems for rs in wl.ref_sets)
     h_buf = torch.empty((max_elems,), dtype=torch.float16, device="cuda")
     preps = [Prepared(torch, cdt, W, wl, rs, h_buf=h_buf) for rs in wl.ref_sets]
     scores, views, cfgs, counts, pooled, auroc_ws = setup_batch(torch, cdt, wl, preps)
+    sweep_elems = sum(len(p.rs.runs) * p.rs.elems for p in preps)
+    # the batched step (the configurations/s the sweep reports)
+    sb = SweepBatches(torch, cdt, wl, preps, views)
+    E = torch.cuda.Event
+    step_b = lambda ev=None: sweep_step_batched(cdt, wl, sb, scores, cfgs, auroc_ws, counts,
+                                                pooled, ev)
+    batched_ms = time_ms(torch, step_b, reps)
+    bev = [[E(enable_timing=True) for _ in range(4)] for _ in sb.sets]
+    step_b(bev)
+    torch.cuda.synchronize()
+    sim_b = sum(e[0].elapsed_time(e[1]) for e in bev)
+    drift_b = sum(e[2].elapsed_time(e[3]) for e in bev)
+    counts_b, pooled_b = cdt.u64(counts), cdt.u64(pooled)
+    del sb
+    torch.cuda.empty_cache()
     gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled)  # warmup
     torch.cuda.synchronize()
     times = []
@@ -563,11 +622,20 @@ def run_sweep(torch, cdt, W, reps):
     strict = [float(x[0]) for x in vals]
     ctrl = sum(int(x[3]) for x in c) / sum(int(x[5]) for x in c)  # pooled over configurations
     ctrl_mean = float(vals[:, 2].mean())
-    log(f"sweep: {ms:.2f} ms for {len(cfgs)} configs")
+    log(f"sweep: {batched_ms:.2f} ms batched, {ms:.2f} ms per-configuration launches, "
+        f"for {len(cfgs)} configs")
     out = {
         "configs": len(cfgs),
-        "ms": round(ms, 3),
-        "configs_per_s": round(len(cfgs) / (ms * 1e-3), 1),
+        "ms": round(batched_ms, 3),
+        "configs_per_s": round(len(cfgs) / (batched_ms * 1e-3), 1),
+        "step": "per reference set: one batched live-pass launch and one batched Eq. 4 launch "
+                "over its 24 configurations; one AUROC launch",
+        "drift_score_GBps": round(sweep_elems * DRIFT_BYTES_PER_ELEM / (drift_b * 1e-3) / 1e9, 1),
+        "canary_sim_GBps": round(sweep_elems * SIM_BYTES_PER_ELEM / (sim_b * 1e-3) / 1e9, 1),
+        "batched_counts_equal": bool(np.array_equal(counts_b, cdt.u64(counts)) and
+                                     np.array_equal(pooled_b, cdt.u64(pooled))),
+        "unbatched_ms": round(ms, 3),
+        "unbatched_configs_per_s": round(len(cfgs) / (ms * 1e-3), 1),
         "fused_ms": round(fused_ms, 3),
         "fused_configs_per_s": round(len(cfgs) / (fused_ms * 1e-3), 1),
         "sim_excluded_ms": round(score_ms, 3),
@@ -578,9 +646,10 @@ def run_sweep(torch, cdt, W, reps):
         "configs_at_auroc_1": sum(1 for x in strict if x == 1.0),
         "control_pooled_mean": round(ctrl_mean, 4),
         "control_pooled_pairs": round(ctrl, 4),
-        "drift_score_GBps": round(sweep_elems * DRIFT_BYTES_PER_ELEM / (drift_total * 1e-3) / 1e9,
-                                  1),
-        "canary_sim_GBps": round(sweep_elems * SIM_BYTES_PER_ELEM / (sim_total * 1e-3) / 1e9, 1),
+        "unbatched_drift_score_GBps": round(
+            sweep_elems * DRIFT_BYTES_PER_ELEM / (drift_total * 1e-3) / 1e9, 1),
+        "unbatched_canary_sim_GBps": round(
+            sweep_elems * SIM_BYTES_PER_ELEM / (sim_total * 1e-3) / 1e9, 1),
     }
     del preps, h_buf, scores
     torch.cuda.empty_cache()
@@ -614,7 +683,23 @@ def config_runs(torch, cdt, W, name):
     # the compute-free read of the same arrays: what a launch of this size gets
     read_ms = time_ms(torch, lambda: cdt.drift_read_stream(prep.h, prep.ref, ws=prep.ws), 5)
     read_gbps = rs.elems * DRIFT_BYTES_PER_ELEM / (read_ms * 1e-3) / 1e9
+    # the runs' Eq. 4 as one batched launch (each run's activations in its own
+    # array; as many runs as fit 16 GiB of activations)
+    nb = max(1, min(len(rs.runs), (16 << 30) // (2 * rs.elems)))
+    hs = torch.empty((nb, rs.S, rs.C, rs.T, rs.H), dtype=torch.float16, device="cuda")
+    scs = torch.empty((nb, rs.C, rs.S), dtype=torch.float32, device="cuda")
+    for k in range(nb):
+        cdt.canary_sim(prep.ref, out=hs[k], **sim_kwargs(wl, rs, rs.runs[k], *prep.scales[k]))
+    drift = cdt.drift_batch([(hs[k], prep.ref, scs[k], None) for k in range(nb)])
+    batch_ms = time_ms(torch, lambda: cdt.drift_score_batch(drift), 5)
+    batch_bytes = nb * nbytes
+    del hs, scs, drift
     out = {"shape_SxCxTxH": [rs.S, rs.C, rs.T, rs.H],
+           "drift_batched": {
+               "runs": nb, "ms": round(batch_ms, 4),
+               "GBps": round(batch_bytes / (batch_ms * 1e-3) / 1e9, 1),
+               "frac_of_hbm_peak": round(batch_bytes / (batch_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                                         4)},
            "drift_ms": round(drift_ms, 4),
            "drift_GBps": round(nbytes / (drift_ms * 1e-3) / 1e9, 1),
            "drift_frac_of_hbm_peak": round(nbytes / (drift_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),

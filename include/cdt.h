@@ -69,11 +69,13 @@ extern "C" {
 #define CDT_STREAM_ALT_T3 11
 
 /* Interface version; changes whenever a layout, a generator rule or the set
- * of entry points changes (8: cdt_drift_score_noalloc added; 7:
- * cdt_auroc_values added, NaN scores rank above every number).
- * cdt_version() returns the library's, which a caller compares with the
- * CDT_INTERFACE_VERSION of the header it was built with. */
-#define CDT_INTERFACE_VERSION 8
+ * of entry points changes (9: batched live pass and Eq. 4, the live-pass
+ * stream aid, exact-norm scales under the propagation model; 8:
+ * cdt_drift_score_noalloc added; 7: cdt_auroc_values added, NaN scores
+ * rank above every number).  cdt_version() returns the library's, which a
+ * caller compares with the CDT_INTERFACE_VERSION of the header it was
+ * built with. */
+#define CDT_INTERFACE_VERSION 9
 int cdt_version(void);
 
 /* Description of the last error on the calling thread ("" if none). */
@@ -189,6 +191,35 @@ typedef struct cdt_sim_params {
 int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
                    const float* ref, uint16_t* h, void* stream);
 
+/* The live pass of several runs in one launch (the factorial sweep generates
+ * the configurations of a reference set together): job j writes its own h
+ * from its ref with its own parameters, bitwise as cdt_canary_sim would.
+ * The chunks of all jobs form one grid, so short runs share the launch's
+ * ramp-up and tail.  Every job must use the same benign_dist and benign_mode
+ * and carry 0 (CDT_EINVAL otherwise); their shapes, tamper settings and
+ * scales may differ.  jobs and each p: HOST, read during the call (the
+ * job table is copied into ws on `stream`).  At most 65536 jobs.
+ * ws: cdt_sim_batch_workspace_bytes(n_jobs) device bytes. */
+typedef struct cdt_sim_job {
+    uint32_t S, C, T, H;
+    const cdt_sim_params* p;  /* host                            */
+    const float* ref;         /* device fp32 [S][C][T][H]        */
+    uint16_t* h;              /* device fp16 bits [S][C][T][H]   */
+} cdt_sim_job;
+
+size_t cdt_sim_batch_workspace_bytes(uint32_t n_jobs);
+int cdt_canary_sim_batch(uint32_t n_jobs, const cdt_sim_job* jobs, void* ws, size_t ws_bytes,
+                         void* stream);
+
+/* Measurement aid for the live pass's memory bound: reads ref and writes h
+ * exactly as cdt_canary_sim does for Gaussian noise on independent stages
+ * (the same chunks, loads, prefetch and stores), with the live-pass
+ * arithmetic replaced by h = fp16_rne(a), no random numbers drawn.  Its rate
+ * is what the memory system delivers for the live pass's 4 B-read and
+ * 2 B-write access pattern.  Errors as cdt_canary_sim. */
+int cdt_canary_sim_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,
+                          uint16_t* h, void* stream);
+
 /* Per-block scale of the exact-norm Gaussian tamper of Section 3.2,
  * tau(v) = v + eps ||v||_F N / ||N||_F: with v the untampered output of the
  * block (a + delta, formed exactly as cdt_canary_sim forms it, or a itself
@@ -258,6 +289,31 @@ int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16
 #define CDT_NOALLOC_SCRATCH_BYTES 8388608u
 int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
                             const float* ref, float* score, double* num_den, void* stream);
+
+/* Eq. 4 over several arrays in one launch (the factorial sweep scores the
+ * configurations of a reference set together): job j scores its own
+ * h[S][C][T][H] against its ref into its score[C][S] (num_den optional),
+ * bitwise as cdt_drift_score would.  The chunks of all jobs form one grid, so
+ * short arrays share the launch's ramp-up and tail instead of paying one
+ * each, and one combine launch finishes every block.  jobs: HOST array,
+ * validated and copied into ws during the call (reusable when the call
+ * returns); jobs with S*C = 0 are skipped.  At most 65536 jobs.
+ * ws: cdt_drift_batch_workspace_bytes(n_jobs, jobs) device bytes (the job
+ * table and every job's partial sums); calls that can overlap need their
+ * own. */
+typedef struct cdt_drift_job {
+    uint32_t S, C, T, H;
+    const uint16_t* h;   /* device fp16 bits [S][C][T][H]      */
+    const float* ref;    /* device fp32 [S][C][T][H]           */
+    float* score;        /* device fp32 [C][S] (written)        */
+    double* num_den;     /* device fp64 [C][S][2] or NULL       */
+} cdt_drift_job;
+
+/* Workspace bytes for cdt_drift_score_batch on these jobs (0 if a job's
+ * shape is invalid; shapes only, pointers are not looked at). */
+size_t cdt_drift_batch_workspace_bytes(uint32_t n_jobs, const cdt_drift_job* jobs);
+int cdt_drift_score_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws, size_t ws_bytes,
+                          void* stream);
 
 /* Measurement aid for Eq. 4's memory bound: reads h and ref exactly as
  * cdt_drift_score does (the same chunks, loads, lane exchange and order)

@@ -64,6 +64,31 @@ class AurocCfg(ctypes.Structure):
     ]
 
 
+class DriftJob(ctypes.Structure):
+    _fields_ = [
+        ("S", ctypes.c_uint32),
+        ("C", ctypes.c_uint32),
+        ("T", ctypes.c_uint32),
+        ("H", ctypes.c_uint32),
+        ("h", ctypes.c_void_p),
+        ("ref", ctypes.c_void_p),
+        ("score", ctypes.c_void_p),
+        ("num_den", ctypes.c_void_p),
+    ]
+
+
+class SimJob(ctypes.Structure):
+    _fields_ = [
+        ("S", ctypes.c_uint32),
+        ("C", ctypes.c_uint32),
+        ("T", ctypes.c_uint32),
+        ("H", ctypes.c_uint32),
+        ("p", ctypes.POINTER(SimParams)),
+        ("ref", ctypes.c_void_p),
+        ("h", ctypes.c_void_p),
+    ]
+
+
 _u32, _u64, _f, _d, _vp, _sz = (ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float, ctypes.c_double,
                                 ctypes.c_void_p, ctypes.c_size_t)
 _SIGS = {
@@ -76,6 +101,11 @@ _SIGS = {
     "cdt_block_scales": ([_u64, _u32, _u32, _vp, _vp, _d, _d, _vp, _vp, _vp], ctypes.c_int),
     "cdt_canary_sim": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp],
                        ctypes.c_int),
+    "cdt_canary_sim_stream": ([_u32, _u32, _u32, _u32, _vp, _vp, _vp], ctypes.c_int),
+    "cdt_sim_batch_workspace_bytes": ([_u32], _sz),
+    "cdt_canary_sim_batch": ([_u32, ctypes.POINTER(SimJob), _vp, _sz, _vp], ctypes.c_int),
+    "cdt_drift_batch_workspace_bytes": ([_u32, ctypes.POINTER(DriftJob)], _sz),
+    "cdt_drift_score_batch": ([_u32, ctypes.POINTER(DriftJob), _vp, _sz, _vp], ctypes.c_int),
     "cdt_tamper_scale_exact": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _d, _vp,
                                 _vp, _vp, _sz, _vp], ctypes.c_int),
     "cdt_sim_score": ([_u32, _u32, _u32, _u32, ctypes.POINTER(SimParams), _vp, _vp, _vp, _vp, _vp,
@@ -101,7 +131,7 @@ _LIB = None
 
 # Interface version of include/cdt.h that the structures and signatures
 # below mirror (cdt_version()).
-ABI_VERSION = 8
+ABI_VERSION = 9
 
 
 def lib():
@@ -257,6 +287,91 @@ def canary_sim(ref, out=None, *, bscale=None, tscale=None, **kw):
     _need(out, "h", torch.float16, (S, C, T, H))
     p = sim_params(bscale=bscale, tscale=tscale, **kw)
     _check(lib().cdt_canary_sim(S, C, T, H, ctypes.byref(p), _ptr(ref), _ptr(out), _stream()))
+    return out
+
+
+class Batch:
+    """A checked ctypes job table (with the tensors and parameter structs it
+    points to kept alive) and its device workspace: built once, launched as
+    often as needed (the tensors' contents may change between launches,
+    not their shapes or storage)."""
+
+    def __init__(self, arr, n, keep, ws):
+        self.arr, self.n, self.keep, self.ws = arr, n, keep, ws
+
+
+def sim_batch(jobs):
+    """Prepare a batched live pass.  jobs: list of (ref [S][C][T][H] fp32,
+    h [S][C][T][H] fp16 output, keywords as sim_params including bscale /
+    tscale tensors).  Every job must use the same benign noise distribution
+    and mode, carry 0 (checked by the library when launched)."""
+    torch = _torch()
+    n = len(jobs)
+    arr = (SimJob * max(1, n))()
+    keep = []
+    for i, (ref, h, kw) in enumerate(jobs):
+        _need(ref, "ref", torch.float32)
+        S, C, T, H = ref.shape
+        _need(h, "h", torch.float16, (S, C, T, H))
+        kw = dict(kw)
+        for name in ("bscale", "tscale"):
+            if kw.get(name) is not None:
+                _need(kw[name], name, torch.float32, (S, C))
+        p = sim_params(**kw)
+        keep.append((p, ref, h, kw.get("bscale"), kw.get("tscale")))
+        arr[i] = SimJob(S, C, T, H, ctypes.pointer(p), ref.data_ptr(), h.data_ptr())
+    nbytes = max(16, lib().cdt_sim_batch_workspace_bytes(n))
+    ws = _empty((nbytes,), torch.uint8, jobs[0][0] if n else None)
+    return Batch(arr, n, keep, ws)
+
+
+def canary_sim_batch(jobs):
+    """The live pass of several runs in one launch (cdt_canary_sim_batch):
+    jobs is a Batch from sim_batch or its list of jobs."""
+    b = jobs if isinstance(jobs, Batch) else sim_batch(jobs)
+    _check(lib().cdt_canary_sim_batch(b.n, b.arr, _ptr(b.ws), b.ws.numel(), _stream()))
+
+
+def drift_batch(jobs):
+    """Prepare a batched Eq. 4.  jobs: list of (h fp16, ref fp32, score out
+    [C][S] fp32, num_den out [C][S][2] fp64 or None)."""
+    torch = _torch()
+    n = len(jobs)
+    arr = (DriftJob * max(1, n))()
+    keep = []
+    for i, (h, ref, score, nd) in enumerate(jobs):
+        _need(h, "h", torch.float16)
+        S, C, T, H = h.shape
+        _need(ref, "ref", torch.float32, (S, C, T, H))
+        _need(score, "score", torch.float32, (C, S))
+        if nd is not None:
+            _need(nd, "num_den", torch.float64, (C, S, 2))
+        keep.append((h, ref, score, nd))
+        arr[i] = DriftJob(S, C, T, H, h.data_ptr(), ref.data_ptr(), score.data_ptr(),
+                          None if nd is None else nd.data_ptr())
+    nbytes = max(16, lib().cdt_drift_batch_workspace_bytes(n, arr))
+    ws = _empty((nbytes,), torch.uint8, jobs[0][0] if n else None)
+    return Batch(arr, n, keep, ws)
+
+
+def drift_score_batch(jobs):
+    """Eq. 4 over several arrays in one launch (cdt_drift_score_batch): jobs
+    is a Batch from drift_batch or its list of jobs; every job's scores are
+    bitwise those of drift_score on it."""
+    b = jobs if isinstance(jobs, Batch) else drift_batch(jobs)
+    _check(lib().cdt_drift_score_batch(b.n, b.arr, _ptr(b.ws), b.ws.numel(), _stream()))
+
+
+def canary_sim_stream(ref, out=None):
+    """The live pass's reads and writes with h = fp16(ref) and no random
+    numbers (a measurement of the memory bound of canary_sim's access
+    pattern); returns h."""
+    torch = _torch()
+    _need(ref, "ref", torch.float32)
+    S, C, T, H = ref.shape
+    out = _empty((S, C, T, H), torch.float16, ref) if out is None else out
+    _need(out, "h", torch.float16, (S, C, T, H))
+    _check(lib().cdt_canary_sim_stream(S, C, T, H, _ptr(ref), _ptr(out), _stream()))
     return out
 
 

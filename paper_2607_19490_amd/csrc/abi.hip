@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <mutex>
+#include <vector>
 
 #include "cdt.h"
 #include "cdt_launch.hpp"
@@ -75,7 +76,7 @@ bool canaries_fit(uint32_t canary_base, uint64_t C) {
 
 extern "C" {
 
-int cdt_version(void) { return 8; }
+int cdt_version(void) { return 9; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -221,6 +222,67 @@ int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim
         return fail(CDT_EALIGN, "cdt_canary_sim: arrays must be 16-byte aligned");
     return device_status(cdt::launch_canary_sim(L, ref, h, static_cast<hipStream_t>(stream)),
                          "cdt_canary_sim");
+}
+
+size_t cdt_sim_batch_workspace_bytes(uint32_t n_jobs) {
+    return (cdt::sim_batch_table_bytes(n_jobs) + 255) & ~static_cast<size_t>(255);
+}
+
+int cdt_canary_sim_batch(uint32_t n_jobs, const cdt_sim_job* jobs, void* ws, size_t ws_bytes,
+                         void* stream) {
+    const char* fn = "cdt_canary_sim_batch";
+    if (n_jobs == 0) return ok();
+    if (n_jobs > (1u << 16)) return fail(CDT_ELIMIT, "%s: n_jobs above 65536", fn);
+    if (!jobs) return fail(CDT_EINVAL, "%s: NULL jobs", fn);
+    std::vector<cdt::SimLaunch> runs(n_jobs);
+    std::vector<const float*> refs(n_jobs);
+    std::vector<uint16_t*> hs(n_jobs);
+    int dist = -1, mode = -1;
+    for (uint32_t j = 0; j < n_jobs; ++j) {
+        const cdt_sim_job& J = jobs[j];
+        int rc = check_sim(fn, J.S, J.C, J.T, J.H, J.p, &runs[j]);
+        if (rc) return rc;
+        if (runs[j].carry != 0.0f)
+            return fail(CDT_EINVAL, "%s: job %u: the propagation model (carry > 0) runs "
+                                    "through cdt_canary_sim", fn, j);
+        if (empty(J.S, J.C, J.T, J.H)) continue;
+        if (dist < 0) {
+            dist = static_cast<int>(runs[j].benign_dist);
+            mode = static_cast<int>(runs[j].benign_mode);
+        } else if (dist != static_cast<int>(runs[j].benign_dist) ||
+                   mode != static_cast<int>(runs[j].benign_mode)) {
+            return fail(CDT_EINVAL, "%s: job %u: every job must use the same benign noise "
+                                    "distribution and mode", fn, j);
+        }
+        if (!J.ref || !J.h) return fail(CDT_EINVAL, "%s: job %u has a NULL array", fn, j);
+        if (!aligned16(J.ref) || !aligned16(J.h))
+            return fail(CDT_EALIGN, "%s: job %u arrays must be 16-byte aligned", fn, j);
+        refs[j] = J.ref;
+        hs[j] = J.h;
+    }
+    if (dist < 0) return ok();
+    const size_t need = cdt_sim_batch_workspace_bytes(n_jobs);
+    if (!ws || ws_bytes < need)
+        return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                    ws ? ws_bytes : 0);
+    if (!aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
+    return device_status(cdt::launch_canary_sim_batch(n_jobs, runs.data(), refs.data(), hs.data(),
+                                                      ws, static_cast<hipStream_t>(stream)),
+                         fn);
+}
+
+int cdt_canary_sim_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,
+                          uint16_t* h, void* stream) {
+    const char* fn = "cdt_canary_sim_stream";
+    int rc = check_shape(fn, S, C, T, H);
+    if (rc) return rc;
+    if (empty(S, C, T, H)) return ok();
+    if (!ref || !h) return fail(CDT_EINVAL, "%s: NULL array", fn);
+    if (!aligned16(ref) || !aligned16(h))
+        return fail(CDT_EALIGN, "%s: arrays must be 16-byte aligned", fn);
+    return device_status(cdt::launch_canary_sim_stream(S, C, T, H, ref, h,
+                                                       static_cast<hipStream_t>(stream)),
+                         fn);
 }
 
 int cdt_sim_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim_params* p,
@@ -391,6 +453,111 @@ int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, cons
     if (rc) return rc;
     return device_status(cdt::launch_drift(cdt::DriftMetric::kL2, S, C, T, H, h, ref, score,
                                            num_den, ws, static_cast<hipStream_t>(stream)),
+                         fn);
+}
+
+}  // extern "C"
+
+namespace {
+
+constexpr uint32_t kMaxDriftJobs = 1u << 16;
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+// Device table of a batched Eq. 4 launch (jobs with no block dropped), the
+// partial sums laid out one job after another behind it in the workspace.
+struct DriftBatchPlan {
+    std::vector<cdt::DriftJobDev> table;
+    uint64_t total_chunks = 0, total_blocks = 0, partial_doubles = 0;
+};
+
+// Shapes only (no pointers): what cdt_drift_batch_workspace_bytes sizes.
+int plan_drift_batch(const char* fn, uint32_t n_jobs, const cdt_drift_job* jobs,
+                     DriftBatchPlan* plan, bool check_arrays) {
+    if (n_jobs > kMaxDriftJobs) return fail(CDT_ELIMIT, "%s: n_jobs above %u", fn, kMaxDriftJobs);
+    if (n_jobs > 0 && !jobs) return fail(CDT_EINVAL, "%s: NULL jobs", fn);
+    for (uint32_t j = 0; j < n_jobs; ++j) {
+        const cdt_drift_job& J = jobs[j];
+        int rc = check_shape(fn, J.S, J.C, J.T, J.H);
+        if (rc) return rc;
+        const uint64_t nb = static_cast<uint64_t>(J.S) * J.C;
+        if (nb == 0) continue;  // nothing to score
+        const uint64_t n = static_cast<uint64_t>(J.T) * J.H;
+        if (check_arrays) {
+            if (!J.score) return fail(CDT_EINVAL, "%s: job %u has a NULL score", fn, j);
+            if (n > 0) {
+                if (!J.h || !J.ref) return fail(CDT_EINVAL, "%s: job %u has a NULL array", fn, j);
+                if (!aligned16(J.h) || !aligned16(J.ref))
+                    return fail(CDT_EALIGN, "%s: job %u arrays must be 16-byte aligned", fn, j);
+            }
+        }
+        cdt::DriftJobDev d{};
+        d.h = J.h;
+        d.ref = J.ref;
+        d.score = J.score;
+        d.sums = J.num_den;
+        d.cpb = cdt::reduce_chunks_per_block(n);
+        d.chunk_begin = plan->total_chunks;
+        d.block_begin = plan->total_blocks;
+        d.n8 = static_cast<uint32_t>(n / 8);
+        d.S = J.S;
+        d.C = J.C;
+        d.direct = d.cpb == 1;
+        const uint64_t chunks = d.cpb * nb;
+        if (!d.direct) {
+            d.partial = reinterpret_cast<double*>(static_cast<uintptr_t>(plan->partial_doubles));
+            plan->partial_doubles += chunks * 2;
+        }
+        plan->total_chunks += (chunks + 7) / 8 * 8;  // every job starts on a multiple of 8
+        plan->total_blocks += nb;
+        plan->table.push_back(d);
+    }
+    if (plan->total_blocks > kMaxBlocks * 16)
+        return fail(CDT_ELIMIT, "%s: the batch holds too many blocks", fn);
+    return CDT_OK;
+}
+
+size_t batch_bytes(const DriftBatchPlan& plan) {
+    return align256(plan.table.size() * sizeof(cdt::DriftJobDev)) +
+           plan.partial_doubles * sizeof(double);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t cdt_drift_batch_workspace_bytes(uint32_t n_jobs, const cdt_drift_job* jobs) {
+    DriftBatchPlan plan;
+    if (plan_drift_batch("cdt_drift_batch_workspace_bytes", n_jobs, jobs, &plan, false))
+        return 0;
+    return batch_bytes(plan);
+}
+
+int cdt_drift_score_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws, size_t ws_bytes,
+                          void* stream) {
+    const char* fn = "cdt_drift_score_batch";
+    DriftBatchPlan plan;
+    int rc = plan_drift_batch(fn, n_jobs, jobs, &plan, true);
+    if (rc) return rc;
+    if (plan.table.empty()) return ok();
+    const size_t need = batch_bytes(plan);
+    if (!ws || ws_bytes < need)
+        return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                    ws ? ws_bytes : 0);
+    if (!aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
+    // partial offsets -> addresses behind the table in ws
+    double* partials = reinterpret_cast<double*>(
+        static_cast<char*>(ws) + align256(plan.table.size() * sizeof(cdt::DriftJobDev)));
+    for (cdt::DriftJobDev& d : plan.table)
+        if (!d.direct) d.partial = partials + reinterpret_cast<uintptr_t>(d.partial);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const hipError_t e = hipMemcpyAsync(ws, plan.table.data(),
+                                        plan.table.size() * sizeof(cdt::DriftJobDev),
+                                        hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return device_status(e, fn);
+    return device_status(cdt::launch_drift_batch(static_cast<const cdt::DriftJobDev*>(ws),
+                                                 static_cast<uint32_t>(plan.table.size()),
+                                                 plan.total_chunks, plan.total_blocks, st),
                          fn);
 }
 

@@ -57,6 +57,18 @@ hipError_t launch_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const d
                                float* bscale, hipStream_t st);
 hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, hipStream_t st);
 
+// Batched live pass over runs of one noise distribution and mode, carry 0:
+// the device table (sim_batch_table_bytes(n_jobs) bytes) is filled from
+// `runs` on the stream, then one grid generates every run's chunks.
+size_t sim_batch_table_bytes(uint32_t n_jobs);
+hipError_t launch_canary_sim_batch(uint32_t n_jobs, const SimLaunch* runs,
+                                   const float* const* refs, uint16_t* const* hs, void* table,
+                                   hipStream_t st);
+
+// The live pass's loads and stores with h = fp16(a): its memory bound.
+hipError_t launch_canary_sim_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H,
+                                    const float* ref, uint16_t* h, hipStream_t st);
+
 hipError_t launch_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const float* ref,
                             double* sumsq, double* sumabs, void* ws, hipStream_t st);
 // Eq. 4 (or its cosine variant) per block: partial sums per chunk into ws,
@@ -64,6 +76,23 @@ hipError_t launch_ref_stats(uint32_t S, uint32_t C, uint32_t T, uint32_t H, cons
 hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, uint32_t H,
                         const uint16_t* h, const void* ref, float* score, double* sums, void* ws,
                         hipStream_t st);
+
+// One array of a batched Eq. 4 launch, as the kernels read it from the
+// device table: its arrays, shape, chunking and place in the batch's chunk
+// and block index ranges.
+struct DriftJobDev {
+    const uint16_t* h;
+    const float* ref;
+    float* score;
+    double* sums;     // [C][S][2] or null
+    double* partial;  // its per-chunk partial sums (unused when direct)
+    uint64_t cpb;     // chunks per block
+    uint64_t chunk_begin, block_begin;
+    uint32_t n8, S, C, direct;
+};
+
+hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs, uint64_t total_chunks,
+                              uint64_t total_blocks, hipStream_t st);
 
 // drift_score's reads (same chunks, loads and order) with no arithmetic; ws
 // is drift_score's workspace and may be overwritten.

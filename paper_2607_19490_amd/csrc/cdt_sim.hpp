@@ -70,6 +70,15 @@ inline SimArgs make_sim_args(const SimLaunch& p, uint64_t chunks_per_block,
     return A;
 }
 
+// One run of a batched live pass, as the kernel reads it from the device
+// table: its launch parameters, arrays and first chunk in the batch.
+struct SimJobDev {
+    SimArgs A;
+    const float* ref;
+    uint16_t* h;
+    uint64_t chunk_begin;
+};
+
 // Block-uniform state: which (shard, canary) and its scales; c is the
 // global canary index that keys the noise.
 struct SimBlock {

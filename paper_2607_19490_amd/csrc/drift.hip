@@ -87,15 +87,18 @@ __device__ __forceinline__ uint32_t fold_group(const u32x4& hv, const u32x4& rv,
 // direct (a block is one chunk): the chunk's sums are the block's, and the
 // score is written here; the combine launch is skipped (it would add the one
 // partial to zero, which changes nothing).
-template <DriftMetric kM, bool kReadOnly = false>
-__global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
-    const uint16_t* __restrict__ h, const void* __restrict__ ref, uint32_t n8,
-    uint64_t chunks_per_block, uint64_t total_chunks, double* __restrict__ partial, bool direct,
-    uint32_t S, uint32_t C, float* __restrict__ score, double* __restrict__ sums) {
+// One chunk of one block array: its partial sums (or, direct, its block's
+// score), in a fixed order.  Shared by the single-array and batched launches.
+template <DriftMetric kM, bool kReadOnly>
+__device__ __forceinline__ void drift_chunk(const uint16_t* __restrict__ h,
+                                            const void* __restrict__ ref, uint32_t n8,
+                                            uint64_t chunks_per_block, uint64_t chunk,
+                                            double* __restrict__ partial, bool direct, uint32_t S,
+                                            uint32_t C, float* __restrict__ score,
+                                            double* __restrict__ sums) {
     using Tr = DriftTraits<kM>;
     const uint64_t n = static_cast<uint64_t>(n8) * 8;
-    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
-        const uint64_t chunk = xcd_contiguous(it, total_chunks);
+    {
         const uint64_t b = chunk / chunks_per_block;
         const uint32_t g0 = static_cast<uint32_t>(chunk - b * chunks_per_block) * kChunkGroups;
         const uint32_t g_end = min(g0 + kChunkGroups, n8);
@@ -175,6 +178,65 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
     }
 }
 
+template <DriftMetric kM, bool kReadOnly = false>
+__global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
+    const uint16_t* __restrict__ h, const void* __restrict__ ref, uint32_t n8,
+    uint64_t chunks_per_block, uint64_t total_chunks, double* __restrict__ partial, bool direct,
+    uint32_t S, uint32_t C, float* __restrict__ score, double* __restrict__ sums) {
+    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x)
+        drift_chunk<kM, kReadOnly>(h, ref, n8, chunks_per_block, xcd_contiguous(it, total_chunks),
+                                   partial, direct, S, C, score, sums);
+}
+
+// Batched Eq. 4: the chunks of every job form one index range (job j owns
+// [chunk_begin_j, chunk_begin_j + its chunks rounded up to a multiple of
+// 8)), walked by one grid; each chunk is scored exactly as the single launch
+// scores it.  Because every job starts on a multiple of 8, iteration index
+// it runs on XCD it % 8 inside each job too, and the XCD-contiguous map is
+// applied per job: the 8 XCDs stream different eighths of the same job,
+// as in a single launch, instead of 8 jobs from their first bytes at once
+// (the jobs of a sweep share their references, and equal offsets of
+// equally sized arrays fall on the same memory channels).  The job of an
+// iteration is found by a binary search of the table (workgroup-uniform).
+__device__ __forceinline__ uint32_t find_job(const DriftJobDev* __restrict__ jobs,
+                                             uint32_t n_jobs, uint64_t x, bool by_block) {
+    uint32_t lo = 0, hi = n_jobs;  // last job whose begin <= x
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) / 2;
+        const uint64_t begin = by_block ? jobs[mid].block_begin : jobs[mid].chunk_begin;
+        if (begin <= x) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(kReduceThreads) void drift_batch_partial_kernel(
+    const DriftJobDev* __restrict__ jobs, uint32_t n_jobs, uint64_t total_chunks) {
+    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
+        const DriftJobDev& J = jobs[find_job(jobs, n_jobs, it, false)];
+        const uint64_t local = it - J.chunk_begin;
+        const uint64_t chunks = J.cpb * J.S * J.C;
+        if (local >= chunks) continue;  // padding to the job's multiple of 8
+        drift_chunk<DriftMetric::kL2, false>(J.h, J.ref, J.n8, J.cpb,
+                                             xcd_contiguous(local, chunks), J.partial, J.direct,
+                                             J.S, J.C, J.score, J.sums);
+    }
+}
+
+__global__ void drift_batch_combine_kernel(const DriftJobDev* __restrict__ jobs, uint32_t n_jobs,
+                                           uint64_t total_blocks) {
+    const uint64_t g = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (g >= total_blocks) return;
+    const DriftJobDev& J = jobs[find_job(jobs, n_jobs, g, true)];
+    if (J.direct) return;  // scored by the partial kernel itself
+    const uint64_t b = g - J.block_begin;
+    double acc[2] = {0.0, 0.0};
+    for (uint64_t i = 0; i < J.cpb; ++i) {
+        acc[0] += J.partial[(b * J.cpb + i) * 2];
+        acc[1] += J.partial[(b * J.cpb + i) * 2 + 1];
+    }
+    finish_block<DriftMetric::kL2>(acc, b, J.S, J.C, J.score, J.sums);
+}
+
 template <DriftMetric kM>
 __global__ void drift_combine_kernel(const double* __restrict__ partial, uint64_t chunks_per_block,
                                      uint64_t nblocks, uint32_t S, uint32_t C,
@@ -222,6 +284,22 @@ hipError_t launch_drift_t(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const 
     }
     if (direct) return hipSuccess;
     return launch_combine_t<kM>(partial, cpb, nblocks, S, C, score, sums, st);
+}
+
+hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs, uint64_t total_chunks,
+                              uint64_t total_blocks, hipStream_t st) {
+    if (n_jobs == 0) return hipSuccess;
+    if (total_chunks > 0) {
+        hipLaunchKernelGGL(drift_batch_partial_kernel, dim3(reduce_grid(total_chunks)),
+                           dim3(kReduceThreads), 0, st, jobs_dev, n_jobs, total_chunks);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (total_blocks == 0) return hipSuccess;
+    const uint64_t grid = (total_blocks + 255) / 256;
+    hipLaunchKernelGGL(drift_batch_combine_kernel, dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
+                       st, jobs_dev, n_jobs, total_blocks);
+    return hipGetLastError();
 }
 
 hipError_t launch_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H,

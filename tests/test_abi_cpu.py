@@ -38,11 +38,16 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 8 == cdt.ABI_VERSION
+    assert L.cdt_version() == 9 == cdt.ABI_VERSION
     assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
     assert L.cdt_auroc_workspace_bytes(216) == 216 * 32
+
+
+def STRUCTS(cdt):
+    return (("cdt_sim_params", cdt.SimParams), ("cdt_auroc_cfg", cdt.AurocCfg),
+            ("cdt_drift_job", cdt.DriftJob), ("cdt_sim_job", cdt.SimJob))
 
 
 def test_struct_layouts_match_the_header(cdt, tmp_path):
@@ -50,7 +55,7 @@ def test_struct_layouts_match_the_header(cdt, tmp_path):
     offset and struct size with the ctypes mirrors of the binding."""
     src = tmp_path / "layout.c"
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "cdt.h"', "int main(void){"]
-    for cname, py in (("cdt_sim_params", cdt.SimParams), ("cdt_auroc_cfg", cdt.AurocCfg)):
+    for cname, py in STRUCTS(cdt):
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
         for f, _ in py._fields_:
             lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
@@ -61,7 +66,7 @@ def test_struct_layouts_match_the_header(cdt, tmp_path):
                    check=True)
     out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
     got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out.strip().splitlines()}
-    for cname, py in (("cdt_sim_params", cdt.SimParams), ("cdt_auroc_cfg", cdt.AurocCfg)):
+    for cname, py in STRUCTS(cdt):
         assert got[(cname, "size")] == ctypes.sizeof(py)
         for f, _ in py._fields_:
             assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
@@ -253,3 +258,45 @@ def test_noalloc_limit_is_checked_on_the_host(cdt):
     assert L.cdt_drift_score_noalloc(64, 1 << 20, 1, 8, None, None, None, None, None) == \
         cdt.EINVAL
     assert "score is NULL" in _err(cdt)
+
+
+def test_batch_calls_validate_every_job_on_the_host(cdt):
+    """The batched live pass and Eq. 4 reject a bad job (and name it) before
+    any device call; a batch whose jobs are all empty does nothing."""
+    L = cdt.lib()
+    jobs = (cdt.DriftJob * 2)()
+    jobs[0] = cdt.DriftJob(2, 2, 3, 16, 16, 16, 16, None)
+    jobs[1] = cdt.DriftJob(2, 2, 3, 12, 16, 16, 16, None)
+    assert L.cdt_drift_score_batch(2, jobs, 16, 1 << 20, None) == cdt.EINVAL
+    assert "multiple of 8" in _err(cdt)
+    assert L.cdt_drift_batch_workspace_bytes(2, jobs) == 0
+    jobs[1] = cdt.DriftJob(2, 2, 3, 16, 8, 16, 16, None)
+    assert L.cdt_drift_score_batch(2, jobs, 16, 1 << 20, None) == cdt.EALIGN
+    assert "job 1" in _err(cdt)
+    jobs[1] = cdt.DriftJob(2, 2, 3, 16, 16, 16, None, None)
+    assert L.cdt_drift_score_batch(2, jobs, 16, 1 << 20, None) == cdt.EINVAL
+    # sizes: the table (rounded to 256 B) and the multi-chunk jobs' partials
+    jobs[0] = cdt.DriftJob(16, 256, 256, 8192, 16, 16, 16, None)
+    jobs[1] = cdt.DriftJob(4, 8, 16, 256, 16, 16, 16, None)  # one chunk per block
+    nbytes = L.cdt_drift_batch_workspace_bytes(2, jobs)
+    assert nbytes > 4096 * 64 * 16 and nbytes - 4096 * 64 * 16 <= 256
+    assert L.cdt_drift_score_batch(2, jobs, 16, nbytes - 16, None) == cdt.EINVAL
+    empty = (cdt.DriftJob * 1)(cdt.DriftJob(0, 2, 3, 16, None, None, None, None))
+    assert L.cdt_drift_score_batch(1, empty, None, 0, None) == cdt.OK
+    p = cdt.sim_params(seed=0, cfg_id=0)
+    p3 = cdt.sim_params(seed=0, cfg_id=0, benign_dist=1)
+    sj = (cdt.SimJob * 2)()
+    sj[0] = cdt.SimJob(4, 2, 2, 16, ctypes.pointer(p), 16, 16)
+    sj[1] = cdt.SimJob(4, 2, 2, 16, ctypes.pointer(p3), 16, 16)
+    assert L.cdt_canary_sim_batch(2, sj, 16, 1 << 20, None) == cdt.EINVAL
+    assert "same benign noise" in _err(cdt)
+    pc = cdt.sim_params(seed=0, cfg_id=0, carry=0.5)
+    sj[1] = cdt.SimJob(4, 2, 2, 16, ctypes.pointer(pc), 16, 16)
+    assert L.cdt_canary_sim_batch(2, sj, 16, 1 << 20, None) == cdt.EINVAL
+    assert "carry" in _err(cdt)
+    sj[1] = cdt.SimJob(65, 2, 2, 16, ctypes.pointer(p), 16, 16)
+    assert L.cdt_canary_sim_batch(2, sj, 16, 1 << 20, None) == cdt.ELIMIT
+    sj[1] = cdt.SimJob(4, 2, 2, 16, ctypes.pointer(p), 16, 16)
+    assert L.cdt_canary_sim_batch(2, sj, 16, 8, None) == cdt.EINVAL
+    assert "workspace" in _err(cdt)
+    assert L.cdt_canary_sim_stream(2, 2, 3, 12, None, None, None) == cdt.EINVAL

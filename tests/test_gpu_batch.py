@@ -1,0 +1,114 @@
+"""Batched launches against the single-run calls, through the C ABI: the
+batched live pass (cdt_canary_sim_batch) and the batched Eq. 4
+(cdt_drift_score_batch) must give every job's output bit for bit as
+cdt_canary_sim / cdt_drift_score give it, over jobs of mixed shapes (one
+and several chunks per block, ragged tails, empty jobs) and parameters;
+one job of each batch is also checked against the oracle.  And the live
+pass's stream aid (cdt_canary_sim_stream) writes exactly fp16(a)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_19490_amd import inputs
+from tests.gpu_util import announce, h_bits, rel_err, require_gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+
+DRIFT_RTOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    return require_gpu()
+
+
+DRIFT_SHAPES = [(16, 4, 4, 32768), (4, 8, 16, 256), (3, 5, 7, 264), (2, 3, 41, 1000),
+                (0, 3, 4, 16), (2, 2, 0, 16), (1, 1, 130, 8192), (5, 2, 1, 8)]
+
+
+def test_drift_score_batch_equals_single(gpu):
+    torch, cdt = gpu
+    announce("drift_score_batch over 8 jobs")
+    jobs, host = [], []
+    for k, shape in enumerate(DRIFT_SHAPES):
+        S, C, T, H = shape
+        a = inputs.ref_normal(shape, seed=200 + k, outlier_frac=0.01)
+        h = inputs.live_near(a, seed=300 + k, rel=1e-3, flip_frac=0.001)
+        hd, ad = to_dev(torch, h).view(torch.float16), to_dev(torch, a)
+        sc = torch.full((C, S), -1.0, dtype=torch.float32, device="cuda")
+        nd = torch.full((C, S, 2), -1.0, dtype=torch.float64, device="cuda")
+        jobs.append((hd, ad, sc, nd if k % 2 == 0 else None))
+        host.append((h, a))
+    cdt.drift_score_batch(jobs)
+    singles = []
+    for hd, ad, sc, nd in jobs:
+        nd1 = torch.empty((sc.shape[0], sc.shape[1], 2), dtype=torch.float64, device="cuda")
+        singles.append((cdt.drift_score(hd, ad, num_den=nd1), nd1))
+    torch.cuda.synchronize()
+    for k, ((hd, ad, sc, nd), (want, nd1)) in enumerate(zip(jobs, singles)):
+        assert torch.equal(sc, want), f"job {k} {DRIFT_SHAPES[k]}: scores differ"
+        if nd is not None:
+            assert torch.equal(nd, nd1), f"job {k}: sums differ"
+    h, a = host[3]
+    s64, _, _ = oracle.drift_score(h, a)
+    assert rel_err(jobs[3][2].cpu().numpy(), s64) < DRIFT_RTOL
+
+
+SIM_JOBS = [
+    ((4, 8, 16, 256), dict(cfg_id=1, sigma_b=1e-3, mal_mask=1 << 2, tamper=1, eps=0.05)),
+    ((8, 6, 9, 1000), dict(cfg_id=2, sigma_b=1e-4, mal_mask=1 << 4, tamper=2, flip_p=0.02)),
+    ((2, 3, 41, 1000), dict(cfg_id=3, sigma_b=1e-2, mal_mask=1, tamper=4, scale=1.05)),
+    ((16, 2, 40, 4096), dict(cfg_id=4, sigma_b=1e-3, mal_mask=(1 << 8) | (1 << 15), tamper=7,
+                             eps=0.1, flip_p=0.1, scale=1.1)),
+    ((0, 2, 3, 16), dict(cfg_id=5)),
+    ((3, 5, 7, 264), dict(cfg_id=6, sigma_b=0.0, tamper_base=1, mal_mask=2, tamper=1, eps=0.2)),
+]
+
+
+@pytest.mark.parametrize("dist,mode", [(0, 0), (1, 1)], ids=["gauss_elementwise", "t3_block"])
+def test_canary_sim_batch_equals_single(gpu, dist, mode):
+    torch, cdt = gpu
+    announce(f"canary_sim_batch dist={dist} mode={mode}")
+    jobs, singles, host = [], [], []
+    for k, (shape, kw) in enumerate(SIM_JOBS):
+        S, C, T, H = shape
+        kw = dict(kw, seed=0xABCDEF12345 + k, benign_dist=dist, benign_mode=mode)
+        eps = kw.pop("eps", 0.0)
+        ref = oracle.ref_synth(S, C, T, H, 40 + k, 0, oracle.outlier_gain(H, max(1, H // 100),
+                                                                          20.0, 40 + k, 0))
+        q, m = oracle.ref_stats(ref)
+        ts, bs = oracle.block_scales(T, H, q, m, eps, kw.get("sigma_b", 1e-3))
+        ref_d = to_dev(torch, ref)
+        kw.update(bscale=to_dev(torch, bs), tscale=to_dev(torch, ts))
+        h = torch.empty((S, C, T, H), dtype=torch.float16, device="cuda")
+        jobs.append((ref_d, h, kw))
+        singles.append(cdt.canary_sim(ref_d, **kw))
+        host.append((ref, bs, ts, kw))
+    cdt.canary_sim_batch(jobs)
+    torch.cuda.synchronize()
+    for k, ((ref_d, h, kw), want) in enumerate(zip(jobs, singles)):
+        assert torch.equal(h.view(torch.int16), want.view(torch.int16)), f"job {k} differs"
+    ref, bs, ts, kw = host[1]
+    kw_o = {key: v for key, v in kw.items() if key not in ("bscale", "tscale")}
+    want = oracle.canary_sim(ref, bscale=bs, tscale=ts, **kw_o)
+    np.testing.assert_array_equal(h_bits(jobs[1][1]), want)
+
+
+def test_canary_sim_batch_rejects_mixed_noise(gpu):
+    torch, cdt = gpu
+    ref = torch.zeros((2, 2, 2, 16), dtype=torch.float32, device="cuda")
+    h = torch.empty((2, 2, 2, 16), dtype=torch.float16, device="cuda")
+    with pytest.raises(cdt.CdtError):
+        cdt.canary_sim_batch([(ref, h, dict(seed=0, cfg_id=0)),
+                              (ref, h, dict(seed=0, cfg_id=1, benign_dist=1))])
+
+
+@pytest.mark.parametrize("shape", [(4, 8, 16, 256), (3, 5, 41, 1000), (2, 2, 9, 8000)])
+def test_canary_sim_stream_is_fp16_of_reference(gpu, shape):
+    torch, cdt = gpu
+    announce(f"canary_sim_stream {shape}")
+    a = inputs.ref_normal(shape, seed=7, outlier_frac=0.05) * np.float32(300.0)
+    ad = to_dev(torch, a)
+    h = cdt.canary_sim_stream(ad)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(h_bits(h), oracle.f16_rne(a))
