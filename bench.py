@@ -405,12 +405,31 @@ def ablation_kernels(torch, cdt, wl, prep):
                                                           **kw_x))
     out["tamper_scale_exact"] = {"ms": round(ex_ms, 4),
                                  "reference_read_GBps": round(elems * 4 / (ex_ms * 1e-3) / 1e9, 1)}
+    # the same with heavy-tailed benign noise (Student-t: four times the
+    # Philox draws of the Gaussian live pass, so bound by the vector ALUs)
+    kw_t = dict(kw, benign_dist=1)
+    t3_ms = time_ms(torch, lambda: cdt.canary_sim(prep.ref, out=r, **kw_t))
+    out["canary_sim_t3"] = {"ms": round(t3_ms, 4),
+                            "GBps": round(elems * SIM_BYTES_PER_ELEM / (t3_ms * 1e-3) / 1e9, 1)}
     # the propagation model: stages in order per canary, live error carried
     kw_c = dict(kw, carry=0.7)
     chain_ms = time_ms(torch, lambda: cdt.canary_sim(prep.ref, out=r, **kw_c))
     out["chain_canary_sim"] = {"ms": round(chain_ms, 4), "carry": 0.7,
                                "GBps": round(elems * SIM_BYTES_PER_ELEM / (chain_ms * 1e-3) / 1e9,
                                              1)}
+    kw_ct = dict(kw_c, benign_dist=1)
+    chain_t3_ms = time_ms(torch, lambda: cdt.canary_sim(prep.ref, out=r, **kw_ct), 3)
+    out["chain_canary_sim_t3"] = {
+        "ms": round(chain_t3_ms, 4), "carry": 0.7,
+        "GBps": round(elems * SIM_BYTES_PER_ELEM / (chain_t3_ms * 1e-3) / 1e9, 1)}
+    # the exact-norm scales under the propagation model (the attacker's chain
+    # walked up to it, its untampered output summed)
+    kw_xc = dict(kw_c, tamper=1, tscale=None)
+    kw_xc.pop("bscale")
+    exc_ms = time_ms(torch, lambda: cdt.tamper_scale_exact(prep.ref, 0.05, ws=prep.ws, bscale=bs,
+                                                           **kw_xc), 3)
+    out["tamper_scale_exact_chain"] = {"ms": round(exc_ms, 4), "carry": 0.7,
+                                       "malicious_stages": bin(rs.mal_mask).count("1")}
     out["run"] = run.label
     del r
     return out
@@ -715,7 +734,8 @@ def config_runs(torch, cdt, W, name):
 def attainable(torch):
     """What torch's own kernels reach on the same box for the detector's two
     byte streams: a read-only reduction (drift_score's stream), a plain copy,
-    and an fp32 -> fp16 conversion (canary_sim's 4 B read + 2 B write).
+    an fp32 -> fp16 conversion (canary_sim's 4 B read + 2 B write) and a
+    write-only fp16 fill (the write half of it alone).
     Context for the roofline fraction, not part of the step."""
     n = 1 << 30
     x = torch.ones((n,), dtype=torch.float32, device="cuda")
@@ -724,7 +744,8 @@ def attainable(torch):
     out = {}
     for name, fn, nbytes in (("sum_fp32_read", lambda: torch.sum(x), 4 * n),
                              ("copy_fp32", lambda: y.copy_(x), 8 * n),
-                             ("convert_fp32_to_fp16", lambda: y16.copy_(x), 6 * n)):
+                             ("convert_fp32_to_fp16", lambda: y16.copy_(x), 6 * n),
+                             ("fill_fp16_write", lambda: y16.fill_(1.0), 2 * n)):
         ms = time_ms(torch, fn, 7)
         out[name] = {"ms": round(ms, 4), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1)}
     del x, y, y16
