@@ -11,6 +11,8 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU check (opt-in through CDT_SLOW=1)")
+    config.addinivalue_line("markers", "statistical: an outcome against a model's distribution "
+                                       "(seeded Monte Carlo), not a parity check")
 
 
 def pytest_collection_modifyitems(config, items):

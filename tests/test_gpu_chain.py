@@ -102,41 +102,13 @@ def test_chain_exact_norm(gpu, shape, case):
     assert int((h_bits(h) != want).sum()) == 0
 
 
-def test_substudies(gpu):
-    """Depth, position and collusion leave the detector at 1.0 (Section
-    5.3); along the frontier (Section 5.5) and as the noise floor rises
-    (Section 5.4) the attacker's lead over the benign floor shrinks.  One
-    configuration is compared whole with the oracle's chain."""
+def test_substudy_parity(gpu):
+    """One substudy configuration (depth k = 4, the attacker's exact-norm
+    Gaussian under the propagation model, Section 5.3) compared whole with
+    the oracle's chain.  The substudies' outcomes are checked against a
+    statistical model in tests/test_gpu_statistical.py."""
     torch, cdt = gpu
-    import bench
-    announce("substudies")
-    res = bench.substudies(torch, cdt, W)["studies"]
-    for study in ("depth", "position", "collusion"):
-        for name, row in res[study].items():
-            assert row["auroc"] == 1.0, (study, name, row)
-    # frontier: the malicious stage's lead over the benign floor shrinks as
-    # eps falls toward the floor (sigma_hw = 0.002 gives a carried floor of
-    # about 1.5e-3); over 36864-element blocks the L2 statistic concentrates
-    # enough to keep ranking the attacker first even there
-    fr = res["frontier"]
-    eps = ("0.1", "0.05", "0.02", "0.01", "0.005", "0.002", "0.001")
-    lead = [fr[f"eps{e}"]["median_m_malicious"] / fr[f"eps{e}"]["max_m_benign"] for e in eps]
-    # flat (the downstream stage carries g m_attacker) while eps >> floor,
-    # then falling; 0.01 allows for the sampling noise of the benign maximum
-    assert all(b <= a + 0.01 for a, b in zip(lead, lead[1:])), lead
-    assert lead[0] > 1.2 and lead[-1] < 1.1, lead
-    assert all(fr[f"eps{e}"]["auroc"] >= 0.5 for e in eps)
-    # SNR (Section 5.4): raising sigma_hw from 0.002 to 0.2 at eps = 0.05
-    # shrinks the lead and, once the benign floor reaches the tamper, the
-    # detector starts to miss (the paper reports 0.46-0.86 at 0.2 on real
-    # models)
-    snr = res["snr"]
-    sig = ("0.002", "0.01", "0.02", "0.05", "0.1", "0.2")
-    lead = [snr[f"sigma{x}"]["median_m_malicious"] / snr[f"sigma{x}"]["max_m_benign"]
-            for x in sig]
-    assert all(b <= a + 0.01 for a, b in zip(lead, lead[1:])), lead
-    assert all(snr[f"sigma{x}"]["auroc"] == 1.0 for x in sig[:4])
-    assert snr["sigma0.2"]["auroc"] < 1.0 and lead[-1] < 1.0, (snr["sigma0.2"], lead)
+    announce("substudy parity")
     # whole-configuration parity: depth k = 4
     wl = W.substudies()
     rs = [r for r in wl.ref_sets if r.runs[0].label == "depth:k4"][0]
