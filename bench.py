@@ -898,7 +898,8 @@ def cpu_baseline(W, args):
     oracle.drift_score(h, refs)
     dt_drift = time.perf_counter() - t1
     # one configuration of the 216-run sweep (the smallest shape) end to end,
-    # scaled to the sweep by its total element count
+    # its blocks spread over the same host threads, scaled to the sweep by
+    # its total element count
     sw = W.sweep()
     srs = min(sw.ref_sets, key=lambda r: r.elems)
     srun = srs.runs[0]
@@ -908,15 +909,28 @@ def cpu_baseline(W, args):
     t3 = time.perf_counter()
     q, m = oracle.ref_stats(sref)
     ts, bs = oracle.block_scales(srs.T, srs.H, q, m, srun.eps, srun.sigma_b)
-    hs = oracle.canary_sim(sref, seed=sw.seed, cfg_id=srun.cfg_id, sigma_b=srun.sigma_b,
-                           mal_mask=srs.mal_mask, tamper=srun.tamper, tscale=ts,
-                           flip_p=srun.flip_p, scale=srun.scale)
-    _, s32, _ = oracle.drift_score(hs, sref)
+
+    def sweep_job(sc):
+        s, c = sc
+        hb = oracle.sim_block(s, c, sref[s, c], seed=sw.seed, cfg_id=srun.cfg_id,
+                              benign_mode=srun.benign_mode, benign_dist=srun.benign_dist,
+                              sigma_b=srun.sigma_b, bscale=bs[s, c],
+                              malicious=s in srs.mal_shards, tamper=srun.tamper,
+                              tamper_base=srun.tamper_base, tscale=ts[s, c],
+                              flip_p=srun.flip_p, scale=srun.scale)
+        _, b32, _ = oracle.drift_score(hb[None, None], sref[s:s + 1, c:c + 1])
+        return s, c, b32[0, 0]
+
+    with ThreadPoolExecutor(max_workers=nthr) as ex:
+        done = list(ex.map(sweep_job, [(s, c) for s in range(srs.S) for c in range(srs.C)]))
+    s32 = np.zeros((srs.C, srs.S), np.float32)
+    for s, c, v in done:
+        s32[c, s] = v
     oracle.auroc_config(s32, srs.mal_mask, seed=sw.seed, cfg_id=srun.cfg_id)
     dt_cfg = time.perf_counter() - t3
     sweep_elems = sum(len(r.runs) * r.elems for r in sw.ref_sets)
     sweep_s = dt_cfg * sweep_elems / srs.elems
-    del sref, hs, sgain
+    del sref, sgain
     # the other rows of the path on one canary of the same sample
     one_ref = np.ascontiguousarray(refs[:, :1])
     one_h = np.ascontiguousarray(h[:, :1])
@@ -958,7 +972,8 @@ def cpu_baseline(W, args):
         "drift_only_GBps": round(h.size * DRIFT_BYTES_PER_ELEM / dt_drift / 1e9, 4),
         "sweep_configs_per_s": round(len([r for x in sw.ref_sets for r in x.runs]) / sweep_s, 4),
         "sweep_sample": f"one {srs.S}x{srs.C}x{srs.T}x{srs.H} configuration (sim + drift + "
-                        f"auroc) in {dt_cfg:.1f} s, scaled by the sweep's element count",
+                        f"auroc) in {dt_cfg:.2f} s on {nthr} threads, scaled by the sweep's "
+                        f"element count",
         "other_rows": rows,
         "other_rows_sample": f"{rs.S} shards x 1 canary x {rs.T} x {rs.H} (cosine, chain, "
                              f"exact-norm scale); 216 random 32-canary tables (auroc)",
