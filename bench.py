@@ -190,6 +190,47 @@ def gpu_step(torch, cdt, wl, preps, scores, score_views, cfgs, auroc_ws, counts,
                      flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED, counts=counts, pooled=pooled)
 
 
+class Batches:
+    """The step's batched launches: per reference set, one live-pass launch
+    over all its runs (each into its own activation array) and one Eq. 4
+    launch over them, tables prepared once.  The runs of a set share their
+    references, so the library reads each reference chunk about once for
+    all of them."""
+
+    def __init__(self, torch, cdt, wl, preps, views):
+        most = max(len(p.rs.runs) * p.rs.elems for p in preps)
+        self.h = torch.empty((most,), dtype=torch.float16, device="cuda")
+        self.sets, k = [], 0
+        for p in preps:
+            rs = p.rs
+            hs = [self.h[r * rs.elems:(r + 1) * rs.elems].view(rs.S, rs.C, rs.T, rs.H)
+                  for r in range(len(rs.runs))]
+            sim = cdt.sim_batch([(p.ref, hs[r], sim_kwargs(wl, rs, run, *p.scales[r]))
+                                 for r, run in enumerate(rs.runs)])
+            drift = cdt.drift_batch([(hs[r], p.ref, views[k + r], None)
+                                     for r in range(len(rs.runs))])
+            self.sets.append((sim, drift, rs))
+            k += len(rs.runs)
+
+
+def batched_step(cdt, wl, sb, scores, cfgs, auroc_ws, counts, pooled, ev=None):
+    """One pass of the hot path with the batched launches (per reference set:
+    the live pass of its runs, then Eq. 4 of them), then the AUROC of every
+    run in one launch.  ev: per set, 4 events around the two launches."""
+    for i, (sim, drift, _) in enumerate(sb.sets):
+        if ev is not None:
+            ev[i][0].record()
+        cdt.canary_sim_batch(sim)
+        if ev is not None:
+            ev[i][1].record()
+            ev[i][2].record()
+        cdt.drift_score_batch(drift)
+        if ev is not None:
+            ev[i][3].record()
+    cdt.auroc_launch(auroc_ws, len(cfgs), scores, seed=wl.seed,
+                     flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED, counts=counts, pooled=pooled)
+
+
 def setup_batch(torch, cdt, wl, preps):
     """Scores slab for every run of the workload plus the batched AUROC table,
     validated and uploaded once into auroc_ws (the step only launches)."""
@@ -217,30 +258,27 @@ def run_main(torch, cdt, W, args):
     log(f"workload {wl.name}: preparing references")
     preps = [Prepared(torch, cdt, W, wl, rs) for rs in wl.ref_sets]
     scores, views, cfgs, counts, pooled, auroc_ws = setup_batch(torch, cdt, wl, preps)
+    sb = Batches(torch, cdt, wl, preps, views)
     torch.cuda.synchronize()
     nrun = len(cfgs)
-    log(f"{nrun} runs; warmup {args.warmup}")
+    nset = len(sb.sets)
+    log(f"{nrun} runs in {nset} reference set(s); warmup {args.warmup}")
     for _ in range(args.warmup):
-        gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled)
+        batched_step(cdt, wl, sb, scores, cfgs, auroc_ws, counts, pooled)
     torch.cuda.synchronize()
 
     E = torch.cuda.Event
-    drift_ev = [[(E(enable_timing=True), E(enable_timing=True)) for _ in range(nrun)]
-                for _ in range(args.steps)]
-    sim_ev = [[(E(enable_timing=True), E(enable_timing=True)) for _ in range(nrun)]
-              for _ in range(args.steps)]
+    ev = [[[E(enable_timing=True) for _ in range(4)] for _ in range(nset)]
+          for _ in range(args.steps)]
     t0, t1 = E(enable_timing=True), E(enable_timing=True)
     torch.cuda.synchronize()
     t0.record()
     for s in range(args.steps):
-        gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled,
-                 drift_ev[s], sim_ev[s])
+        batched_step(cdt, wl, sb, scores, cfgs, auroc_ws, counts, pooled, ev[s])
     t1.record()
     torch.cuda.synchronize()
     ms_total = t0.elapsed_time(t1)
     ms_step = ms_total / args.steps
-    drift_ms = [a.elapsed_time(b) for st in drift_ev for (a, b) in st]
-    sim_ms = [a.elapsed_time(b) for st in sim_ev for (a, b) in st]
     log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
 
     elems_per_step = sum(len(p.rs.runs) * p.rs.elems for p in preps)
@@ -248,24 +286,42 @@ def run_main(torch, cdt, W, args):
     scored_bytes = elems_per_step * DRIFT_BYTES_PER_ELEM + blocks_per_step * DRIFT_BYTES_PER_BLOCK
     value = scored_bytes / (ms_step * 1e-3) / 1e9
 
-    # dominant kernel: drift_score of the largest reference set
-    big = max(preps, key=lambda p: p.rs.elems)
-    per_launch = big.rs.elems * DRIFT_BYTES_PER_ELEM + big.rs.S * big.rs.C * DRIFT_BYTES_PER_BLOCK
-    k0 = sum(len(p.rs.runs) for p in preps[:preps.index(big)])
-    big_ms = [drift_ms[s * nrun + k0 + r] for s in range(args.steps) for r in range(len(big.rs.runs))]
-    big_sim = [sim_ms[s * nrun + k0 + r] for s in range(args.steps) for r in range(len(big.rs.runs))]
-    drift_avg = sum(big_ms) / len(big_ms)
-    sim_avg = sum(big_sim) / len(big_sim)
+    # dominant kernel: the batched Eq. 4 launch of the largest reference set.
+    # Its algorithmic bytes: every run's fp16 activations (2 B/element), the
+    # shared fp32 reference once (4 B/element), and the scores (4 B/block/run).
+    bi = max(range(nset), key=lambda i: preps[i].rs.elems)
+    big = preps[bi]
+    nr = len(big.rs.runs)
+    per_launch = big.rs.elems * (2 * nr + 4) + nr * big.rs.S * big.rs.C * DRIFT_BYTES_PER_BLOCK
+    drift_avg = sum(e[bi][2].elapsed_time(e[bi][3]) for e in ev) / args.steps
+    sim_avg = sum(e[bi][0].elapsed_time(e[bi][1]) for e in ev) / args.steps
     achieved = per_launch / (drift_avg * 1e-3) / 1e9
-    sim_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (sim_avg * 1e-3) / 1e9
+    # the live pass writes every run's activations and reads the reference
+    # once for them (its minimum traffic)
+    sim_bytes = big.rs.elems * (2 * nr + 4)
+    sim_gbps = sim_bytes / (sim_avg * 1e-3) / 1e9
     valu_busy, valu_per_el = measured_valu(wl.name)
-    # The same reads with no arithmetic (after the timed region): what the
-    # memory system gives the drift kernel's access pattern.
+
+    # The same step with one launch per run (each run reading the reference
+    # itself): the per-run rates, and the memory bounds of those launches'
+    # access patterns (no arithmetic), after the timed region.
+    per_run_ms = time_ms(torch, lambda: gpu_step(torch, cdt, wl, preps, scores, views, cfgs,
+                                                  auroc_ws, counts, pooled))
+    dev = [(E(enable_timing=True), E(enable_timing=True)) for _ in range(nrun)]
+    sev = [(E(enable_timing=True), E(enable_timing=True)) for _ in range(nrun)]
+    gpu_step(torch, cdt, wl, preps, scores, views, cfgs, auroc_ws, counts, pooled, dev, sev)
+    torch.cuda.synchronize()
+    k0 = sum(len(p.rs.runs) for p in preps[:bi])
+    one_drift = sum(dev[k0 + r][0].elapsed_time(dev[k0 + r][1]) for r in range(nr)) / nr
+    one_sim = sum(sev[k0 + r][0].elapsed_time(sev[k0 + r][1]) for r in range(nr)) / nr
+    one_bytes = big.rs.elems * DRIFT_BYTES_PER_ELEM + big.rs.S * big.rs.C * DRIFT_BYTES_PER_BLOCK
+    one_gbps = one_bytes / (one_drift * 1e-3) / 1e9
     read_ms = time_ms(torch, lambda: cdt.drift_read_stream(big.h, big.ref, ws=big.ws), 7)
     read_gbps = big.rs.elems * DRIFT_BYTES_PER_ELEM / (read_ms * 1e-3) / 1e9
-    # and the live pass's reads and writes with no random numbers (h = fp16(a))
+    one_sim_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (one_sim * 1e-3) / 1e9
     sim_stream_ms = time_ms(torch, lambda: cdt.canary_sim_stream(big.ref, out=big.h), 7)
     sim_stream_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (sim_stream_ms * 1e-3) / 1e9
+    batched_step(cdt, wl, sb, scores, cfgs, auroc_ws, counts, pooled)  # the reported counts
 
     res = {
         "metric": "drift-scored activation GB/s",
@@ -285,32 +341,45 @@ def run_main(torch, cdt, W, args):
             "shape_SxCxTxH": [big.rs.S, big.rs.C, big.rs.T, big.rs.H],
             "runs": [r.label for p in preps for r in p.rs.runs],
             "inputs": "fp16 live activations vs fp32 references, sums in fp64",
-            "step": "canary_sim + drift_score per run, one batched auroc",
+            "step": "per reference set: one batched canary_sim and one batched drift_score "
+                    "launch over its runs; one batched auroc",
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "drift_score (drift_partial_kernel + drift_combine_kernel)",
+            "kernel": "drift_score over the set's runs (drift_batch_partial_kernel + "
+                      "drift_batch_combine_kernel)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": measured_traffic(wl.name),
             "bytes_per_launch": per_launch,
+            "runs_per_launch": nr,
             "avg_launch_ms": round(drift_avg, 4),
-            "read_stream_GBps": round(read_gbps, 1),
-            "frac_of_read_stream": round(achieved / read_gbps, 4),
+            "scored_GBps": round(nr * one_bytes / (drift_avg * 1e-3) / 1e9, 1),
         },
         "canary_sim": {
             "avg_launch_ms": round(sim_avg, 4),
+            "runs_per_launch": nr,
             "GBps": round(sim_gbps, 1),
             "frac_of_hbm_peak": round(sim_gbps / HBM_PEAK_GBPS, 4),
-            "share_of_step": round(sim_avg * len(big.rs.runs) / ms_step, 4)
-            if len(preps) == 1 else None,
+            "share_of_step": round(sim_avg / ms_step, 4) if nset == 1 else None,
             "bound": "valu+hbm",
-            "stream_GBps": round(sim_stream_gbps, 1),
-            "frac_of_stream": round(sim_gbps / sim_stream_gbps, 4),
-            "valu_busy": valu_busy,
-            "valu_instr_per_element": valu_per_el,
+        },
+        "per_run_launches": {
+            "ms_per_step": round(per_run_ms, 4),
+            "value": round(scored_bytes / (per_run_ms * 1e-3) / 1e9, 2),
+            "drift_avg_launch_ms": round(one_drift, 4),
+            "drift_GBps": round(one_gbps, 1),
+            "drift_frac_of_hbm_peak": round(one_gbps / HBM_PEAK_GBPS, 4),
+            "read_stream_GBps": round(read_gbps, 1),
+            "drift_frac_of_read_stream": round(one_gbps / read_gbps, 4),
+            "canary_sim_avg_launch_ms": round(one_sim, 4),
+            "canary_sim_GBps": round(one_sim_gbps, 1),
+            "canary_sim_stream_GBps": round(sim_stream_gbps, 1),
+            "canary_sim_frac_of_stream": round(one_sim_gbps / sim_stream_gbps, 4),
+            "canary_sim_valu_busy": valu_busy,
+            "canary_sim_valu_instr_per_element": valu_per_el,
         },
     }
     vals = cdt.auroc_values(counts, pooled).cpu().numpy()  # Eq. 6 on the device
@@ -328,6 +397,8 @@ def run_main(torch, cdt, W, args):
         "reference_read_GBps": round(elems_per_step * 4 / (fused_ms * 1e-3) / 1e9, 1),
         "detection": {lab: round(float(vals[i][0]), 4) for i, lab in enumerate(labels)},
     }
+    del sb
+    torch.cuda.empty_cache()
     if not args.no_ablations:
         res["ablation_kernels"] = ablation_kernels(torch, cdt, wl, big)
     del preps, scores, views
@@ -530,44 +601,6 @@ def substudies(torch, cdt, W):
             "studies": out}
 
 
-class SweepBatches:
-    """The sweep's batched launches: per reference set, one live-pass launch
-    over all its configurations (each into its own activation array) and one
-    Eq. 4 launch over them, tables prepared once."""
-
-    def __init__(self, torch, cdt, wl, preps, views):
-        most = max(len(p.rs.runs) * p.rs.elems for p in preps)
-        self.h = torch.empty((most,), dtype=torch.float16, device="cuda")
-        self.sets, k = [], 0
-        for p in preps:
-            rs = p.rs
-            hs = [self.h[r * rs.elems:(r + 1) * rs.elems].view(rs.S, rs.C, rs.T, rs.H)
-                  for r in range(len(rs.runs))]
-            sim = cdt.sim_batch([(p.ref, hs[r], sim_kwargs(wl, rs, run, *p.scales[r]))
-                                 for r, run in enumerate(rs.runs)])
-            drift = cdt.drift_batch([(hs[r], p.ref, views[k + r], None)
-                                     for r in range(len(rs.runs))])
-            self.sets.append((sim, drift, rs))
-            k += len(rs.runs)
-
-
-def sweep_step_batched(cdt, wl, sb, scores, cfgs, auroc_ws, counts, pooled, ev=None):
-    """One pass of the sweep with the batched launches (per reference set: the
-    live pass of its configurations, then Eq. 4 of them), then the AUROC."""
-    for i, (sim, drift, _) in enumerate(sb.sets):
-        if ev is not None:
-            ev[i][0].record()
-        cdt.canary_sim_batch(sim)
-        if ev is not None:
-            ev[i][1].record()
-            ev[i][2].record()
-        cdt.drift_score_batch(drift)
-        if ev is not None:
-            ev[i][3].record()
-    cdt.auroc_launch(auroc_ws, len(cfgs), scores, seed=wl.seed,
-                     flags=cdt.AUROC_CONTROL | cdt.AUROC_POOLED, counts=counts, pooled=pooled)
-
-
 def run_sweep(torch, cdt, W, reps):
     import numpy as np
     wl = W.sweep()
@@ -578,16 +611,24 @@ def run_sweep(torch, cdt, W, reps):
     scores, views, cfgs, counts, pooled, auroc_ws = setup_batch(torch, cdt, wl, preps)
     sweep_elems = sum(len(p.rs.runs) * p.rs.elems for p in preps)
     # the batched step (the configurations/s the sweep reports)
-    sb = SweepBatches(torch, cdt, wl, preps, views)
+    sb = Batches(torch, cdt, wl, preps, views)
     E = torch.cuda.Event
-    step_b = lambda ev=None: sweep_step_batched(cdt, wl, sb, scores, cfgs, auroc_ws, counts,
-                                                pooled, ev)
+    step_b = lambda ev=None: batched_step(cdt, wl, sb, scores, cfgs, auroc_ws, counts, pooled,
+                                          ev)
     batched_ms = time_ms(torch, step_b, reps)
-    bev = [[E(enable_timing=True) for _ in range(4)] for _ in sb.sets]
-    step_b(bev)
-    torch.cuda.synchronize()
-    sim_b = sum(e[0].elapsed_time(e[1]) for e in bev)
-    drift_b = sum(e[2].elapsed_time(e[3]) for e in bev)
+    sims, drifts = [], []
+    for _ in range(max(3, reps)):
+        bev = [[E(enable_timing=True) for _ in range(4)] for _ in sb.sets]
+        step_b(bev)
+        torch.cuda.synchronize()
+        sims.append(sum(e[0].elapsed_time(e[1]) for e in bev))
+        drifts.append(sum(e[2].elapsed_time(e[3]) for e in bev))
+    sim_b = sorted(sims)[len(sims) // 2]
+    drift_b = sorted(drifts)[len(drifts) // 2]
+    # bytes the batched launches must move: every run's activations and each
+    # set's reference once
+    drift_moved = sum(p.rs.elems * (2 * len(p.rs.runs) + 4) for p in preps)
+    sim_moved = drift_moved
     counts_b, pooled_b = cdt.u64(counts), cdt.u64(pooled)
     del sb
     torch.cuda.empty_cache()
@@ -648,9 +689,16 @@ def run_sweep(torch, cdt, W, reps):
         "ms": round(batched_ms, 3),
         "configs_per_s": round(len(cfgs) / (batched_ms * 1e-3), 1),
         "step": "per reference set: one batched live-pass launch and one batched Eq. 4 launch "
-                "over its 24 configurations; one AUROC launch",
-        "drift_score_GBps": round(sweep_elems * DRIFT_BYTES_PER_ELEM / (drift_b * 1e-3) / 1e9, 1),
-        "canary_sim_GBps": round(sweep_elems * SIM_BYTES_PER_ELEM / (sim_b * 1e-3) / 1e9, 1),
+                "over its 24 configurations (reference shared); one AUROC launch",
+        "drift_ms": round(drift_b, 3),
+        "drift_moved_GBps": round(drift_moved / (drift_b * 1e-3) / 1e9, 1),
+        "drift_frac_of_hbm_peak": round(drift_moved / (drift_b * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "drift_scored_GBps": round(sweep_elems * DRIFT_BYTES_PER_ELEM / (drift_b * 1e-3) / 1e9,
+                                   1),
+        "canary_sim_ms": round(sim_b, 3),
+        "canary_sim_moved_GBps": round(sim_moved / (sim_b * 1e-3) / 1e9, 1),
+        "canary_sim_scored_GBps": round(sweep_elems * SIM_BYTES_PER_ELEM / (sim_b * 1e-3) / 1e9,
+                                        1),
         "batched_counts_equal": bool(np.array_equal(counts_b, cdt.u64(counts)) and
                                      np.array_equal(pooled_b, cdt.u64(pooled))),
         "unbatched_ms": round(ms, 3),
@@ -702,8 +750,8 @@ def config_runs(torch, cdt, W, name):
     # the compute-free read of the same arrays: what a launch of this size gets
     read_ms = time_ms(torch, lambda: cdt.drift_read_stream(prep.h, prep.ref, ws=prep.ws), 5)
     read_gbps = rs.elems * DRIFT_BYTES_PER_ELEM / (read_ms * 1e-3) / 1e9
-    # the runs' Eq. 4 as one batched launch (each run's activations in its own
-    # array; as many runs as fit 16 GiB of activations)
+    # the runs' Eq. 4 as one batched launch over the shared reference (each
+    # run's activations in its own array; as many runs as fit 16 GiB of them)
     nb = max(1, min(len(rs.runs), (16 << 30) // (2 * rs.elems)))
     hs = torch.empty((nb, rs.S, rs.C, rs.T, rs.H), dtype=torch.float16, device="cuda")
     scs = torch.empty((nb, rs.C, rs.S), dtype=torch.float32, device="cuda")
@@ -711,14 +759,15 @@ def config_runs(torch, cdt, W, name):
         cdt.canary_sim(prep.ref, out=hs[k], **sim_kwargs(wl, rs, rs.runs[k], *prep.scales[k]))
     drift = cdt.drift_batch([(hs[k], prep.ref, scs[k], None) for k in range(nb)])
     batch_ms = time_ms(torch, lambda: cdt.drift_score_batch(drift), 5)
-    batch_bytes = nb * nbytes
+    # the runs share the reference: the launch must read it once
+    moved = rs.elems * (2 * nb + 4) + nb * rs.S * rs.C * DRIFT_BYTES_PER_BLOCK
     del hs, scs, drift
     out = {"shape_SxCxTxH": [rs.S, rs.C, rs.T, rs.H],
            "drift_batched": {
                "runs": nb, "ms": round(batch_ms, 4),
-               "GBps": round(batch_bytes / (batch_ms * 1e-3) / 1e9, 1),
-               "frac_of_hbm_peak": round(batch_bytes / (batch_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-                                         4)},
+               "moved_GBps": round(moved / (batch_ms * 1e-3) / 1e9, 1),
+               "frac_of_hbm_peak": round(moved / (batch_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+               "scored_GBps": round(nb * nbytes / (batch_ms * 1e-3) / 1e9, 1)},
            "drift_ms": round(drift_ms, 4),
            "drift_GBps": round(nbytes / (drift_ms * 1e-3) / 1e9, 1),
            "drift_frac_of_hbm_peak": round(nbytes / (drift_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),

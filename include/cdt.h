@@ -195,10 +195,17 @@ int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim
  * the configurations of a reference set together): job j writes its own h
  * from its ref with its own parameters, bitwise as cdt_canary_sim would.
  * The chunks of all jobs form one grid, so short runs share the launch's
- * ramp-up and tail.  Every job must use the same benign_dist and benign_mode
- * and carry 0 (CDT_EINVAL otherwise); their shapes, tamper settings and
- * scales may differ.  jobs and each p: HOST, read during the call (the
- * job table is copied into ws on `stream`).  At most 65536 jobs.
+ * ramp-up and tail.  Consecutive jobs that read the same ref array (and
+ * have the same chunk count) are generated together, so that each
+ * reference chunk is read from HBM about once for all of them: with fewer
+ * than 8 such jobs their work is walked chunk by chunk, the jobs of a chunk
+ * one after another (re-reads from L2); with 8 or more, each XCD takes its
+ * own jobs over the same reference offsets (re-reads from the last-level
+ * cache).  Order the jobs so that runs sharing references are adjacent.
+ * Every job must use the same benign_dist and benign_mode and carry 0
+ * (CDT_EINVAL otherwise); their shapes, tamper settings and scales may
+ * differ.  jobs and each p: HOST, read during the call (the job and group
+ * tables are copied into ws on `stream`).  At most 65536 jobs.
  * ws: cdt_sim_batch_workspace_bytes(n_jobs) device bytes. */
 typedef struct cdt_sim_job {
     uint32_t S, C, T, H;
@@ -291,16 +298,22 @@ int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, cons
                             const float* ref, float* score, double* num_den, void* stream);
 
 /* Eq. 4 over several arrays in one launch (the factorial sweep scores the
- * configurations of a reference set together): job j scores its own
- * h[S][C][T][H] against its ref into its score[C][S] (num_den optional),
- * bitwise as cdt_drift_score would.  The chunks of all jobs form one grid, so
- * short arrays share the launch's ramp-up and tail instead of paying one
- * each, and one combine launch finishes every block.  jobs: HOST array,
+ * configurations of a reference set together; several runs against one
+ * reference set): job j scores its own h[S][C][T][H] against its ref into
+ * its score[C][S] (num_den optional), bitwise as cdt_drift_score would.  The
+ * chunks of all jobs form one grid, so short arrays share the launch's
+ * ramp-up and tail instead of paying one each, and one combine launch
+ * finishes every block.  Consecutive jobs that read the same ref array (and
+ * have the same chunk count) share its reads: one workgroup scores a chunk
+ * of up to 4 of them, reading the reference chunk once, so a group of up to
+ * 4 jobs moves 2k + 4 bytes per element instead of 6k (larger groups read
+ * the chunk once per 4 jobs, the repeats mostly from L2).  Order the jobs so
+ * that arrays scored against one reference are adjacent.  jobs: HOST array,
  * validated and copied into ws during the call (reusable when the call
  * returns); jobs with S*C = 0 are skipped.  At most 65536 jobs.
  * ws: cdt_drift_batch_workspace_bytes(n_jobs, jobs) device bytes (the job
- * table and every job's partial sums); calls that can overlap need their
- * own. */
+ * and group tables and every job's partial sums); calls that can overlap
+ * need their own. */
 typedef struct cdt_drift_job {
     uint32_t S, C, T, H;
     const uint16_t* h;   /* device fp16 bits [S][C][T][H]      */

@@ -468,7 +468,8 @@ size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 // partial sums laid out one job after another behind it in the workspace.
 struct DriftBatchPlan {
     std::vector<cdt::DriftJobDev> table;
-    uint64_t total_chunks = 0, total_blocks = 0, partial_doubles = 0;
+    std::vector<cdt::BatchGroupDev> groups;
+    uint64_t total_iters = 0, total_blocks = 0, partial_doubles = 0;
 };
 
 // Shapes only (no pointers): what cdt_drift_batch_workspace_bytes sizes.
@@ -497,7 +498,6 @@ int plan_drift_batch(const char* fn, uint32_t n_jobs, const cdt_drift_job* jobs,
         d.score = J.score;
         d.sums = J.num_den;
         d.cpb = cdt::reduce_chunks_per_block(n);
-        d.chunk_begin = plan->total_chunks;
         d.block_begin = plan->total_blocks;
         d.n8 = static_cast<uint32_t>(n / 8);
         d.S = J.S;
@@ -508,18 +508,41 @@ int plan_drift_batch(const char* fn, uint32_t n_jobs, const cdt_drift_job* jobs,
             d.partial = reinterpret_cast<double*>(static_cast<uintptr_t>(plan->partial_doubles));
             plan->partial_doubles += chunks * 2;
         }
-        plan->total_chunks += (chunks + 7) / 8 * 8;  // every job starts on a multiple of 8
         plan->total_blocks += nb;
         plan->table.push_back(d);
     }
+    // jobs in a row over one reference array, with equal chunk counts, share
+    // its chunks (BatchGroupDev)
+    const uint32_t nt = static_cast<uint32_t>(plan->table.size());
+    std::vector<const void*> refs(nt);
+    std::vector<uint64_t> chunks(nt);
+    for (uint32_t j = 0; j < nt; ++j) {
+        refs[j] = plan->table[j].ref;
+        chunks[j] = plan->table[j].cpb * plan->table[j].S * plan->table[j].C;
+    }
+    plan->groups.resize(nt);
+    uint32_t ng = 0;
+    plan->total_iters = cdt::plan_batch_groups(nt, refs.data(), chunks.data(),
+                                               cdt::kDriftJobsPerIter, cdt::kDriftJobMajorFrom,
+                                               plan->groups.data(), &ng);
+    plan->groups.resize(ng);
     if (plan->total_blocks > kMaxBlocks * 16)
         return fail(CDT_ELIMIT, "%s: the batch holds too many blocks", fn);
     return CDT_OK;
 }
 
+// Workspace: the job table, the group table, then the partial sums.
+size_t batch_groups_offset(const DriftBatchPlan& plan) {
+    return align256(plan.table.size() * sizeof(cdt::DriftJobDev));
+}
+
+// (room for one group per job, so that the size depends on the shapes only)
+size_t batch_partials_offset(const DriftBatchPlan& plan) {
+    return batch_groups_offset(plan) + align256(plan.table.size() * sizeof(cdt::BatchGroupDev));
+}
+
 size_t batch_bytes(const DriftBatchPlan& plan) {
-    return align256(plan.table.size() * sizeof(cdt::DriftJobDev)) +
-           plan.partial_doubles * sizeof(double);
+    return batch_partials_offset(plan) + plan.partial_doubles * sizeof(double);
 }
 
 }  // namespace
@@ -545,20 +568,27 @@ int cdt_drift_score_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws, 
         return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
                     ws ? ws_bytes : 0);
     if (!aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
-    // partial offsets -> addresses behind the table in ws
-    double* partials = reinterpret_cast<double*>(
-        static_cast<char*>(ws) + align256(plan.table.size() * sizeof(cdt::DriftJobDev)));
+    // partial offsets -> addresses behind the tables in ws; the two tables
+    // go up in one copy (staged contiguously on the host)
+    char* base = static_cast<char*>(ws);
+    double* partials = reinterpret_cast<double*>(base + batch_partials_offset(plan));
     for (cdt::DriftJobDev& d : plan.table)
         if (!d.direct) d.partial = partials + reinterpret_cast<uintptr_t>(d.partial);
+    std::vector<char> staged(batch_partials_offset(plan), 0);
+    memcpy(staged.data(), plan.table.data(), plan.table.size() * sizeof(cdt::DriftJobDev));
+    memcpy(staged.data() + batch_groups_offset(plan), plan.groups.data(),
+           plan.groups.size() * sizeof(cdt::BatchGroupDev));
     hipStream_t st = static_cast<hipStream_t>(stream);
-    const hipError_t e = hipMemcpyAsync(ws, plan.table.data(),
-                                        plan.table.size() * sizeof(cdt::DriftJobDev),
-                                        hipMemcpyHostToDevice, st);
+    const hipError_t e = hipMemcpyAsync(ws, staged.data(), staged.size(), hipMemcpyHostToDevice,
+                                        st);
     if (e != hipSuccess) return device_status(e, fn);
-    return device_status(cdt::launch_drift_batch(static_cast<const cdt::DriftJobDev*>(ws),
-                                                 static_cast<uint32_t>(plan.table.size()),
-                                                 plan.total_chunks, plan.total_blocks, st),
-                         fn);
+    return device_status(
+        cdt::launch_drift_batch(
+            reinterpret_cast<const cdt::DriftJobDev*>(base),
+            static_cast<uint32_t>(plan.table.size()),
+            reinterpret_cast<const cdt::BatchGroupDev*>(base + batch_groups_offset(plan)),
+            static_cast<uint32_t>(plan.groups.size()), plan.total_iters, plan.total_blocks, st),
+        fn);
 }
 
 int cdt_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,

@@ -26,6 +26,19 @@ __device__ __forceinline__ uint64_t xcd_contiguous(uint64_t it, uint64_t total) 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Pointers into device memory (the global address space).  Loads and stores
+// through them compile to global_* instructions also where the pointer was
+// read from memory (a batched launch's job table), where a generic pointer
+// would give flat_* instructions, which also count against the LDS and
+// scalar-load counter and so make every wait on either one wait for them.
+template <typename T>
+using gptr = __attribute__((address_space(1))) T*;
+
+template <typename T>
+__device__ __forceinline__ gptr<T> global_ptr(T* p) {
+    return (gptr<T>)p;
+}
+
 // Random stream ids (fourth counter word = stream << 24 | id).
 enum : uint32_t {
     kStreamRef = 0,

@@ -6,6 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "cdt_device.hpp"
 #include "cdt_reduce.hpp"
 
 namespace cdt {
@@ -19,6 +20,12 @@ namespace cdt {
 // reference is always loaded before the current one is generated, so only
 // the first load of a chunk is exposed).
 constexpr int kGenThreads = 1024;
+// Batch groups (BatchGroupDev): jobs per iteration, and the unit count
+// from which a group is walked job-major, for the live pass and Eq. 4.
+constexpr uint32_t kSimJobsPerIter = 1;
+constexpr uint32_t kSimJobMajorFrom = 8;
+constexpr uint32_t kDriftJobsPerIter = 4;
+constexpr uint32_t kDriftJobMajorFrom = 0xFFFFFFFFu;
 constexpr int kGenItems = 8;
 constexpr uint32_t kGenChunkGroups = kGenThreads * kGenItems;
 
@@ -57,9 +64,111 @@ hipError_t launch_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const d
                                float* bscale, hipStream_t st);
 hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, hipStream_t st);
 
+// A run of consecutive jobs of a batched launch that read one reference
+// array, and the order its iterations take.  An iteration is one chunk of
+// up to `jobs_per_iter` of the group's jobs (a unit); each XCD takes one
+// contiguous eighth of the group's iterations, and
+//   * chunk-major: on each chunk, the group's units one after another, so
+//     neighbouring workgroups of one XCD read the same reference chunk at
+//     nearly the same time and all but the first read of it are served by
+//     the XCD's L2;
+//   * job-major: each unit from its first chunk on, so with at least 8
+//     units the 8 XCDs generate 8 different jobs over the same reference
+//     offsets at the same time and the last-level cache serves most of the
+//     re-reads.
+// Eq. 4 scores up to 4 jobs per iteration, chunk-major, reading each
+// reference chunk once for them.  The live pass generates one job per
+// iteration (its work is the random numbers, not the reads), job-major from
+// 8 jobs on: for the sweep's 24-run groups that beats chunk-major (33.5 ms
+// against 39.4-45.8 ms over the sweep), whose reuse in L2 does not make up
+// for the traffic it adds there; with fewer jobs chunk-major wins (3 runs of
+// the 16 x 256 x 256 x 8192 shape: 25.9 ms against 29 ms).
+struct BatchGroupDev {
+    uint64_t iter_begin;  // first iteration of the group (a multiple of 8)
+    uint64_t chunks;      // chunks of one of its jobs
+    uint32_t first_job, n_jobs;
+    uint32_t chunk_major, jobs_per_iter;
+};
+
+// Iteration `it` of a grouped batch -> (first job of its unit, jobs in the
+// unit, chunk, jobs in the group); false for the padding that rounds each
+// group up to a multiple of 8 iterations.  The group is found by a binary
+// search (workgroup-uniform).  Iteration it runs on XCD it % 8 (a grid
+// stride that is a multiple of 8), and so does the group-local index, since
+// every group starts on a multiple of 8.
+__device__ __forceinline__ bool batch_iter(const BatchGroupDev* __restrict__ groups,
+                                           uint32_t n_groups, uint64_t it, uint32_t* job,
+                                           uint32_t* unit_jobs, uint64_t* chunk,
+                                           uint32_t* group_jobs) {
+    uint32_t lo = 0, hi = n_groups;  // last group whose first iteration <= it
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (groups[mid].iter_begin <= it) lo = mid; else hi = mid;
+    }
+    const BatchGroupDev& G = groups[lo];
+    const uint64_t units = (G.n_jobs + G.jobs_per_iter - 1) / G.jobs_per_iter;
+    const uint64_t local = it - G.iter_begin, span = G.chunks * units;
+    if (local >= span) return false;
+    const uint64_t x = xcd_contiguous(local, span);
+    uint64_t u;
+    if (G.chunk_major) {
+        *chunk = x / units;
+        u = x - *chunk * units;
+    } else {
+        u = x / G.chunks;
+        *chunk = x - u * G.chunks;
+    }
+    const uint32_t first = static_cast<uint32_t>(u) * G.jobs_per_iter;
+    *job = G.first_job + first;
+    *unit_jobs = G.n_jobs - first < G.jobs_per_iter ? G.n_jobs - first : G.jobs_per_iter;
+    *group_jobs = G.n_jobs;
+    return true;
+}
+
+// Host side: the groups of a batch whose job j (jobs without chunks left
+// out by the caller) reads reference refs[j] and has chunks[j] chunks;
+// consecutive jobs with the same reference and chunk count form a group
+// (every group's chunk index is then in range for each of its jobs).  A
+// group is walked chunk-major when it has fewer than `job_major_from`
+// units.  Fills groups[0 .. *n_groups) and returns the padded iteration
+// count.
+inline uint64_t plan_batch_groups(uint32_t n_jobs, const void* const* refs,
+                                  const uint64_t* chunks, uint32_t jobs_per_iter,
+                                  uint32_t job_major_from, BatchGroupDev* groups,
+                                  uint32_t* n_groups) {
+    *n_groups = 0;
+    for (uint32_t j = 0; j < n_jobs; ++j) {
+        if (*n_groups) {
+            BatchGroupDev& last = groups[*n_groups - 1];
+            if (refs[last.first_job] == refs[j] && last.chunks == chunks[j]) {
+                ++last.n_jobs;
+                continue;
+            }
+        }
+        BatchGroupDev g;
+        g.iter_begin = 0;
+        g.chunks = chunks[j];
+        g.first_job = j;
+        g.n_jobs = 1;
+        g.chunk_major = 1;
+        g.jobs_per_iter = jobs_per_iter;
+        groups[(*n_groups)++] = g;
+    }
+    uint64_t total = 0;
+    for (uint32_t k = 0; k < *n_groups; ++k) {
+        BatchGroupDev& g = groups[k];
+        const uint64_t units = (g.n_jobs + jobs_per_iter - 1) / jobs_per_iter;
+        g.chunk_major = units < job_major_from;
+        g.iter_begin = total;
+        total += (g.chunks * units + 7) / 8 * 8;
+    }
+    return total;
+}
+
 // Batched live pass over runs of one noise distribution and mode, carry 0:
-// the device table (sim_batch_table_bytes(n_jobs) bytes) is filled from
-// `runs` on the stream, then one grid generates every run's chunks.
+// the device table (sim_batch_table_bytes(n_jobs) bytes: jobs, then groups)
+// is filled from `runs` on the stream, then one grid generates every run's
+// chunks.
 size_t sim_batch_table_bytes(uint32_t n_jobs);
 hipError_t launch_canary_sim_batch(uint32_t n_jobs, const SimLaunch* runs,
                                    const float* const* refs, uint16_t* const* hs, void* table,
@@ -78,8 +187,8 @@ hipError_t launch_drift(DriftMetric metric, uint32_t S, uint32_t C, uint32_t T, 
                         hipStream_t st);
 
 // One array of a batched Eq. 4 launch, as the kernels read it from the
-// device table: its arrays, shape, chunking and place in the batch's chunk
-// and block index ranges.
+// device table: its arrays, shape, chunking and place in the batch's block
+// index range.
 struct DriftJobDev {
     const uint16_t* h;
     const float* ref;
@@ -87,12 +196,13 @@ struct DriftJobDev {
     double* sums;     // [C][S][2] or null
     double* partial;  // its per-chunk partial sums (unused when direct)
     uint64_t cpb;     // chunks per block
-    uint64_t chunk_begin, block_begin;
+    uint64_t block_begin;
     uint32_t n8, S, C, direct;
 };
 
-hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs, uint64_t total_chunks,
-                              uint64_t total_blocks, hipStream_t st);
+hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs,
+                              const BatchGroupDev* groups_dev, uint32_t n_groups,
+                              uint64_t total_iters, uint64_t total_blocks, hipStream_t st);
 
 // drift_score's reads (same chunks, loads and order) with no arithmetic; ws
 // is drift_score's workspace and may be overwritten.

@@ -71,12 +71,11 @@ inline SimArgs make_sim_args(const SimLaunch& p, uint64_t chunks_per_block,
 }
 
 // One run of a batched live pass, as the kernel reads it from the device
-// table: its launch parameters, arrays and first chunk in the batch.
+// table: its launch parameters and arrays.
 struct SimJobDev {
     SimArgs A;
     const float* ref;
     uint16_t* h;
-    uint64_t chunk_begin;
 };
 
 // Block-uniform state: which (shard, canary) and its scales; c is the

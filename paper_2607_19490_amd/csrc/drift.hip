@@ -102,13 +102,15 @@ __device__ __forceinline__ void drift_chunk(const uint16_t* __restrict__ h,
         const uint64_t b = chunk / chunks_per_block;
         const uint32_t g0 = static_cast<uint32_t>(chunk - b * chunks_per_block) * kChunkGroups;
         const uint32_t g_end = min(g0 + kChunkGroups, n8);
-        const u32x4* hb = reinterpret_cast<const u32x4*>(h + b * n);
-        const f32x4* ab = nullptr;  // fp32 reference block
-        const u32x4* rb = nullptr;  // fp16 reference block
+        const gptr<const u32x4> hb = global_ptr(reinterpret_cast<const u32x4*>(h + b * n));
+        gptr<const f32x4> ab = nullptr;  // fp32 reference block
+        gptr<const u32x4> rb = nullptr;  // fp16 reference block
         if constexpr (Tr::kHalfRef)
-            rb = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(ref) + b * n);
+            rb = global_ptr(
+                reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(ref) + b * n));
         else
-            ab = reinterpret_cast<const f32x4*>(static_cast<const float*>(ref) + b * n);
+            ab = global_ptr(
+                reinterpret_cast<const f32x4*>(static_cast<const float*>(ref) + b * n));
         double acc[Tr::kSums];
 #pragma unroll
         for (int k = 0; k < Tr::kSums; ++k) acc[k] = 0.0;
@@ -122,7 +124,7 @@ __device__ __forceinline__ void drift_chunk(const uint16_t* __restrict__ h,
 #pragma unroll
                 for (int u = 0; u < kReduceUnroll; ++u) {
                     const uint32_t g = base + u * kReduceThreads + threadIdx.x;
-                    const f32x4* aw = ab + 2 * (base + u * kReduceThreads + wave0);
+                    const gptr<const f32x4> aw = ab + 2 * (base + u * kReduceThreads + wave0);
                     hv[u] = __builtin_nontemporal_load(hb + g);
                     rv[u] = u32x4{0u, 0u, 0u, 0u};
                     quads_to_groups(__builtin_nontemporal_load(aw + lane),
@@ -188,37 +190,134 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
                                    partial, direct, S, C, score, sums);
 }
 
-// Batched Eq. 4: the chunks of every job form one index range (job j owns
-// [chunk_begin_j, chunk_begin_j + its chunks rounded up to a multiple of
-// 8)), walked by one grid; each chunk is scored exactly as the single launch
-// scores it.  Because every job starts on a multiple of 8, iteration index
-// it runs on XCD it % 8 inside each job too, and the XCD-contiguous map is
-// applied per job: the 8 XCDs stream different eighths of the same job,
-// as in a single launch, instead of 8 jobs from their first bytes at once
-// (the jobs of a sweep share their references, and equal offsets of
-// equally sized arrays fall on the same memory channels).  The job of an
-// iteration is found by a binary search of the table (workgroup-uniform).
+// One chunk of kJ arrays scored against one shared reference (Eq. 4): each
+// step's reference groups are loaded once (nontemporally, as in
+// drift_chunk) and every job's activations of the step are loaded at once
+// and accumulated against them.  The step is kMultiUnroll groups per thread
+// (not drift_chunk's kReduceUnroll, so that every job's loads fit in
+// registers together); a thread still visits its groups g0 + tid + 256 m in
+// the order m = 0, 1, 2, ... and adds the same values in the same order as
+// drift_chunk, so each job's sums are bitwise those of one launch per job.
+constexpr int kMultiUnroll = 4;
+
+template <int kJ>
+__device__ __forceinline__ void drift_chunk_jobs(const DriftJobDev* __restrict__ jobs,
+                                                 uint64_t chunk) {
+    constexpr int kU = kMultiUnroll;
+    const DriftJobDev& J0 = jobs[0];
+    const uint64_t n = static_cast<uint64_t>(J0.n8) * 8;
+    const uint64_t b = chunk / J0.cpb;
+    const uint32_t g0 = static_cast<uint32_t>(chunk - b * J0.cpb) * kChunkGroups;
+    const uint32_t g_end = min(g0 + kChunkGroups, J0.n8);
+    const gptr<const f32x4> ab = global_ptr(reinterpret_cast<const f32x4*>(J0.ref + b * n));
+    gptr<const u32x4> hb[kJ];
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) hb[j] = global_ptr(reinterpret_cast<const u32x4*>(jobs[j].h + b * n));
+    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+    double acc[kJ][2];
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) acc[j][0] = acc[j][1] = 0.0;
+    for (uint32_t base = g0; base < g_end; base += kReduceThreads * kU) {
+        f32x4 a0[kU], a1[kU];
+        u32x4 hv[kJ][kU];
+        if (base + kReduceThreads * kU <= g_end) {
+            // every group of the step is in range (workgroup-uniform)
+            const uint32_t lane = threadIdx.x % kWave, wave0 = threadIdx.x - lane;
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const gptr<const f32x4> aw = ab + 2 * (base + u * kReduceThreads + wave0);
+                quads_to_groups(__builtin_nontemporal_load(aw + lane),
+                                __builtin_nontemporal_load(aw + kWave + lane), a0[u], a1[u]);
+            }
+#pragma unroll
+            for (int j = 0; j < kJ; ++j)
+#pragma unroll
+                for (int u = 0; u < kU; ++u)
+                    hv[j][u] =
+                        __builtin_nontemporal_load(hb[j] + base + u * kReduceThreads + threadIdx.x);
+        } else {
+            // the last, partial step of a ragged block: every lane loads an
+            // element in range (its own, or the chunk's last) and keeps zeros
+            // where its own is out of range
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const uint32_t g = base + u * kReduceThreads + threadIdx.x;
+                const uint32_t gc = g < g_end ? g : g_end - 1;
+                const f32x4 l0 = __builtin_nontemporal_load(ab + 2 * gc);
+                const f32x4 l1 = __builtin_nontemporal_load(ab + 2 * gc + 1);
+                const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+                a0[u] = g < g_end ? l0 : z;
+                a1[u] = g < g_end ? l1 : z;
+#pragma unroll
+                for (int j = 0; j < kJ; ++j) {
+                    const u32x4 l = __builtin_nontemporal_load(hb[j] + gc);
+                    hv[j][u] = g < g_end ? l : zero;
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u)
+                accumulate8<DriftMetric::kL2>(hv[j][u], zero, a0[u], a1[u], acc[j]);
+            // an empty register constraint: the compiler must assume the
+            // reference changed, so it widens it to fp64 again per job
+            // instead of keeping the widened copies of every job alive
+#pragma unroll
+            for (int u = 0; u < kU; ++u) asm volatile("" : "+v"(a0[u]), "+v"(a1[u]));
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) {
+        block_sum<2>(acc[j]);
+        if (threadIdx.x == 0) {
+            const DriftJobDev& J = jobs[j];
+            if (J.direct) {
+                finish_block<DriftMetric::kL2>(acc[j], chunk, J.S, J.C, J.score, J.sums);
+            } else {
+                J.partial[chunk * 2] = acc[j][0];
+                J.partial[chunk * 2 + 1] = acc[j][1];
+            }
+        }
+    }
+}
+
+// Batched Eq. 4: the jobs' chunks form one iteration range walked by one
+// grid, group by group (batch_iter): jobs sharing a reference are taken up
+// to kDriftJobsPerIter at a time per chunk (drift_chunk_jobs reads the
+// reference chunk once for them), chunk-major, each XCD on its own eighth
+// of the group.  Every job's sums are bitwise those of the single launch.
+// The combine kernel finds a block's job by a binary search over the jobs'
+// first blocks.
 __device__ __forceinline__ uint32_t find_job(const DriftJobDev* __restrict__ jobs,
-                                             uint32_t n_jobs, uint64_t x, bool by_block) {
-    uint32_t lo = 0, hi = n_jobs;  // last job whose begin <= x
+                                             uint32_t n_jobs, uint64_t block) {
+    uint32_t lo = 0, hi = n_jobs;  // last job whose first block <= block
     while (hi - lo > 1) {
         const uint32_t mid = (lo + hi) / 2;
-        const uint64_t begin = by_block ? jobs[mid].block_begin : jobs[mid].chunk_begin;
-        if (begin <= x) lo = mid; else hi = mid;
+        if (jobs[mid].block_begin <= block) lo = mid; else hi = mid;
     }
     return lo;
 }
 
 __global__ __launch_bounds__(kReduceThreads) void drift_batch_partial_kernel(
-    const DriftJobDev* __restrict__ jobs, uint32_t n_jobs, uint64_t total_chunks) {
-    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
-        const DriftJobDev& J = jobs[find_job(jobs, n_jobs, it, false)];
-        const uint64_t local = it - J.chunk_begin;
-        const uint64_t chunks = J.cpb * J.S * J.C;
-        if (local >= chunks) continue;  // padding to the job's multiple of 8
-        drift_chunk<DriftMetric::kL2, false>(J.h, J.ref, J.n8, J.cpb,
-                                             xcd_contiguous(local, chunks), J.partial, J.direct,
-                                             J.S, J.C, J.score, J.sums);
+    const DriftJobDev* __restrict__ jobs, const BatchGroupDev* __restrict__ groups,
+    uint32_t n_groups, uint64_t total_iters) {
+    for (uint64_t it = blockIdx.x; it < total_iters; it += gridDim.x) {
+        uint32_t j, unit_jobs, group_jobs;
+        uint64_t chunk;
+        if (!batch_iter(groups, n_groups, it, &j, &unit_jobs, &chunk, &group_jobs)) continue;
+        static_assert(kDriftJobsPerIter == 4, "one case per unit size");
+        if (unit_jobs == 4) {
+            drift_chunk_jobs<4>(jobs + j, chunk);
+        } else if (unit_jobs == 3) {
+            drift_chunk_jobs<3>(jobs + j, chunk);
+        } else if (unit_jobs == 2) {
+            drift_chunk_jobs<2>(jobs + j, chunk);
+        } else {
+            const DriftJobDev& J = jobs[j];
+            drift_chunk<DriftMetric::kL2, false>(J.h, J.ref, J.n8, J.cpb, chunk, J.partial,
+                                                 J.direct, J.S, J.C, J.score, J.sums);
+        }
     }
 }
 
@@ -226,7 +325,7 @@ __global__ void drift_batch_combine_kernel(const DriftJobDev* __restrict__ jobs,
                                            uint64_t total_blocks) {
     const uint64_t g = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (g >= total_blocks) return;
-    const DriftJobDev& J = jobs[find_job(jobs, n_jobs, g, true)];
+    const DriftJobDev& J = jobs[find_job(jobs, n_jobs, g)];
     if (J.direct) return;  // scored by the partial kernel itself
     const uint64_t b = g - J.block_begin;
     double acc[2] = {0.0, 0.0};
@@ -286,12 +385,14 @@ hipError_t launch_drift_t(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const 
     return launch_combine_t<kM>(partial, cpb, nblocks, S, C, score, sums, st);
 }
 
-hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs, uint64_t total_chunks,
-                              uint64_t total_blocks, hipStream_t st) {
+hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs,
+                              const BatchGroupDev* groups_dev, uint32_t n_groups,
+                              uint64_t total_iters, uint64_t total_blocks, hipStream_t st) {
     if (n_jobs == 0) return hipSuccess;
-    if (total_chunks > 0) {
-        hipLaunchKernelGGL(drift_batch_partial_kernel, dim3(reduce_grid(total_chunks)),
-                           dim3(kReduceThreads), 0, st, jobs_dev, n_jobs, total_chunks);
+    if (total_iters > 0) {
+        hipLaunchKernelGGL(drift_batch_partial_kernel, dim3(reduce_grid(total_iters)),
+                           dim3(kReduceThreads), 0, st, jobs_dev, groups_dev, n_groups,
+                           total_iters);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -8,6 +8,7 @@
 // (one 16-byte store).  All fp32 arithmetic is written one operation per
 // step with FMA contraction off, so results are reproducible bit for bit.
 #include <math.h>
+#include <string.h>
 
 #include <vector>
 
@@ -48,8 +49,10 @@ __global__ __launch_bounds__(256) void outlier_gain_kernel(uint32_t H, uint32_t 
 // once per launch).  The fp16 output is stored nontemporally: it leaves no
 // dirty lines behind in L2 / the Infinity Cache for the next kernel to evict.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ f32x4 load_stream(const f32x4* p) { return *p; }
-__device__ __forceinline__ void store_stream(u32x4* p, u32x4 v) {
+template <typename P>
+__device__ __forceinline__ f32x4 load_stream(P p) { return *p; }
+template <typename P>
+__device__ __forceinline__ void store_stream(P p, u32x4 v) {
     __builtin_nontemporal_store(v, p);
 }
 
@@ -143,8 +146,8 @@ __device__ __forceinline__ void sim_chunk(const SimArgs& A, uint64_t chunk,
     {
         const ChunkPos p = chunk_pos(chunk, A.chunks_per_block, A.C, sim_chunk_groups<kT3>());
         const SimBlock B = sim_block<kBlock>(A, p.block);
-        const f32x4* in = reinterpret_cast<const f32x4*>(ref + p.block * n);
-        u32x4* out = reinterpret_cast<u32x4*>(h + p.block * n);
+        const gptr<const f32x4> in = global_ptr(reinterpret_cast<const f32x4*>(ref + p.block * n));
+        const gptr<u32x4> out = global_ptr(reinterpret_cast<u32x4*>(h + p.block * n));
         // Double buffer: the next group's reference loads are issued before
         // the Philox work on the current group, so loads overlap the ALU work.
         uint32_t g = p.g0 + threadIdx.x;
@@ -179,29 +182,22 @@ __global__ __launch_bounds__(sim_threads<kT3>()) void canary_sim_kernel(
         sim_chunk<kT3, kBlock, kStream>(A, xcd_contiguous(it, A.total_chunks), ref, h);
 }
 
-// Batched live pass: the chunks of every job (a run's parameters, its
-// references and its output) form one index range walked by one grid in the
-// XCD-contiguous order over the whole batch, so each XCD generates its own
-// jobs from their first chunk on; the job of a chunk is found by a binary
-// search of the table (workgroup-uniform) and the chunk is generated exactly
-// as the single-run launch generates it.  The sweep's jobs share their
-// references: 8 XCDs generating 8 configurations of one reference set read
-// the same reference lines at nearly the same time, and most of those reads
-// are served by the last-level cache (the 216-configuration sweep's live
-// pass: 7.15 TB/s of algorithmic bytes against 5.9 TB/s when each job is
-// split over the XCDs instead, which spaces the re-reads too far apart).
+// Batched live pass: the jobs' chunks form one iteration range walked by
+// one grid, group by group (batch_iter): the runs of a group share their
+// references and are walked chunk-major, so a reference chunk is read from
+// HBM once and served from L2 to the group's other runs, and each XCD
+// generates its own eighth of the group.  Each chunk is generated exactly as
+// the single-run launch generates it.
 template <bool kT3, bool kBlock>
 __global__ __launch_bounds__(sim_threads<kT3>()) void canary_sim_batch_kernel(
-    const SimJobDev* __restrict__ jobs, uint32_t n_jobs, uint64_t total_chunks) {
-    for (uint64_t it = blockIdx.x; it < total_chunks; it += gridDim.x) {
-        const uint64_t chunk = xcd_contiguous(it, total_chunks);
-        uint32_t lo = 0, hi = n_jobs;  // last job whose first chunk <= chunk
-        while (hi - lo > 1) {
-            const uint32_t mid = (lo + hi) / 2;
-            if (jobs[mid].chunk_begin <= chunk) lo = mid; else hi = mid;
-        }
-        const SimJobDev& J = jobs[lo];
-        sim_chunk<kT3, kBlock, false>(J.A, chunk - J.chunk_begin, J.ref, J.h);
+    const SimJobDev* __restrict__ jobs, const BatchGroupDev* __restrict__ groups,
+    uint32_t n_groups, uint64_t total_iters) {
+    for (uint64_t it = blockIdx.x; it < total_iters; it += gridDim.x) {
+        uint32_t j, unit_jobs, group_jobs;
+        uint64_t chunk;
+        if (!batch_iter(groups, n_groups, it, &j, &unit_jobs, &chunk, &group_jobs)) continue;
+        const SimJobDev& J = jobs[j];
+        sim_chunk<kT3, kBlock, false>(J.A, chunk, J.ref, J.h);
     }
 }
 
@@ -340,22 +336,30 @@ hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, 
                               : launch_sim_t<false>(p, ref, h, st);
 }
 
+// Table layout: n_jobs SimJobDev, then (256-byte aligned) up to n_jobs
+// BatchGroupDev.
+size_t sim_batch_groups_offset(uint32_t n_jobs) {
+    return (static_cast<size_t>(n_jobs) * sizeof(SimJobDev) + 255) & ~static_cast<size_t>(255);
+}
+
 size_t sim_batch_table_bytes(uint32_t n_jobs) {
-    return static_cast<size_t>(n_jobs) * sizeof(SimJobDev);
+    return sim_batch_groups_offset(n_jobs) + static_cast<size_t>(n_jobs) * sizeof(BatchGroupDev);
 }
 
 template <bool kT3, bool kBlock>
-void launch_sim_batch_t(const SimJobDev* jobs, uint32_t n_jobs, uint64_t total, hipStream_t st) {
+void launch_sim_batch_t(const SimJobDev* jobs, const BatchGroupDev* groups, uint32_t n_groups,
+                        uint64_t total, hipStream_t st) {
     hipLaunchKernelGGL((canary_sim_batch_kernel<kT3, kBlock>), dim3(gen_grid(total)),
-                       dim3(sim_threads<kT3>()), 0, st, jobs, n_jobs, total);
+                       dim3(sim_threads<kT3>()), 0, st, jobs, groups, n_groups, total);
 }
 
 hipError_t launch_canary_sim_batch(uint32_t n_jobs, const SimLaunch* runs,
                                    const float* const* refs, uint16_t* const* hs, void* table,
                                    hipStream_t st) {
     std::vector<SimJobDev> jobs;
+    std::vector<const void*> job_refs;
+    std::vector<uint64_t> job_chunks;
     jobs.reserve(n_jobs);
-    uint64_t total = 0;
     bool t3 = false, block_mode = false;
     for (uint32_t j = 0; j < n_jobs; ++j) {
         const SimLaunch& p = runs[j];
@@ -370,24 +374,34 @@ hipError_t launch_canary_sim_batch(uint32_t n_jobs, const SimLaunch* runs,
         d.A = make_sim_args(p, cpb, cpb * nblocks);
         d.ref = refs[j];
         d.h = hs[j];
-        d.chunk_begin = total;
-        total += cpb * nblocks;
         jobs.push_back(d);
+        job_refs.push_back(refs[j]);
+        job_chunks.push_back(cpb * nblocks);
     }
     if (jobs.empty()) return hipSuccess;
-    hipError_t e = hipMemcpyAsync(table, jobs.data(), jobs.size() * sizeof(SimJobDev),
-                                  hipMemcpyHostToDevice, st);
+    const uint32_t n = static_cast<uint32_t>(jobs.size());
+    const size_t goff = sim_batch_groups_offset(n);
+    std::vector<char> staged(goff + n * sizeof(BatchGroupDev), 0);
+    BatchGroupDev* groups = reinterpret_cast<BatchGroupDev*>(staged.data() + goff);
+    uint32_t n_groups = 0;
+    const uint64_t total = plan_batch_groups(n, job_refs.data(), job_chunks.data(),
+                                             kSimJobsPerIter, kSimJobMajorFrom, groups,
+                                             &n_groups);
+    memcpy(staged.data(), jobs.data(), n * sizeof(SimJobDev));
+    const size_t bytes = goff + n_groups * sizeof(BatchGroupDev);
+    hipError_t e = hipMemcpyAsync(table, staged.data(), bytes, hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return e;
     const SimJobDev* dev = static_cast<const SimJobDev*>(table);
-    const uint32_t n = static_cast<uint32_t>(jobs.size());
+    const BatchGroupDev* gdev =
+        reinterpret_cast<const BatchGroupDev*>(static_cast<const char*>(table) + goff);
     if (t3 && block_mode)
-        launch_sim_batch_t<true, true>(dev, n, total, st);
+        launch_sim_batch_t<true, true>(dev, gdev, n_groups, total, st);
     else if (t3)
-        launch_sim_batch_t<true, false>(dev, n, total, st);
+        launch_sim_batch_t<true, false>(dev, gdev, n_groups, total, st);
     else if (block_mode)
-        launch_sim_batch_t<false, true>(dev, n, total, st);
+        launch_sim_batch_t<false, true>(dev, gdev, n_groups, total, st);
     else
-        launch_sim_batch_t<false, false>(dev, n, total, st);
+        launch_sim_batch_t<false, false>(dev, gdev, n_groups, total, st);
     return hipGetLastError();
 }
 

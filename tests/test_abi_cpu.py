@@ -275,11 +275,12 @@ def test_batch_calls_validate_every_job_on_the_host(cdt):
     assert "job 1" in _err(cdt)
     jobs[1] = cdt.DriftJob(2, 2, 3, 16, 16, 16, None, None)
     assert L.cdt_drift_score_batch(2, jobs, 16, 1 << 20, None) == cdt.EINVAL
-    # sizes: the table (rounded to 256 B) and the multi-chunk jobs' partials
+    # sizes: the job table and the group table (each rounded to 256 B), then
+    # the multi-chunk jobs' partials
     jobs[0] = cdt.DriftJob(16, 256, 256, 8192, 16, 16, 16, None)
     jobs[1] = cdt.DriftJob(4, 8, 16, 256, 16, 16, 16, None)  # one chunk per block
     nbytes = L.cdt_drift_batch_workspace_bytes(2, jobs)
-    assert nbytes > 4096 * 64 * 16 and nbytes - 4096 * 64 * 16 <= 256
+    assert nbytes == 256 + 256 + 4096 * 64 * 16
     assert L.cdt_drift_score_batch(2, jobs, 16, nbytes - 16, None) == cdt.EINVAL
     empty = (cdt.DriftJob * 1)(cdt.DriftJob(0, 2, 3, 16, None, None, None, None))
     assert L.cdt_drift_score_batch(1, empty, None, 0, None) == cdt.OK

@@ -3,7 +3,9 @@ batched live pass (cdt_canary_sim_batch) and the batched Eq. 4
 (cdt_drift_score_batch) must give every job's output bit for bit as
 cdt_canary_sim / cdt_drift_score give it, over jobs of mixed shapes (one
 and several chunks per block, ragged tails, empty jobs) and parameters;
-one job of each batch is also checked against the oracle.  And the live
+one job of each batch is also checked against the oracle.  Jobs that share
+a reference array (walked chunk-major, the reference read once per chunk
+for the group) are covered with groups of one to three jobs.  And the live
 pass's stream aid (cdt_canary_sim_stream) writes exactly fp16(a)."""
 import numpy as np
 import pytest
@@ -92,6 +94,70 @@ def test_canary_sim_batch_equals_single(gpu, dist, mode):
     kw_o = {key: v for key, v in kw.items() if key not in ("bscale", "tscale")}
     want = oracle.canary_sim(ref, bscale=bs, tscale=ts, **kw_o)
     np.testing.assert_array_equal(h_bits(jobs[1][1]), want)
+
+
+# Jobs over shared references, in the order given: consecutive jobs over one
+# reference array form a group walked chunk-major (the reference read once
+# per chunk for the group); a reference that comes back after another one
+# starts a new group.  Per entry: (reference index, shape index).
+SHARED_ORDER = [(0, 0), (0, 0), (0, 0), (1, 1), (1, 1), (0, 0), (2, 2), (3, 3), (3, 3), (2, 2)]
+SHARED_SHAPES = [(16, 4, 4, 32768), (3, 5, 7, 264), (4, 8, 16, 256), (2, 3, 41, 1000)]
+
+
+def test_drift_score_batch_shared_references(gpu):
+    """Groups of jobs over one reference (several chunks per block, one chunk
+    per block, ragged tails; groups of 1 to 3 jobs, a reference coming back
+    after another) score every job as the single launch does, bit for bit."""
+    torch, cdt = gpu
+    announce("drift_score_batch over shared references")
+    refs = []
+    for k, shape in enumerate(SHARED_SHAPES):
+        refs.append(to_dev(torch, inputs.ref_normal(shape, seed=500 + k, outlier_frac=0.01)))
+    jobs = []
+    for k, (r, si) in enumerate(SHARED_ORDER):
+        S, C, T, H = SHARED_SHAPES[si]
+        a = refs[r].cpu().numpy()
+        h = to_dev(torch, inputs.live_near(a, seed=600 + k, rel=1e-3, flip_frac=0.001))
+        sc = torch.full((C, S), -1.0, dtype=torch.float32, device="cuda")
+        nd = torch.full((C, S, 2), -1.0, dtype=torch.float64, device="cuda")
+        jobs.append((h.view(torch.float16), refs[r], sc, nd))
+    cdt.drift_score_batch(jobs)
+    for k, (hd, ad, sc, nd) in enumerate(jobs):
+        nd1 = torch.empty_like(nd)
+        want = cdt.drift_score(hd, ad, num_den=nd1)
+        torch.cuda.synchronize()
+        assert torch.equal(sc, want), f"job {k}: scores differ"
+        assert torch.equal(nd, nd1), f"job {k}: sums differ"
+
+
+@pytest.mark.parametrize("dist", [0, 1], ids=["gauss", "t3"])
+def test_canary_sim_batch_shared_references(gpu, dist):
+    """The live pass of groups of runs over one reference (different
+    configurations, attackers and tampers per run) equals one launch per
+    run, bit for bit."""
+    torch, cdt = gpu
+    announce(f"canary_sim_batch over shared references dist={dist}")
+    refs, scales = [], []
+    for k, (S, C, T, H) in enumerate(SHARED_SHAPES):
+        ref = oracle.ref_synth(S, C, T, H, 70 + k, 0, oracle.outlier_gain(H, max(1, H // 100),
+                                                                          20.0, 70 + k, 0))
+        q, m = oracle.ref_stats(ref)
+        ts, _ = oracle.block_scales(T, H, q, m, 0.05, 1e-3)
+        refs.append(to_dev(torch, ref))
+        scales.append(to_dev(torch, ts))
+    jobs, singles = [], []
+    for k, (r, si) in enumerate(SHARED_ORDER):
+        S, C, T, H = SHARED_SHAPES[si]
+        kw = dict(seed=77, cfg_id=10 + k, sigma_b=1e-3, benign_dist=dist,
+                  mal_mask=1 << (k % S), tamper=(1, 2, 4, 7)[k % 4], tscale=scales[r],
+                  flip_p=0.05, scale=1.05)
+        h = torch.empty((S, C, T, H), dtype=torch.float16, device="cuda")
+        jobs.append((refs[r], h, kw))
+        singles.append(cdt.canary_sim(refs[r], **kw))
+    cdt.canary_sim_batch(jobs)
+    torch.cuda.synchronize()
+    for k, ((_, h, _), want) in enumerate(zip(jobs, singles)):
+        assert torch.equal(h.view(torch.int16), want.view(torch.int16)), f"job {k} differs"
 
 
 def test_canary_sim_batch_rejects_mixed_noise(gpu):

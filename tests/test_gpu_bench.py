@@ -40,5 +40,12 @@ def test_bench_line_on_tiny():
     assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == bench.HBM_PEAK_GBPS
     assert r["frac"] == pytest.approx(r["achieved"] / r["peak"], abs=1e-4)
     assert r["traffic"] is None  # counters are committed for the 70B workload only
-    assert r["read_stream_GBps"] > 0
+    nr = len(rs.runs)
+    assert r["runs_per_launch"] == nr
+    assert r["bytes_per_launch"] == (rs.elems * (2 * nr + 4)
+                                     + nr * rs.S * rs.C * bench.DRIFT_BYTES_PER_BLOCK)
+    assert r["achieved"] == pytest.approx(
+        r["bytes_per_launch"] / (r["avg_launch_ms"] * 1e-3) / 1e9, rel=1e-2)  # rounded ms
+    pr = res["per_run_launches"]
+    assert pr["read_stream_GBps"] > 0 and pr["ms_per_step"] > 0
     assert res["detection"]["add0.05"] == 1.0

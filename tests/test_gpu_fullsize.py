@@ -1,9 +1,10 @@
 """Full-size parity, every block: the SNR study (40 runs of 16 x 128 x 128 x
 4096), the 216-configuration sweep and the 70B-shaped workload (3 runs of
 16 x 256 x 256 x 8192), run in the launch configuration the benchmark times
-(per run canary_sim then drift_score; for the sweep, per reference set one
-batched live-pass launch and one batched Eq. 4 launch over its 24
-configurations; then one batched AUROC launch), against the
+(the SNR study per run, canary_sim then drift_score; the sweep and the 70B
+runs per reference set, one batched live-pass launch and one batched Eq. 4
+launch over its runs, which share the reference; then one batched AUROC
+launch), against the
 CPU oracle's stored results for every (shard, canary) block of every run
 (tests/golden/fullsize_*.npz, written by tests/golden/make_fullsize.py from
 oracle/ alone; tests/test_golden_fullsize.py re-derives sampled blocks of
@@ -197,7 +198,7 @@ def test_sweep_every_block(gpu):
 
 def test_llama70b_every_block(gpu):
     torch, cdt = gpu
-    out = run_workload(torch, cdt, "llama70b")
+    out = run_workload(torch, cdt, "llama70b", batched=True)
     assert out["configs"] == 3
     assert (out["values"][:, 0] == 1.0).all()  # the detector separates every run fully
     announce(f"llama70b: worst score error {out['worst_rel']:.2e}")
