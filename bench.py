@@ -54,7 +54,7 @@ SIM_BYTES_PER_ELEM = 6        # fp32 a read + fp16 h written
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "drift_score_llama70b_hbm_traffic.md")
-DRIFT_SOURCES = ("drift.hip", "cdt_reduce.hpp", "cdt_device.hpp")
+DRIFT_SOURCES = ("drift.hip", "cdt_reduce.hpp", "cdt_device.hpp", "cdt_launch.hpp")
 VALU_FILE = os.path.join(ROOT, "profiles", "llama70b_valu_busy.md")
 SIM_SOURCES = ("generate.hip", "cdt_sim.hpp", "cdt_launch.hpp", "cdt_device.hpp")
 
