@@ -24,7 +24,9 @@ def test_traffic_is_read_only_for_its_workload_and_sources(tmp_path):
     assert bench.measured_traffic("llama7b") is None
     t = bench.measured_traffic("llama70b")
     if t is not None:  # None once the drift sources change before a new counter pass
-        alg = ELEMS_70B * bench.DRIFT_BYTES_PER_ELEM + 16 * 256 * bench.DRIFT_BYTES_PER_BLOCK
+        # the step's batched launch over the 3 runs sharing the reference:
+        # every run's fp16 activations and the reference once, and the scores
+        alg = ELEMS_70B * (3 * 2 + 4) + 3 * 16 * 256 * bench.DRIFT_BYTES_PER_BLOCK
         assert abs(t / alg - 1.0) < 0.01
     # a summary whose recorded source hash does not match is ignored
     fake = tmp_path / "traffic.md"
