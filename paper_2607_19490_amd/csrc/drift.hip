@@ -190,10 +190,37 @@ __global__ __launch_bounds__(kReduceThreads) void drift_partial_kernel(
                                    partial, direct, S, C, score, sums);
 }
 
+// Eq. 4's element step for kJ arrays against one reference: the reference
+// value is widened once, its square added once to the shared R (it is the
+// same sum for every job), and each job's d = h - a squared into its own D.
+// Each accumulator sees the same values in the same order as accumulate8's.
+template <int kJ>
+__device__ __forceinline__ void accumulate8_jobs(const u32x4 (&hv)[kJ], const f32x4& a0,
+                                                 const f32x4& a1, double (&d_acc)[kJ],
+                                                 double& r_acc) {
+    const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const double a = static_cast<double>(av[2 * k + half]);
+            r_acc = fma(a, a, r_acc);
+#pragma unroll
+            for (int j = 0; j < kJ; ++j) {
+                const uint32_t w = (k == 0 ? hv[j].x : k == 1 ? hv[j].y : k == 2 ? hv[j].z : hv[j].w);
+                const double h = static_cast<double>(half_bits_to_float(half ? w >> 16 : w & 0xFFFFu));
+                const double d = h - a;
+                d_acc[j] = fma(d, d, d_acc[j]);
+            }
+        }
+    }
+}
+
 // One chunk of kJ arrays scored against one shared reference (Eq. 4): each
 // step's reference groups are loaded once (nontemporally, as in
 // drift_chunk) and every job's activations of the step are loaded at once
-// and accumulated against them.  The step is kMultiUnroll groups per thread
+// and accumulated against them; the reference's own sum R is formed once
+// for all of them.  The step is kMultiUnroll groups per thread
 // (not drift_chunk's kReduceUnroll, so that every job's loads fit in
 // registers together); a thread still visits its groups g0 + tid + 256 m in
 // the order m = 0, 1, 2, ... and adds the same values in the same order as
@@ -214,9 +241,9 @@ __device__ __forceinline__ void drift_chunk_jobs(const DriftJobDev* __restrict__
 #pragma unroll
     for (int j = 0; j < kJ; ++j) hb[j] = global_ptr(reinterpret_cast<const u32x4*>(jobs[j].h + b * n));
     const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
-    double acc[kJ][2];
+    double d_acc[kJ], r_acc = 0.0;
 #pragma unroll
-    for (int j = 0; j < kJ; ++j) acc[j][0] = acc[j][1] = 0.0;
+    for (int j = 0; j < kJ; ++j) d_acc[j] = 0.0;
     for (uint32_t base = g0; base < g_end; base += kReduceThreads * kU) {
         f32x4 a0[kU], a1[kU];
         u32x4 hv[kJ][kU];
@@ -256,27 +283,28 @@ __device__ __forceinline__ void drift_chunk_jobs(const DriftJobDev* __restrict__
             }
         }
 #pragma unroll
-        for (int j = 0; j < kJ; ++j) {
+        for (int u = 0; u < kU; ++u) {
+            u32x4 hu[kJ];
 #pragma unroll
-            for (int u = 0; u < kU; ++u)
-                accumulate8<DriftMetric::kL2>(hv[j][u], zero, a0[u], a1[u], acc[j]);
-            // an empty register constraint: the compiler must assume the
-            // reference changed, so it widens it to fp64 again per job
-            // instead of keeping the widened copies of every job alive
-#pragma unroll
-            for (int u = 0; u < kU; ++u) asm volatile("" : "+v"(a0[u]), "+v"(a1[u]));
+            for (int j = 0; j < kJ; ++j) hu[j] = hv[j][u];
+            accumulate8_jobs<kJ>(hu, a0[u], a1[u], d_acc, r_acc);
         }
     }
+    double sums[kJ + 1];
 #pragma unroll
-    for (int j = 0; j < kJ; ++j) {
-        block_sum<2>(acc[j]);
-        if (threadIdx.x == 0) {
+    for (int j = 0; j < kJ; ++j) sums[j] = d_acc[j];
+    sums[kJ] = r_acc;
+    block_sum<kJ + 1>(sums);
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
             const DriftJobDev& J = jobs[j];
+            const double acc[2] = {sums[j], sums[kJ]};
             if (J.direct) {
-                finish_block<DriftMetric::kL2>(acc[j], chunk, J.S, J.C, J.score, J.sums);
+                finish_block<DriftMetric::kL2>(acc, chunk, J.S, J.C, J.score, J.sums);
             } else {
-                J.partial[chunk * 2] = acc[j][0];
-                J.partial[chunk * 2 + 1] = acc[j][1];
+                J.partial[chunk * 2] = acc[0];
+                J.partial[chunk * 2 + 1] = acc[1];
             }
         }
     }
