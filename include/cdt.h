@@ -195,8 +195,8 @@ int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim
  * the configurations of a reference set together): job j writes its own h
  * from its ref with its own parameters, bitwise as cdt_canary_sim would.
  * The chunks of all jobs form one grid, so short runs share the launch's
- * ramp-up and tail.  Consecutive jobs that read the same ref array (and
- * have the same chunk count) are generated together, so that each
+ * ramp-up and tail.  Consecutive jobs that read the same ref array in the
+ * same shape are generated together, so that each
  * reference chunk is read from HBM about once for all of them: with fewer
  * than 8 such jobs their work is walked chunk by chunk, the jobs of a chunk
  * one after another (re-reads from L2); with 8 or more, each XCD takes its
@@ -303,8 +303,8 @@ int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, cons
  * its score[C][S] (num_den optional), bitwise as cdt_drift_score would.  The
  * chunks of all jobs form one grid, so short arrays share the launch's
  * ramp-up and tail instead of paying one each, and one combine launch
- * finishes every block.  Consecutive jobs that read the same ref array (and
- * have the same chunk count) share its reads: one workgroup scores a chunk
+ * finishes every block.  Consecutive jobs that read the same ref array in
+ * the same shape share its reads: one workgroup scores a chunk
  * of up to 4 of them, reading the reference chunk once, so a group of up to
  * 4 jobs moves 2k + 4 bytes per element instead of 6k (larger groups read
  * the chunk once per 4 jobs, the repeats mostly from L2).  Order the jobs so

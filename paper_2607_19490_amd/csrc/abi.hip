@@ -511,18 +511,17 @@ int plan_drift_batch(const char* fn, uint32_t n_jobs, const cdt_drift_job* jobs,
         plan->total_blocks += nb;
         plan->table.push_back(d);
     }
-    // jobs in a row over one reference array, with equal chunk counts, share
-    // its chunks (BatchGroupDev)
+    // jobs in a row over one reference array in one layout share its chunks
+    // (BatchGroupDev)
     const uint32_t nt = static_cast<uint32_t>(plan->table.size());
-    std::vector<const void*> refs(nt);
-    std::vector<uint64_t> chunks(nt);
+    std::vector<cdt::BatchKey> keys(nt);
     for (uint32_t j = 0; j < nt; ++j) {
-        refs[j] = plan->table[j].ref;
-        chunks[j] = plan->table[j].cpb * plan->table[j].S * plan->table[j].C;
+        const cdt::DriftJobDev& d = plan->table[j];
+        keys[j] = cdt::BatchKey{d.ref, d.cpb * d.S * d.C, d.S, d.C, d.n8};
     }
     plan->groups.resize(nt);
     uint32_t ng = 0;
-    plan->total_iters = cdt::plan_batch_groups(nt, refs.data(), chunks.data(),
+    plan->total_iters = cdt::plan_batch_groups(nt, keys.data(),
                                                cdt::kDriftJobsPerIter, cdt::kDriftJobMajorFrom,
                                                plan->groups.data(), &ng);
     plan->groups.resize(ng);

@@ -65,7 +65,7 @@ hipError_t launch_block_scales(uint64_t nblocks, uint32_t T, uint32_t H, const d
 hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, hipStream_t st);
 
 // A run of consecutive jobs of a batched launch that read one reference
-// array, and the order its iterations take.  An iteration is one chunk of
+// array in one layout, and the order its iterations take.  An iteration is one chunk of
 // up to `jobs_per_iter` of the group's jobs (a unit); each XCD takes one
 // contiguous eighth of the group's iterations, and
 //   * chunk-major: on each chunk, the group's units one after another, so
@@ -125,29 +125,39 @@ __device__ __forceinline__ bool batch_iter(const BatchGroupDev* __restrict__ gro
     return true;
 }
 
+// What decides whether two jobs of a batch can share their reference reads:
+// the same reference array in the same layout (blocks, elements per block,
+// chunks), so that a chunk index means the same elements for both.
+struct BatchKey {
+    const void* ref;
+    uint64_t chunks;
+    uint32_t S, C, n8;
+    bool operator==(const BatchKey& o) const {
+        return ref == o.ref && chunks == o.chunks && S == o.S && C == o.C && n8 == o.n8;
+    }
+};
+
 // Host side: the groups of a batch whose job j (jobs without chunks left
-// out by the caller) reads reference refs[j] and has chunks[j] chunks;
-// consecutive jobs with the same reference and chunk count form a group
-// (every group's chunk index is then in range for each of its jobs).  A
-// group is walked chunk-major when it has fewer than `job_major_from`
-// units.  Fills groups[0 .. *n_groups) and returns the padded iteration
-// count.
-inline uint64_t plan_batch_groups(uint32_t n_jobs, const void* const* refs,
-                                  const uint64_t* chunks, uint32_t jobs_per_iter,
+// out by the caller) has key keys[j]; consecutive jobs with equal keys form
+// a group (the kernels may then read one job's reference layout for all of
+// them).  A group is walked chunk-major when it has fewer than
+// `job_major_from` units.  Fills groups[0 .. *n_groups) and returns the
+// padded iteration count.
+inline uint64_t plan_batch_groups(uint32_t n_jobs, const BatchKey* keys, uint32_t jobs_per_iter,
                                   uint32_t job_major_from, BatchGroupDev* groups,
                                   uint32_t* n_groups) {
     *n_groups = 0;
     for (uint32_t j = 0; j < n_jobs; ++j) {
         if (*n_groups) {
             BatchGroupDev& last = groups[*n_groups - 1];
-            if (refs[last.first_job] == refs[j] && last.chunks == chunks[j]) {
+            if (keys[last.first_job] == keys[j]) {
                 ++last.n_jobs;
                 continue;
             }
         }
         BatchGroupDev g;
         g.iter_begin = 0;
-        g.chunks = chunks[j];
+        g.chunks = keys[j].chunks;
         g.first_job = j;
         g.n_jobs = 1;
         g.chunk_major = 1;

@@ -357,8 +357,7 @@ hipError_t launch_canary_sim_batch(uint32_t n_jobs, const SimLaunch* runs,
                                    const float* const* refs, uint16_t* const* hs, void* table,
                                    hipStream_t st) {
     std::vector<SimJobDev> jobs;
-    std::vector<const void*> job_refs;
-    std::vector<uint64_t> job_chunks;
+    std::vector<BatchKey> keys;
     jobs.reserve(n_jobs);
     bool t3 = false, block_mode = false;
     for (uint32_t j = 0; j < n_jobs; ++j) {
@@ -375,8 +374,7 @@ hipError_t launch_canary_sim_batch(uint32_t n_jobs, const SimLaunch* runs,
         d.ref = refs[j];
         d.h = hs[j];
         jobs.push_back(d);
-        job_refs.push_back(refs[j]);
-        job_chunks.push_back(cpb * nblocks);
+        keys.push_back(BatchKey{refs[j], cpb * nblocks, p.S, p.C, static_cast<uint32_t>(n8)});
     }
     if (jobs.empty()) return hipSuccess;
     const uint32_t n = static_cast<uint32_t>(jobs.size());
@@ -384,9 +382,8 @@ hipError_t launch_canary_sim_batch(uint32_t n_jobs, const SimLaunch* runs,
     std::vector<char> staged(goff + n * sizeof(BatchGroupDev), 0);
     BatchGroupDev* groups = reinterpret_cast<BatchGroupDev*>(staged.data() + goff);
     uint32_t n_groups = 0;
-    const uint64_t total = plan_batch_groups(n, job_refs.data(), job_chunks.data(),
-                                             kSimJobsPerIter, kSimJobMajorFrom, groups,
-                                             &n_groups);
+    const uint64_t total = plan_batch_groups(n, keys.data(), kSimJobsPerIter, kSimJobMajorFrom,
+                                             groups, &n_groups);
     memcpy(staged.data(), jobs.data(), n * sizeof(SimJobDev));
     const size_t bytes = goff + n_groups * sizeof(BatchGroupDev);
     hipError_t e = hipMemcpyAsync(table, staged.data(), bytes, hipMemcpyHostToDevice, st);

@@ -130,6 +130,41 @@ def test_drift_score_batch_shared_references(gpu):
         assert torch.equal(nd, nd1), f"job {k}: sums differ"
 
 
+def test_batches_share_only_identical_layouts(gpu):
+    """Jobs that pass one reference array in different shapes with the same
+    chunk count (and even different element counts) must not share its
+    reads: each is scored, and generated, in its own layout."""
+    torch, cdt = gpu
+    announce("batches over one reference array in different shapes")
+    pairs = [((1, 2, 4, 16384), (2, 2, 2, 16384)),   # 4 chunks each, same size
+             ((1, 1, 5, 8192), (2, 1, 1, 8192))]      # 2 chunks each, sizes differ
+    for sa, sb in pairs:
+        na = int(np.prod(sa))
+        flat = to_dev(torch, inputs.ref_normal((na,), seed=900 + na, outlier_frac=0.01))
+        ra = flat.view(*sa)
+        rb = flat[:int(np.prod(sb))].view(*sb)
+        jobs = []
+        for k, (shape, ref) in enumerate(((sa, ra), (sb, rb))):
+            S, C, T, H = shape
+            h = to_dev(torch, inputs.live_near(ref.cpu().numpy(), seed=910 + k, rel=1e-3))
+            sc = torch.full((C, S), -1.0, dtype=torch.float32, device="cuda")
+            jobs.append((h.view(torch.float16), ref, sc, None))
+        cdt.drift_score_batch(jobs)
+        for hd, ad, sc, _ in jobs:
+            want = cdt.drift_score(hd, ad)
+            torch.cuda.synchronize()
+            assert torch.equal(sc, want), (sa, sb)
+        sims = []
+        for k, (shape, ref) in enumerate(((sa, ra), (sb, rb))):
+            kw = dict(seed=5, cfg_id=20 + k, sigma_b=1e-3)
+            sims.append((ref, torch.empty(shape, dtype=torch.float16, device="cuda"), kw))
+        cdt.canary_sim_batch(sims)
+        for ref, h, kw in sims:
+            want = cdt.canary_sim(ref, **kw)
+            torch.cuda.synchronize()
+            assert torch.equal(h.view(torch.int16), want.view(torch.int16)), (sa, sb)
+
+
 @pytest.mark.parametrize("dist", [0, 1], ids=["gauss", "t3"])
 def test_canary_sim_batch_shared_references(gpu, dist):
     """The live pass of groups of runs over one reference (different
