@@ -48,6 +48,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+# vector-ALU issue peak: one wave instruction per CU per cycle, 256 CUs at
+# the 2.4 GHz peak engine clock (giga wave-instructions per second)
+VALU_PEAK_GIPS = 256 * 2.4
 DRIFT_BYTES_PER_ELEM = 6      # fp16 h + fp32 a, each read once
 DRIFT_BYTES_PER_BLOCK = 4     # one fp32 score written
 SIM_BYTES_PER_ELEM = 6        # fp32 a read + fp16 h written
@@ -92,13 +95,15 @@ def measured_traffic(workload):
     return None if f is None else int(f["drift_score_traffic_bytes_per_launch"])
 
 
-def measured_valu(workload):
-    """canary_sim's VALUBusy share and VALU instructions per element from the
-    committed rocprofv3 counter pass, or (None, None) as above."""
+def measured_valu(workload, batch=False):
+    """canary_sim's VALUBusy share and VALU instructions per element (and run)
+    from the committed rocprofv3 counter pass, single-run or batched launch,
+    or (None, None) as above."""
     f = _profile_fields(VALU_FILE, "canary_sim_", SIM_SOURCES, workload)
     if f is None:
         return None, None
-    return float(f["canary_sim_valu_busy"]), float(f["canary_sim_valu_per_element"])
+    key = "canary_sim_batch_" if batch else "canary_sim_"
+    return float(f[key + "valu_busy"]), float(f[key + "valu_per_element"])
 
 
 def parse():
@@ -301,6 +306,16 @@ def run_main(torch, cdt, W, args):
     sim_bytes = big.rs.elems * (2 * nr + 4)
     sim_gbps = sim_bytes / (sim_avg * 1e-3) / 1e9
     valu_busy, valu_per_el = measured_valu(wl.name)
+    # the batched live pass against the vector-ALU issue peak: one wave
+    # instruction per CU per cycle, 256 CUs at 2.4 GHz, with the committed
+    # counter pass's instruction count per element and run
+    b_busy, b_per_el = measured_valu(wl.name, batch=True)
+    alu = None
+    if b_per_el is not None:
+        instr_rate = nr * big.rs.elems * b_per_el / 64 / (sim_avg * 1e-3) / 1e9
+        alu = {"bound": "alu", "achieved": round(instr_rate, 1), "peak": VALU_PEAK_GIPS,
+               "unit": "G wave-instructions/s", "frac": round(instr_rate / VALU_PEAK_GIPS, 4),
+               "instr_per_element": b_per_el, "valu_busy": b_busy}
 
     # The same step with one launch per run (each run reading the reference
     # itself): the per-run rates, and the memory bounds of those launches'
@@ -364,7 +379,8 @@ def run_main(torch, cdt, W, args):
             "GBps": round(sim_gbps, 1),
             "frac_of_hbm_peak": round(sim_gbps / HBM_PEAK_GBPS, 4),
             "share_of_step": round(sim_avg / ms_step, 4) if nset == 1 else None,
-            "bound": "valu+hbm",
+            "bound": "alu",
+            "alu_roofline": alu,
         },
         "per_run_launches": {
             "ms_per_step": round(per_run_ms, 4),
