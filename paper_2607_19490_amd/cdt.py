@@ -304,7 +304,8 @@ def sim_batch(jobs):
     """Prepare a batched live pass.  jobs: list of (ref [S][C][T][H] fp32,
     h [S][C][T][H] fp16 output, keywords as sim_params including bscale /
     tscale tensors).  Every job must use the same benign noise distribution
-    and mode, carry 0 (checked by the library when launched)."""
+    and mode, carry 0 (checked by the library when launched).  Jobs in a row
+    over one reference tensor share its reads (cdt_canary_sim_batch)."""
     torch = _torch()
     n = len(jobs)
     arr = (SimJob * max(1, n))()
@@ -334,7 +335,8 @@ def canary_sim_batch(jobs):
 
 def drift_batch(jobs):
     """Prepare a batched Eq. 4.  jobs: list of (h fp16, ref fp32, score out
-    [C][S] fp32, num_den out [C][S][2] fp64 or None)."""
+    [C][S] fp32, num_den out [C][S][2] fp64 or None).  Jobs in a row over
+    one reference tensor share its reads (cdt_drift_score_batch)."""
     torch = _torch()
     n = len(jobs)
     arr = (DriftJob * max(1, n))()
