@@ -97,16 +97,19 @@ def test_canary_sim_batch_equals_single(gpu, dist, mode):
 
 
 # Jobs over shared references, in the order given: consecutive jobs over one
-# reference array form a group walked chunk-major (the reference read once
-# per chunk for the group); a reference that comes back after another one
-# starts a new group.  Per entry: (reference index, shape index).
-SHARED_ORDER = [(0, 0), (0, 0), (0, 0), (1, 1), (1, 1), (0, 0), (2, 2), (3, 3), (3, 3), (2, 2)]
+# reference array form a group (Eq. 4: units of up to 4 jobs per reference
+# read; the live pass: chunk-major below 8 jobs, job-major from 8 on); a
+# reference that comes back after another one starts a new group.  Per
+# entry: (reference index, shape index).  Groups of 1, 2, 3, 6 (4 + 2) and
+# 9 jobs, ragged shapes among them.
+SHARED_ORDER = ([(0, 0), (0, 0), (0, 0), (1, 1), (1, 1), (0, 0), (2, 2), (3, 3), (3, 3), (2, 2)]
+                + [(1, 1)] * 6 + [(3, 3)] * 9)
 SHARED_SHAPES = [(16, 4, 4, 32768), (3, 5, 7, 264), (4, 8, 16, 256), (2, 3, 41, 1000)]
 
 
 def test_drift_score_batch_shared_references(gpu):
     """Groups of jobs over one reference (several chunks per block, one chunk
-    per block, ragged tails; groups of 1 to 3 jobs, a reference coming back
+    per block, ragged tails; groups of 1 to 9 jobs, a reference coming back
     after another) score every job as the single launch does, bit for bit."""
     torch, cdt = gpu
     announce("drift_score_batch over shared references")
