@@ -418,8 +418,9 @@ int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, ui
  * cdt_auroc_upload validates the HOST table cfgs exactly as cdt_auroc does,
  * against n_scores scores and the flags the launches will use, and copies
  * it into the device buffer `table` (cdt_auroc_workspace_bytes(n_cfg)
- * bytes, 16-byte aligned) on `stream`.  cfgs may be reused as soon as the
- * call returns.
+ * bytes, 16-byte aligned) on `stream`.  The table is copied into library
+ * host memory before it is checked, so cfgs (pinned or not) may be reused
+ * as soon as the call returns.
  *
  * cdt_auroc_launch scores `scores` against an uploaded table: it only
  * launches kernels (no copies, no host reads of device memory), so a stream

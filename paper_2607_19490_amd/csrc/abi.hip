@@ -568,7 +568,8 @@ int cdt_drift_score_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws, 
                     ws ? ws_bytes : 0);
     if (!aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
     // partial offsets -> addresses behind the tables in ws; the two tables
-    // go up in one copy (staged contiguously on the host)
+    // go up in one copy, staged contiguously in pageable host memory (such a
+    // copy completes before hipMemcpyAsync returns, so `staged` may go)
     char* base = static_cast<char*>(ws);
     double* partials = reinterpret_cast<double*>(base + batch_partials_offset(plan));
     for (cdt::DriftJobDev& d : plan.table)
@@ -674,17 +675,32 @@ int check_auroc_outputs(const char* fn, uint32_t flags, uint64_t* counts, uint64
     return CDT_OK;
 }
 
-// Copy a validated table into the device buffer `table` on `st`.
-int upload_table(const char* fn, uint32_t n_cfg, const cdt_auroc_cfg* cfgs, void* table,
+// Copy a validated table (held in library-owned pageable memory, see
+// validated_table) into the device buffer `table` on `st`.  A copy from
+// pageable host memory completes before hipMemcpyAsync returns, so the host
+// table may be released afterwards.
+int upload_table(const char* fn, const std::vector<cdt_auroc_cfg>& cfgs, void* table,
                  size_t table_bytes, hipStream_t st) {
-    const size_t need = cdt_auroc_workspace_bytes(n_cfg);
+    const size_t need = cdt_auroc_workspace_bytes(static_cast<uint32_t>(cfgs.size()));
     if (!table || table_bytes < need)
         return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
                     table ? table_bytes : 0);
     if (!aligned16(table)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
-    const hipError_t e = hipMemcpyAsync(table, cfgs, need, hipMemcpyHostToDevice, st);
+    const hipError_t e = hipMemcpyAsync(table, cfgs.data(), need, hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return device_status(e, fn);
     return CDT_OK;
+}
+
+// The caller's table copied once into library memory and validated there:
+// what is checked is what is uploaded, even if the caller's memory changes
+// meanwhile, and the caller may reuse it (pinned or not) once the call
+// returns.
+int validated_table(const char* fn, uint32_t n_cfg, const cdt_auroc_cfg* cfgs,
+                    uint64_t n_scores, uint32_t flags, std::vector<cdt_auroc_cfg>* out) {
+    if (!cfgs) return fail(CDT_EINVAL, "%s: NULL cfgs", fn);
+    if (n_cfg > (1u << 24)) return fail(CDT_ELIMIT, "%s: n_cfg above 2^24", fn);
+    out->assign(cfgs, cfgs + n_cfg);
+    return check_auroc_table(fn, n_cfg, out->data(), n_scores, flags);
 }
 
 }  // namespace
@@ -697,15 +713,16 @@ int cdt_auroc(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores, ui
     if (n_cfg == 0) return ok();
     int rc = check_auroc_outputs("cdt_auroc", flags, counts, pooled, baseline);
     if (rc) return rc;
-    rc = check_auroc_table("cdt_auroc", n_cfg, cfgs, n_scores, flags);
+    std::vector<cdt_auroc_cfg> table;
+    rc = validated_table("cdt_auroc", n_cfg, cfgs, n_scores, flags, &table);
     if (rc) return rc;
     if (!scores) {
-        for (uint32_t g = 0; g < n_cfg; ++g)
-            if (static_cast<uint64_t>(cfgs[g].S) * cfgs[g].C > 0)
+        for (const cdt_auroc_cfg& c : table)
+            if (static_cast<uint64_t>(c.S) * c.C > 0)
                 return fail(CDT_EINVAL, "cdt_auroc: scores is NULL");
     }
     hipStream_t st = static_cast<hipStream_t>(stream);
-    rc = upload_table("cdt_auroc", n_cfg, cfgs, ws, ws_bytes, st);
+    rc = upload_table("cdt_auroc", table, ws, ws_bytes, st);
     if (rc) return rc;
     return device_status(cdt::launch_auroc(n_cfg, static_cast<const cdt::AurocCfgDev*>(ws),
                                            scores, n_scores, seed, flags, counts, pooled,
@@ -717,9 +734,10 @@ int cdt_auroc_upload(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, uint64_t n_score
                      uint32_t flags, void* table, size_t table_bytes, void* stream) {
     if (flags & ~15u) return fail(CDT_EINVAL, "cdt_auroc_upload: bad flags");
     if (n_cfg == 0) return ok();
-    int rc = check_auroc_table("cdt_auroc_upload", n_cfg, cfgs, n_scores, flags);
+    std::vector<cdt_auroc_cfg> staged;
+    int rc = validated_table("cdt_auroc_upload", n_cfg, cfgs, n_scores, flags, &staged);
     if (rc) return rc;
-    rc = upload_table("cdt_auroc_upload", n_cfg, cfgs, table, table_bytes,
+    rc = upload_table("cdt_auroc_upload", staged, table, table_bytes,
                       static_cast<hipStream_t>(stream));
     if (rc) return rc;
     return ok();

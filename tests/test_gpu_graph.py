@@ -48,6 +48,49 @@ def test_upload_launch_equals_auroc(gpu):
         np.testing.assert_array_equal(cdt.u64(got[1])[k], p_o)
 
 
+def test_upload_from_pinned_memory_is_reusable_at_return(gpu):
+    """The table is taken from the caller during the call, also when it sits
+    in pinned host memory (where a device copy could still be reading it
+    after the call): overwriting it right after cdt_auroc_upload and
+    cdt_auroc return, before the stream has run, changes nothing."""
+    import ctypes
+    torch, cdt = gpu
+    announce("auroc upload from pinned host memory")
+    tables, cfgs = _auroc_batch()
+    flat = to_dev(torch, np.concatenate([t.ravel() for t in tables]).astype(np.float32))
+    want = cdt.auroc(cfgs, flat, seed=7, flags=ALL)
+    arr, n = cdt.auroc_cfg_array(cfgs)
+    nbytes = ctypes.sizeof(arr)
+    pinned = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    ctypes.memmove(pinned.data_ptr(), ctypes.addressof(arr), nbytes)
+    cfg_ptr = ctypes.cast(pinned.data_ptr(), ctypes.POINTER(cdt.AurocCfg))
+    L, stream = cdt.lib(), torch.cuda.current_stream().cuda_stream
+    # keep the stream busy so that an asynchronous read of `pinned` would
+    # still be pending when it is overwritten
+    busy = torch.empty(1 << 26, dtype=torch.float32, device="cuda")
+    busy.uniform_()
+    for _ in range(4):
+        busy.mul_(1.0001)
+    table = torch.empty(max(16, L.cdt_auroc_workspace_bytes(n)), dtype=torch.uint8, device="cuda")
+    assert L.cdt_auroc_upload(n, cfg_ptr, flat.numel(), ALL, table.data_ptr(), table.numel(),
+                              stream) == 0
+    pinned.fill_(0xFF)  # S = C = 2^32 - 1 everywhere: never a valid table
+    got = cdt.auroc_launch(table, n, flat, seed=7, flags=ALL)
+    ctypes.memmove(pinned.data_ptr(), ctypes.addressof(arr), nbytes)
+    ws = torch.empty(max(16, L.cdt_auroc_workspace_bytes(n)), dtype=torch.uint8, device="cuda")
+    counts = torch.empty((n, 6), dtype=torch.int64, device="cuda")
+    pooled = torch.empty((n, 3), dtype=torch.int64, device="cuda")
+    base = torch.empty((n, 3), dtype=torch.int64, device="cuda")
+    assert L.cdt_auroc(n, cfg_ptr, flat.data_ptr(), flat.numel(), 7, ALL, counts.data_ptr(),
+                       pooled.data_ptr(), base.data_ptr(), ws.data_ptr(), ws.numel(),
+                       stream) == 0
+    pinned.fill_(0xFF)
+    torch.cuda.synchronize()
+    for w, g, d in zip(want, got, (counts, pooled, base)):
+        np.testing.assert_array_equal(cdt.u64(g), cdt.u64(w))
+        np.testing.assert_array_equal(cdt.u64(d), cdt.u64(w))
+
+
 def test_launch_bounds_checks(gpu):
     """A table uploaded for N scores, launched with a score array that claims
     fewer: configurations past the claim get all-ones counts; the others are
