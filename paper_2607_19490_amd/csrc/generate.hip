@@ -386,7 +386,6 @@ hipError_t launch_canary_sim_batch(uint32_t n_jobs, const SimLaunch* runs,
                                              groups, &n_groups);
     memcpy(staged.data(), jobs.data(), n * sizeof(SimJobDev));
     const size_t bytes = goff + n_groups * sizeof(BatchGroupDev);
-    // from pageable host memory: the copy completes before the call returns
     hipError_t e = hipMemcpyAsync(table, staged.data(), bytes, hipMemcpyHostToDevice, st);
     if (e != hipSuccess) return e;
     const SimJobDev* dev = static_cast<const SimJobDev*>(table);
