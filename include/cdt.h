@@ -292,7 +292,9 @@ int cdt_drift_score(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16
  * All calls on one GPU share its array: calls that can overlap there (on
  * different streams, or from several threads without ordering) race and
  * must be serialised by the caller.  The first call on a device looks up
- * the array's device address (with that device current). */
+ * the array's device address (with that device current).  `stream` must
+ * belong to the current device (CDT_EINVAL otherwise): the array used is
+ * the current device's. */
 #define CDT_NOALLOC_SCRATCH_BYTES 8388608u
 int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const uint16_t* h,
                             const float* ref, float* score, double* num_den, void* stream);

@@ -403,14 +403,24 @@ std::mutex g_scratch_mu;
 void* g_scratch_ptr[kMaxScratchDevices] = {};
 
 // Device address of the current device's `scratch` (looked up on its first
-// use on that device).
-int scratch_of_current_device(const char* fn, void** out) {
+// use on that device).  The kernels run on `stream`'s device, so a stream of
+// another device is refused: its kernels would reach into this device's
+// array.
+int scratch_of_current_device(const char* fn, hipStream_t stream, void** out) {
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return device_status(e, fn);
     if (dev < 0 || dev >= kMaxScratchDevices)
         return fail(CDT_ELIMIT, "%s: device %d beyond the %d the library serves", fn, dev,
                     kMaxScratchDevices);
+    if (stream != nullptr && stream != hipStreamLegacy && stream != hipStreamPerThread) {
+        hipDevice_t sdev = -1;
+        e = hipStreamGetDevice(stream, &sdev);
+        if (e != hipSuccess) return device_status(e, fn);
+        if (sdev != dev)
+            return fail(CDT_EINVAL, "%s: stream of device %d while device %d is current", fn,
+                        static_cast<int>(sdev), dev);
+    }
     std::lock_guard<std::mutex> lock(g_scratch_mu);
     if (!g_scratch_ptr[dev]) {
         void* p = nullptr;
@@ -449,7 +459,7 @@ int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, cons
             return fail(CDT_EALIGN, "%s: arrays must be 16-byte aligned", fn);
     }
     void* ws = nullptr;
-    rc = scratch_of_current_device(fn, &ws);
+    rc = scratch_of_current_device(fn, static_cast<hipStream_t>(stream), &ws);
     if (rc) return rc;
     return device_status(cdt::launch_drift(cdt::DriftMetric::kL2, S, C, T, H, h, ref, score,
                                            num_den, ws, static_cast<hipStream_t>(stream)),

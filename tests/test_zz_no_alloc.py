@@ -6,7 +6,9 @@ Calls run back to back on one GPU: a large multi-chunk shape, then a
 smaller ragged one that reuses the library's scratch (its partial sums
 must not leak from the first call), then a shape whose blocks are single
 chunks (scored directly).  Scores and fp64 sums must equal the workspace
-entry point's bit for bit, and the oracle's within 1e-5 relative.
+entry point's bit for bit, and the oracle's within 1e-5 relative.  A
+stream capture of the call replays exactly, with other calls using the
+scratch between replays.
 """
 import numpy as np
 import pytest
@@ -69,3 +71,52 @@ def test_noalloc_rejects_shapes_beyond_its_scratch():
     want = cdt.drift_score(hd, ad)
     torch.cuda.synchronize()
     assert torch.equal(out, want)
+
+
+def test_noalloc_under_graph_capture():
+    """The caller it exists for: a stream capture records the no-allocation
+    call (kernel launches only), and each replay scores the inputs copied in
+    before it, equal to cdt_drift_score's eager result, also after an eager
+    call of another shape has overwritten the library's scratch in between."""
+    torch, cdt = require_gpu()
+    S, C, T, H = 4, 6, 64, 1024  # two chunks per block: the scratch is used
+    announce(f"drift_score_noalloc under graph capture {(S, C, T, H)}")
+    cases = []
+    for k in range(3):
+        a = inputs.ref_normal((S, C, T, H), seed=100 + k, outlier_frac=0.01)
+        h = inputs.live_near(a, seed=110 + k, rel=1e-3 * (k + 1), flip_frac=0.001)
+        cases.append((to_dev(torch, a), to_dev(torch, h).view(torch.float16)))
+    ad = torch.empty_like(cases[0][0])
+    hd = torch.empty_like(cases[0][1])
+    out = torch.empty((C, S), dtype=torch.float32, device="cuda")
+    want = [cdt.drift_score(h_, a_) for a_, h_ in cases]
+    # another shape's eager call between replays reuses the scratch
+    a2 = inputs.ref_normal((3, 5, 41, 1000), seed=120)
+    ad2 = to_dev(torch, a2)
+    hd2 = to_dev(torch, inputs.live_near(a2, seed=121, rel=1e-2)).view(torch.float16)
+    out2 = torch.empty((5, 3), dtype=torch.float32, device="cuda")
+    want2 = cdt.drift_score(hd2, ad2)
+    torch.cuda.synchronize()
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up on the capture stream
+        cdt.drift_score_noalloc(hd, ad, out=out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cdt.drift_score_noalloc(hd, ad, out=out)
+    torch.cuda.synchronize()
+    for rep in range(2):
+        for k, (a_, h_) in enumerate(cases):
+            ad.copy_(a_)
+            hd.copy_(h_)
+            out.fill_(-1.0)
+            cdt.drift_score_noalloc(hd2, ad2, out=out2)
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(out, want[k]), (rep, k)
+            assert torch.equal(out2, want2), (rep, k)
+    del graph
