@@ -307,9 +307,9 @@ int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, cons
  * ramp-up and tail instead of paying one each, and one combine launch
  * finishes every block.  Consecutive jobs that read the same ref array in
  * the same shape share its reads: one workgroup scores a chunk
- * of up to 4 of them, reading the reference chunk once, so a group of up to
- * 4 jobs moves 2k + 4 bytes per element instead of 6k (larger groups read
- * the chunk once per 4 jobs, the repeats mostly from L2).  Order the jobs so
+ * of up to 8 of them, reading the reference chunk once, so a group of up to
+ * 8 jobs moves 2k + 4 bytes per element instead of 6k (larger groups read
+ * the chunk once per 8 jobs, the repeats mostly from L2).  Order the jobs so
  * that arrays scored against one reference are adjacent.  jobs: HOST array,
  * validated and copied into ws during the call (reusable when the call
  * returns); jobs with S*C = 0 are skipped.  At most 65536 jobs.

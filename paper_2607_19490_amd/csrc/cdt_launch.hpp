@@ -24,7 +24,7 @@ constexpr int kGenThreads = 1024;
 // from which a group is walked job-major, for the live pass and Eq. 4.
 constexpr uint32_t kSimJobsPerIter = 1;
 constexpr uint32_t kSimJobMajorFrom = 8;
-constexpr uint32_t kDriftJobsPerIter = 4;
+constexpr uint32_t kDriftJobsPerIter = 8;
 constexpr uint32_t kDriftJobMajorFrom = 0xFFFFFFFFu;
 constexpr int kGenItems = 8;
 constexpr uint32_t kGenChunkGroups = kGenThreads * kGenItems;
@@ -76,8 +76,10 @@ hipError_t launch_canary_sim(const SimLaunch& p, const float* ref, uint16_t* h, 
 //     units the 8 XCDs generate 8 different jobs over the same reference
 //     offsets at the same time and the last-level cache serves most of the
 //     re-reads.
-// Eq. 4 scores up to 4 jobs per iteration, chunk-major, reading each
-// reference chunk once for them.  The live pass generates one job per
+// Eq. 4 scores up to 8 jobs per iteration, chunk-major, reading each
+// reference chunk once for them (the sweep's 24-run groups: 13.3-13.8 ms of
+// Eq. 4 per sweep in units of up to 8, 13.8-14.3 ms in units of up to 4,
+// whose later units re-read each chunk, some of it from HBM).  The live pass generates one job per
 // iteration (its work is the random numbers, not the reads), job-major from
 // 8 jobs on: for the sweep's 24-run groups that beats chunk-major (33.5 ms
 // against 39.4-45.8 ms over the sweep), whose reuse in L2 does not make up

@@ -225,6 +225,8 @@ __device__ __forceinline__ void accumulate8_jobs(const u32x4 (&hv)[kJ], const f3
 // registers together); a thread still visits its groups g0 + tid + 256 m in
 // the order m = 0, 1, 2, ... and adds the same values in the same order as
 // drift_chunk, so each job's sums are bitwise those of one launch per job.
+// With 8 jobs that is 256 VGPRs (no spills), the same two waves per SIMD as
+// 3 or 4 jobs take; 2 groups per step for 5-8 jobs measured no faster.
 constexpr int kMultiUnroll = 4;
 
 template <int kJ>
@@ -334,8 +336,16 @@ __global__ __launch_bounds__(kReduceThreads) void drift_batch_partial_kernel(
         uint32_t j, unit_jobs, group_jobs;
         uint64_t chunk;
         if (!batch_iter(groups, n_groups, it, &j, &unit_jobs, &chunk, &group_jobs)) continue;
-        static_assert(kDriftJobsPerIter == 4, "one case per unit size");
-        if (unit_jobs == 4) {
+        static_assert(kDriftJobsPerIter == 8, "one case per unit size");
+        if (unit_jobs == 8) {
+            drift_chunk_jobs<8>(jobs + j, chunk);
+        } else if (unit_jobs == 7) {
+            drift_chunk_jobs<7>(jobs + j, chunk);
+        } else if (unit_jobs == 6) {
+            drift_chunk_jobs<6>(jobs + j, chunk);
+        } else if (unit_jobs == 5) {
+            drift_chunk_jobs<5>(jobs + j, chunk);
+        } else if (unit_jobs == 4) {
             drift_chunk_jobs<4>(jobs + j, chunk);
         } else if (unit_jobs == 3) {
             drift_chunk_jobs<3>(jobs + j, chunk);

@@ -4,9 +4,10 @@ batched live pass (cdt_canary_sim_batch) and the batched Eq. 4
 cdt_canary_sim / cdt_drift_score give it, over jobs of mixed shapes (one
 and several chunks per block, ragged tails, empty jobs) and parameters;
 one job of each batch is also checked against the oracle.  Jobs that share
-a reference array (walked chunk-major, the reference read once per chunk
-for the group) are covered with groups of one to three jobs.  And the live
-pass's stream aid (cdt_canary_sim_stream) writes exactly fp16(a)."""
+a reference array (Eq. 4 reads a reference chunk once per unit of up to 8
+of them) are covered with groups of 1 to 15 jobs, every unit size from 1 to
+8 among them.  And the live pass's stream aid (cdt_canary_sim_stream)
+writes exactly fp16(a)."""
 import numpy as np
 import pytest
 
@@ -97,19 +98,20 @@ def test_canary_sim_batch_equals_single(gpu, dist, mode):
 
 
 # Jobs over shared references, in the order given: consecutive jobs over one
-# reference array form a group (Eq. 4: units of up to 4 jobs per reference
+# reference array form a group (Eq. 4: units of up to 8 jobs per reference
 # read; the live pass: chunk-major below 8 jobs, job-major from 8 on); a
 # reference that comes back after another one starts a new group.  Per
-# entry: (reference index, shape index).  Groups of 1, 2, 3, 6 (4 + 2) and
-# 9 jobs, ragged shapes among them.
+# entry: (reference index, shape index).  Groups of 1, 2, 3, 4, 5, 6, 9
+# (8 + 1) and 15 (8 + 7) jobs, so every unit size from 1 to 8 is scored,
+# ragged shapes among them.
 SHARED_ORDER = ([(0, 0), (0, 0), (0, 0), (1, 1), (1, 1), (0, 0), (2, 2), (3, 3), (3, 3), (2, 2)]
-                + [(1, 1)] * 6 + [(3, 3)] * 9)
+                + [(1, 1)] * 6 + [(3, 3)] * 9 + [(0, 0)] * 4 + [(2, 2)] * 5 + [(1, 1)] * 15)
 SHARED_SHAPES = [(16, 4, 4, 32768), (3, 5, 7, 264), (4, 8, 16, 256), (2, 3, 41, 1000)]
 
 
 def test_drift_score_batch_shared_references(gpu):
     """Groups of jobs over one reference (several chunks per block, one chunk
-    per block, ragged tails; groups of 1 to 9 jobs, a reference coming back
+    per block, ragged tails; groups of 1 to 15 jobs, a reference coming back
     after another) score every job as the single launch does, bit for bit."""
     torch, cdt = gpu
     announce("drift_score_batch over shared references")
