@@ -405,6 +405,48 @@ def test_largest_block(gpu):
     torch.cuda.empty_cache()
 
 
+def test_largest_block_batched(gpu):
+    """The batched launches on blocks of T*H = 2^32 - 2^19 elements: three
+    runs over one reference (different tampers) generate bitwise what one
+    launch per run generates, and Eq. 4 of the three in one launch gives
+    exactly known sums on differences placed past 2^31."""
+    torch, cdt = gpu
+    T, H = 1 << 16, (1 << 16) - 8
+    n = T * H
+    announce(f"largest block batched n={n}")
+    gain = torch.ones((H,), dtype=torch.float32, device="cuda")
+    ref = cdt.ref_synth(1, 1, T, H, 6, 10, gain)
+    ts = torch.full((1, 1), 0.02, dtype=torch.float32, device="cuda")
+    kws = [dict(seed=6, cfg_id=20, sigma_b=1e-2, mal_mask=1, tamper=2, flip_p=0.25),
+           dict(seed=6, cfg_id=21, sigma_b=1e-3, mal_mask=1, tamper=1, tscale=ts),
+           dict(seed=6, cfg_id=22, sigma_b=1e-3, mal_mask=0, tamper=4, scale=1.05)]
+    hs = [torch.empty((1, 1, T, H), dtype=torch.float16, device="cuda") for _ in kws]
+    cdt.canary_sim_batch([(ref, h, kw) for h, kw in zip(hs, kws)])
+    one = torch.empty_like(hs[0])
+    for k, kw in enumerate(kws):
+        cdt.canary_sim(ref, out=one, **kw)
+        torch.cuda.synchronize()
+        assert torch.equal(one.view(torch.int16), hs[k].view(torch.int16)), k
+    del one
+    # exact sums: a = 1, run k has k + 1 elements at 2 (past 2^31 among them)
+    ref.fill_(1.0)
+    spots = [0, (1 << 31) - 1, 1 << 31, (1 << 31) + 4099, n - 1]
+    for k, h in enumerate(hs):
+        h.fill_(1.0)
+        idx = torch.tensor(spots[-(k + 1):], dtype=torch.int64, device="cuda")
+        h.view(-1)[idx] = 2.0
+    scores = [torch.empty((1, 1), dtype=torch.float32, device="cuda") for _ in hs]
+    nds = [torch.empty((1, 1, 2), dtype=torch.float64, device="cuda") for _ in hs]
+    cdt.drift_score_batch([(h, ref, sc, nd) for h, sc, nd in zip(hs, scores, nds)])
+    torch.cuda.synchronize()
+    for k in range(len(hs)):
+        D, R = nds[k].cpu().numpy().ravel()
+        assert D == float(k + 1) and R == float(n), (k, D, R)
+        assert scores[k].item() == np.float32(math.sqrt((k + 1) / n))
+    del ref, hs
+    torch.cuda.empty_cache()
+
+
 def test_table1_structure(gpu, gold):
     """Table 1 on the paper's shape: the full detector, the recompute
     ceiling and the noisy-reference ablation at 1.0 on all six attacks; the
