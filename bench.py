@@ -796,6 +796,37 @@ def config_runs(torch, cdt, W, name):
     return out
 
 
+def snr_seeds(torch, cdt, W, seeds=(0, 1, 2)):
+    """The SNR study's detection curve over several seeds (the paper plots
+    it as the mean and 95% CI of three seeds): per noise distribution and
+    level, each seed's strict AUROC (Eq. 6), their mean and the half-width
+    of the t-interval (2 degrees of freedom for three seeds).  Each seed
+    draws its own references and noise."""
+    import dataclasses
+    base = W.snr()
+    per = {}
+    for seed in seeds:
+        wl = dataclasses.replace(base, seed=base.seed + seed)
+        rs = wl.ref_sets[0]
+        prep = Prepared(torch, cdt, W, wl, rs)
+        score = torch.empty((rs.C, rs.S), dtype=torch.float32, device="cuda")
+        for k, run in enumerate(rs.runs):
+            cdt.canary_sim(prep.ref, out=prep.h, **sim_kwargs(wl, rs, run, *prep.scales[k]))
+            cdt.drift_score(prep.h, prep.ref, out=score, ws=prep.ws)
+            row = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, cdt.AUROC_CONTROL)
+            per.setdefault(run.label, []).append(row["auroc"])
+        del prep, score
+        torch.cuda.empty_cache()
+    t975 = {2: 12.706, 3: 4.303, 4: 3.182, 5: 2.776}.get(len(seeds))
+    curve = {}
+    for label, v in per.items():
+        m = sum(v) / len(v)
+        sd = (sum((x - m) ** 2 for x in v) / (len(v) - 1)) ** 0.5 if len(v) > 1 else 0.0
+        curve[label] = {"auroc": v, "mean": round(m, 4),
+                        "ci95_half": round(t975 * sd / len(v) ** 0.5, 4) if t975 else None}
+    return {"seeds": [base.seed + s for s in seeds], "curve": curve}
+
+
 def attainable(torch):
     """What torch's own kernels reach on the same box for the detector's two
     byte streams: a read-only reduction (drift_score's stream), a plain copy,
@@ -1080,6 +1111,7 @@ def main():
         log("llama7b and snr workloads")
         res["configs"] = {"llama7b": config_runs(torch, cdt, W, "llama7b"),
                           "snr": config_runs(torch, cdt, W, "snr")}
+        res["configs"]["snr"]["three_seeds"] = snr_seeds(torch, cdt, W)
     if not args.no_sweep:
         res["sweep"] = run_sweep(torch, cdt, W, args.sweep_reps)
     if not args.no_ablations:
