@@ -91,6 +91,7 @@ _SIGS = {
     "orc_score_cmp": ([_f, _f], _i),
     "orc_scramble_jstar": ([_u32, _u64, _u64, _u32, _u32], _i),
     "orc_auroc_config": ([_u32, _u32, _f32p, _u64, _u64, _u32, _u32, _u64p, _u64p, _u64p], _i),
+    "orc_auroc_canaries": ([_u32, _u32, _f32p, _u64, _u64, _u32, _u32, _u32, _u32p], _i),
 }
 
 
@@ -447,6 +448,20 @@ def auroc_config(scores, pos_mask, *, seed=0, cfg_id=0, flags=AUROC_CONTROL | AU
     if rc:
         raise ValueError(f"orc_auroc_config failed ({rc})")
     return counts, pooled
+
+
+def auroc_canaries(scores, pos_mask, *, seed=0, cfg_id=0, canary_base=0,
+                   flags=AUROC_CONTROL | AUROC_RANDOM):
+    """Eq. 5 per canary: scores [C][S] fp32 -> uint32 [C][6] = (G_t, E_t,
+    control G_t, E_t, random-baseline G_t, E_t), draws keyed by canary_base + t."""
+    sc = _c(scores, np.float32)
+    C, S = sc.shape
+    out = np.zeros((C, 6), np.uint32)
+    rc = lib().orc_auroc_canaries(S, C, _p(sc, ctypes.c_float), pos_mask, seed, cfg_id,
+                                  canary_base, flags, _p(out, ctypes.c_uint32))
+    if rc:
+        raise ValueError(f"orc_auroc_canaries failed ({rc})")
+    return out
 
 
 def random_score(seed, cfg_id, t, s):

@@ -817,6 +817,61 @@ int orc_scramble_jstar(uint32_t S, uint64_t pos_mask, uint64_t seed, uint32_t cf
     return (int)benign[w[0] % B];
 }
 
+/* Eq. 5 per canary: for each canary t of one configuration (scores [C][S],
+ * positives = shards in pos_mask), out[t][0..5] = the counts whose ratio is
+ * A^(t): G_t, E_t (positive i beats / ties negative j, over all such pairs
+ * of that canary), then the same two for the scrambled-label control (the
+ * chosen benign stage j* against the others, Section 4.5) and for the
+ * random baseline (every score replaced by its uniform, Section 4.5).  The
+ * control and baseline entries are 0 unless their flag is set.  Draws use
+ * the canary's global index canary_base + t. */
+int orc_auroc_canaries(uint32_t S, uint32_t C, const float* scores, uint64_t pos_mask,
+                       uint64_t seed, uint32_t cfg_id, uint32_t canary_base, uint32_t flags,
+                       uint32_t* out)
+{
+    if (S > 64)
+        return 1;
+    for (uint32_t t = 0; t < C; ++t) {
+        const float* m = scores + (uint64_t)t * S;
+        const uint32_t tg = canary_base + t;
+        uint32_t* o = out + (uint64_t)t * 6;
+        for (int k = 0; k < 6; ++k)
+            o[k] = 0;
+        for (uint32_t i = 0; i < S; ++i) {
+            if (!((pos_mask >> i) & 1u))
+                continue;
+            for (uint32_t j = 0; j < S; ++j) {
+                if ((pos_mask >> j) & 1u)
+                    continue;
+                int r = score_cmp(m[i], m[j]);
+                o[0] += (r > 0);
+                o[1] += (r == 0);
+                if (flags & ORC_AUROC_RANDOM) {
+                    int q = score_cmp(orc_random_score(seed, cfg_id, tg, i),
+                                      orc_random_score(seed, cfg_id, tg, j));
+                    o[4] += (q > 0);
+                    o[5] += (q == 0);
+                }
+            }
+        }
+        if (flags & ORC_AUROC_CONTROL) {
+            const int skip_true = !(flags & ORC_CTRL_INCLUDE_TRUE);
+            int js = orc_scramble_jstar(S, pos_mask, seed, cfg_id, tg);
+            if (js >= 0)
+                for (uint32_t j = 0; j < S; ++j) {
+                    if (j == (uint32_t)js)
+                        continue;
+                    if (skip_true && ((pos_mask >> j) & 1u))
+                        continue;
+                    int r = score_cmp(m[js], m[j]);
+                    o[2] += (r > 0);
+                    o[3] += (r == 0);
+                }
+        }
+    }
+    return 0;
+}
+
 /* One configuration: scores [C][S] (fp32), positives = shards in pos_mask.
  * counts[0..5] = G, E, pairs (Eq. 5 summed over canaries: G counts
  *   m_i > m_j, E counts m_i == m_j, over i in M, j not in M),

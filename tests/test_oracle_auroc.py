@@ -174,3 +174,51 @@ def test_degenerate_label_sets(orc):
     assert counts[2] == 0
     with pytest.raises(ValueError):
         orc.auroc_config(inputs.scores(2, 65, seed=8), 1)
+
+
+@pytest.mark.parametrize("flags,base", [(1 | 8, 0), (1 | 4 | 8, 0), (1 | 8, 1000), (0, 7)])
+def test_per_canary_counts_brute_force(orc, flags, base):
+    """Eq. 5 per canary (A^(t) = G_t / (|M| |N|)): every canary's detector,
+    control and random-baseline counts equal a pure-Python count over that
+    canary's pairs, with ties and NaNs, the control's chosen stage and the
+    baseline's uniforms taken from the oracle's draws for the canary's
+    global index; summed over canaries they give the configuration totals."""
+    C, S = 9, 7
+    pos = (1, 4)
+    sc = inputs.scores(C, S, seed=5, mal=pos, gap=0.1, tie_levels=5)
+    sc[2, 3] = np.nan
+    sc[5, 1] = np.nan
+    sc[6, :] = -0.0
+    sc[6, 2] = 0.0
+    mask = _mask(pos)
+    got = orc.auroc_canaries(sc, mask, seed=3, cfg_id=11, canary_base=base, flags=flags)
+    assert got.shape == (C, 6) and got.dtype == np.uint32
+    neg = [j for j in range(S) if j not in pos]
+    for t in range(C):
+        G, E, _ = _brute(sc[t:t + 1], pos)
+        want = [G, E, 0, 0, 0, 0]
+        if flags & 1:
+            js = orc.scramble_jstar(S, mask, 3, 11, base + t)
+            others = [j for j in range(S) if j != js and (flags & 4 or j not in pos)]
+            kj = _key(sc[t, js])
+            want[2] = sum(kj > _key(sc[t, j]) for j in others)
+            want[3] = sum(kj == _key(sc[t, j]) for j in others)
+        if flags & 8:
+            u = [orc.random_score(3, 11, base + t, s) for s in range(S)]
+            want[4] = sum(u[i] > u[j] for i in pos for j in neg)
+            want[5] = sum(u[i] == u[j] for i in pos for j in neg)
+        np.testing.assert_array_equal(got[t], want, err_msg=f"canary {t}")
+    if base == 0:
+        counts, _ = orc.auroc_config(sc, mask, seed=3, cfg_id=11, flags=flags & 5)
+        tot = got.astype(np.uint64).sum(axis=0)
+        assert tot[0] == counts[0] and tot[1] == counts[1]
+        if flags & 1:
+            assert tot[2] == counts[3] and tot[3] == counts[4]
+        if flags & 8:
+            b = orc.random_baseline(C, S, mask, seed=3, cfg_id=11)
+            assert tot[4] == b[0] and tot[5] == b[1]
+
+
+def test_per_canary_rejects_more_than_64_stages(orc):
+    with pytest.raises(ValueError):
+        orc.auroc_canaries(np.zeros((2, 65), np.float32), 1)

@@ -93,6 +93,15 @@ MUTANTS = [
      "if ((flags & ORC_CTRL_INCLUDE_TRUE) && ((pos_mask >> j) & 1u))"),
     ("random score bits", "(double)(w[0] >> 8) * 0x1p-24", "(double)(w[0] >> 9) * 0x1p-24"),
     ("pooled order reversed", "pooled[0] += (r > 0);", "pooled[0] += (r < 0);"),
+    # Eq. 5 per canary
+    ("per-canary ties as wins", "o[0] += (r > 0);", "o[0] += (r >= 0);"),
+    ("per-canary draws at the local index", "const uint32_t tg = canary_base + t;",
+     "const uint32_t tg = t;"),
+    ("per-canary control keeps true positives", "if (skip_true && ((pos_mask >> j) & 1u))",
+     "if (!skip_true && ((pos_mask >> j) & 1u))"),
+    ("per-canary baseline compares a stage with itself",
+     "int q = score_cmp(orc_random_score(seed, cfg_id, tg, i),",
+     "int q = score_cmp(orc_random_score(seed, cfg_id, tg, j),"),
 ]
 
 CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math"]
