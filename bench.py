@@ -700,6 +700,7 @@ def run_sweep(torch, cdt, W, reps):
     ctrl_mean = float(vals[:, 2].mean())
     log(f"sweep: {batched_ms:.2f} ms batched, {ms:.2f} ms per-configuration launches, "
         f"for {len(cfgs)} configs")
+    per_canary = sweep_per_canary(torch, cdt, wl, cfgs, scores)
     out = {
         "configs": len(cfgs),
         "ms": round(batched_ms, 3),
@@ -733,10 +734,46 @@ def run_sweep(torch, cdt, W, reps):
             sweep_elems * DRIFT_BYTES_PER_ELEM / (drift_total * 1e-3) / 1e9, 1),
         "unbatched_canary_sim_GBps": round(
             sweep_elems * SIM_BYTES_PER_ELEM / (sim_total * 1e-3) / 1e9, 1),
+        "per_canary": per_canary,
     }
     del preps, h_buf, scores
     torch.cuda.empty_cache()
     return out
+
+
+def sweep_per_canary(torch, cdt, wl, cfgs, scores):
+    """Eq. 5 per canary pooled over the factorial: each canary's A^(t)
+    (strict) for the detector, the scrambled-label control and the random
+    baseline, from the counts of cdt_auroc_canaries, summarised as the
+    paper shows them (the detector at 1.0, the controls spread around 0.5)."""
+    import numpy as np
+    E = torch.cuda.Event
+    a, b = E(enable_timing=True), E(enable_timing=True)
+    a.record()
+    pc = cdt.auroc_canaries(cfgs, scores, seed=wl.seed,
+                            flags=cdt.AUROC_CONTROL | cdt.AUROC_RANDOM)
+    b.record()
+    torch.cuda.synchronize()
+    per = pc.cpu().numpy().view(np.uint32).astype(np.float64)
+    det, ctl, rnd, o = [], [], [], 0
+    for S, C, _off, mask, _cid in cfgs:
+        n_pos = bin(mask).count("1")
+        n_neg = S - n_pos
+        det.append(per[o:o + C, 0] / (n_pos * n_neg))
+        ctl.append(per[o:o + C, 2] / (n_neg - 1))
+        rnd.append(per[o:o + C, 4] / (n_pos * n_neg))
+        o += C
+    det, ctl, rnd = (np.concatenate(x) for x in (det, ctl, rnd))
+
+    def spread(x):
+        return {"mean": round(float(x.mean()), 4), "sd": round(float(x.std()), 4),
+                "q05": round(float(np.quantile(x, 0.05)), 4),
+                "q95": round(float(np.quantile(x, 0.95)), 4)}
+
+    return {"canaries": int(det.size), "launch_ms": round(a.elapsed_time(b), 4),
+            "detector_at_1": round(float((det == 1.0).mean()), 4),
+            "detector_min": round(float(det.min()), 4),
+            "control": spread(ctl), "random_baseline": spread(rnd)}
 
 
 def config_runs(torch, cdt, W, name):

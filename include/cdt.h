@@ -69,13 +69,14 @@ extern "C" {
 #define CDT_STREAM_ALT_T3 11
 
 /* Interface version; changes whenever a layout, a generator rule or the set
- * of entry points changes (9: batched live pass and Eq. 4, the live-pass
- * stream aid, exact-norm scales under the propagation model; 8:
+ * of entry points changes (10: cdt_auroc_canaries added; 9: batched live
+ * pass and Eq. 4, the live-pass stream aid, exact-norm scales under the
+ * propagation model; 8:
  * cdt_drift_score_noalloc added; 7: cdt_auroc_values added, NaN scores
  * rank above every number).  cdt_version() returns the library's, which a
  * caller compares with the CDT_INTERFACE_VERSION of the header it was
  * built with. */
-#define CDT_INTERFACE_VERSION 9
+#define CDT_INTERFACE_VERSION 10
 int cdt_version(void);
 
 /* Description of the last error on the calling thread ("" if none). */
@@ -450,6 +451,30 @@ int cdt_auroc_launch(uint32_t n_cfg, const void* table, const float* scores, uin
  * NULL; values: device [n_cfg][8] fp64 (written, caller-owned). */
 int cdt_auroc_values(uint32_t n_cfg, const uint64_t* counts, const uint64_t* pooled,
                      const uint64_t* baseline, double* values, void* stream);
+
+/* Eq. 5 per canary: the counts behind each canary's A^(t) = G_t / (|M| |N|)
+ * (Eq. 6 is their mean), the paper's per-canary view of the detector against
+ * its controls (Section 4.5).  For configuration g of cfgs (HOST array,
+ * validated exactly as cdt_auroc validates it and copied into ws during the
+ * call) and each of its canaries t:
+ *   per_canary[o_g + t][0..1] = G_t, E_t: positive shard i beats / ties
+ *       negative shard j, over that canary's pairs (i in M, j not in M);
+ *   per_canary[o_g + t][2..3] = the same for the scrambled-label control
+ *       (its chosen benign stage against the others, as in cdt_auroc), 0
+ *       without CDT_AUROC_CONTROL;
+ *   per_canary[o_g + t][4..5] = the same with the random-baseline scores, 0
+ *       without CDT_AUROC_RANDOM;
+ * with o_g = C_0 + ... + C_{g-1}.  Summed over a configuration's canaries
+ * they give cdt_auroc's counts.  Same score order as cdt_auroc.
+ * flags: CDT_AUROC_CONTROL, CDT_CTRL_INCLUDE_TRUE, CDT_AUROC_RANDOM
+ * (CDT_AUROC_POOLED has no per-canary form: CDT_EINVAL).
+ * per_canary: device uint32 [sum of C][6] (written, caller-owned).
+ * ws: cdt_auroc_canaries_workspace_bytes(n_cfg) device bytes, 16-byte
+ * aligned (the table and the canary offsets). */
+size_t cdt_auroc_canaries_workspace_bytes(uint32_t n_cfg);
+int cdt_auroc_canaries(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores,
+                       uint64_t n_scores, uint64_t seed, uint32_t flags, uint32_t* per_canary,
+                       void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -124,6 +124,9 @@ _SIGS = {
     "cdt_auroc_upload": ([_u32, ctypes.POINTER(AurocCfg), _u64, _u32, _vp, _sz, _vp], ctypes.c_int),
     "cdt_auroc_launch": ([_u32, _vp, _vp, _u64, _u64, _u32, _vp, _vp, _vp, _vp], ctypes.c_int),
     "cdt_auroc_values": ([_u32, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
+    "cdt_auroc_canaries_workspace_bytes": ([_u32], _sz),
+    "cdt_auroc_canaries": ([_u32, ctypes.POINTER(AurocCfg), _vp, _u64, _u64, _u32, _vp, _vp, _sz,
+                            _vp], ctypes.c_int),
 }
 
 _LIB = None
@@ -131,7 +134,7 @@ _LIB = None
 
 # Interface version of include/cdt.h that the structures and signatures
 # below mirror (cdt_version()).
-ABI_VERSION = 9
+ABI_VERSION = 10
 
 
 def lib():
@@ -554,6 +557,27 @@ def auroc_launch(table, n_cfg, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_PO
                                   _ptr(counts), _ptr(pooled), _ptr(baseline), _stream()))
     return (counts, pooled if flags & AUROC_POOLED else None,
             baseline if flags & AUROC_RANDOM else None)
+
+
+def auroc_canaries(cfgs, scores, *, seed=0, flags=AUROC_CONTROL | AUROC_RANDOM, out=None,
+                   ws=None):
+    """Eq. 5 per canary (cdt_auroc_canaries).  cfgs as for auroc; returns
+    int32 [sum of C][6] holding the uint32 counts (G_t, E_t of the detector,
+    the control and the random baseline), configurations in order."""
+    torch = _torch()
+    _need(scores, "scores", torch.float32)
+    arr, n = auroc_cfg_array(cfgs)
+    total = sum(int(c[1]) for c in cfgs)
+    out = _empty((max(total, 1), 6), torch.int32, scores) if out is None else out
+    _need(out, "out", torch.int32)
+    if out.numel() < 6 * total:
+        raise ValueError(f"out holds {out.numel()} counts, {6 * total} needed")
+    if ws is None:
+        ws = _empty((max(16, lib().cdt_auroc_canaries_workspace_bytes(n)),), torch.uint8, scores)
+    _need(ws, "ws", torch.uint8)
+    _check(lib().cdt_auroc_canaries(n, arr, _ptr(scores), scores.numel(), seed, flags, _ptr(out),
+                                    _ptr(ws), ws.numel(), _stream()))
+    return out[:total]
 
 
 VALUE_NAMES = ("auroc", "auroc_mw", "control", "control_mw", "pooled", "pooled_mw", "random",

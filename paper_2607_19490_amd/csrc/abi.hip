@@ -11,6 +11,7 @@
 
 #include "cdt.h"
 #include "cdt_launch.hpp"
+#include "cdt_rank.hpp"
 
 namespace {
 
@@ -76,7 +77,7 @@ bool canaries_fit(uint32_t canary_base, uint64_t C) {
 
 extern "C" {
 
-int cdt_version(void) { return 9; }
+int cdt_version(void) { return 10; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -767,6 +768,53 @@ int cdt_auroc_launch(uint32_t n_cfg, const void* table, const float* scores, uin
                                            scores, n_scores, seed, flags, counts, pooled,
                                            baseline, static_cast<hipStream_t>(stream)),
                          "cdt_auroc_launch");
+}
+
+size_t cdt_auroc_canaries_workspace_bytes(uint32_t n_cfg) {
+    return align256(static_cast<size_t>(n_cfg) * sizeof(cdt_auroc_cfg)) +
+           static_cast<size_t>(n_cfg) * sizeof(uint64_t);
+}
+
+int cdt_auroc_canaries(uint32_t n_cfg, const cdt_auroc_cfg* cfgs, const float* scores,
+                       uint64_t n_scores, uint64_t seed, uint32_t flags, uint32_t* per_canary,
+                       void* ws, size_t ws_bytes, void* stream) {
+    const char* fn = "cdt_auroc_canaries";
+    if (flags & ~(CDT_AUROC_CONTROL | CDT_CTRL_INCLUDE_TRUE | CDT_AUROC_RANDOM))
+        return fail(CDT_EINVAL, "%s: bad flags (the pooled ranking has no per-canary form)", fn);
+    if (n_cfg == 0) return ok();
+    std::vector<cdt_auroc_cfg> table;
+    int rc = validated_table(fn, n_cfg, cfgs, n_scores, flags, &table);
+    if (rc) return rc;
+    // each configuration's canaries follow the previous ones' in per_canary
+    const size_t table_bytes = align256(static_cast<size_t>(n_cfg) * sizeof(cdt_auroc_cfg));
+    std::vector<char> staged(cdt_auroc_canaries_workspace_bytes(n_cfg), 0);
+    memcpy(staged.data(), table.data(), n_cfg * sizeof(cdt_auroc_cfg));
+    uint64_t* offsets = reinterpret_cast<uint64_t*>(staged.data() + table_bytes);
+    uint64_t total = 0;
+    bool any_scores = false;
+    for (uint32_t g = 0; g < n_cfg; ++g) {
+        offsets[g] = total;
+        total += table[g].C;
+        any_scores = any_scores || static_cast<uint64_t>(table[g].S) * table[g].C > 0;
+    }
+    if (total == 0) return ok();
+    if (!per_canary) return fail(CDT_EINVAL, "%s: per_canary is NULL", fn);
+    if (any_scores && !scores) return fail(CDT_EINVAL, "%s: scores is NULL", fn);
+    if (!ws || ws_bytes < staged.size())
+        return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, staged.size(),
+                    ws ? ws_bytes : 0);
+    if (!aligned16(ws)) return fail(CDT_EALIGN, "%s: ws must be 16-byte aligned", fn);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    // from pageable host memory: the copy completes before the call returns
+    const hipError_t e = hipMemcpyAsync(ws, staged.data(), staged.size(), hipMemcpyHostToDevice,
+                                        st);
+    if (e != hipSuccess) return device_status(e, fn);
+    char* base = static_cast<char*>(ws);
+    return device_status(
+        cdt::launch_auroc_canaries(n_cfg, reinterpret_cast<const cdt::AurocCfgDev*>(base),
+                                   reinterpret_cast<const uint64_t*>(base + table_bytes), scores,
+                                   n_scores, seed, flags, per_canary, st),
+        fn);
 }
 
 int cdt_auroc_values(uint32_t n_cfg, const uint64_t* counts, const uint64_t* pooled,

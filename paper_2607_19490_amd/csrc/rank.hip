@@ -18,6 +18,7 @@
 // only the stages that span waves go through LDS, with one barrier each.
 #include "cdt_device.hpp"
 #include "cdt_launch.hpp"
+#include "cdt_rank.hpp"
 
 namespace cdt {
 namespace {
@@ -56,6 +57,71 @@ __device__ __forceinline__ bool cfg_in_bounds(const AurocCfgDev& cfg, uint64_t n
 
 constexpr unsigned long long kBadCfg = ~0ull;  // counts of a configuration out of bounds
 
+// What one wave needs to rank a configuration's canaries (lane = shard).
+struct RankCtx {
+    uint64_t pos, neg;
+    uint32_t n_benign, tag, tag_random;
+    bool lane_in, lane_pos, control, include_true, random;
+};
+
+__device__ __forceinline__ RankCtx rank_ctx(const AurocCfgDev& cfg, uint32_t flags) {
+    const uint32_t lane = threadIdx.x % kWave;
+    const uint64_t all = shard_mask(cfg.S);
+    RankCtx r;
+    r.pos = cfg.pos_mask & all;
+    r.neg = all & ~r.pos;
+    r.lane_in = lane < cfg.S;
+    r.lane_pos = r.lane_in && ((r.pos >> lane) & 1u);
+    r.control = flags & 1u;
+    r.include_true = flags & 4u;
+    r.random = flags & 8u;
+    r.n_benign = __builtin_popcountll(r.neg);
+    r.tag = stream_tag(kStreamScramble, cfg.cfg_id);
+    r.tag_random = stream_tag(kStreamRandom, cfg.cfg_id);
+    return r;
+}
+
+// One canary's Eq. 5 counts as this lane sees them: a positive lane's wins
+// and ties over the negative shards (q = 0, 1), the scrambled-label
+// control's chosen stage against this lane's (q = 2, 3) and the random
+// baseline's (q = 4, 5).  cur is this lane's score, t the canary's local
+// index.  Every lane of the wave must call it.
+__device__ __forceinline__ void rank_canary(const RankCtx& r, const AurocCfgDev& cfg, Key key,
+                                            uint32_t t, float cur, uint32_t (&c)[6]) {
+    const uint32_t lane = threadIdx.x % kWave;
+    for (int q = 0; q < 6; ++q) c[q] = 0;
+    const uint32_t k = r.lane_in ? order_key(cur) : 0u;
+    for (uint32_t j = 0; j < cfg.S; ++j) {
+        const uint32_t kj = __shfl(k, j, kWave);
+        if (r.lane_pos && ((r.neg >> j) & 1u)) {
+            c[0] += k > kj;
+            c[1] += k == kj;
+        }
+    }
+    if (r.random) {
+        const uint32_t kr =
+            r.lane_in ? order_key(random_score(key, cfg.canary_base + t, lane, r.tag_random)) : 0u;
+        for (uint32_t j = 0; j < cfg.S; ++j) {
+            const uint32_t kj = __shfl(kr, j, kWave);
+            if (r.lane_pos && ((r.neg >> j) & 1u)) {
+                c[4] += kr > kj;
+                c[5] += kr == kj;
+            }
+        }
+    }
+    if (r.control && r.n_benign > 0) {
+        const uint32_t u = draw(key, cfg.canary_base + t, 0, 0, r.tag).x;
+        const uint32_t js = nth_set_bit(r.neg, u % r.n_benign);
+        const uint32_t kjs = __shfl(k, js, kWave);
+        const bool counted =
+            r.lane_in && lane != js && (r.include_true || !((r.pos >> lane) & 1u));
+        if (counted) {
+            c[2] += kjs > k;
+            c[3] += kjs == k;
+        }
+    }
+}
+
 __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
     const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, uint64_t n_scores,
     Key key, uint32_t flags, unsigned long long* __restrict__ counts,
@@ -70,55 +136,27 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
         return;
     }
     const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const uint64_t all = shard_mask(cfg.S);
-    const uint64_t pos = cfg.pos_mask & all;
-    const uint64_t neg = all & ~pos;
-    const bool lane_in = lane < cfg.S;
-    const bool lane_pos = lane_in && ((pos >> lane) & 1u);
-    const bool control = flags & 1u;
-    const bool include_true = flags & 4u;
-    const bool random = flags & 8u;
-    const uint32_t n_benign = __builtin_popcountll(neg);
-    const uint32_t tag = stream_tag(kStreamScramble, cfg.cfg_id);
-    const uint32_t tag_random = stream_tag(kStreamRandom, cfg.cfg_id);
+    const RankCtx r = rank_ctx(cfg, flags);
+    const uint64_t pos = r.pos;
+    const bool control = r.control, include_true = r.include_true, random = r.random;
+    const uint32_t n_benign = r.n_benign;
 
     unsigned long long g = 0, e = 0, gc = 0, ec = 0, gr = 0, er = 0;
     const float* base = scores + cfg.score_off;
+    const bool lane_in = r.lane_in;
     float next = (wave < cfg.C && lane_in) ? base[static_cast<uint64_t>(wave) * cfg.S + lane] : 0.f;
     for (uint32_t t = wave; t < cfg.C; t += kCountWaves) {
         const float cur = next;
         const uint32_t tn = t + kCountWaves;
         if (tn < cfg.C && lane_in) next = base[static_cast<uint64_t>(tn) * cfg.S + lane];
-        const uint32_t k = lane_in ? order_key(cur) : 0u;
-        for (uint32_t j = 0; j < cfg.S; ++j) {
-            const uint32_t kj = __shfl(k, j, kWave);
-            if (lane_pos && ((neg >> j) & 1u)) {
-                g += k > kj;
-                e += k == kj;
-            }
-        }
-        if (random) {
-            const uint32_t kr =
-                lane_in ? order_key(random_score(key, cfg.canary_base + t, lane, tag_random)) : 0u;
-            for (uint32_t j = 0; j < cfg.S; ++j) {
-                const uint32_t kj = __shfl(kr, j, kWave);
-                if (lane_pos && ((neg >> j) & 1u)) {
-                    gr += kr > kj;
-                    er += kr == kj;
-                }
-            }
-        }
-        if (control && n_benign > 0) {
-            const uint32_t u = draw(key, cfg.canary_base + t, 0, 0, tag).x;
-            const uint32_t js = nth_set_bit(neg, u % n_benign);
-            const uint32_t kjs = __shfl(k, js, kWave);
-            const bool counted =
-                lane_in && lane != js && (include_true || !((pos >> lane) & 1u));
-            if (counted) {
-                gc += kjs > k;
-                ec += kjs == k;
-            }
-        }
+        uint32_t c[6];
+        rank_canary(r, cfg, key, t, cur, c);
+        g += c[0];
+        e += c[1];
+        gc += c[2];
+        ec += c[3];
+        gr += c[4];
+        er += c[5];
     }
 
     __shared__ unsigned long long lds[6][kCountWaves];
@@ -149,6 +187,41 @@ __global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
             rb[0] = tot[4];
             rb[1] = tot[5];
             rb[2] = out[2];
+        }
+    }
+}
+
+// Eq. 5 per canary: the same ranking as auroc_counts_kernel, each canary's
+// six counts summed over its wave and written by lane 0 to
+// out[(offset[g] + t) * 6 + q].  A configuration out of bounds gets
+// 0xFFFFFFFF in its entries instead of being read.
+__global__ __launch_bounds__(kCountThreads) void auroc_canaries_kernel(
+    const AurocCfgDev* __restrict__ cfgs, const uint64_t* __restrict__ offsets,
+    const float* __restrict__ scores, uint64_t n_scores, Key key, uint32_t flags,
+    uint32_t* __restrict__ out) {
+    const AurocCfgDev cfg = cfgs[blockIdx.x];
+    uint32_t* o = out + 6ull * offsets[blockIdx.x];
+    const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    if (!cfg_in_bounds(cfg, n_scores)) {  // uniform over the workgroup
+        for (uint64_t i = threadIdx.x; i < 6ull * cfg.C; i += kCountThreads) o[i] = ~0u;
+        return;
+    }
+    const RankCtx r = rank_ctx(cfg, flags);
+    const float* base = scores + cfg.score_off;
+    float next =
+        (wave < cfg.C && r.lane_in) ? base[static_cast<uint64_t>(wave) * cfg.S + lane] : 0.f;
+    for (uint32_t t = wave; t < cfg.C; t += kCountWaves) {
+        const float cur = next;
+        const uint32_t tn = t + kCountWaves;
+        if (tn < cfg.C && r.lane_in) next = base[static_cast<uint64_t>(tn) * cfg.S + lane];
+        uint32_t c[6];
+        rank_canary(r, cfg, key, t, cur, c);
+        unsigned long long w[6];
+#pragma unroll
+        for (int q = 0; q < 6; ++q) w[q] = wave_sum(static_cast<unsigned long long>(c[q]));
+        if (lane == 0) {
+#pragma unroll
+            for (int q = 0; q < 6; ++q) o[6ull * t + q] = static_cast<uint32_t>(w[q]);
         }
     }
 }
@@ -381,6 +454,17 @@ hipError_t launch_auroc_values(uint32_t n_cfg, const uint64_t* counts, const uin
                        reinterpret_cast<const unsigned long long*>(counts),
                        reinterpret_cast<const unsigned long long*>(pooled),
                        reinterpret_cast<const unsigned long long*>(baseline), values);
+    return hipGetLastError();
+}
+
+hipError_t launch_auroc_canaries(uint32_t n_cfg, const AurocCfgDev* cfgs_dev,
+                                 const uint64_t* offsets_dev, const float* scores,
+                                 uint64_t n_scores, uint64_t seed, uint32_t flags,
+                                 uint32_t* per_canary, hipStream_t st) {
+    if (n_cfg == 0) return hipSuccess;
+    const Key key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)};
+    hipLaunchKernelGGL(auroc_canaries_kernel, dim3(n_cfg), dim3(kCountThreads), 0, st, cfgs_dev,
+                       offsets_dev, scores, n_scores, key, flags, per_canary);
     return hipGetLastError();
 }
 

@@ -38,7 +38,7 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 9 == cdt.ABI_VERSION
+    assert L.cdt_version() == 10 == cdt.ABI_VERSION
     assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
@@ -230,6 +230,35 @@ def test_auroc_upload_and_launch_validation(cdt):
     assert run(1, 8, 16, 32, 0, 0, 16, None, None, None) == cdt.EALIGN
     assert run((1 << 24) + 1, 16, 16, 32, 0, 0, 16, None, None, None) == cdt.ELIMIT
     assert run(0, None, None, 0, 0, 0, None, None, None, None) == cdt.OK
+
+
+def test_auroc_canaries_validation(cdt):
+    """Eq. 5 per canary: the table is checked as cdt_auroc checks it, the
+    pooled flag is refused (it has no per-canary form), and the outputs and
+    the workspace (table plus canary offsets) are checked before any device
+    work."""
+    L = cdt.lib()
+    f = L.cdt_auroc_canaries
+    need = L.cdt_auroc_canaries_workspace_bytes
+    assert need(0) == 0 and need(1) == 256 + 8 and need(9) == 512 + 72
+    arr, n = cdt.auroc_cfg_array([(8, 4, 0, 1, 0)])
+    assert f(n, arr, 16, 32, 0, cdt.AUROC_POOLED, 16, 16, 264, None) == cdt.EINVAL
+    assert "pooled" in _err(cdt)
+    assert f(n, arr, 16, 32, 0, 16, 16, 16, 264, None) == cdt.EINVAL  # bad flags
+    arr65, n65 = cdt.auroc_cfg_array([(65, 4, 0, 1, 0)])
+    assert f(n65, arr65, 16, 1000, 0, 0, 16, 16, 264, None) == cdt.ELIMIT
+    arr2, n2 = cdt.auroc_cfg_array([(8, 4, 0, 1, 0), (8, 4, 30, 1, 1)])
+    assert f(n2, arr2, 16, 60, 0, 0, 16, 16, 264, None) == cdt.EINVAL and "outside" in _err(cdt)
+    assert f(n, None, 16, 32, 0, 0, 16, 16, 264, None) == cdt.EINVAL
+    assert f(n, arr, 16, 32, 0, 0, None, 16, 264, None) == cdt.EINVAL  # no per_canary
+    assert "per_canary" in _err(cdt)
+    assert f(n, arr, None, 32, 0, 0, 16, 16, 264, None) == cdt.EINVAL  # no scores
+    assert f(n, arr, 16, 32, 0, 0, 16, 16, 263, None) == cdt.EINVAL  # workspace too small
+    assert f(n, arr, 16, 32, 0, 0, 16, None, 264, None) == cdt.EINVAL
+    assert f(n, arr, 16, 32, 0, 0, 16, 8, 264, None) == cdt.EALIGN
+    assert f(0, None, None, 0, 0, 0, None, None, 0, None) == cdt.OK
+    empty, ne = cdt.auroc_cfg_array([(8, 0, 0, 1, 0)])  # no canaries: nothing to write
+    assert f(ne, empty, None, 0, 0, 1, None, None, 0, None) == cdt.OK
 
 
 def test_scale_and_outlier_validation(cdt):

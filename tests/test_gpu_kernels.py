@@ -389,6 +389,35 @@ def test_auroc_counts(gpu, flags):
             np.testing.assert_array_equal(got_p[g], want_p, err_msg=f"pooled cfg {g}")
 
 
+@pytest.mark.parametrize("flags,base", [(1 | 8, 0), (0, 0), (1 | 4 | 8, 0), (1 | 8, 4000)])
+def test_auroc_canaries(gpu, flags, base):
+    """Eq. 5 per canary, bit for bit against the oracle on every canary of
+    the batch (ties, NaNs, S = 1 and 64, colluders, C = 0, every stage
+    positive, canary_base > 0), and summed over canaries equal to
+    cdt_auroc's counts."""
+    torch, cdt = gpu
+    announce(f"auroc per canary flags={flags} base={base}")
+    tables, cfgs = _auroc_batch()
+    cfgs = [c + (base,) for c in cfgs]
+    flat = to_dev(torch, np.concatenate([t.ravel() for t in tables]).astype(np.float32))
+    per = cdt.auroc_canaries(cfgs, flat, seed=42, flags=flags)
+    counts, _, rb = cdt.auroc(cfgs, flat, seed=42, flags=flags)
+    torch.cuda.synchronize()
+    got = per.cpu().numpy().view(np.uint32)
+    assert got.shape == (sum(c[1] for c in cfgs), 6)
+    tot, tot_b = cdt.u64(counts), cdt.u64(rb) if rb is not None else None
+    o = 0
+    for g, (t, (S, C, off, mask, cid, cb)) in enumerate(zip(tables, cfgs)):
+        want = oracle.auroc_canaries(t, mask, seed=42, cfg_id=cid, canary_base=cb, flags=flags)
+        np.testing.assert_array_equal(got[o:o + C], want, err_msg=f"cfg {g} S={S} C={C}")
+        s = got[o:o + C].astype(np.uint64).sum(axis=0)
+        assert s[0] == tot[g][0] and s[1] == tot[g][1], g
+        assert s[2] == tot[g][3] and s[3] == tot[g][4], g
+        if flags & 8:
+            assert s[4] == tot_b[g][0] and s[5] == tot_b[g][1], g
+        o += C
+
+
 # Pooled sizes C*S padded to P2 = 64 .. 16384: every width of the pooled
 # sort (1, 2, 4, 8 and 16 elements per thread), lengths just off a power of
 # two, many positives, ties and NaNs.
