@@ -529,6 +529,7 @@ def table1(torch, cdt, W):
     ceiling).  With independent stages the noisy-reference ablation and the
     recompute ceiling compare the live output with the same independent
     benign pass."""
+    import numpy as np
     wl = W.paper()
     rs = wl.ref_sets[0]
     prep = Prepared(torch, cdt, W, wl, rs)
@@ -543,6 +544,13 @@ def table1(torch, cdt, W):
         cdt.canary_sim(prep.ref, out=r, **dict(kw, mal_mask=0, redraw=True))
         cdt.drift_score(prep.h, prep.ref, out=score, ws=prep.ws)
         full = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
+        # the gap Eq. 4 measures: the malicious stage's median mismatch over
+        # the benign stages' median (the paper's margin of Section 6)
+        m = score.cpu().numpy()
+        mal = np.array([(rs.mal_mask >> s_) & 1 for s_ in range(rs.S)], bool)
+        full["margin"] = round(float(np.median(m[:, mal]) / np.median(m[:, ~mal])), 1)
+        full["median_m_malicious"] = round(float(np.median(m[:, mal])), 6)
+        full["median_m_benign"] = round(float(np.median(m[:, ~mal])), 6)
         cdt.drift_score_f16ref(prep.h, r, out=score, ws=prep.ws)
         ceil = auroc_row(cdt, torch, score, rs, run.cfg_id, wl.seed, flags)
         cdt.cosine_score(prep.h, prep.ref, out=score, ws=prep.ws)

@@ -473,3 +473,13 @@ def test_table1_structure(gpu, gold):
         assert row["auroc_l2"] == 1.0, (label, row)
         if not label.startswith("rescale"):
             assert row["auroc_cosine"] == 1.0, (label, row)
+    # the gap Eq. 4 measures (Section 7: 22x at the smallest eps, past 2000x
+    # for the sign flip), statistical: the malicious stage's median mismatch
+    # over the benign stages' median.  The synthetic floor at sigma_hw =
+    # 0.002 is sigma E|a| / rms(a) of the outlier-mixed references plus the
+    # fp16 rounding, close to the realized floor the paper reports, so the
+    # margins land near its figures.
+    full = t["per_attack"]["full_detector"]
+    want = gold["margin_smallest_eps"]["value"]
+    assert 0.8 * want < full["gauss0.02"]["margin"] < 1.25 * want, full["gauss0.02"]
+    assert full["signflip"]["margin"] > 2000.0, full["signflip"]
