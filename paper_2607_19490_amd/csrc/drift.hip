@@ -217,10 +217,13 @@ __device__ __forceinline__ void accumulate8_jobs(const u32x4 (&hv)[kJ], const f3
 }
 
 // One chunk of kJ arrays scored against one shared reference (Eq. 4): each
-// step's reference groups are loaded once (nontemporally, as in
-// drift_chunk) and every job's activations of the step are loaded at once
-// and accumulated against them; the reference's own sum R is formed once
-// for all of them.  The step is kMultiUnroll groups per thread
+// step's reference groups are loaded once and every job's activations of
+// the step are loaded at once and accumulated against them; the
+// reference's own sum R is formed once for all of them.  The reference is
+// read with ordinary (cached) loads, unlike drift_chunk's nontemporal ones:
+// the later units of a group of more than 8 jobs re-read the chunk, and
+// then find it in L2 (the 216-configuration sweep's Eq. 4: 12.9-13.2 ms
+// against 13.6-13.8 ms; the 70B step's single unit is unchanged).  The step is kMultiUnroll groups per thread
 // (not drift_chunk's kReduceUnroll, so that every job's loads fit in
 // registers together); a thread still visits its groups g0 + tid + 256 m in
 // the order m = 0, 1, 2, ... and adds the same values in the same order as
@@ -255,8 +258,8 @@ __device__ __forceinline__ void drift_chunk_jobs(const DriftJobDev* __restrict__
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const gptr<const f32x4> aw = ab + 2 * (base + u * kReduceThreads + wave0);
-                quads_to_groups(__builtin_nontemporal_load(aw + lane),
-                                __builtin_nontemporal_load(aw + kWave + lane), a0[u], a1[u]);
+                const f32x4 r0 = aw[lane], r1 = aw[kWave + lane];
+                quads_to_groups(r0, r1, a0[u], a1[u]);
             }
 #pragma unroll
             for (int j = 0; j < kJ; ++j)
@@ -272,8 +275,8 @@ __device__ __forceinline__ void drift_chunk_jobs(const DriftJobDev* __restrict__
             for (int u = 0; u < kU; ++u) {
                 const uint32_t g = base + u * kReduceThreads + threadIdx.x;
                 const uint32_t gc = g < g_end ? g : g_end - 1;
-                const f32x4 l0 = __builtin_nontemporal_load(ab + 2 * gc);
-                const f32x4 l1 = __builtin_nontemporal_load(ab + 2 * gc + 1);
+                const f32x4 l0 = ab[2 * gc];
+                const f32x4 l1 = ab[2 * gc + 1];
                 const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
                 a0[u] = g < g_end ? l0 : z;
                 a1[u] = g < g_end ? l1 : z;
