@@ -2,7 +2,7 @@
 of a run passes canary_base = c0.  It must get, bit for bit, the whole
 run's values for those canaries: references, live activations (with and
 without propagation), exact-norm scales, drift scores and per-canary AUROC
-counts.  The integer counts of the slices must also add up to the whole
+counts, also with every slice as one job of the batched launches.  The integer counts of the slices must also add up to the whole
 run's.  The whole run is computed both by the oracle and by one unsharded
 GPU call.  This checks, on one device, the by-canary split of the detector:
 no exchange but one sum of integer counts per configuration."""
@@ -58,6 +58,7 @@ def test_canary_slices_match_the_whole_run(gpu, split):
     assert int((h_bits(h_all) != h_want).sum()) == 0
 
     tables, cfgs, off = [], [], 0
+    sim_jobs, drift_jobs, batch_out = [], [], []
     for c0, sl in _slices(parts):
         Cp = sl.stop - sl.start
         bs_p = bs_d[:, sl].contiguous()
@@ -79,9 +80,22 @@ def test_canary_slices_match_the_whole_run(gpu, split):
         assert torch.equal(score_p, score_all[sl]), where
         assert torch.equal(fused_p, score_all[sl]), where
         assert torch.equal(exact_p, exact_all[:, sl]), where
+        # the slice as one job of the batched launches (its own canary_base)
+        hb, sb = torch.empty_like(h_p), torch.empty_like(score_p)
+        sim_jobs.append((ref_p, hb, dict(kw, bscale=bs_p, tscale=ts_p, canary_base=c0)))
+        drift_jobs.append((hb, ref_p, sb, None))
+        batch_out.append((hb, sb, h_want[:, sl], score_all[sl], where))
         tables.append(score_p.reshape(-1))
         cfgs.append((S, Cp, off, mal, CFG, c0))
         off += Cp * S
+
+    # every slice in one batched live pass and one batched Eq. 4
+    cdt.canary_sim_batch(sim_jobs)
+    cdt.drift_score_batch(drift_jobs)
+    torch.cuda.synchronize()
+    for hb, sb, h_w, s_w, where in batch_out:
+        assert int((h_bits(hb) != h_w).sum()) == 0, "batched " + where
+        assert torch.equal(sb, s_w), "batched " + where
 
     # per-canary counts: slices add up to the whole run, bit for bit
     flags = cdt.AUROC_CONTROL | cdt.AUROC_RANDOM
