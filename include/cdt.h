@@ -206,7 +206,9 @@ int cdt_canary_sim(uint32_t S, uint32_t C, uint32_t T, uint32_t H, const cdt_sim
  * Every job must use the same benign_dist and benign_mode and carry 0
  * (CDT_EINVAL otherwise); their shapes, tamper settings and scales may
  * differ.  jobs and each p: HOST, read during the call (the job and group
- * tables are copied into ws on `stream`).  At most 65536 jobs.
+ * tables are copied into ws on `stream` from library-held host memory, a
+ * copy a stream capture must not record: call it outside captures).  At
+ * most 65536 jobs.
  * ws: cdt_sim_batch_workspace_bytes(n_jobs) device bytes. */
 typedef struct cdt_sim_job {
     uint32_t S, C, T, H;
@@ -313,7 +315,9 @@ int cdt_drift_score_noalloc(uint32_t S, uint32_t C, uint32_t T, uint32_t H, cons
  * the chunk once per 8 jobs, the repeats mostly from L2).  Order the jobs so
  * that arrays scored against one reference are adjacent.  jobs: HOST array,
  * validated and copied into ws during the call (reusable when the call
- * returns); jobs with S*C = 0 are skipped.  At most 65536 jobs.
+ * returns; the copy comes from library-held host memory, so a stream
+ * capture must not record the call); jobs with S*C = 0 are skipped.  At
+ * most 65536 jobs.
  * ws: cdt_drift_batch_workspace_bytes(n_jobs, jobs) device bytes (the job
  * and group tables and every job's partial sums); calls that can overlap
  * need their own. */
@@ -456,7 +460,7 @@ int cdt_auroc_values(uint32_t n_cfg, const uint64_t* counts, const uint64_t* poo
  * (Eq. 6 is their mean), the paper's per-canary view of the detector against
  * its controls (Section 4.5).  For configuration g of cfgs (HOST array,
  * validated exactly as cdt_auroc validates it and copied into ws during the
- * call) and each of its canaries t:
+ * call, so a stream capture must not record it) and each of its canaries t:
  *   per_canary[o_g + t][0..1] = G_t, E_t: positive shard i beats / ties
  *       negative shard j, over that canary's pairs (i in M, j not in M);
  *   per_canary[o_g + t][2..3] = the same for the scrambled-label control
