@@ -1,11 +1,13 @@
 """Benchmark of the canary-versus-reference drift detector on one MI355X.
 
-A step is one pass of the detector's hot path over the workload: for every
-run (tamper setting) of the workload, simulate the live fp16 activations
-(canary_sim), score every (shard, canary) block by Eq. 4 (drift_score), then
-rank all runs in one batched AUROC launch (Eqs. 5-6, scrambled-label control
-and pooled Mann-Whitney).  The fp32 references and their block statistics
-are the verifier's offline precomputation and are built before timing.
+A step is one pass of the detector's hot path over the workload: per
+reference set, one batched live pass over its runs (tamper settings) that
+simulates their fp16 activations (cdt_canary_sim_batch), one batched Eq. 4
+that scores every (shard, canary) block of every run (cdt_drift_score_batch;
+the runs share the reference, which is read once for them), then one AUROC
+launch over all runs (Eqs. 5-6, scrambled-label control and pooled
+Mann-Whitney).  The fp32 references and their block statistics are the
+verifier's offline precomputation and are built before timing.
 
 Default workload: Llama-70B-shaped, 16 shards x 256 canaries x 256 tokens x
 hidden 8192 (48 GiB of activations), three runs: additive Gaussian eps 0.05,
@@ -13,26 +15,29 @@ sign flip of 0.1% of elements, uniform rescale by 1.05.
 
 Prints one JSON line:
   value          drift-scored activation bytes (2 B fp16 + 4 B fp32 per
-                 element, each read once) per second of the whole step;
-  roofline       the drift kernel alone against the 8 TB/s HBM peak, with
-                 the HBM traffic of the committed counter pass, and against
-                 a compute-free read of the same bytes in the same access
-                 pattern (cdt_drift_read_stream, timed after the steps);
-  canary_sim, fused_step
-                 the live pass's own rate, its share of the step and its
-                 vector-ALU load from the committed counter pass (it takes
-                 more of the step than drift_score, but stands in for the
-                 activations that the pipeline's stages deliver); the step
-                 with the live pass and Eq. 4 fused into one launch per run;
+                 element and run, 4 B per block score) per second of the
+                 whole step;
+  roofline       the batched Eq. 4 launch against the 8 TB/s HBM peak: its
+                 algorithmic bytes (every run's activations and the
+                 reference once) over its HIP-event time, with the HBM
+                 traffic of the committed counter pass;
+  canary_sim, per_run_launches, fused_step
+                 the batched live pass against the vector-ALU issue peak
+                 (committed counter pass); the same step with one launch per
+                 run, with each kernel against its compute-free access
+                 pattern; the step with the live pass and Eq. 4 fused;
   ablation_kernels, table1, substudies
                  the reference conditions and ablations of Sections 4.4-4.5,
-                 Table 1's structure on the paper's shape, the propagation
-                 substudies of Sections 5.3-5.5;
-  sweep          the 216-run factorial in configurations per second;
+                 Table 1's structure on the paper's shape with the margin
+                 Eq. 4 measures, the propagation substudies of Sections
+                 5.3-5.5;
+  sweep          the 216-run factorial in configurations per second, with
+                 Eq. 5 per canary pooled over it;
   attainable, small, configs
                  torch's own kernels on the same byte streams, latencies of
                  the cache-resident tiny workload (eager, fused, HIP graph),
-                 the 7B-shaped and SNR workloads run by themselves;
+                 the 7B-shaped and SNR workloads run by themselves (the SNR
+                 curve also over three seeds);
   cpu_baseline   the CPU oracle on a bounded sample of the same step, spread
                  over up to 16 host threads (and on one thread).
 """
