@@ -19,7 +19,10 @@
  *     owned by the caller, unless a comment says "host".  The library never
  *     allocates or frees memory.
  *   - Calls are asynchronous on `stream` (a hipStream_t passed as void*,
- *     NULL = the default stream); nothing synchronises implicitly.
+ *     NULL = the default stream).  The calls that take a HOST table
+ *     (cdt_auroc, cdt_auroc_upload, cdt_auroc_canaries and the batched
+ *     launches) copy it from library-held pageable memory, a copy that is
+ *     complete when the call returns; nothing else waits on the host.
  *   - Arguments are validated before any device work; on failure nothing is
  *     launched and an error code is returned.  cdt_last_error() gives a
  *     per-thread description of the last failure.
