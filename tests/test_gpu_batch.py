@@ -135,6 +135,48 @@ def test_drift_score_batch_shared_references(gpu):
         assert torch.equal(nd, nd1), f"job {k}: sums differ"
 
 
+def test_drift_score_batch_special_values(gpu):
+    """Non-finite, extreme and degenerate operands in a group of 9 runs over
+    one shared reference (a unit of 8 and one of 1; two chunks per block,
+    the second ragged): fp16 infinities and NaNs in h, infinite reference
+    elements, fp16 subnormals, values near the fp16 limit, and an all-zero
+    reference block that one run matches exactly (score 0) and the others
+    do not (+inf).  Every run's scores and sums equal the single launch's
+    bit for bit, NaNs included."""
+    torch, cdt = gpu
+    announce("drift_score_batch special values")
+    S, C, T, H = 6, 3, 5, 7000
+    a = inputs.ref_normal((S, C, T, H), seed=31)
+    a[3] *= np.float32(1e-6)
+    a[4] *= np.float32(6e4 / np.abs(a[4]).max())
+    a[5, 2] = 0.0
+    a[2, 1, 4, 39] = np.inf
+    a[5, 0, 0, 0] = np.inf
+    ad = to_dev(torch, a)
+    jobs = []
+    for j in range(9):
+        h = inputs.live_near(a, seed=40 + j, rel=1e-2)
+        h[0, j % C, 1, 3 + j] = 0x7C00
+        h[1, (j + 1) % C, 2, 5] = 0xFC00 if j % 2 else 0x7E00
+        h[2, 1, 4, 39] = 0x7C00
+        h[5, 2] = 0
+        if j:
+            h[5, 2, j % T, 17 * j] = 0x3C00  # 1.0 where the reference is 0
+        sc = torch.full((C, S), -1.0, dtype=torch.float32, device="cuda")
+        nd = torch.full((C, S, 2), -1.0, dtype=torch.float64, device="cuda")
+        jobs.append((to_dev(torch, h).view(torch.float16), ad, sc, nd))
+    cdt.drift_score_batch(jobs)
+    for j, (hd, _, sc, nd) in enumerate(jobs):
+        nd1 = torch.empty_like(nd)
+        want = cdt.drift_score(hd, ad, num_den=nd1)
+        torch.cuda.synchronize()
+        assert torch.equal(sc.view(torch.int32), want.view(torch.int32)), f"run {j}: scores"
+        assert torch.equal(nd.view(torch.int64), nd1.view(torch.int64)), f"run {j}: sums"
+        s_ = sc.cpu().numpy()
+        assert (s_[2, 5] == 0.0) if j == 0 else np.isposinf(s_[2, 5]), (j, s_[2, 5])
+        assert np.isnan(s_[1, 2]) and np.all(np.isfinite(s_[:, 3:5])), j
+
+
 def test_batches_share_only_identical_layouts(gpu):
     """Jobs that pass one reference array in different shapes with the same
     chunk count (and even different element counts) must not share its
