@@ -177,6 +177,38 @@ def test_drift_score_batch_special_values(gpu):
         assert np.isnan(s_[1, 2]) and np.all(np.isfinite(s_[:, 3:5])), j
 
 
+@pytest.mark.parametrize("dist", [0, 1], ids=["gauss", "t3"])
+def test_canary_sim_batch_special_references(gpu, dist):
+    """A group of 9 runs (different tampers and scales) over one reference
+    holding infinities, NaNs, values beyond the fp16 range and fp32
+    subnormals: the batched live pass writes every run's activations bit
+    for bit as one launch per run does, NaN payloads included."""
+    torch, cdt = gpu
+    announce(f"canary_sim_batch special references dist={dist}")
+    S, C, T, H = 4, 3, 5, 4096  # 20480 elements per block: one partial live-pass chunk
+    ref = inputs.ref_normal((S, C, T, H), seed=33)
+    flat = ref.reshape(-1)
+    specials = [np.inf, -np.inf, np.nan, 1e30, -7e4, 65519.0, 1e-40, -1e-45, 0.0, -0.0]
+    flat[::997][:len(specials)] = np.array(specials, np.float32)
+    ref[S // 2, 1, 2, :8] = np.float32(1e6)
+    q, m = oracle.ref_stats(ref)
+    ts, bs = oracle.block_scales(T, H, q, m, 0.05, 1e-2)
+    rd, tsd, bsd = to_dev(torch, ref), to_dev(torch, ts), to_dev(torch, bs)
+    jobs = []
+    for j in range(9):
+        kw = dict(seed=6, cfg_id=50 + j, sigma_b=1e-2, benign_dist=dist, mal_mask=1 << (j % S),
+                  tamper=(1, 2, 4, 7)[j % 4], tscale=tsd, bscale=bsd, flip_p=0.25,
+                  scale=1.5)
+        jobs.append((rd, torch.empty((S, C, T, H), dtype=torch.float16, device="cuda"), kw))
+    cdt.canary_sim_batch(jobs)
+    for j, (_, hb, kw) in enumerate(jobs):
+        one = cdt.canary_sim(rd, **kw)
+        torch.cuda.synchronize()
+        assert torch.equal(hb.view(torch.int16), one.view(torch.int16)), f"run {j}"
+    bits = h_bits(jobs[0][1])
+    assert np.any((bits & 0x7C00) == 0x7C00)  # the specials reached the output
+
+
 def test_batches_share_only_identical_layouts(gpu):
     """Jobs that pass one reference array in different shapes with the same
     chunk count (and even different element counts) must not share its
