@@ -222,3 +222,34 @@ def test_per_canary_counts_brute_force(orc, flags, base):
 def test_per_canary_rejects_more_than_64_stages(orc):
     with pytest.raises(ValueError):
         orc.auroc_canaries(np.zeros((2, 65), np.float32), 1)
+
+
+def test_per_canary_sums_are_the_totals_on_random_tables(orc):
+    """Property over random tables (S 1..12, C 0..9, any positive set, ties,
+    NaNs, both control variants): the per-canary counts of Eq. 5 add up to
+    the configuration's totals, and each canary's detector counts never
+    exceed its number of pairs."""
+    from hypothesis import given, settings, strategies as st
+
+    @settings(max_examples=150, deadline=None, derandomize=True)
+    @given(S=st.integers(1, 12), C=st.integers(0, 9), mask_bits=st.integers(0, (1 << 12) - 1),
+           levels=st.integers(1, 6), nan_frac=st.sampled_from([0.0, 0.1]),
+           include_true=st.booleans(), seed=st.integers(0, 2**31))
+    def check(S, C, mask_bits, levels, nan_frac, include_true, seed):
+        rng = np.random.default_rng(seed)
+        sc = (rng.integers(0, levels, (C, S)) / levels).astype(np.float32)
+        sc[rng.random((C, S)) < nan_frac] = np.nan
+        mask = mask_bits & ((1 << S) - 1)
+        flags = 1 | 8 | (4 if include_true else 0)
+        per = orc.auroc_canaries(sc, mask, seed=seed, cfg_id=3, flags=flags)
+        counts, _ = orc.auroc_config(sc, mask, seed=seed, cfg_id=3, flags=flags & 5)
+        n_pos = bin(mask).count("1")
+        tot = per.astype(np.uint64).sum(axis=0) if C else np.zeros(6, np.uint64)
+        assert tot[0] == counts[0] and tot[1] == counts[1]
+        assert tot[2] == counts[3] and tot[3] == counts[4]
+        base = orc.random_baseline(C, S, mask, seed=seed, cfg_id=3)
+        assert tot[4] == base[0] and tot[5] == base[1]
+        if C:
+            assert np.all(per[:, 0] + per[:, 1] <= n_pos * (S - n_pos))
+
+    check()
