@@ -122,7 +122,9 @@ __device__ __forceinline__ void rank_canary(const RankCtx& r, const AurocCfgDev&
     }
 }
 
-__global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
+// Eqs. 5-6 counts of configuration blockIdx.x (every thread of the
+// workgroup calls it).
+__device__ __forceinline__ void counts_body(
     const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, uint64_t n_scores,
     Key key, uint32_t flags, unsigned long long* __restrict__ counts,
     unsigned long long* __restrict__ baseline) {
@@ -311,7 +313,9 @@ __device__ void pooled_sort(const float* tab, uint32_t n, uint32_t P2, uint32_t 
 
 // Element layout in the pooled sort: key << 32 | label (label 1 = positive);
 // after the negative scan: key << 32 | negatives_before << 1 | label.
-__global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
+// Pooled Mann-Whitney counts of configuration blockIdx.x (every thread of
+// the workgroup calls it).
+__device__ __forceinline__ void pooled_body(
     const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, uint64_t n_scores,
     unsigned long long* __restrict__ pooled) {
     __shared__ uint64_t v[kPoolMax];
@@ -409,6 +413,26 @@ __global__ __launch_bounds__(kPoolThreads) void auroc_pooled_kernel(
     }
 }
 
+
+__global__ __launch_bounds__(kCountThreads) void auroc_counts_kernel(
+    const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, uint64_t n_scores,
+    Key key, uint32_t flags, unsigned long long* __restrict__ counts,
+    unsigned long long* __restrict__ baseline) {
+    counts_body(cfgs, scores, n_scores, key, flags, counts, baseline);
+}
+
+// The counts and the pooled ranking of a configuration in one workgroup:
+// one launch instead of two when the pooled form is asked for (the two
+// parts share nothing but the configuration; the counts use a few hundred
+// bytes of LDS, the sort up to 128 KiB).
+static_assert(kCountThreads == kPoolThreads, "one workgroup shape for both parts");
+__global__ __launch_bounds__(kCountThreads) void auroc_counts_pooled_kernel(
+    const AurocCfgDev* __restrict__ cfgs, const float* __restrict__ scores, uint64_t n_scores,
+    Key key, uint32_t flags, unsigned long long* __restrict__ counts,
+    unsigned long long* __restrict__ baseline, unsigned long long* __restrict__ pooled) {
+    counts_body(cfgs, scores, n_scores, key, flags, counts, baseline);
+    pooled_body(cfgs, scores, n_scores, pooled);
+}
 // Eq. 6 from integer counts: G / pairs (ties count 0, the equation as
 // printed) and (G + E / 2) / pairs (ties count one half, the Mann-Whitney
 // form), in fp64.  A triple with no pairs, or one holding the out-of-bounds
@@ -473,13 +497,18 @@ hipError_t launch_auroc(uint32_t n_cfg, const AurocCfgDev* cfgs_dev, const float
                         uint64_t* pooled, uint64_t* baseline, hipStream_t st) {
     if (n_cfg == 0) return hipSuccess;
     const Key key{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)};
-    hipLaunchKernelGGL(auroc_counts_kernel, dim3(n_cfg), dim3(kCountThreads), 0, st, cfgs_dev,
-                       scores, n_scores, key, flags, reinterpret_cast<unsigned long long*>(counts),
-                       reinterpret_cast<unsigned long long*>(baseline));
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !(flags & 2u)) return e;
-    hipLaunchKernelGGL(auroc_pooled_kernel, dim3(n_cfg), dim3(kPoolThreads), 0, st, cfgs_dev,
-                       scores, n_scores, reinterpret_cast<unsigned long long*>(pooled));
+    if (flags & 2u) {
+        hipLaunchKernelGGL(auroc_counts_pooled_kernel, dim3(n_cfg), dim3(kCountThreads), 0, st,
+                           cfgs_dev, scores, n_scores, key, flags,
+                           reinterpret_cast<unsigned long long*>(counts),
+                           reinterpret_cast<unsigned long long*>(baseline),
+                           reinterpret_cast<unsigned long long*>(pooled));
+    } else {
+        hipLaunchKernelGGL(auroc_counts_kernel, dim3(n_cfg), dim3(kCountThreads), 0, st,
+                           cfgs_dev, scores, n_scores, key, flags,
+                           reinterpret_cast<unsigned long long*>(counts),
+                           reinterpret_cast<unsigned long long*>(baseline));
+    }
     return hipGetLastError();
 }
 
