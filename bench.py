@@ -341,6 +341,10 @@ def run_main(torch, cdt, W, args):
     one_sim_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (one_sim * 1e-3) / 1e9
     sim_stream_ms = time_ms(torch, lambda: cdt.canary_sim_stream(big.ref, out=big.h), 7)
     sim_stream_gbps = big.rs.elems * SIM_BYTES_PER_ELEM / (sim_stream_ms * 1e-3) / 1e9
+    # the batched Eq. 4's own memory bound: the same launch's loads with no
+    # arithmetic, on the same arrays
+    batch_read_ms = time_ms(torch, lambda: cdt.drift_read_stream_batch(sb.sets[bi][1]), 7)
+    batch_read_gbps = big.rs.elems * (2 * nr + 4) / (batch_read_ms * 1e-3) / 1e9
     batched_step(cdt, wl, sb, scores, cfgs, auroc_ws, counts, pooled)  # the reported counts
 
     res = {
@@ -377,6 +381,9 @@ def run_main(torch, cdt, W, args):
             "runs_per_launch": nr,
             "avg_launch_ms": round(drift_avg, 4),
             "scored_GBps": round(nr * one_bytes / (drift_avg * 1e-3) / 1e9, 1),
+            "read_stream_ms": round(batch_read_ms, 4),
+            "read_stream_GBps": round(batch_read_gbps, 1),
+            "frac_of_read_stream": round(batch_read_ms / drift_avg, 4),
         },
         "canary_sim": {
             "avg_launch_ms": round(sim_avg, 4),

@@ -72,14 +72,15 @@ extern "C" {
 #define CDT_STREAM_ALT_T3 11
 
 /* Interface version; changes whenever a layout, a generator rule or the set
- * of entry points changes (10: cdt_auroc_canaries added; 9: batched live
+ * of entry points changes (11: cdt_drift_read_stream_batch added; 10:
+ * cdt_auroc_canaries added; 9: batched live
  * pass and Eq. 4, the live-pass stream aid, exact-norm scales under the
  * propagation model; 8:
  * cdt_drift_score_noalloc added; 7: cdt_auroc_values added, NaN scores
  * rank above every number).  cdt_version() returns the library's, which a
  * caller compares with the CDT_INTERFACE_VERSION of the header it was
  * built with. */
-#define CDT_INTERFACE_VERSION 10
+#define CDT_INTERFACE_VERSION 11
 int cdt_version(void);
 
 /* Description of the last error on the calling thread ("" if none). */
@@ -337,6 +338,15 @@ typedef struct cdt_drift_job {
 size_t cdt_drift_batch_workspace_bytes(uint32_t n_jobs, const cdt_drift_job* jobs);
 int cdt_drift_score_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws, size_t ws_bytes,
                           void* stream);
+
+/* Measurement aid for the batched Eq. 4's memory bound: the same checks,
+ * tables, grid, chunks, loads, lane exchange and order as
+ * cdt_drift_score_batch on the same arguments, with the arithmetic replaced
+ * by an XOR fold of the loaded words; it writes nothing (a fold equal to a
+ * fixed 32-bit sentinel would overwrite one score, which does not occur in
+ * practice). */
+int cdt_drift_read_stream_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws,
+                                size_t ws_bytes, void* stream);
 
 /* Measurement aid for Eq. 4's memory bound: reads h and ref exactly as
  * cdt_drift_score does (the same chunks, loads, lane exchange and order)

@@ -124,6 +124,8 @@ _SIGS = {
     "cdt_auroc_upload": ([_u32, ctypes.POINTER(AurocCfg), _u64, _u32, _vp, _sz, _vp], ctypes.c_int),
     "cdt_auroc_launch": ([_u32, _vp, _vp, _u64, _u64, _u32, _vp, _vp, _vp, _vp], ctypes.c_int),
     "cdt_auroc_values": ([_u32, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
+    "cdt_drift_read_stream_batch": ([_u32, ctypes.POINTER(DriftJob), _vp, _sz, _vp],
+                                    ctypes.c_int),
     "cdt_auroc_canaries_workspace_bytes": ([_u32], _sz),
     "cdt_auroc_canaries": ([_u32, ctypes.POINTER(AurocCfg), _vp, _u64, _u64, _u32, _vp, _vp, _sz,
                             _vp], ctypes.c_int),
@@ -134,7 +136,7 @@ _LIB = None
 
 # Interface version of include/cdt.h that the structures and signatures
 # below mirror (cdt_version()).
-ABI_VERSION = 10
+ABI_VERSION = 11
 
 
 def lib():
@@ -365,6 +367,14 @@ def drift_score_batch(jobs):
     bitwise those of drift_score on it."""
     b = jobs if isinstance(jobs, Batch) else drift_batch(jobs)
     _check(lib().cdt_drift_score_batch(b.n, b.arr, _ptr(b.ws), b.ws.numel(), _stream()))
+
+
+def drift_read_stream_batch(jobs):
+    """The batched Eq. 4's loads with no arithmetic (a measurement of that
+    launch's memory bound): jobs is a Batch from drift_batch (or its list of
+    jobs); nothing is written."""
+    b = jobs if isinstance(jobs, Batch) else drift_batch(jobs)
+    _check(lib().cdt_drift_read_stream_batch(b.n, b.arr, _ptr(b.ws), b.ws.numel(), _stream()))
 
 
 def canary_sim_stream(ref, out=None):

@@ -77,7 +77,7 @@ bool canaries_fit(uint32_t canary_base, uint64_t C) {
 
 extern "C" {
 
-int cdt_version(void) { return 10; }
+int cdt_version(void) { return 11; }
 
 const char* cdt_last_error(void) { return g_error; }
 
@@ -566,14 +566,21 @@ size_t cdt_drift_batch_workspace_bytes(uint32_t n_jobs, const cdt_drift_job* job
     return batch_bytes(plan);
 }
 
-int cdt_drift_score_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws, size_t ws_bytes,
-                          void* stream) {
-    const char* fn = "cdt_drift_score_batch";
-    DriftBatchPlan plan;
-    int rc = plan_drift_batch(fn, n_jobs, jobs, &plan, true);
+}  // extern "C"
+
+namespace {
+
+// The batched Eq. 4's set-up shared by the launch and its read-stream aid:
+// plan the jobs, check ws, and copy the job and group tables into it (with
+// the partial-sum addresses filled in).  *launch is false when there is no
+// work.
+int stage_drift_batch(const char* fn, uint32_t n_jobs, const cdt_drift_job* jobs, void* ws,
+                      size_t ws_bytes, hipStream_t st, DriftBatchPlan* plan, bool* launch) {
+    *launch = false;
+    int rc = plan_drift_batch(fn, n_jobs, jobs, plan, true);
     if (rc) return rc;
-    if (plan.table.empty()) return ok();
-    const size_t need = batch_bytes(plan);
+    if (plan->table.empty()) return ok();
+    const size_t need = batch_bytes(*plan);
     if (!ws || ws_bytes < need)
         return fail(CDT_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need,
                     ws ? ws_bytes : 0);
@@ -582,23 +589,56 @@ int cdt_drift_score_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws, 
     // go up in one copy, staged contiguously in pageable host memory (such a
     // copy completes before hipMemcpyAsync returns, so `staged` may go)
     char* base = static_cast<char*>(ws);
-    double* partials = reinterpret_cast<double*>(base + batch_partials_offset(plan));
-    for (cdt::DriftJobDev& d : plan.table)
+    double* partials = reinterpret_cast<double*>(base + batch_partials_offset(*plan));
+    for (cdt::DriftJobDev& d : plan->table)
         if (!d.direct) d.partial = partials + reinterpret_cast<uintptr_t>(d.partial);
-    std::vector<char> staged(batch_partials_offset(plan), 0);
-    memcpy(staged.data(), plan.table.data(), plan.table.size() * sizeof(cdt::DriftJobDev));
-    memcpy(staged.data() + batch_groups_offset(plan), plan.groups.data(),
-           plan.groups.size() * sizeof(cdt::BatchGroupDev));
-    hipStream_t st = static_cast<hipStream_t>(stream);
+    std::vector<char> staged(batch_partials_offset(*plan), 0);
+    memcpy(staged.data(), plan->table.data(), plan->table.size() * sizeof(cdt::DriftJobDev));
+    memcpy(staged.data() + batch_groups_offset(*plan), plan->groups.data(),
+           plan->groups.size() * sizeof(cdt::BatchGroupDev));
     const hipError_t e = hipMemcpyAsync(ws, staged.data(), staged.size(), hipMemcpyHostToDevice,
                                         st);
     if (e != hipSuccess) return device_status(e, fn);
+    *launch = true;
+    return CDT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cdt_drift_score_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws, size_t ws_bytes,
+                          void* stream) {
+    const char* fn = "cdt_drift_score_batch";
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    DriftBatchPlan plan;
+    bool launch = false;
+    int rc = stage_drift_batch(fn, n_jobs, jobs, ws, ws_bytes, st, &plan, &launch);
+    if (rc || !launch) return rc;
+    char* base = static_cast<char*>(ws);
     return device_status(
         cdt::launch_drift_batch(
             reinterpret_cast<const cdt::DriftJobDev*>(base),
             static_cast<uint32_t>(plan.table.size()),
             reinterpret_cast<const cdt::BatchGroupDev*>(base + batch_groups_offset(plan)),
             static_cast<uint32_t>(plan.groups.size()), plan.total_iters, plan.total_blocks, st),
+        fn);
+}
+
+int cdt_drift_read_stream_batch(uint32_t n_jobs, const cdt_drift_job* jobs, void* ws,
+                                size_t ws_bytes, void* stream) {
+    const char* fn = "cdt_drift_read_stream_batch";
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    DriftBatchPlan plan;
+    bool launch = false;
+    int rc = stage_drift_batch(fn, n_jobs, jobs, ws, ws_bytes, st, &plan, &launch);
+    if (rc || !launch) return rc;
+    char* base = static_cast<char*>(ws);
+    return device_status(
+        cdt::launch_drift_batch_read_stream(
+            reinterpret_cast<const cdt::DriftJobDev*>(base),
+            reinterpret_cast<const cdt::BatchGroupDev*>(base + batch_groups_offset(plan)),
+            static_cast<uint32_t>(plan.groups.size()), plan.total_iters, st),
         fn);
 }
 

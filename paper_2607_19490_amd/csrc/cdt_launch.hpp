@@ -216,6 +216,12 @@ hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs,
                               const BatchGroupDev* groups_dev, uint32_t n_groups,
                               uint64_t total_iters, uint64_t total_blocks, hipStream_t st);
 
+// The batched Eq. 4's reads (same iterations, chunks, loads, lane exchange
+// and order) with no arithmetic; nothing is written in practice.
+hipError_t launch_drift_batch_read_stream(const DriftJobDev* jobs_dev,
+                                          const BatchGroupDev* groups_dev, uint32_t n_groups,
+                                          uint64_t total_iters, hipStream_t st);
+
 // drift_score's reads (same chunks, loads and order) with no arithmetic; ws
 // is drift_score's workspace and may be overwritten.
 hipError_t launch_drift_read_stream(uint32_t S, uint32_t C, uint32_t T, uint32_t H,

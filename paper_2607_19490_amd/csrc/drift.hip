@@ -165,7 +165,10 @@ __device__ __forceinline__ void drift_chunk(const uint16_t* __restrict__ h,
             }
         }
         if constexpr (kReadOnly) {
-            if (fold == kFoldSentinel) partial[chunk * Tr::kSums] = static_cast<double>(fold);
+            if (fold == kFoldSentinel) {
+                if (direct) score[0] = __uint_as_float(fold);
+                else partial[chunk * Tr::kSums] = static_cast<double>(fold);
+            }
         } else {
             block_sum<Tr::kSums>(acc);
             if (threadIdx.x == 0) {
@@ -232,7 +235,7 @@ __device__ __forceinline__ void accumulate8_jobs(const u32x4 (&hv)[kJ], const f3
 // 3 or 4 jobs take; 2 groups per step for 5-8 jobs measured no faster.
 constexpr int kMultiUnroll = 4;
 
-template <int kJ>
+template <int kJ, bool kReadOnly = false>
 __device__ __forceinline__ void drift_chunk_jobs(const DriftJobDev* __restrict__ jobs,
                                                  uint64_t chunk) {
     constexpr int kU = kMultiUnroll;
@@ -249,6 +252,7 @@ __device__ __forceinline__ void drift_chunk_jobs(const DriftJobDev* __restrict__
     double d_acc[kJ], r_acc = 0.0;
 #pragma unroll
     for (int j = 0; j < kJ; ++j) d_acc[j] = 0.0;
+    uint32_t fold = 0;
     for (uint32_t base = g0; base < g_end; base += kReduceThreads * kU) {
         f32x4 a0[kU], a1[kU];
         u32x4 hv[kJ][kU];
@@ -292,8 +296,18 @@ __device__ __forceinline__ void drift_chunk_jobs(const DriftJobDev* __restrict__
             u32x4 hu[kJ];
 #pragma unroll
             for (int j = 0; j < kJ; ++j) hu[j] = hv[j][u];
-            accumulate8_jobs<kJ>(hu, a0[u], a1[u], d_acc, r_acc);
+            if constexpr (kReadOnly) {
+                fold ^= fold_group(hu[0], zero, a0[u], a1[u]);
+#pragma unroll
+                for (int j = 1; j < kJ; ++j) fold ^= hu[j].x ^ hu[j].y ^ hu[j].z ^ hu[j].w;
+            } else {
+                accumulate8_jobs<kJ>(hu, a0[u], a1[u], d_acc, r_acc);
+            }
         }
+    }
+    if constexpr (kReadOnly) {  // keeps the loads; the sentinel never occurs in practice
+        if (fold == kFoldSentinel) jobs[0].score[0] = __uint_as_float(fold);
+        return;
     }
     double sums[kJ + 1];
 #pragma unroll
@@ -332,6 +346,7 @@ __device__ __forceinline__ uint32_t find_job(const DriftJobDev* __restrict__ job
     return lo;
 }
 
+template <bool kReadOnly>
 __global__ __launch_bounds__(kReduceThreads) void drift_batch_partial_kernel(
     const DriftJobDev* __restrict__ jobs, const BatchGroupDev* __restrict__ groups,
     uint32_t n_groups, uint64_t total_iters) {
@@ -341,23 +356,23 @@ __global__ __launch_bounds__(kReduceThreads) void drift_batch_partial_kernel(
         if (!batch_iter(groups, n_groups, it, &j, &unit_jobs, &chunk, &group_jobs)) continue;
         static_assert(kDriftJobsPerIter == 8, "one case per unit size");
         if (unit_jobs == 8) {
-            drift_chunk_jobs<8>(jobs + j, chunk);
+            drift_chunk_jobs<8, kReadOnly>(jobs + j, chunk);
         } else if (unit_jobs == 7) {
-            drift_chunk_jobs<7>(jobs + j, chunk);
+            drift_chunk_jobs<7, kReadOnly>(jobs + j, chunk);
         } else if (unit_jobs == 6) {
-            drift_chunk_jobs<6>(jobs + j, chunk);
+            drift_chunk_jobs<6, kReadOnly>(jobs + j, chunk);
         } else if (unit_jobs == 5) {
-            drift_chunk_jobs<5>(jobs + j, chunk);
+            drift_chunk_jobs<5, kReadOnly>(jobs + j, chunk);
         } else if (unit_jobs == 4) {
-            drift_chunk_jobs<4>(jobs + j, chunk);
+            drift_chunk_jobs<4, kReadOnly>(jobs + j, chunk);
         } else if (unit_jobs == 3) {
-            drift_chunk_jobs<3>(jobs + j, chunk);
+            drift_chunk_jobs<3, kReadOnly>(jobs + j, chunk);
         } else if (unit_jobs == 2) {
-            drift_chunk_jobs<2>(jobs + j, chunk);
+            drift_chunk_jobs<2, kReadOnly>(jobs + j, chunk);
         } else {
             const DriftJobDev& J = jobs[j];
-            drift_chunk<DriftMetric::kL2, false>(J.h, J.ref, J.n8, J.cpb, chunk, J.partial,
-                                                 J.direct, J.S, J.C, J.score, J.sums);
+            drift_chunk<DriftMetric::kL2, kReadOnly>(J.h, J.ref, J.n8, J.cpb, chunk, J.partial,
+                                                     J.direct, J.S, J.C, J.score, J.sums);
         }
     }
 }
@@ -431,7 +446,7 @@ hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs,
                               uint64_t total_iters, uint64_t total_blocks, hipStream_t st) {
     if (n_jobs == 0) return hipSuccess;
     if (total_iters > 0) {
-        hipLaunchKernelGGL(drift_batch_partial_kernel, dim3(reduce_grid(total_iters)),
+        hipLaunchKernelGGL(drift_batch_partial_kernel<false>, dim3(reduce_grid(total_iters)),
                            dim3(kReduceThreads), 0, st, jobs_dev, groups_dev, n_groups,
                            total_iters);
         const hipError_t e = hipGetLastError();
@@ -441,6 +456,15 @@ hipError_t launch_drift_batch(const DriftJobDev* jobs_dev, uint32_t n_jobs,
     const uint64_t grid = (total_blocks + 255) / 256;
     hipLaunchKernelGGL(drift_batch_combine_kernel, dim3(static_cast<uint32_t>(grid)), dim3(256), 0,
                        st, jobs_dev, n_jobs, total_blocks);
+    return hipGetLastError();
+}
+
+hipError_t launch_drift_batch_read_stream(const DriftJobDev* jobs_dev,
+                                          const BatchGroupDev* groups_dev, uint32_t n_groups,
+                                          uint64_t total_iters, hipStream_t st) {
+    if (total_iters == 0) return hipSuccess;
+    hipLaunchKernelGGL(drift_batch_partial_kernel<true>, dim3(reduce_grid(total_iters)),
+                       dim3(kReduceThreads), 0, st, jobs_dev, groups_dev, n_groups, total_iters);
     return hipGetLastError();
 }
 

@@ -38,7 +38,7 @@ def test_header_declarations_are_exported(cdt):
 
 def test_version_and_sizes(cdt):
     L = cdt.lib()
-    assert L.cdt_version() == 10 == cdt.ABI_VERSION
+    assert L.cdt_version() == 11 == cdt.ABI_VERSION
     assert L.cdt_reduce_workspace_bytes(16, 256, 256, 8192) == 4096 * 64 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 16, 256) == 32 * 1 * 24
     assert L.cdt_reduce_workspace_bytes(4, 8, 0, 256) == 0
@@ -313,6 +313,13 @@ def test_batch_calls_validate_every_job_on_the_host(cdt):
     assert L.cdt_drift_score_batch(2, jobs, 16, nbytes - 16, None) == cdt.EINVAL
     empty = (cdt.DriftJob * 1)(cdt.DriftJob(0, 2, 3, 16, None, None, None, None))
     assert L.cdt_drift_score_batch(1, empty, None, 0, None) == cdt.OK
+    # the read-stream aid takes the same arguments and checks them the same way
+    rs = L.cdt_drift_read_stream_batch
+    assert rs(2, jobs, 16, nbytes - 16, None) == cdt.EINVAL
+    assert rs(2, jobs, 8, nbytes, None) == cdt.EALIGN
+    assert rs(1, empty, None, 0, None) == cdt.OK
+    bad = (cdt.DriftJob * 1)(cdt.DriftJob(2, 2, 3, 12, 16, 16, 16, None))
+    assert rs(1, bad, 16, 1 << 20, None) == cdt.EINVAL and "multiple of 8" in _err(cdt)
     p = cdt.sim_params(seed=0, cfg_id=0)
     p3 = cdt.sim_params(seed=0, cfg_id=0, benign_dist=1)
     sj = (cdt.SimJob * 2)()

@@ -209,6 +209,30 @@ def test_canary_sim_batch_special_references(gpu, dist):
     assert np.any((bits & 0x7C00) == 0x7C00)  # the specials reached the output
 
 
+def test_drift_read_stream_batch_writes_nothing(gpu):
+    """The batched Eq. 4's read-stream aid runs the same launch's loads over
+    mixed groups (units of 8, 3 and 1; one and several chunks per block)
+    and leaves every score and sum untouched."""
+    torch, cdt = gpu
+    announce("drift_read_stream_batch")
+    jobs = []
+    for k, (r, si) in enumerate(SHARED_ORDER[:12] + [(2, 2)] * 8):
+        S, C, T, H = SHARED_SHAPES[si]
+        a = to_dev(torch, inputs.ref_normal((S, C, T, H), seed=700 + r))
+        h = to_dev(torch, inputs.live_near(a.cpu().numpy(), seed=800 + k, rel=1e-3))
+        jobs.append((h.view(torch.float16), a,
+                     torch.full((C, S), -1.0, dtype=torch.float32, device="cuda"),
+                     torch.full((C, S, 2), -1.0, dtype=torch.float64, device="cuda")))
+    b = cdt.drift_batch(jobs)
+    cdt.drift_read_stream_batch(b)
+    torch.cuda.synchronize()
+    for k, (_, _, sc, nd) in enumerate(jobs):
+        assert bool((sc == -1.0).all()) and bool((nd == -1.0).all()), k
+    cdt.drift_score_batch(b)  # the same batch object still scores
+    torch.cuda.synchronize()
+    assert all(bool((sc >= 0).all()) for _, _, sc, _ in jobs)
+
+
 def test_batches_share_only_identical_layouts(gpu):
     """Jobs that pass one reference array in different shapes with the same
     chunk count (and even different element counts) must not share its
