@@ -450,6 +450,26 @@ def time_ms(torch, fn, reps=5):
     return t[len(t) // 2]
 
 
+def time_ms_chain(torch, fn, k=20, reps=3):
+    """Time per call of k back-to-back calls of fn() between two HIP events
+    (median of reps): a short launch's cost in a stream of such launches,
+    its ramp and tail included, without the start of an idle queue that a
+    single timed call also pays."""
+    fn()
+    torch.cuda.synchronize()
+    t = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(k):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        t.append(a.elapsed_time(b) / k)
+    t.sort()
+    return t[len(t) // 2]
+
+
 def auroc_row(cdt, torch, score, rs, cfg_id, seed, flags):
     counts, _, base = cdt.auroc([(rs.S, rs.C, 0, rs.mal_mask, cfg_id)], score.reshape(-1),
                                 seed=seed, flags=flags)
@@ -823,6 +843,11 @@ def config_runs(torch, cdt, W, name):
     # the compute-free read of the same arrays: what a launch of this size gets
     read_ms = time_ms(torch, lambda: cdt.drift_read_stream(prep.h, prep.ref, ws=prep.ws), 5)
     read_gbps = rs.elems * DRIFT_BYTES_PER_ELEM / (read_ms * 1e-3) / 1e9
+    # the same launches back to back (the last run's activations)
+    chain_ms = time_ms_chain(
+        torch, lambda: cdt.drift_score(prep.h, prep.ref, out=score, ws=prep.ws))
+    chain_read_ms = time_ms_chain(
+        torch, lambda: cdt.drift_read_stream(prep.h, prep.ref, ws=prep.ws))
     # the runs' Eq. 4 as one batched launch over the shared reference (each
     # run's activations in its own array; as many runs as fit 16 GiB of them)
     nb = max(1, min(len(rs.runs), (16 << 30) // (2 * rs.elems)))
@@ -846,6 +871,12 @@ def config_runs(torch, cdt, W, name):
            "drift_frac_of_hbm_peak": round(nbytes / (drift_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
            "read_stream_GBps": round(read_gbps, 1),
            "drift_frac_of_read_stream": round(nbytes / (drift_ms * 1e-3) / 1e9 / read_gbps, 4),
+           "drift_back_to_back": {
+               "launches": 20, "ms_per_launch": round(chain_ms, 4),
+               "GBps": round(nbytes / (chain_ms * 1e-3) / 1e9, 1),
+               "frac_of_hbm_peak": round(nbytes / (chain_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+               "read_stream_ms_per_launch": round(chain_read_ms, 4),
+               "frac_of_read_stream": round(chain_read_ms / chain_ms, 4)},
            "canary_sim_ms": round(sim_ms, 4),
            "runs": rows}
     del prep, score
