@@ -87,7 +87,8 @@ def test_fp16_conversion_exhaustive(gpu):
         pick = np.sort(rng.integers(0, n, 1 << 14))
         xs = x.reshape(-1)[torch.from_numpy(pick).cuda()].cpu().numpy()
         gs = got[torch.from_numpy(pick).cuda()].cpu().numpy().view(np.uint16)
-        ws = xs.astype(np.float16).view(np.uint16)
+        with np.errstate(over="ignore"):  # values past the fp16 range round to inf
+            ws = xs.astype(np.float16).view(np.uint16)
         ok = (gs == ws) | (((gs & 0x7FFF) == 0) & ((ws & 0x7FFF) == 0)) | np.isnan(xs)
         assert ok.all()
         del x, got, want, same, zeros, nans
