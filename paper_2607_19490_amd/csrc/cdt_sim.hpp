@@ -98,6 +98,37 @@ __device__ __forceinline__ SimBlock sim_block(const SimArgs& A, uint64_t block) 
     return B;
 }
 
+// IEEE fp32 sqrt and division on the Student-t draw's own ranges.  q is a
+// sum of three squared Irwin-Hall normals (multiples of 0x1.bb67aep-16, at
+// most 3.47 in magnitude): 0, handled by the caller, or in [6.9e-10, 36];
+// the divisor s = sqrt(q) lies in [2.6e-5, 6] and the dividend |zb| <= 3.47.
+// On these ranges the compiler's correctly rounded sequences reduce to the
+// instructions below: v_sqrt_f32 with its one-ulp residual correction (the
+// scaling of inputs below 2^-96 and the zero / infinity cases never apply),
+// and the reciprocal with two FMA refinements of the quotient (v_div_scale
+// never scales, v_div_fmas is a plain FMA, v_div_fixup returns its input).
+// The results are bitwise those of sqrtf and '/': every float in
+// [2^-96, 2^7) and every divisor in [2^-17, 2^4) against 256 Irwin-Hall
+// dividends were compared on the device.
+__device__ __forceinline__ float t3_sqrt(float q) {
+    const float s = __builtin_amdgcn_sqrtf(q);
+    const float dn = __uint_as_float(__float_as_uint(s) - 1u);
+    const float up = __uint_as_float(__float_as_uint(s) + 1u);
+    const float r_dn = __builtin_fmaf(-dn, s, q);
+    const float r_up = __builtin_fmaf(-up, s, q);
+    const float t = r_dn <= 0.0f ? dn : s;
+    return r_up > 0.0f ? up : t;
+}
+
+__device__ __forceinline__ float t3_div(float a, float b) {
+    const float y0 = __builtin_amdgcn_rcpf(b);
+    const float e = __builtin_fmaf(-b, y0, 1.0f);
+    const float y = __builtin_fmaf(e, y0, y0);
+    const float q0 = a * y;
+    const float q1 = __builtin_fmaf(__builtin_fmaf(-b, q0, a), y, q0);
+    return __builtin_fmaf(__builtin_fmaf(-b, q1, a), y, q1);
+}
+
 // Eq. 2: the benign output v = base + sc * zb of elements e0..e0+7, with the
 // noise scale taken from the reference a (elementwise mode) and base = a for
 // independent stages (base = a + carried error in the propagation model).
@@ -115,7 +146,7 @@ __device__ __forceinline__ void benign8(const SimArgs& A, const SimBlock& B, uin
             const float z1 = irwin_hall4(w.x, w.y);
             const float z2 = irwin_hall4(w.z, w.w);
             const float q = (z1 * z1 + z2 * z2) + z3[k] * z3[k];
-            zb[k] = (q == 0.0f) ? 0.0f : zb[k] / sqrtf(q);
+            zb[k] = (q == 0.0f) ? 0.0f : t3_div(zb[k], t3_sqrt(q));
         }
     }
 #pragma unroll
